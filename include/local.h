@@ -1,0 +1,246 @@
+/*
+ * local.h — C ABI of the mixed-adapter LoRA step and version-tagged paged
+ * attention ("LOCAL: Enabling Learning On-device Contiguously for Agent LLMs").
+ *
+ * The library implements the data-parallel step that every foreground request
+ * of the runtime shares:
+ *   - a projection made of a frozen base weight plus a low-rank adapter delta,
+ *     with every token routed to its own adapter (§2.2, "LoRA adapters": many
+ *     adapters share one frozen base model and each request is routed to its
+ *     adapter);
+ *   - attention over a paged KV cache whose blocks carry the adapter version
+ *     that produced them, so that KV written under another version is rejected
+ *     (§1 challenge (2) and §5.1: the adapter and its version are part of the
+ *     validity key kappa; §3: a publish stales only KV owned by that adapter).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  Memory      Every pointer is DEVICE memory owned by the caller. The library
+ *              allocates nothing and keeps no pointer after the call returns.
+ *              All tensors are dense, row-major and contiguous in the layout
+ *              stated per argument.
+ *  bf16        `uint16_t` storage of IEEE bfloat16. Conversions to bf16 inside
+ *              the library round to nearest even.
+ *  Streams     `stream` is a hipStream_t passed as `void*` (NULL = the null
+ *              stream). All work is enqueued asynchronously on it; outputs are
+ *              valid once the stream has reached that point.
+ *  Workspace   Scratch device memory is supplied by the caller. Call once with
+ *              `ws == NULL`: the required size is written to `*ws_bytes`, the
+ *              call returns LOCAL_OK and launches nothing. Then call with
+ *              `ws != NULL` and `*ws_bytes` >= that size. The size depends only
+ *              on the host-side scalar arguments. The workspace needs no
+ *              initial contents and its contents after the call are undefined.
+ *              Calls that share one workspace must be ordered on one stream.
+ *  Errors      Arguments are validated on the host before anything is
+ *              launched; on error nothing is launched and nothing is written.
+ *              `local_last_error()` returns a message for the calling thread's
+ *              most recent failure. Values held in device memory (block ids,
+ *              lengths, adapter indices) cannot be checked on the host: they
+ *              are the caller's contract, stated per argument.
+ *  Version tags are read-only. The library never writes `block_version`: tags
+ *              belong to the KV manager, which changes them only when an
+ *              adapter version is published (§4.2, §5.3: in-progress adapter
+ *              state and the KV it produces stay private until publication;
+ *              §4.3: failed work creates no reusable coverage).
+ *
+ * KV block pool layout (one attention layer)
+ * ------------------------------------------
+ *  The pool holds `num_blocks` physical blocks of BS = 16 token slots for Hkv
+ *  KV heads of head dimension D (D = 64 or 128). K and V use different
+ *  in-block orders so that the matrix-core operands load as contiguous rows:
+ *    k_cache  [num_blocks][Hkv][D/8][BS][8]   K(p,g,slot,d) at
+ *             (((p*Hkv + g)*(D/8) + d/8)*BS + slot)*8 + d%8
+ *    v_cache  [num_blocks][Hkv][D][BS]        V(p,g,slot,d) at
+ *             ((p*Hkv + g)*D + d)*BS + slot
+ *  A (block, head) pair therefore owns one contiguous 16*D*2-byte tile in each
+ *  of k_cache and v_cache. A multi-layer pool is the caller's business: it
+ *  passes the base pointers of one layer's K and V pools.
+ *
+ *  Logical position pi of request b lives in physical block
+ *  block_table[b*max_blocks + pi/16], slot pi%16. Request b owns
+ *  ceil(ctx_lens[b]/16) logical blocks; table entries beyond them are never
+ *  read. Block ids must lie in [0, num_blocks).
+ *
+ * Staleness (one rule for every entry point)
+ * ------------------------------------------
+ *  Logical block j of request b is STALE iff
+ *      block_version[block_table[b][j]] != req_version[b].
+ *  Any inequality is stale: an older tag was produced by a superseded version,
+ *  a newer one by a staged version that is not yet published (§5.3). Tags are
+ *  meant to be unique across adapters (for instance a runtime-wide publish
+ *  counter), so that one equality test checks both the adapter and its
+ *  version of the validity key (§5.1). A stale block is excluded as a whole.
+ */
+#ifndef LOCAL_H_
+#define LOCAL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LOCAL_OK = 0,
+  LOCAL_ERR_NULL = 1,        /* a required pointer is NULL                    */
+  LOCAL_ERR_SHAPE = 2,       /* inconsistent or non-positive sizes            */
+  LOCAL_ERR_UNSUPPORTED = 3, /* a size outside what the kernels implement     */
+  LOCAL_ERR_WORKSPACE = 4,   /* ws_bytes NULL, or *ws_bytes below the need    */
+  LOCAL_ERR_HIP = 5          /* the HIP runtime reported an error on launch   */
+} local_status_t;
+
+/* Message for the calling thread's most recent failed call ("" if none). */
+const char* local_last_error(void);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int32_t local_version(void);
+
+/*
+ * local_lora_linear — mixed-adapter LoRA projection (§2.2 "LoRA adapters";
+ * the adapter delta is the low-rank update of the LoRA method the paper
+ * builds on).
+ *
+ *   y[t,n] = sum_k x[t,k] W[n,k]
+ *            + scale[t] * sum_{j < rank(a)} (sum_k x[t,k] A[a,j,k]) B[a,n,j]
+ *   with a = adapter_idx[t]; the second term is absent when a < 0.
+ *
+ *   x            [T][K]               bf16, activations
+ *   W            [N][K]               bf16, frozen base weight (out x in)
+ *   A            [n_adapters][r_max][K]  bf16, adapter down-projections
+ *   B            [n_adapters][N][r_max]  bf16, adapter up-projections
+ *   ranks        [n_adapters] int32 in [1, r_max], or NULL (every rank = r_max).
+ *                Rows j >= rank of A and columns j >= rank of B are never used.
+ *   adapter_idx  [T] int32 in [-1, n_adapters); -1 = base projection only
+ *   scale        [T] float32, the per-token adapter scale s
+ *   y            [T][N]               bf16 output; must not alias the inputs
+ *
+ *  Sizes: T >= 0 (T = 0 launches nothing), K and N positive multiples of 64,
+ *  0 <= n_adapters <= 256, r_max a multiple of 8 in [8, 128] (ignored when
+ *  n_adapters = 0, in which case A, B, ranks, adapter_idx and scale may be
+ *  NULL and every adapter_idx is taken as -1).
+ *  Accumulation is float32; y is rounded once to bf16. The low-rank
+ *  intermediate s*(x A^T) is rounded to bf16 before the up-projection.
+ */
+local_status_t local_lora_linear(
+    const uint16_t* x, int64_t T, int64_t K,
+    const uint16_t* W, int64_t N,
+    const uint16_t* A, const uint16_t* B,
+    int32_t n_adapters, int32_t r_max,
+    const int32_t* ranks,
+    const int32_t* adapter_idx, const float* scale,
+    uint16_t* y,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
+ * local_paged_attn_decode — one new token per request attends over its paged
+ * KV cache with the per-block version mask (§2.2 "KV cache and prefix
+ * caching"; §5.1 validity key; stale coverage is rejected, never reused).
+ *
+ *  First, when k_new/v_new are given, the new token's key and value are
+ *  written at logical position ctx_lens[b]-1 (the decoded token is part of its
+ *  own context). Then for every request b and query head h, with
+ *  g = h / (Hq/Hkv):
+ *    S = { pi < ctx_lens[b] : logical block pi/16 of b is not stale }
+ *    s_pi = sm_scale * sum_d q[b,h,d] K(bt[b][pi/16], g, pi%16, d)
+ *    out[b,h,:] = sum_{pi in S} softmax(s)_pi V(bt[b][pi/16], g, pi%16, :)
+ *    lse[b,h]   = log sum_{pi in S} exp(s_pi)            (natural log)
+ *  If S is empty, out[b,h,:] = 0 and lse[b,h] = -inf.
+ *
+ *   q            [B][Hq][D]  bf16
+ *   k_new,v_new  [B][Hkv][D] bf16, or both NULL (nothing appended)
+ *   k_cache,v_cache  pool of num_blocks blocks, layout above; written only at
+ *                the appended slots
+ *   block_table  [B][max_blocks] int32; ceil(ctx_lens[b]/16) <= max_blocks
+ *   ctx_lens     [B] int32 in [1, 16*max_blocks]
+ *   block_version [num_blocks] int32, req_version [B] int32
+ *   out          [B][Hq][D] bf16;  lse [B][Hq] float32 or NULL
+ *
+ *  Sizes: B >= 0, Hq % Hkv == 0, Hq/Hkv <= 16, D in {64,128},
+ *  block_size == 16. The appended slots of different requests must be
+ *  distinct physical slots.
+ */
+local_status_t local_paged_attn_decode(
+    const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new,
+    uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size,
+    const int32_t* block_table, int32_t max_blocks,
+    const int32_t* ctx_lens,
+    const int32_t* block_version, const int32_t* req_version,
+    float sm_scale,
+    uint16_t* out, float* lse,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
+ * local_paged_attn_prefill — a chunk of new tokens per request is appended to
+ * the paged cache and attends causally over the cached prefix plus the chunk,
+ * with the per-block version mask (§4.1 chunked prefill; §5.3 stale-coverage
+ * prefill runs this same computation under a staged version).
+ *
+ *  Request b owns query rows [q_indptr[b], q_indptr[b+1]) (n_b rows) and has
+ *  ctx_lens[b] = P_b + n_b tokens after the chunk, P_b its cached prefix.
+ *  When k_new/v_new are given, row t of the chunk is first written at logical
+ *  position P_b + (t - q_indptr[b]). Query row i of request b (position
+ *  P_b + i) then attends over
+ *    S_i = { pi <= P_b + i : logical block pi/16 of b is not stale }
+ *  with the same score, softmax, output and empty-set rule as decode.
+ *
+ *   q            [T][Hq][D] bf16;  q_indptr [B+1] int32, q_indptr[0] = 0,
+ *                non-decreasing, q_indptr[B] = T, n_b <= ctx_lens[b]
+ *   k_new,v_new  [T][Hkv][D] bf16, or both NULL
+ *   out          [T][Hq][D] bf16;  lse [T][Hq] float32 or NULL
+ *   other arguments as in decode.
+ */
+local_status_t local_paged_attn_prefill(
+    const uint16_t* q, const int32_t* q_indptr, int32_t B, int64_t T,
+    int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new,
+    uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size,
+    const int32_t* block_table, int32_t max_blocks,
+    const int32_t* ctx_lens,
+    const int32_t* block_version, const int32_t* req_version,
+    float sm_scale,
+    uint16_t* out, float* lse,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
+ * local_block_version_check — report the KV blocks that the validity key
+ * rejects (§5.1; §1: stale coverage is rejected at lookup, and reusing it
+ * would mix hidden states of different adapter versions).
+ *
+ *  For request b with nb_b = ceil(ctx_lens[b]/16) blocks and j < nb_b,
+ *  tok(b,j) = min(16, ctx_lens[b] - 16*j) live tokens:
+ *    valid_tokens[b] = sum of tok(b,j) over the blocks that are not stale
+ *    stale list      = every stale (b, j), ordered by b, then by j
+ *  stale_pairs receives the first min(n, cap) entries of the list as int32
+ *  pairs (b, j) (j is the LOGICAL block index; its physical id is
+ *  block_table[b][j]); *n_stale receives n, the full length, even when
+ *  n > cap, so a caller can detect truncation.
+ *
+ *   block_table  [B][max_blocks] int32;  ctx_lens [B] int32 in
+ *                [0, 16*max_blocks]
+ *   block_version [num_blocks] int32 (num_blocks is implied by the ids)
+ *   req_version  [B] int32
+ *   stale_pairs  [cap][2] int32 (may be NULL when cap == 0)
+ *   n_stale      one int32 (device)
+ *   valid_tokens [B] int32
+ *
+ *  Sizes: B >= 0, max_blocks >= 1, block_size == 16, cap >= 0.
+ *  The result is exact and deterministic.
+ */
+local_status_t local_block_version_check(
+    const int32_t* block_table, int32_t B, int32_t max_blocks,
+    const int32_t* ctx_lens, int32_t block_size,
+    const int32_t* block_version, const int32_t* req_version,
+    int32_t* stale_pairs, int64_t cap,
+    int32_t* n_stale,
+    int32_t* valid_tokens,
+    void* ws, size_t* ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOCAL_H_ */
