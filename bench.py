@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the mixed-adapter LoRA decode step on one MI355X.
+
+One step = one pass of the whole path over one batch: the version check, the
+q/k/v LoRA projections, the appending, version-masked paged decode attention,
+and the output LoRA projection, for the 7B-class single-layer decode workload
+(hidden 4096, 32x128 MHA, batch 32, context U[256,4096], 8 rank-16 adapters on
+q/k/v/o). Inputs are seeded synthetic tensors already resident in HBM. Two
+independent input sets (weights, KV pools, activations) alternate between
+steps, so that the last-level cache cannot serve one step's weights to the
+next.
+
+Prints ONE JSON line. `value` is decode tokens/s. `roofline` is for the
+dominant kernel (decode attention), timed with HIP events around its launches
+inside the timed region. `prefill` reports the matrix-core utilisation of the
+LoRA-fused projections of the chunked-prefill workload, timed the same way.
+`cpu_baseline` is the CPU oracle timed on this host on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix cores
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--sets", type=int, default=2, help="input sets rotated across steps")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-prefill", action="store_true")
+    p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    return p.parse_args()
+
+
+def decode_bytes(w, meta):
+    """Algorithmic HBM bytes of one decode step and of its attention launch."""
+    D, hq, hkv, H = w.head_dim, w.hq, w.hkv, w.hidden
+    B = meta.B
+    nb = (meta.ctx_lens.astype(np.int64) + 15) // 16
+    # valid KV tokens: live tokens of non-stale blocks (version check rule)
+    valid_tokens = 0
+    for b in range(B):
+        L = int(meta.ctx_lens[b])
+        tags = meta.block_version[meta.block_table[b, :nb[b]]]
+        live = np.minimum(16, L - 16 * np.arange(nb[b]))
+        valid_tokens += int(live[tags == meta.req_version[b]].sum())
+    kv = valid_tokens * hkv * D * 2 * 2
+    attn = (kv + B * hq * D * 2 * 2 + B * hq * 4      # q, out, lse
+            + B * hkv * D * 2 * 2 * 2                  # k_new/v_new read + append write
+            + int(nb.sum()) * 8)                       # table entry + tag
+    present = np.unique(meta.token_adapter[meta.token_adapter >= 0])
+    proj = 0
+    for name in ("q", "k", "v", "o"):
+        N, K = w.proj_shape(name)
+        proj += N * K * 2 + B * (K + N) * 2
+        if name in w.lora_targets:
+            for a in present:
+                r = w.ranks[a]
+                proj += r * K * 2 + N * r * 2
+    vc = int(nb.sum()) * 8 + B * 4 * 3
+    return attn, attn + proj + vc, valid_tokens
+
+
+def prefill_gemm_flops(w, meta):
+    T = meta.T
+    f = 0
+    for name in ("q", "k", "v", "o"):
+        N, K = w.proj_shape(name)
+        f += 2 * T * K * N
+        if name in w.lora_targets:
+            r = w.r_max
+            f += 2 * T * r * (K + N)
+    return f
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; --gpus %d is not supported "
+              "(multi-GPU sharding is described in DESIGN.md, not built)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads
+    import paper_2608_15241_amd as lk
+    from paper_2608_15241_amd.step import Step, meta_to_device
+
+    lk.load_library()
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    w = workloads.DECODE_7B
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
+    sets = []
+    for s in range(args.sets):
+        weights = [workloads.make_layer_weights(w, 0, dev, seed=100 + s)]
+        pool = workloads.make_kv_pool(w, meta, dev, seed=100 + s)
+        x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=200 + s)
+        st = Step("decode", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
+        sets.append((st, pool, weights, x))
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    # warmup
+    for i in range(args.warmup):
+        sets[i % len(sets)][0]()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(K):
+        st = sets[i % len(sets)][0]
+        st.version_check()
+        lc = st.layer_calls[0]
+        lc["q"]()
+        lc["k"]()
+        lc["v"]()
+        ev_a[i].record(stream)
+        lc["attn"]()
+        ev_b[i].record(stream)
+        lc["o"]()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / K
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]))
+
+    attn_bytes, step_bytes, valid_tokens = decode_bytes(w, meta)
+    tokens_per_s = meta.B / (ms_per_step / 1e3)
+    attn_gbps = attn_bytes / (attn_ms / 1e3) / 1e9
+    step_gbps = step_bytes / (ms_per_step / 1e3) / 1e9
+
+    result = {
+        "metric": "decode tokens/s + achieved HBM GB/s (% peak); prefill LoRA-GEMM MFMA util",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": w.n_layers, "hidden": w.hidden,
+                   "heads": "%dq/%dkv x %d" % (w.hq, w.hkv, w.head_dim), "batch": meta.B,
+                   "context": "U[256,4096]", "sum_context": int(meta.ctx_lens.sum()),
+                   "adapters": "%d x rank %d on q/k/v/o" % (w.n_adapters, w.r_max),
+                   "input_sets": args.sets},
+        "roofline": {"kernel": "local_paged_attn_decode", "bound": "hbm",
+                     "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5)},
+        "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
+                     "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
+    }
+
+    if not args.no_prefill:
+        result["prefill"] = bench_prefill(torch, workloads, lk, dev)
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(torch, workloads, w, meta, sets[0], args)
+
+    del sets
+    print(json.dumps(result), flush=True)
+
+
+def bench_prefill(torch, workloads, lk, dev, reps=20):
+    """Matrix-core utilisation of the 4 LoRA-fused projections (prefill workload)."""
+    from paper_2608_15241_amd.step import meta_to_device
+    w = workloads.PREFILL_7B
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
+    calls = []
+    for s in range(2):
+        lw = workloads.make_layer_weights(w, 0, dev, seed=300 + s)
+        x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=400 + s)
+        ws = lk.Workspace(dev)
+        for name in ("q", "k", "v", "o"):
+            N, K = w.proj_shape(name)
+            inp = x if K == w.hidden else torch.empty((meta.T, K), dtype=torch.bfloat16,
+                                                      device=dev).normal_()
+            out = torch.empty((meta.T, N), dtype=torch.bfloat16, device=dev)
+            calls.append(lk.prepare_lora_linear(inp, lw["W_" + name], lw["A_" + name],
+                                                lw["B_" + name], lw["ranks_" + name],
+                                                md.token_adapter, md.token_scale, out=out,
+                                                workspace=ws))
+    per_set = 4
+    for c in calls:
+        c()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for r in range(reps):
+        for c in calls[(r % 2) * per_set:(r % 2 + 1) * per_set]:
+            c()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flops = prefill_gemm_flops(w, meta)
+    tflops = flops / (ms / 1e3) / 1e12
+    return {"workload": w.name, "kernel": "local_lora_linear x4 (q,k,v,o), T=%d" % meta.T,
+            "bound": "mfma", "flops_per_step": flops, "ms_per_step": round(ms, 5),
+            "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
+def cpu_baseline(torch, workloads, w, meta, set0, args):
+    """The oracle (float64 C, OpenMP) on the same decode step, on this host."""
+    import oracle
+    import oracle.chain as ochain
+    st, pool, weights, x = set0
+    D = w.head_dim
+
+    def h(t):
+        return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    lw = {k: (h(v) if v.dtype == torch.bfloat16 else v.cpu().numpy())
+          for k, v in weights[0].items()}
+    kpool = h(pool[0, 0]).reshape(-1)
+    vpool = h(pool[0, 1]).reshape(-1)
+    xh = h(x)
+    qi = np.arange(meta.B + 1, dtype=np.int32)
+    times = []
+    t_budget = time.time() + args.cpu_budget_s
+    n_req = meta.B
+    while True:
+        kc, vc = kpool.copy(), vpool.copy()
+        t0 = time.perf_counter()
+        oracle.block_version_check(meta.block_table, meta.ctx_lens, meta.block_version,
+                                   meta.req_version)
+        ochain.layer(xh, lw, kc, vc, w.hq, w.hkv, D, meta.block_table, qi, meta.ctx_lens,
+                     meta.block_version, meta.req_version, meta.token_adapter,
+                     meta.token_scale, residual=False)
+        times.append(time.perf_counter() - t0)
+        if time.time() > t_budget or len(times) >= 5:
+            break
+    t = float(np.median(times))
+    return {"value": round(n_req / t, 2), "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "sample": "the whole decode step of the same workload "
+            "(%d requests, 1 layer), median of %d runs" % (n_req, len(times)),
+            "s_per_step": round(t, 3)}
+
+
+if __name__ == "__main__":
+    main()

@@ -101,9 +101,11 @@ int32_t local_version(void);
  * the adapter delta is the low-rank update of the LoRA method the paper
  * builds on).
  *
- *   y[t,n] = sum_k x[t,k] W[n,k]
+ *   y[t,n] = res[t,n] + sum_k x[t,k] W[n,k]
  *            + scale[t] * sum_{j < rank(a)} (sum_k x[t,k] A[a,j,k]) B[a,n,j]
- *   with a = adapter_idx[t]; the second term is absent when a < 0.
+ *   with a = adapter_idx[t]; the adapter term is absent when a < 0 and the
+ *   residual term when `residual` is NULL (it carries the layer's residual
+ *   stream into the output projection without a separate pass).
  *
  *   x            [T][K]               bf16, activations
  *   W            [N][K]               bf16, frozen base weight (out x in)
@@ -113,14 +115,16 @@ int32_t local_version(void);
  *                Rows j >= rank of A and columns j >= rank of B are never used.
  *   adapter_idx  [T] int32 in [-1, n_adapters); -1 = base projection only
  *   scale        [T] float32, the per-token adapter scale s
+ *   residual     [T][N]               bf16, or NULL
  *   y            [T][N]               bf16 output; must not alias the inputs
  *
  *  Sizes: T >= 0 (T = 0 launches nothing), K and N positive multiples of 64,
  *  0 <= n_adapters <= 256, r_max a multiple of 8 in [8, 128] (ignored when
  *  n_adapters = 0, in which case A, B, ranks, adapter_idx and scale may be
  *  NULL and every adapter_idx is taken as -1).
- *  Accumulation is float32; y is rounded once to bf16. The low-rank
- *  intermediate s*(x A^T) is rounded to bf16 before the up-projection.
+ *  Accumulation is float32 (residual included); y is rounded once to bf16.
+ *  The low-rank intermediate s*(x A^T) is rounded to bf16 before the
+ *  up-projection.
  */
 local_status_t local_lora_linear(
     const uint16_t* x, int64_t T, int64_t K,
@@ -129,6 +133,7 @@ local_status_t local_lora_linear(
     int32_t n_adapters, int32_t r_max,
     const int32_t* ranks,
     const int32_t* adapter_idx, const float* scale,
+    const uint16_t* residual,
     uint16_t* y,
     void* ws, size_t* ws_bytes, void* stream);
 
@@ -158,7 +163,8 @@ local_status_t local_lora_linear(
  *
  *  Sizes: B >= 0, Hq % Hkv == 0, Hq/Hkv <= 16, D in {64,128},
  *  block_size == 16. The appended slots of different requests must be
- *  distinct physical slots.
+ *  distinct physical slots, and no other request of the same call may read
+ *  them (a request's newest slot belongs to that request alone).
  */
 local_status_t local_paged_attn_decode(
     const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,

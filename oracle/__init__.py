@@ -43,7 +43,7 @@ def _load():
     P = ctypes.c_void_p
     i32, i64, dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
     lib.oracle_num_threads.restype = ctypes.c_int
-    lib.oracle_lora_linear.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P]
+    lib.oracle_lora_linear.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P]
     lib.oracle_lora_linear.restype = None
     lib.oracle_block_version_check.argtypes = [P, i32, i32, P, P, P, P, i64, P]
     lib.oracle_block_version_check.restype = i64
@@ -72,10 +72,12 @@ def num_threads() -> int:
     return int(_load().oracle_num_threads())
 
 
-def lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scale=None):
-    """y = x W^T + scale * (x A_a^T) B_a^T per token, float64 [T, N].
+def lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scale=None,
+                residual=None):
+    """y = x W^T + scale * (x A_a^T) B_a^T (+ residual) per token, float64 [T, N].
 
-    x [T,K], W [N,K], A [n_ad,r_max,K], B [n_ad,N,r_max] as uint16 bf16 bits.
+    x [T,K], W [N,K], A [n_ad,r_max,K], B [n_ad,N,r_max], residual [T,N] as
+    uint16 bf16 bits.
     """
     lib = _load()
     x = _c(x, np.uint16)
@@ -93,9 +95,12 @@ def lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scale=None):
         scale = _c(scale, np.float32)
         ranks = _c(ranks, np.int32)
         assert r_max <= 256
+    res = _c(residual, np.uint16)
+    if res is not None:
+        assert res.shape == (T, N)
     y = np.empty((T, N), dtype=np.float64)
     lib.oracle_lora_linear(_p(x), T, K, _p(W), N, _p(A), _p(B), n_ad, r_max,
-                           _p(ranks), _p(adapter_idx), _p(scale), _p(y))
+                           _p(ranks), _p(adapter_idx), _p(scale), _p(res), _p(y))
     return y
 
 

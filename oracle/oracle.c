@@ -61,8 +61,11 @@ int oracle_num_threads(void) {
  * adapter). For token t with adapter a = adapter_idx[t]:
  *   u_j      = sum_k x[t,k] * A[a,j,k]                    (j < rank(a))
  *   y[t,n]   = sum_k x[t,k] * W[n,k] + scale[t] * sum_j u_j * B[a,n,j]
- * a < 0 (or n_adapters == 0) leaves the base term alone.
- * Shapes: x[T][K], W[N][K], A[n_ad][r_max][K], B[n_ad][N][r_max], y[T][N].
+ *              + res[t,n]
+ * a < 0 (or n_adapters == 0) leaves the base term alone; res (the layer's
+ * residual stream, optional) is added as given.
+ * Shapes: x[T][K], W[N][K], A[n_ad][r_max][K], B[n_ad][N][r_max], res and
+ * y [T][N].
  */
 void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
                         const uint16_t* W, int64_t N,
@@ -70,7 +73,7 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
                         int32_t n_adapters, int32_t r_max,
                         const int32_t* ranks,
                         const int32_t* adapter_idx, const float* scale,
-                        double* y) {
+                        const uint16_t* res, double* y) {
 #pragma omp parallel for schedule(dynamic, 1)
   for (int64_t t = 0; t < T; ++t) {
     int a = (n_adapters > 0 && adapter_idx) ? adapter_idx[t] : -1;
@@ -92,7 +95,9 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
       double delta = 0.0;
       for (int j = 0; j < rank; ++j)
         delta += u[j] * bf(B[((int64_t)a * N + n) * r_max + j]);
-      y[t * N + n] = base + (a >= 0 ? (double)scale[t] * delta : 0.0);
+      double v = base + (a >= 0 ? (double)scale[t] * delta : 0.0);
+      if (res) v += bf(res[t * N + n]);
+      y[t * N + n] = v;
     }
   }
 }

@@ -1,0 +1,331 @@
+"""Thin ctypes binding of liblocal.so (argument marshalling only).
+
+Every function here checks and marshals torch tensors to the C ABI declared in
+include/local.h and enqueues the library's HIP kernels on the current torch
+stream. No computation happens in Python and there is no fallback: if the
+built library is missing or fails to load, every call raises.
+
+torch is imported before the library is loaded so that the library binds to
+the HIP runtime torch already loaded (both use the soname libamdhip64.so.7),
+which lets it run on torch's streams and memory.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblocal.so")
+BLOCK_SIZE = 16
+
+EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
+           "local_paged_attn_decode", "local_paged_attn_prefill",
+           "local_block_version_check")
+
+_STATUS = {0: "LOCAL_OK", 1: "LOCAL_ERR_NULL", 2: "LOCAL_ERR_SHAPE",
+           3: "LOCAL_ERR_UNSUPPORTED", 4: "LOCAL_ERR_WORKSPACE", 5: "LOCAL_ERR_HIP"}
+
+
+class LocalError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (_STATUS.get(status, str(status)), message))
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load liblocal.so and declare its signatures. Raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(
+            "liblocal.so is not built (%s); run `python -m paper_2608_15241_amd.build`" % path)
+    lib = ctypes.CDLL(path)
+    P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    SZ = ctypes.POINTER(ctypes.c_size_t)
+    lib.local_last_error.restype = ctypes.c_char_p
+    lib.local_last_error.argtypes = []
+    lib.local_version.restype = i32
+    lib.local_version.argtypes = []
+    lib.local_lora_linear.restype = ctypes.c_int
+    lib.local_lora_linear.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
+                                      P, SZ, P]
+    lib.local_paged_attn_decode.restype = ctypes.c_int
+    lib.local_paged_attn_decode.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64, i32, P,
+                                            i32, P, P, P, f32, P, P, P, SZ, P]
+    lib.local_paged_attn_prefill.restype = ctypes.c_int
+    lib.local_paged_attn_prefill.argtypes = [P, P, i32, i64, i32, i32, i32, P, P, P, P, i64,
+                                             i32, P, i32, P, P, P, f32, P, P, P, SZ, P]
+    lib.local_block_version_check.restype = ctypes.c_int
+    lib.local_block_version_check.argtypes = [P, i32, i32, P, i32, P, P, P, i64, P, P, P,
+                                              SZ, P]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise LocalError(status, _lib.local_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _req(t: torch.Tensor, name: str, dtype, ndim: Optional[int] = None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError("%s must have %d dims, got %d" % (name, ndim, t.dim()))
+    return t
+
+
+class Workspace:
+    """A grow-only device byte buffer reused across calls on one stream."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                   device=self.device or "cuda")
+        return self.buf
+
+
+_default_ws = {}
+
+
+def _ws_for(device) -> Workspace:
+    key = torch.device(device).index
+    if key not in _default_ws:
+        _default_ws[key] = Workspace(device)
+    return _default_ws[key]
+
+
+class Call:
+    """One prepared C-ABI call: arguments marshalled once, replayed cheaply.
+
+    The workspace size is queried once at preparation; the call then runs on
+    the torch stream that was current when it was prepared.
+    """
+
+    def __init__(self, fn, args_before_ws, workspace: Optional[Workspace], device):
+        n = ctypes.c_size_t(0)
+        stream = _stream()
+        _check(fn(*args_before_ws, None, ctypes.byref(n), stream))
+        self.ws = (workspace or _ws_for(device)).get(n.value)
+        self.ws_bytes = ctypes.c_size_t(self.ws.numel())
+        self.fn = fn
+        self.args = tuple(args_before_ws) + (_ptr(self.ws), ctypes.byref(self.ws_bytes), stream)
+        self.outputs = None
+
+    def __call__(self):
+        _check(self.fn(*self.args))
+        return self.outputs
+
+
+def prepare_lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scale=None,
+                        residual=None, out=None, workspace: Optional[Workspace] = None) -> Call:
+    """Prepared y = residual + x W^T + scale_t (x A_a^T) B_a^T (bf16 in and out)."""
+    lib = load_library()
+    _req(x, "x", torch.bfloat16, 2)
+    _req(W, "W", torch.bfloat16, 2)
+    T, K = x.shape
+    N = W.shape[0]
+    if W.shape[1] != K:
+        raise ValueError("W must be [N, K=%d], got %s" % (K, tuple(W.shape)))
+    n_ad, r_max = 0, 0
+    if A is not None:
+        _req(A, "A", torch.bfloat16, 3)
+        _req(B, "B", torch.bfloat16, 3)
+        n_ad, r_max = A.shape[0], A.shape[1]
+        if A.shape[2] != K or tuple(B.shape) != (n_ad, N, r_max):
+            raise ValueError("A must be [n_ad, r_max, K] and B [n_ad, N, r_max]")
+        _req(adapter_idx, "adapter_idx", torch.int32, 1)
+        _req(scale, "scale", torch.float32, 1)
+        if adapter_idx.shape[0] != T or scale.shape[0] != T:
+            raise ValueError("adapter_idx and scale must have T=%d entries" % T)
+        if ranks is not None:
+            _req(ranks, "ranks", torch.int32, 1)
+            if ranks.shape[0] != n_ad:
+                raise ValueError("ranks must have n_adapters entries")
+    if residual is not None:
+        _req(residual, "residual", torch.bfloat16, 2)
+        if tuple(residual.shape) != (T, N):
+            raise ValueError("residual must be [T, N]")
+    if out is None:
+        out = torch.empty((T, N), dtype=torch.bfloat16, device=x.device)
+    _req(out, "out", torch.bfloat16, 2)
+    if tuple(out.shape) != (T, N):
+        raise ValueError("out must be [T, N]")
+    args = [_ptr(x), T, K, _ptr(W), N, _ptr(A), _ptr(B), n_ad, r_max, _ptr(ranks),
+            _ptr(adapter_idx), _ptr(scale), _ptr(residual), _ptr(out)]
+    c = Call(lib.local_lora_linear, args, workspace, x.device)
+    c.outputs = out
+    return c
+
+
+def local_lora_linear(*args, **kwargs):
+    """y = residual + x W^T + scale_t (x A_a^T) B_a^T per token (bf16 in and out)."""
+    return prepare_lora_linear(*args, **kwargs)()
+
+
+def _pool_checks(k_cache, v_cache, Hkv, D):
+    _req(k_cache, "k_cache", torch.bfloat16)
+    _req(v_cache, "v_cache", torch.bfloat16)
+    per_block = Hkv * BLOCK_SIZE * D
+    if k_cache.numel() % per_block or k_cache.numel() != v_cache.numel():
+        raise ValueError("k_cache/v_cache must hold num_blocks * Hkv * 16 * D elements")
+    return k_cache.numel() // per_block
+
+
+def _meta_checks(block_table, ctx_lens, block_version, req_version, B):
+    _req(block_table, "block_table", torch.int32, 2)
+    _req(ctx_lens, "ctx_lens", torch.int32, 1)
+    _req(block_version, "block_version", torch.int32, 1)
+    _req(req_version, "req_version", torch.int32, 1)
+    if block_table.shape[0] != B or ctx_lens.shape[0] != B or req_version.shape[0] != B:
+        raise ValueError("block_table, ctx_lens and req_version must have B=%d rows" % B)
+
+
+def prepare_paged_attn_decode(q, k_cache, v_cache, block_table, ctx_lens, block_version,
+                              req_version, sm_scale: float, k_new=None, v_new=None,
+                              Hkv: Optional[int] = None, out=None, lse=None,
+                              workspace: Optional[Workspace] = None) -> Call:
+    """Prepared decode attention; the call returns (out, lse)."""
+    lib = load_library()
+    _req(q, "q", torch.bfloat16, 3)
+    B, Hq, D = q.shape
+    if Hkv is None:
+        if k_new is None:
+            raise ValueError("Hkv is required when k_new is not given")
+        Hkv = k_new.shape[1]
+    num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B)
+    if k_new is not None:
+        _req(k_new, "k_new", torch.bfloat16, 3)
+        _req(v_new, "v_new", torch.bfloat16, 3)
+        if tuple(k_new.shape) != (B, Hkv, D) or tuple(v_new.shape) != (B, Hkv, D):
+            raise ValueError("k_new/v_new must be [B, Hkv, D]")
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    _req(out, "out", torch.bfloat16, 3)
+    _req(lse, "lse", torch.float32, 2)
+    args = [_ptr(q), B, Hq, Hkv, D, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+            num_blocks, BLOCK_SIZE, _ptr(block_table), block_table.shape[1], _ptr(ctx_lens),
+            _ptr(block_version), _ptr(req_version), float(sm_scale), _ptr(out), _ptr(lse)]
+    c = Call(lib.local_paged_attn_decode, args, workspace, q.device)
+    c.outputs = (out, lse)
+    return c
+
+
+def local_paged_attn_decode(*args, **kwargs):
+    """One query token per request over its paged, version-masked KV cache.
+
+    q [B, Hq, D]; pools as documented in include/local.h; returns (out, lse).
+    """
+    return prepare_paged_attn_decode(*args, **kwargs)()
+
+
+def prepare_paged_attn_prefill(q, q_indptr, k_cache, v_cache, block_table, ctx_lens,
+                               block_version, req_version, sm_scale: float, k_new=None,
+                               v_new=None, Hkv: Optional[int] = None, out=None, lse=None,
+                               workspace: Optional[Workspace] = None) -> Call:
+    """Prepared chunked-prefill attention; the call returns (out, lse)."""
+    lib = load_library()
+    _req(q, "q", torch.bfloat16, 3)
+    T, Hq, D = q.shape
+    _req(q_indptr, "q_indptr", torch.int32, 1)
+    B = q_indptr.shape[0] - 1
+    if Hkv is None:
+        if k_new is None:
+            raise ValueError("Hkv is required when k_new is not given")
+        Hkv = k_new.shape[1]
+    num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B)
+    if k_new is not None:
+        _req(k_new, "k_new", torch.bfloat16, 3)
+        _req(v_new, "v_new", torch.bfloat16, 3)
+        if tuple(k_new.shape) != (T, Hkv, D) or tuple(v_new.shape) != (T, Hkv, D):
+            raise ValueError("k_new/v_new must be [T, Hkv, D]")
+    if out is None:
+        out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None:
+        lse = torch.empty((T, Hq), dtype=torch.float32, device=q.device)
+    _req(out, "out", torch.bfloat16, 3)
+    _req(lse, "lse", torch.float32, 2)
+    args = [_ptr(q), _ptr(q_indptr), B, T, Hq, Hkv, D, _ptr(k_new), _ptr(v_new),
+            _ptr(k_cache), _ptr(v_cache), num_blocks, BLOCK_SIZE, _ptr(block_table),
+            block_table.shape[1], _ptr(ctx_lens), _ptr(block_version), _ptr(req_version),
+            float(sm_scale), _ptr(out), _ptr(lse)]
+    c = Call(lib.local_paged_attn_prefill, args, workspace, q.device)
+    c.outputs = (out, lse)
+    return c
+
+
+def local_paged_attn_prefill(*args, **kwargs):
+    """Chunked prefill: append each request's chunk, then causal attention.
+
+    q [T, Hq, D], q_indptr [B+1]; returns (out [T, Hq, D], lse [T, Hq]).
+    """
+    return prepare_paged_attn_prefill(*args, **kwargs)()
+
+
+def prepare_block_version_check(block_table, ctx_lens, block_version, req_version,
+                                cap: Optional[int] = None, stale_pairs=None, n_stale=None,
+                                valid_tokens=None, workspace: Optional[Workspace] = None
+                                ) -> Call:
+    """Prepared version check; the call returns (stale_pairs, n_stale, valid_tokens)."""
+    lib = load_library()
+    _req(block_table, "block_table", torch.int32, 2)
+    B, max_blocks = block_table.shape
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B)
+    dev = block_table.device
+    if cap is None:
+        cap = B * max_blocks
+    if stale_pairs is None:
+        stale_pairs = torch.empty((max(cap, 1), 2), dtype=torch.int32, device=dev)
+    if n_stale is None:
+        n_stale = torch.empty((1,), dtype=torch.int32, device=dev)
+    if valid_tokens is None:
+        valid_tokens = torch.empty((B,), dtype=torch.int32, device=dev)
+    _req(stale_pairs, "stale_pairs", torch.int32, 2)
+    _req(n_stale, "n_stale", torch.int32, 1)
+    _req(valid_tokens, "valid_tokens", torch.int32, 1)
+    if stale_pairs.shape[0] < cap:
+        raise ValueError("stale_pairs must have at least cap rows")
+    args = [_ptr(block_table), B, max_blocks, _ptr(ctx_lens), BLOCK_SIZE,
+            _ptr(block_version), _ptr(req_version), _ptr(stale_pairs), cap, _ptr(n_stale),
+            _ptr(valid_tokens)]
+    c = Call(lib.local_block_version_check, args, workspace, dev)
+    c.outputs = (stale_pairs, n_stale, valid_tokens)
+    return c
+
+
+def local_block_version_check(*args, **kwargs
+                              ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Returns (stale_pairs [cap, 2], n_stale [1], valid_tokens [B]) on the device.
+
+    Only the first min(n_stale, cap) rows of stale_pairs are written.
+    """
+    return prepare_block_version_check(*args, **kwargs)()

@@ -1,0 +1,185 @@
+"""GPU parity of local_paged_attn_decode / local_paged_attn_prefill against the
+oracle, including the in-kernel version mask, the KV append (bit-exact pool
+contents) and the degenerate cases (one key, no valid key, ragged tails)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_15241_amd as lk
+from tests.gpu_helpers import assert_lse, assert_rel, dev, dev_u16, f64, host_u16, say
+from tests.pool_helpers import make_table, rand_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _pool(rng, num, hkv, D):
+    return rand_bf16(rng, (num * hkv * 16 * D,)), rand_bf16(rng, (num * hkv * 16 * D,))
+
+
+def _tags(rng, table, ctx, rv, num, stale_frac, stale_last=True):
+    bv = np.full(num, -7, np.int32)
+    for b, L in enumerate(ctx):
+        nb = (int(L) + 15) // 16
+        tags = np.full(nb, rv[b], np.int32)
+        pick = rng.random(nb) < stale_frac
+        if not stale_last and nb:
+            pick[nb - 1] = False
+        tags[pick] = rv[b] + rng.choice([-1, 1, 5000], size=int(pick.sum()))
+        bv[table[b, :nb]] = tags
+    return bv
+
+
+def _decode_case(rng, ctx, Hq, Hkv, D, stale_frac, append=True, max_blocks=None):
+    ctx = np.asarray(ctx, np.int32)
+    B = len(ctx)
+    table, num = make_table(rng, ctx, extra_blocks=3, max_blocks=max_blocks)
+    rv = (rng.integers(1, 9, size=B) * 1000).astype(np.int32)
+    bv = _tags(rng, table, ctx, rv, num, stale_frac)
+    kc, vc = _pool(rng, num, Hkv, D)
+    q = rand_bf16(rng, (B, Hq, D))
+    kn = rand_bf16(rng, (B, Hkv, D)) if append else None
+    vn = rand_bf16(rng, (B, Hkv, D)) if append else None
+    return dict(ctx=ctx, table=table, rv=rv, bv=bv, kc=kc, vc=vc, q=q, kn=kn, vn=vn,
+                Hq=Hq, Hkv=Hkv, D=D, B=B)
+
+
+def _run_decode(c):
+    kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    out, lse = lk.local_paged_attn_decode(
+        dev_u16(c["q"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]), dev(c["bv"]),
+        dev(c["rv"]), 1.0 / math.sqrt(c["D"]),
+        k_new=None if c["kn"] is None else dev_u16(c["kn"]),
+        v_new=None if c["vn"] is None else dev_u16(c["vn"]), Hkv=c["Hkv"])
+    torch.cuda.synchronize()
+    return out, lse, kc_d, vc_d
+
+
+def _oracle_decode(c):
+    kc, vc = c["kc"].copy(), c["vc"].copy()
+    qi = np.arange(c["B"] + 1, dtype=np.int32)
+    if c["kn"] is not None:
+        oracle.kv_append(kc, vc, c["Hkv"], c["D"], c["table"], qi, c["ctx"], c["kn"], c["vn"])
+    out, lse = oracle.paged_attn(c["q"], qi, c["Hq"], c["Hkv"], c["D"], kc, vc, c["table"],
+                                 c["ctx"], c["bv"], c["rv"], 1.0 / math.sqrt(c["D"]))
+    return out, lse, kc, vc
+
+
+CTX = [1, 15, 16, 17, 31, 100, 511, 512, 513, 1025, 2000, 3333]
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(4, 4, 64), (32, 32, 128), (32, 8, 128), (8, 1, 128),
+                                      (16, 16, 64), (12, 4, 64)])
+def test_decode_matches_oracle(Hq, Hkv, D):
+    say("decode", Hq, Hkv, D)
+    rng = np.random.default_rng(Hq * 31 + Hkv * 7 + D)
+    c = _decode_case(rng, CTX, Hq, Hkv, D, stale_frac=0.2)
+    out, lse, kc_d, vc_d = _run_decode(c)
+    ro, rl, rkc, rvc = _oracle_decode(c)
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+    assert np.array_equal(host_u16(kc_d), rkc), "appended K pool differs"
+    assert np.array_equal(host_u16(vc_d), rvc), "appended V pool differs"
+
+
+def test_decode_without_append_and_long_contexts():
+    rng = np.random.default_rng(3)
+    c = _decode_case(rng, [16384, 9000, 4097, 1], 32, 8, 128, stale_frac=0.1, append=False)
+    out, lse, kc_d, _ = _run_decode(c)
+    ro, rl, rkc, _ = _oracle_decode(c)
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+    assert np.array_equal(host_u16(kc_d), rkc)
+
+
+def test_decode_degenerate_cases():
+    # request 0: every block stale; request 1: one valid key (position 0 of a
+    # fully stale tail); request 2: context 1 (only the appended token).
+    rng = np.random.default_rng(4)
+    Hq = Hkv = 4
+    D = 128
+    ctx = np.array([70, 40, 1], np.int32)
+    table, num = make_table(rng, ctx)
+    rv = np.array([10, 20, 30], np.int32)
+    bv = np.full(num, 0, np.int32)
+    bv[table[1, 0]] = 20                       # tokens 0..15 valid
+    bv[table[2, 0]] = 30
+    kc, vc = _pool(rng, num, Hkv, D)
+    q = rand_bf16(rng, (3, Hq, D))
+    kn, vn = rand_bf16(rng, (3, Hkv, D)), rand_bf16(rng, (3, Hkv, D))
+    c = dict(ctx=ctx, table=table, rv=rv, bv=bv, kc=kc, vc=vc, q=q, kn=kn, vn=vn,
+             Hq=Hq, Hkv=Hkv, D=D, B=3)
+    out, lse, _, _ = _run_decode(c)
+    ro, rl, _, _ = _oracle_decode(c)
+    o = f64(out)
+    assert np.all(o[0] == 0.0) and np.all(np.isneginf(lse[0].cpu().numpy()))
+    assert_rel(o[1:], ro[1:], "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+    # context 1: the output is exactly the appended V row (rounded once)
+    assert np.array_equal(host_u16(out)[2], vn[2].reshape(Hkv, D))
+
+
+def test_decode_wide_block_table_and_batch():
+    rng = np.random.default_rng(8)
+    ctx = rng.integers(1, 700, size=97)
+    c = _decode_case(rng, ctx, 16, 2, 128, stale_frac=0.3, max_blocks=200)
+    out, lse, _, _ = _run_decode(c)
+    ro, rl, _, _ = _oracle_decode(c)
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+
+
+# ------------------------------------------------------------------ prefill
+
+def _prefill_case(rng, prefix, chunk, Hq, Hkv, D, stale_frac):
+    prefix = np.asarray(prefix, np.int32)
+    chunk = np.asarray(chunk, np.int32)
+    ctx = prefix + chunk
+    B = len(ctx)
+    table, num = make_table(rng, ctx, extra_blocks=2)
+    rv = (rng.integers(1, 9, size=B) * 1000).astype(np.int32)
+    bv = _tags(rng, table, ctx, rv, num, stale_frac)
+    kc, vc = _pool(rng, num, Hkv, D)
+    qi = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    T = int(qi[-1])
+    return dict(ctx=ctx, table=table, rv=rv, bv=bv, kc=kc, vc=vc, qi=qi, T=T,
+                q=rand_bf16(rng, (T, Hq, D)), kn=rand_bf16(rng, (T, Hkv, D)),
+                vn=rand_bf16(rng, (T, Hkv, D)), Hq=Hq, Hkv=Hkv, D=D)
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(4, 4, 64), (8, 2, 128), (32, 32, 128)])
+def test_prefill_matches_oracle(Hq, Hkv, D):
+    say("prefill", Hq, Hkv, D)
+    rng = np.random.default_rng(Hq + 100 * Hkv + D)
+    c = _prefill_case(rng, [0, 5, 16, 100, 700, 33], [1, 17, 64, 130, 200, 0], Hq, Hkv, D, 0.2)
+    kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    out, lse = lk.local_paged_attn_prefill(
+        dev_u16(c["q"]), dev(c["qi"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]),
+        dev(c["bv"]), dev(c["rv"]), 1.0 / math.sqrt(D), k_new=dev_u16(c["kn"]),
+        v_new=dev_u16(c["vn"]), Hkv=Hkv)
+    torch.cuda.synchronize()
+    kc, vc = c["kc"].copy(), c["vc"].copy()
+    oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
+    ro, rl = oracle.paged_attn(c["q"], c["qi"], Hq, Hkv, D, kc, vc, c["table"], c["ctx"],
+                               c["bv"], c["rv"], 1.0 / math.sqrt(D))
+    assert np.array_equal(host_u16(kc_d), kc), "appended K pool differs"
+    assert np.array_equal(host_u16(vc_d), vc), "appended V pool differs"
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+
+
+def test_prefill_one_token_chunk_equals_decode():
+    rng = np.random.default_rng(21)
+    Hq, Hkv, D = 8, 2, 128
+    c = _decode_case(rng, [40, 1000, 17], Hq, Hkv, D, stale_frac=0.25)
+    out_d, lse_d, _, _ = _run_decode(c)
+    qi = np.arange(4, dtype=np.int32)
+    out_p, lse_p = lk.local_paged_attn_prefill(
+        dev_u16(c["q"]), dev(qi), dev_u16(c["kc"]), dev_u16(c["vc"]), dev(c["table"]),
+        dev(c["ctx"]), dev(c["bv"]), dev(c["rv"]), 1.0 / math.sqrt(D),
+        k_new=dev_u16(c["kn"]), v_new=dev_u16(c["vn"]), Hkv=Hkv)
+    torch.cuda.synchronize()
+    assert_rel(f64(out_p), f64(out_d), "prefill vs decode", tol=1e-2)
+    assert_lse(lse_p.cpu().numpy(), lse_d.cpu().numpy(), "lse", tol=1e-3)

@@ -1,0 +1,134 @@
+"""GPU parity of local_lora_linear against the oracle, plus exact
+self-consistency (a zero up-projection changes nothing, bit for bit)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_15241_amd as lk
+from tests.gpu_helpers import assert_rel, dev, dev_u16, f64, host_u16, say
+from tests.pool_helpers import rand_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(rng, T, K, N, n_ad, r_max, ranks=None, neg_frac=0.15):
+    x = rand_bf16(rng, (T, K))
+    W = rand_bf16(rng, (N, K), 0.02)
+    if n_ad == 0:
+        return x, W, None, None, None, None, None
+    if ranks is None:
+        ranks = [r_max] * n_ad
+    A = np.zeros((n_ad, r_max, K), np.uint16)
+    B = np.zeros((n_ad, N, r_max), np.uint16)
+    for a, r in enumerate(ranks):
+        A[a, :r] = rand_bf16(rng, (r, K), 1 / math.sqrt(r))
+        B[a, :, :r] = rand_bf16(rng, (N, r), 0.01)
+    idx = rng.integers(0, n_ad, size=T).astype(np.int32)
+    idx[rng.random(T) < neg_frac] = -1
+    scale = np.full(T, 2.0, np.float32)
+    return x, W, A, B, np.array(ranks, np.int32), idx, scale
+
+
+def _run_gpu(x, W, A, B, ranks, idx, scale, residual=None):
+    args = [dev_u16(x), dev_u16(W)]
+    kw = {}
+    if A is not None:
+        kw = dict(A=dev_u16(A), B=dev_u16(B), ranks=dev(ranks), adapter_idx=dev(idx),
+                  scale=dev(scale, torch.float32))
+    if residual is not None:
+        kw["residual"] = dev_u16(residual)
+    y = lk.local_lora_linear(*args, **kw)
+    torch.cuda.synchronize()
+    return y
+
+
+CASES = [
+    # T, K, N, n_ad, r_max, ranks
+    (1, 256, 256, 3, 8, None),
+    (5, 512, 256, 4, 16, None),
+    (32, 1024, 512, 8, 16, None),
+    (33, 256, 320, 3, 8, None),
+    (64, 512, 1024, 16, 64, [8, 16, 32, 64] * 4),
+    (100, 256, 512, 3, 8, None),
+    (128, 512, 512, 32, 16, None),
+    (257, 512, 256, 4, 16, None),
+    (300, 512, 640, 4, 16, [16, 3, 9, 16]),
+    (1000, 256, 512, 4, 16, None),
+    (64, 512, 512, 0, 0, None),
+    (700, 256, 384, 0, 0, None),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "T%d_K%d_N%d_ad%d_r%d" % c[:5])
+def test_matches_oracle(case):
+    T, K, N, n_ad, r_max, ranks = case
+    say("lora_linear", case)
+    rng = np.random.default_rng(T * 7 + K + N + n_ad)
+    x, W, A, B, rk, idx, scale = _inputs(rng, T, K, N, n_ad, r_max, ranks)
+    y = _run_gpu(x, W, A, B, rk, idx, scale)
+    ref = oracle.lora_linear(x, W, A, B, rk, idx, scale)
+    assert_rel(f64(y), ref, "y")
+    # the adapter delta itself (y - base) must also match where adapters apply
+    if n_ad:
+        base = oracle.lora_linear(x, W)
+        rows = idx >= 0
+        if rows.any():
+            y0 = _run_gpu(x, W, None, None, None, None, None)
+            assert_rel(f64(y)[rows] - f64(y0)[rows], (ref - base)[rows], "delta", tol=5e-2)
+
+
+def test_random_scales_and_residual():
+    rng = np.random.default_rng(9)
+    T, K, N = 48, 512, 256
+    x, W, A, B, rk, idx, _ = _inputs(rng, T, K, N, 5, 16)
+    scale = rng.uniform(-3, 3, size=T).astype(np.float32)
+    res = rand_bf16(rng, (T, N), 1.5)
+    y = _run_gpu(x, W, A, B, rk, idx, scale, residual=res)
+    ref = oracle.lora_linear(x, W, A, B, rk, idx, scale, residual=res)
+    assert_rel(f64(y), ref, "y+res")
+    # prefill tiling too
+    T = 400
+    x, W, A, B, rk, idx, _ = _inputs(rng, T, K, N, 5, 16)
+    scale = rng.uniform(-3, 3, size=T).astype(np.float32)
+    res = rand_bf16(rng, (T, N), 1.5)
+    y = _run_gpu(x, W, A, B, rk, idx, scale, residual=res)
+    ref = oracle.lora_linear(x, W, A, B, rk, idx, scale, residual=res)
+    assert_rel(f64(y), ref, "y+res prefill")
+
+
+@pytest.mark.parametrize("T", [32, 300])
+def test_zero_up_projection_is_bitwise_base(T):
+    rng = np.random.default_rng(T)
+    K, N = 1024, 512
+    x, W, A, B, rk, idx, scale = _inputs(rng, T, K, N, 6, 16, neg_frac=0.0)
+    y_zero = _run_gpu(x, W, A, np.zeros_like(B), rk, idx, scale)
+    y_none = _run_gpu(x, W, A, B, rk, np.full(T, -1, np.int32), scale)
+    y_base = _run_gpu(x, W, None, None, None, None, None)
+    assert torch.equal(y_zero.view(torch.int16), y_base.view(torch.int16))
+    assert torch.equal(y_none.view(torch.int16), y_base.view(torch.int16))
+
+
+def test_padding_beyond_rank_is_never_read():
+    # NaN beyond each adapter's rank: any read of it would poison the output.
+    rng = np.random.default_rng(77)
+    T, K, N = 80, 512, 256
+    ranks = [3, 8, 13, 16]
+    x, W, A, B, rk, idx, scale = _inputs(rng, T, K, N, 4, 16, ranks)
+    nan = np.uint16(0x7FC0)
+    for a, r in enumerate(ranks):
+        A[a, r:] = nan
+        B[a, :, r:] = nan
+    y = _run_gpu(x, W, A, B, rk, idx, scale)
+    ref = oracle.lora_linear(x, W, A, B, rk, idx, scale)
+    assert_rel(f64(y), ref, "y")
+
+
+def test_empty_batch_launches_nothing():
+    W = dev_u16(np.zeros((64, 64), np.uint16))
+    x = dev_u16(np.zeros((0, 64), np.uint16))
+    y = lk.local_lora_linear(x, W)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 64)

@@ -1,0 +1,162 @@
+"""Full-size workloads on the GPU against the oracle.
+
+Decode workloads run the whole step (version check, q/k/v projections,
+appending attention, output projection; in the 32-layer workload each layer's
+output is the next layer's input) and compare every stage with the oracle's own
+chain on the same generated inputs, for all requests or a seeded sample of
+them (requests are independent within a step, so a sample is exact). The
+chunked-prefill workload's projections and attention are each checked at full
+size on sampled output rows. Integer outputs are compared bit for bit.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.chain as ochain
+import paper_2608_15241_amd as lk
+import workloads
+from paper_2608_15241_amd.step import Step, meta_to_device
+from tests.gpu_helpers import (assert_lse, assert_rel, dev, f64, gather_requests, host_u16,
+                               say)
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_weights(lw):
+    out = {}
+    for k, v in lw.items():
+        out[k] = host_u16(v) if v.dtype == torch.bfloat16 else v.cpu().numpy()
+    return out
+
+
+def _setup(w, seed=0):
+    say("generate", w.name)
+    meta = workloads.make_meta(w, seed)
+    weights = [workloads.make_layer_weights(w, l, "cuda", seed) for l in range(w.n_layers)]
+    pool = workloads.make_kv_pool(w, meta, "cuda", seed)
+    x = workloads.randn_bf16((meta.T, w.hidden), 1.0, "cuda", seed * 31 + 5)
+    torch.cuda.synchronize()
+    return meta, weights, pool, x
+
+
+def _decode_chain_check(w, reqs, seed=0, layers_to_compare=None):
+    meta, weights, pool, x = _setup(w, seed)
+    D = w.head_dim
+    reqs = np.asarray(reqs)
+    # host copies of the sampled requests' blocks, taken before the GPU step
+    pools = []
+    for l in range(w.n_layers):
+        kh, vh, table, bv = gather_requests(pool[l, 0], pool[l, 1], w.hkv, D,
+                                            meta.block_table, meta.ctx_lens,
+                                            meta.block_version, reqs)
+        pools.append((kh, vh))
+    x_host = host_u16(x)[reqs]
+    say("GPU step", w.name, "layers", w.n_layers)
+    st = Step("decode", x, weights, meta_to_device(meta, "cuda"), pool, w.hq, w.hkv, D,
+              residual=False)
+    st()
+    torch.cuda.synchronize()
+    # version check of the step: bit-exact
+    pairs, n, valid = st.version_check.outputs
+    ep, en, ev = oracle.block_version_check(meta.block_table, meta.ctx_lens,
+                                            meta.block_version, meta.req_version)
+    assert int(n.item()) == en
+    assert np.array_equal(pairs[:en].cpu().numpy(), ep)
+    assert np.array_equal(valid.cpu().numpy(), ev)
+    # oracle chain on the sample
+    say("oracle chain", w.name, "requests", len(reqs))
+    ctx = meta.ctx_lens[reqs]
+    rv = meta.req_version[reqs]
+    tok_a = meta.token_adapter[reqs]
+    tok_s = meta.token_scale[reqs]
+    qi = np.arange(len(reqs) + 1, dtype=np.int32)
+    xo = x_host
+    compare = set(range(w.n_layers)) if layers_to_compare is None else set(layers_to_compare)
+    for l in range(w.n_layers):
+        lw = _host_weights(weights[l])
+        kh, vh = pools[l]
+        xo, stages = ochain.layer(xo, lw, kh, vh, w.hq, w.hkv, D, table, qi, ctx, bv, rv,
+                                  tok_a, tok_s, residual=False)
+        if l in compare:
+            buf = st.buffers[l]
+            for name in ("q", "k", "v", "o", "y"):
+                assert_rel(f64(buf[name])[reqs], stages[name], "layer %d %s" % (l, name))
+            assert_lse(buf["lse"].cpu().numpy()[reqs], stages["lse"], "layer %d lse" % l)
+    assert_rel(f64(st.out)[reqs], oracle.bf16_to_f64(xo), "final output")
+    del st, pool, weights
+    torch.cuda.empty_cache()
+
+
+def test_tiny_decode_step():
+    w = workloads.TINY_DECODE
+    _decode_chain_check(w, np.arange(w.batch))
+
+
+def test_decode_7b_step():
+    w = workloads.DECODE_7B
+    _decode_chain_check(w, np.arange(w.batch))
+
+
+def test_gqa_skew_step():
+    w = workloads.GQA_SKEW
+    _decode_chain_check(w, np.arange(w.batch))
+
+
+def test_churn_32_layer_step_sampled():
+    w = workloads.CHURN_32L
+    rng = np.random.default_rng(2024)
+    reqs = np.sort(rng.choice(w.batch, size=4, replace=False))
+    _decode_chain_check(w, reqs, layers_to_compare=(0, 1, 15, 31))
+
+
+def test_prefill_7b_sampled():
+    w = workloads.PREFILL_7B
+    meta = workloads.make_meta(w, 0)
+    D, T = w.head_dim, meta.T
+    rng = np.random.default_rng(7)
+    rows = np.unique(np.concatenate([meta.q_indptr[:-1], meta.q_indptr[1:] - 1,
+                                     rng.choice(T, size=40, replace=False)]))
+    # --- projections at full size (q and o shapes), sampled rows
+    lw = workloads.make_layer_weights(w, 0, "cuda", 0)
+    x = workloads.randn_bf16((T, w.hidden), 1.0, "cuda", 11)
+    md = meta_to_device(meta, "cuda")
+    for name in ("q", "o"):
+        say("prefill projection", name)
+        y = lk.local_lora_linear(x, lw["W_" + name], lw["A_" + name], lw["B_" + name],
+                                 lw["ranks_" + name], md.token_adapter, md.token_scale)
+        torch.cuda.synchronize()
+        hw = _host_weights(lw)
+        ref = ochain.project(host_u16(x)[rows], hw, name, meta.token_adapter[rows],
+                             meta.token_scale[rows])
+        assert_rel(f64(y)[rows], ref, "proj " + name)
+    # --- appending causal attention at full size, sampled query rows
+    pool = workloads.make_kv_pool(w, meta, "cuda", 0)
+    q = workloads.randn_bf16((T, w.hq, D), 1.0, "cuda", 21)
+    kn = workloads.randn_bf16((T, w.hkv, D), 1.0, "cuda", 22)
+    vn = workloads.randn_bf16((T, w.hkv, D), 1.0, "cuda", 23)
+    kh, vh = host_u16(pool[0, 0]).reshape(-1), host_u16(pool[0, 1]).reshape(-1)
+    say("prefill attention")
+    out, lse = lk.local_paged_attn_prefill(q, md.q_indptr, pool[0, 0], pool[0, 1],
+                                           md.block_table, md.ctx_lens, md.block_version,
+                                           md.req_version, 1 / math.sqrt(D), k_new=kn,
+                                           v_new=vn, Hkv=w.hkv)
+    torch.cuda.synchronize()
+    oracle.kv_append(kh, vh, w.hkv, D, meta.block_table, meta.q_indptr, meta.ctx_lens,
+                     host_u16(kn), host_u16(vn))
+    assert np.array_equal(host_u16(pool[0, 0]).reshape(-1), kh)
+    assert np.array_equal(host_u16(pool[0, 1]).reshape(-1), vh)
+    # row r of request b at position P_b + i attends over positions <= P_b + i:
+    # the one-row problem with context P_b + i + 1 (a decode of that row)
+    b_of = np.searchsorted(meta.q_indptr, rows, side="right") - 1
+    pos = meta.ctx_lens[b_of] - meta.n_new[b_of] + (rows - meta.q_indptr[b_of])
+    ro, rl = oracle.paged_attn(host_u16(q)[rows], np.arange(len(rows) + 1, dtype=np.int32),
+                               w.hq, w.hkv, D, kh, vh, meta.block_table[b_of],
+                               (pos + 1).astype(np.int32), meta.block_version,
+                               meta.req_version[b_of], 1 / math.sqrt(D))
+    assert_rel(f64(out)[rows], ro, "prefill out")
+    assert_lse(lse.cpu().numpy()[rows], rl, "prefill lse")
+    del pool
+    torch.cuda.empty_cache()

@@ -1,0 +1,114 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects bad
+arguments on the host before launching anything. Nothing here needs a GPU:
+only workspace-size queries and argument errors are exercised, and both return
+before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_15241_amd as lk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_WORKSPACE = 0, 1, 2, 3, 4
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails or only sizes
+
+
+def declared_symbols():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            names |= set(re.findall(r"^\s*(?:[\w\*]+\s+)+\**(local_\w+)\s*\(", text, re.M))
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return lk.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_symbols()
+    assert {"local_lora_linear", "local_paged_attn_decode", "local_paged_attn_prefill",
+            "local_block_version_check", "local_last_error", "local_version"} <= names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(lk.EXPORTS) == names
+
+
+def _size(fn, *args):
+    n = ctypes.c_size_t(0)
+    st = fn(*args, None, ctypes.byref(n), None)
+    return st, n.value
+
+
+def test_lora_linear_workspace_and_errors(lib):
+    f = lib.local_lora_linear
+    # sizes only: T=32, K=N=4096, 8 adapters of rank 16
+    st, n = _size(f, FAKE, 32, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
+    assert st == OK
+    assert n >= 32 * 8 * 16 * 2 + 8 * 32 * 4096 * 4
+    st, n0 = _size(f, FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)
+    assert st == OK and n0 < n
+    assert _size(f, FAKE, 32, 100, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 32, 4096, FAKE, 4096, FAKE, FAKE, 8, 12, None, FAKE, FAKE, None, FAKE)[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, -1, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_SHAPE
+    assert b"lora_linear" in lib.local_last_error()
+    # NULL pointers are reported before any launch
+    n = ctypes.c_size_t(1 << 30)
+    st = f(None, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE,
+           FAKE, ctypes.byref(n), None)
+    assert st == ERR_NULL
+    st = f(FAKE, 32, 4096, FAKE, 4096, FAKE, None, 8, 16, None, FAKE, FAKE, None, FAKE,
+           FAKE, ctypes.byref(n), None)
+    assert st == ERR_NULL
+    # too small a workspace
+    n = ctypes.c_size_t(16)
+    st = f(FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE,
+           FAKE, ctypes.byref(n), None)
+    assert st == ERR_WORKSPACE
+    assert f(FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE,
+             FAKE, None, None) == ERR_WORKSPACE
+
+
+def test_decode_workspace_and_errors(lib):
+    f = lib.local_paged_attn_decode
+
+    def call(B=32, Hq=32, Hkv=32, D=128, bs=16, mb=256, kn=FAKE, vn=FAKE, nblocks=5000):
+        return _size(f, FAKE, B, Hq, Hkv, D, kn, vn, FAKE, FAKE, nblocks, bs, FAKE, mb, FAKE,
+                     FAKE, FAKE, 0.088, FAKE, FAKE)
+
+    st, n = call()
+    assert st == OK and n == 32 * 32 * 8 * (128 + 2) * 4    # 8 partitions of 512 tokens
+    assert call(Hq=32, Hkv=6)[0] == ERR_SHAPE
+    assert call(D=96)[0] == ERR_UNSUPPORTED
+    assert call(bs=32)[0] == ERR_UNSUPPORTED
+    assert call(Hq=64, Hkv=2)[0] == ERR_UNSUPPORTED          # group 32 > 16
+    assert call(kn=None)[0] == ERR_NULL                        # k_new without v_new
+
+
+def test_prefill_and_version_check_errors(lib):
+    st, n = _size(lib.local_paged_attn_prefill, FAKE, FAKE, 4, 2048, 32, 32, 128, FAKE, FAKE,
+                  FAKE, FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE)
+    assert st == OK and n == 0
+    st, _ = _size(lib.local_paged_attn_prefill, FAKE, FAKE, 4, 2048, 32, 32, 80, FAKE, FAKE,
+                  FAKE, FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE)
+    assert st == ERR_UNSUPPORTED
+    f = lib.local_block_version_check
+    st, n = _size(f, FAKE, 128, 1024, FAKE, 16, FAKE, FAKE, FAKE, 1000, FAKE, FAKE)
+    assert st == OK and n == 128 * 4
+    assert _size(f, FAKE, 128, 1024, FAKE, 8, FAKE, FAKE, FAKE, 1000, FAKE, FAKE)[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 128, 0, FAKE, 16, FAKE, FAKE, FAKE, 1000, FAKE, FAKE)[0] == ERR_SHAPE
+    nn = ctypes.c_size_t(4096)
+    assert f(FAKE, 128, 1024, FAKE, 16, FAKE, FAKE, None, 10, FAKE, FAKE, FAKE,
+             ctypes.byref(nn), None) == ERR_NULL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros((4, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        lk.local_lora_linear(x, torch.zeros((64, 64), dtype=torch.bfloat16))

@@ -122,3 +122,14 @@ def test_empty_batch():
     y = oracle.lora_linear(np.zeros((0, 64), np.uint16), W, A, B, ranks,
                            np.zeros(0, np.int32), np.zeros(0, np.float32))
     assert y.shape == (0, W.shape[0])
+
+
+def test_residual_is_added_as_given():
+    rng = np.random.default_rng(8)
+    x, W, A, B, ranks = _setup(rng, T=4, K=64, N=16)
+    idx = np.array([0, 1, -1, 2], np.int32)
+    s = np.full(4, 2.0, np.float32)
+    res = rand_bf16(rng, (4, 16), 3.0)
+    y0 = oracle.lora_linear(x, W, A, B, ranks, idx, s)
+    y1 = oracle.lora_linear(x, W, A, B, ranks, idx, s, residual=res)
+    np.testing.assert_allclose(y1 - y0, bits_to_f64(res), rtol=1e-12, atol=1e-12)

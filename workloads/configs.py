@@ -12,6 +12,12 @@ weights N(0,0.02^2), adapter A ~ N(0, 1/r) with r that adapter's rank,
 adapter B ~ N(0, 0.01^2), KV cache N(0,1); every float is drawn in float32
 and rounded to bf16 (nearest even). LoRA scale s = 2.0 for every routed
 token. KV block size 16.
+
+Layers of the multi-layer workload are chained output-to-input (layer l+1
+consumes layer l's output projection). The paper defines no normalisation
+and no residual stream for this path, and without a normalisation a residual
+sum of these distributions grows by orders of magnitude over 32 layers
+(attention collapses onto the newest token), so none is added.
 """
 from __future__ import annotations
 
