@@ -112,18 +112,35 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
-    # warmup
-    for i in range(args.warmup):
+    # warmup (eager: sets kernel attributes on first launch), then one HIP
+    # graph per input set; a step is one graph replay
+    for i in range(max(args.warmup, len(sets))):
         sets[i % len(sets)][0]()
+    torch.cuda.synchronize()
+    graphs = [st.capture() for st, *_ in sets]
+    for i in range(args.warmup):
+        graphs[i % len(graphs)].replay()
     torch.cuda.synchronize()
 
     K = args.steps
-    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
+    for i in range(K):
+        graphs[i % len(graphs)].replay()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / K
+
+    # the dominant kernel (decode attention), timed with HIP events around
+    # each of its launches in K eager steps on the same stream
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
+    e_start.record(stream)
     for i in range(K):
         st = sets[i % len(sets)][0]
         st.version_check()
@@ -135,10 +152,9 @@ def main():
         lc["attn"]()
         ev_b[i].record(stream)
         lc["o"]()
-    t_end.record(stream)
+    e_end.record(stream)
     torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_per_step = total_ms / K
+    eager_ms = e_start.elapsed_time(e_end) / K
     attn_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]))
 
     attn_bytes, step_bytes, valid_tokens = decode_bytes(w, meta)
@@ -170,6 +186,7 @@ def main():
                      "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5)},
         "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
                      "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
+        "step_launch": {"mode": "hip_graph_replay", "eager_ms_per_step": round(eager_ms, 5)},
     }
 
     if not args.no_prefill:
@@ -206,13 +223,26 @@ def bench_prefill(torch, workloads, lk, dev, reps=20):
     for c in calls:
         c()
     torch.cuda.synchronize()
+    graphs = []
+    for sidx in range(2):
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                for c in calls[sidx * per_set:(sidx + 1) * per_set]:
+                    c()
+        torch.cuda.current_stream().wait_stream(s)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
     a.record(stream)
     for r in range(reps):
-        for c in calls[(r % 2) * per_set:(r % 2 + 1) * per_set]:
-            c()
+        graphs[r % 2].replay()
     b.record(stream)
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / reps

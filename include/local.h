@@ -58,13 +58,17 @@
  *
  *  Logical position pi of request b lives in physical block
  *  block_table[b*max_blocks + pi/16], slot pi%16. Request b owns
- *  ceil(ctx_lens[b]/16) logical blocks; table entries beyond them are never
- *  read. Block ids must lie in [0, num_blocks).
+ *  nb_b = min(ceil(ctx_lens[b]/16), max_blocks) logical blocks; table entries
+ *  beyond them are never read. Block ids should lie in [0, num_blocks); an
+ *  id outside that range is never dereferenced and its block is treated as
+ *  stale (so a corrupt table degrades to excluded context, never to a wild
+ *  memory access).
  *
  * Staleness (one rule for every entry point)
  * ------------------------------------------
- *  Logical block j of request b is STALE iff
- *      block_version[block_table[b][j]] != req_version[b].
+ *  Logical block j < nb_b of request b is STALE iff its id p =
+ *  block_table[b][j] lies outside [0, num_blocks) or
+ *      block_version[p] != req_version[b].
  *  Any inequality is stale: an older tag was produced by a superseded version,
  *  a newer one by a staged version that is not yet published (§5.3). Tags are
  *  meant to be unique across adapters (for instance a runtime-wide publish
@@ -114,6 +118,7 @@ int32_t local_version(void);
  *   ranks        [n_adapters] int32 in [1, r_max], or NULL (every rank = r_max).
  *                Rows j >= rank of A and columns j >= rank of B are never used.
  *   adapter_idx  [T] int32 in [-1, n_adapters); -1 = base projection only
+ *                (any value outside [0, n_adapters) is read as -1)
  *   scale        [T] float32, the per-token adapter scale s
  *   residual     [T][N]               bf16, or NULL
  *   y            [T][N]               bf16 output; must not alias the inputs
@@ -146,7 +151,8 @@ local_status_t local_lora_linear(
  *  written at logical position ctx_lens[b]-1 (the decoded token is part of its
  *  own context). Then for every request b and query head h, with
  *  g = h / (Hq/Hkv):
- *    S = { pi < ctx_lens[b] : logical block pi/16 of b is not stale }
+ *    S = { pi < ctx_lens[b], pi < 16*nb_b : logical block pi/16 of b is
+ *          not stale }
  *    s_pi = sm_scale * sum_d q[b,h,d] K(bt[b][pi/16], g, pi%16, d)
  *    out[b,h,:] = sum_{pi in S} softmax(s)_pi V(bt[b][pi/16], g, pi%16, :)
  *    lse[b,h]   = log sum_{pi in S} exp(s_pi)            (natural log)
@@ -156,8 +162,9 @@ local_status_t local_lora_linear(
  *   k_new,v_new  [B][Hkv][D] bf16, or both NULL (nothing appended)
  *   k_cache,v_cache  pool of num_blocks blocks, layout above; written only at
  *                the appended slots
- *   block_table  [B][max_blocks] int32; ceil(ctx_lens[b]/16) <= max_blocks
- *   ctx_lens     [B] int32 in [1, 16*max_blocks]
+ *   block_table  [B][max_blocks] int32
+ *   ctx_lens     [B] int32 in [1, 16*max_blocks] (the append is skipped when
+ *                position ctx_lens[b]-1 has no block or an out-of-range id)
  *   block_version [num_blocks] int32, req_version [B] int32
  *   out          [B][Hq][D] bf16;  lse [B][Hq] float32 or NULL
  *
@@ -184,7 +191,8 @@ local_status_t local_paged_attn_decode(
  * with the per-block version mask (§4.1 chunked prefill; §5.3 stale-coverage
  * prefill runs this same computation under a staged version).
  *
- *  Request b owns query rows [q_indptr[b], q_indptr[b+1]) (n_b rows) and has
+ *  Request b owns query rows [q_indptr[b], q_indptr[b+1]) (n_b rows; a
+ *  request whose range is not inside [0, T] is skipped) and has
  *  ctx_lens[b] = P_b + n_b tokens after the chunk, P_b its cached prefix.
  *  When k_new/v_new are given, row t of the chunk is first written at logical
  *  position P_b + (t - q_indptr[b]). Query row i of request b (position
@@ -216,8 +224,8 @@ local_status_t local_paged_attn_prefill(
  * rejects (§5.1; §1: stale coverage is rejected at lookup, and reusing it
  * would mix hidden states of different adapter versions).
  *
- *  For request b with nb_b = ceil(ctx_lens[b]/16) blocks and j < nb_b,
- *  tok(b,j) = min(16, ctx_lens[b] - 16*j) live tokens:
+ *  For request b with nb_b = min(ceil(ctx_lens[b]/16), max_blocks) blocks
+ *  and j < nb_b, tok(b,j) = min(16, ctx_lens[b] - 16*j) live tokens:
  *    valid_tokens[b] = sum of tok(b,j) over the blocks that are not stale
  *    stale list      = every stale (b, j), ordered by b, then by j
  *  stale_pairs receives the first min(n, cap) entries of the list as int32
@@ -227,19 +235,21 @@ local_status_t local_paged_attn_prefill(
  *
  *   block_table  [B][max_blocks] int32;  ctx_lens [B] int32 in
  *                [0, 16*max_blocks]
- *   block_version [num_blocks] int32 (num_blocks is implied by the ids)
+ *   block_version [num_blocks] int32
  *   req_version  [B] int32
  *   stale_pairs  [cap][2] int32 (may be NULL when cap == 0)
  *   n_stale      one int32 (device)
  *   valid_tokens [B] int32
  *
- *  Sizes: B >= 0, max_blocks >= 1, block_size == 16, cap >= 0.
+ *  Sizes: B >= 0, max_blocks >= 1, num_blocks >= 1, block_size == 16,
+ *  cap >= 0.
  *  The result is exact and deterministic.
  */
 local_status_t local_block_version_check(
     const int32_t* block_table, int32_t B, int32_t max_blocks,
     const int32_t* ctx_lens, int32_t block_size,
-    const int32_t* block_version, const int32_t* req_version,
+    const int32_t* block_version, int64_t num_blocks,
+    const int32_t* req_version,
     int32_t* stale_pairs, int64_t cap,
     int32_t* n_stale,
     int32_t* valid_tokens,

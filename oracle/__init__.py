@@ -45,11 +45,11 @@ def _load():
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_lora_linear.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P]
     lib.oracle_lora_linear.restype = None
-    lib.oracle_block_version_check.argtypes = [P, i32, i32, P, P, P, P, i64, P]
+    lib.oracle_block_version_check.argtypes = [P, i32, i32, P, P, i64, P, P, i64, P]
     lib.oracle_block_version_check.restype = i64
-    lib.oracle_kv_append.argtypes = [P, P, i32, i32, P, i32, i32, P, P, P, P]
+    lib.oracle_kv_append.argtypes = [P, P, i32, i32, P, i32, i64, i32, P, P, P, P]
     lib.oracle_kv_append.restype = None
-    lib.oracle_paged_attn.argtypes = [P, P, i32, i32, i32, i32, P, P, P, i32, P,
+    lib.oracle_paged_attn.argtypes = [P, P, i32, i32, i32, i32, P, P, P, i32, i64, P,
                                       P, P, dbl, P, P]
     lib.oracle_paged_attn.restype = None
     lib.oracle_to_bf16_array.argtypes = [P, i64, P]
@@ -117,8 +117,8 @@ def block_version_check(block_table, ctx_lens, block_version, req_version,
         cap = int(sum((int(L) + 15) // 16 for L in ctx))
     pairs = np.zeros((max(cap, 1), 2), dtype=np.int32)
     valid = np.zeros(Bn, dtype=np.int32)
-    n = lib.oracle_block_version_check(_p(bt), Bn, mb, _p(ctx), _p(bv), _p(rv),
-                                       _p(pairs), cap, _p(valid))
+    n = lib.oracle_block_version_check(_p(bt), Bn, mb, _p(ctx), _p(bv), bv.shape[0],
+                                       _p(rv), _p(pairs), cap, _p(valid))
     return pairs[:min(n, cap)].copy(), int(n), valid
 
 
@@ -133,7 +133,8 @@ def kv_append(k_cache, v_cache, Hkv, D, block_table, q_indptr, ctx_lens,
     ctx = _c(ctx_lens, np.int32)
     kn = _c(k_new, np.uint16)
     vn = _c(v_new, np.uint16)
-    lib.oracle_kv_append(_p(k_cache), _p(v_cache), Hkv, D, _p(bt), bt.shape[1],
+    num_blocks = k_cache.size // (Hkv * 16 * D)
+    lib.oracle_kv_append(_p(k_cache), _p(v_cache), Hkv, D, _p(bt), bt.shape[1], num_blocks,
                          bt.shape[0], _p(qi), _p(ctx), _p(kn), _p(vn))
 
 
@@ -150,8 +151,9 @@ def paged_attn(q, q_indptr, Hq, Hkv, D, k_cache, v_cache, block_table,
     bt = _c(block_table, np.int32)
     out = np.empty((T, Hq, D), dtype=np.float64)
     lse = np.empty((T, Hq), dtype=np.float64)
+    num_blocks = kc.size // (Hkv * 16 * D)
     lib.oracle_paged_attn(_p(q), _p(qi), bt.shape[0], Hq, Hkv, D, _p(kc), _p(vc),
-                          _p(bt), bt.shape[1], _p(_c(ctx_lens, np.int32)),
+                          _p(bt), bt.shape[1], num_blocks, _p(_c(ctx_lens, np.int32)),
                           _p(_c(block_version, np.int32)),
                           _p(_c(req_version, np.int32)), float(sm_scale),
                           _p(out), _p(lse))

@@ -77,6 +77,7 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
 #pragma omp parallel for schedule(dynamic, 1)
   for (int64_t t = 0; t < T; ++t) {
     int a = (n_adapters > 0 && adapter_idx) ? adapter_idx[t] : -1;
+    if (a >= n_adapters) a = -1; /* outside [0, n_adapters): no adapter */
     int rank = 0;
     double u[256];
     if (a >= 0) {
@@ -102,6 +103,20 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
   }
 }
 
+/* Blocks request b owns: ceil(L/16), at most the table's width. */
+static int owned_blocks(int L, int max_blocks) {
+  if (L <= 0) return 0;
+  int nb = (L + ORACLE_BS - 1) / ORACLE_BS;
+  return nb < max_blocks ? nb : max_blocks;
+}
+
+/* A block is stale when its id is outside the pool or its tag differs from
+ * the request's version (the id is then never used to read anything). */
+static int block_stale(int p, int64_t num_blocks, const int32_t* block_version,
+                       int32_t rv) {
+  return p < 0 || p >= num_blocks || block_version[p] != rv;
+}
+
 /*
  * Version check (§5.1: KV is reusable only when its validity key — which
  * includes the adapter and the adapter version — matches the request; §1:
@@ -112,20 +127,20 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
  */
 int64_t oracle_block_version_check(const int32_t* block_table, int32_t Bn,
                                    int32_t max_blocks, const int32_t* ctx_lens,
-                                   const int32_t* block_version,
+                                   const int32_t* block_version, int64_t num_blocks,
                                    const int32_t* req_version,
                                    int32_t* stale_pairs, int64_t cap,
                                    int32_t* valid_tokens) {
   int64_t n = 0;
   for (int b = 0; b < Bn; ++b) {
     int L = ctx_lens[b];
-    int nb = (L + ORACLE_BS - 1) / ORACLE_BS;
+    int nb = owned_blocks(L, max_blocks);
     int valid = 0;
     for (int j = 0; j < nb; ++j) {
       int p = block_table[(int64_t)b * max_blocks + j];
       int live = L - j * ORACLE_BS;
       if (live > ORACLE_BS) live = ORACLE_BS;
-      if (block_version[p] != req_version[b]) {
+      if (block_stale(p, num_blocks, block_version, req_version[b])) {
         if (n < cap) {
           stale_pairs[2 * n] = b;
           stale_pairs[2 * n + 1] = j;
@@ -148,15 +163,18 @@ int64_t oracle_block_version_check(const int32_t* block_table, int32_t Bn,
  */
 void oracle_kv_append(uint16_t* k_cache, uint16_t* v_cache, int32_t Hkv,
                       int32_t D, const int32_t* block_table,
-                      int32_t max_blocks, int32_t Bn, const int32_t* q_indptr,
-                      const int32_t* ctx_lens, const uint16_t* k_new,
-                      const uint16_t* v_new) {
+                      int32_t max_blocks, int64_t num_blocks, int32_t Bn,
+                      const int32_t* q_indptr, const int32_t* ctx_lens,
+                      const uint16_t* k_new, const uint16_t* v_new) {
   for (int b = 0; b < Bn; ++b) {
     int nb_new = q_indptr[b + 1] - q_indptr[b];
     int start = ctx_lens[b] - nb_new;
     for (int i = 0; i < nb_new; ++i) {
       int pos = start + i;
+      /* a position without a block, or an id outside the pool: no write */
+      if (pos < 0 || pos / ORACLE_BS >= max_blocks) continue;
       int p = block_table[(int64_t)b * max_blocks + pos / ORACLE_BS];
+      if (p < 0 || p >= num_blocks) continue;
       int s = pos % ORACLE_BS;
       int64_t row = q_indptr[b] + i;
       for (int g = 0; g < Hkv; ++g)
@@ -172,7 +190,8 @@ void oracle_kv_append(uint16_t* k_cache, uint16_t* v_cache, int32_t Hkv,
  * Paged attention with the per-block version mask (§2.2 "KV cache and prefix
  * caching"; §5.1 validity key). Query row i of request b sits at position
  * P = ctx_lens[b] - n_b + i and attends over
- *   S = { pi <= P : logical block pi/16 of b is not stale }
+ *   S = { pi <= P, pi/16 < nb_b : logical block pi/16 of b is not stale }
+ * with nb_b = min(ceil(ctx_lens[b]/16), max_blocks)
  * with s_pi = sm_scale * <q, K_pi>, out = sum softmax(s)_pi V_pi and
  * lse = log sum exp(s_pi) (natural log). Empty S gives out = 0, lse = -inf.
  * Query head h reads KV head h / (Hq/Hkv). Decode is the case n_b = 1.
@@ -182,7 +201,8 @@ void oracle_paged_attn(const uint16_t* q, const int32_t* q_indptr, int32_t Bn,
                        int32_t Hq, int32_t Hkv, int32_t D,
                        const uint16_t* k_cache, const uint16_t* v_cache,
                        const int32_t* block_table, int32_t max_blocks,
-                       const int32_t* ctx_lens, const int32_t* block_version,
+                       int64_t num_blocks, const int32_t* ctx_lens,
+                       const int32_t* block_version,
                        const int32_t* req_version, double sm_scale,
                        double* out, double* lse) {
   int64_t T = q_indptr[Bn];
@@ -194,6 +214,8 @@ void oracle_paged_attn(const uint16_t* q, const int32_t* q_indptr, int32_t Bn,
       while (q_indptr[b + 1] <= t) ++b;
       int n_b = q_indptr[b + 1] - q_indptr[b];
       int P = ctx_lens[b] - n_b + (int)(t - q_indptr[b]);
+      int nb = owned_blocks(ctx_lens[b], max_blocks);
+      if (P > nb * ORACLE_BS - 1) P = nb * ORACLE_BS - 1;
       int g = h / group;
       const uint16_t* qv = q + (t * Hq + h) * D;
       double* o = out + (t * Hq + h) * D;
@@ -202,7 +224,7 @@ void oracle_paged_attn(const uint16_t* q, const int32_t* q_indptr, int32_t Bn,
       int64_t count = 0;
       for (int pi = 0; pi <= P; ++pi) {
         int p = block_table[(int64_t)b * max_blocks + pi / ORACLE_BS];
-        if (block_version[p] != req_version[b]) continue;
+        if (block_stale(p, num_blocks, block_version, req_version[b])) continue;
         double s = 0.0;
         for (int d = 0; d < D; ++d)
           s += bf(qv[d]) * bf(k_cache[k_off(p, g, pi % ORACLE_BS, d, Hkv, D)]);
@@ -219,7 +241,7 @@ void oracle_paged_attn(const uint16_t* q, const int32_t* q_indptr, int32_t Bn,
       double denom = 0.0;
       for (int pi = 0; pi <= P; ++pi) {
         int p = block_table[(int64_t)b * max_blocks + pi / ORACLE_BS];
-        if (block_version[p] != req_version[b]) continue;
+        if (block_stale(p, num_blocks, block_version, req_version[b])) continue;
         double s = 0.0;
         for (int d = 0; d < D; ++d)
           s += bf(qv[d]) * bf(k_cache[k_off(p, g, pi % ORACLE_BS, d, Hkv, D)]);

@@ -63,8 +63,8 @@ def load_library(path: str = LIB_PATH):
     lib.local_paged_attn_prefill.argtypes = [P, P, i32, i64, i32, i32, i32, P, P, P, P, i64,
                                              i32, P, i32, P, P, P, f32, P, P, P, SZ, P]
     lib.local_block_version_check.restype = ctypes.c_int
-    lib.local_block_version_check.argtypes = [P, i32, i32, P, i32, P, P, P, i64, P, P, P,
-                                              SZ, P]
+    lib.local_block_version_check.argtypes = [P, i32, i32, P, i32, P, i64, P, P, i64, P, P,
+                                              P, SZ, P]
     _lib = lib
     return lib
 
@@ -123,22 +123,26 @@ def _ws_for(device) -> Workspace:
 class Call:
     """One prepared C-ABI call: arguments marshalled once, replayed cheaply.
 
-    The workspace size is queried once at preparation; the call then runs on
-    the torch stream that was current when it was prepared.
+    The workspace size is queried once at preparation. Each call enqueues on
+    the torch stream current at call time, so a sequence of prepared calls
+    can be captured into a HIP graph (torch.cuda.graph) and replayed.
     """
 
-    def __init__(self, fn, args_before_ws, workspace: Optional[Workspace], device):
+    def __init__(self, fn, args_before_ws, workspace: Optional[Workspace], device,
+                 keep=()):
+        # The call holds raw device pointers: keep every tensor it points to
+        # alive for as long as the call can run (including graph replays).
+        self.keep = tuple(t for t in keep if t is not None)
         n = ctypes.c_size_t(0)
-        stream = _stream()
-        _check(fn(*args_before_ws, None, ctypes.byref(n), stream))
+        _check(fn(*args_before_ws, None, ctypes.byref(n), _stream()))
         self.ws = (workspace or _ws_for(device)).get(n.value)
         self.ws_bytes = ctypes.c_size_t(self.ws.numel())
         self.fn = fn
-        self.args = tuple(args_before_ws) + (_ptr(self.ws), ctypes.byref(self.ws_bytes), stream)
+        self.args = tuple(args_before_ws) + (_ptr(self.ws), ctypes.byref(self.ws_bytes))
         self.outputs = None
 
     def __call__(self):
-        _check(self.fn(*self.args))
+        _check(self.fn(*self.args, _stream()))
         return self.outputs
 
 
@@ -178,7 +182,8 @@ def prepare_lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scal
         raise ValueError("out must be [T, N]")
     args = [_ptr(x), T, K, _ptr(W), N, _ptr(A), _ptr(B), n_ad, r_max, _ptr(ranks),
             _ptr(adapter_idx), _ptr(scale), _ptr(residual), _ptr(out)]
-    c = Call(lib.local_lora_linear, args, workspace, x.device)
+    c = Call(lib.local_lora_linear, args, workspace, x.device,
+             keep=(x, W, A, B, ranks, adapter_idx, scale, residual, out))
     c.outputs = out
     return c
 
@@ -234,7 +239,9 @@ def prepare_paged_attn_decode(q, k_cache, v_cache, block_table, ctx_lens, block_
     args = [_ptr(q), B, Hq, Hkv, D, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
             num_blocks, BLOCK_SIZE, _ptr(block_table), block_table.shape[1], _ptr(ctx_lens),
             _ptr(block_version), _ptr(req_version), float(sm_scale), _ptr(out), _ptr(lse)]
-    c = Call(lib.local_paged_attn_decode, args, workspace, q.device)
+    c = Call(lib.local_paged_attn_decode, args, workspace, q.device,
+             keep=(q, k_new, v_new, k_cache, v_cache, block_table, ctx_lens, block_version,
+                   req_version, out, lse))
     c.outputs = (out, lse)
     return c
 
@@ -278,7 +285,9 @@ def prepare_paged_attn_prefill(q, q_indptr, k_cache, v_cache, block_table, ctx_l
             _ptr(k_cache), _ptr(v_cache), num_blocks, BLOCK_SIZE, _ptr(block_table),
             block_table.shape[1], _ptr(ctx_lens), _ptr(block_version), _ptr(req_version),
             float(sm_scale), _ptr(out), _ptr(lse)]
-    c = Call(lib.local_paged_attn_prefill, args, workspace, q.device)
+    c = Call(lib.local_paged_attn_prefill, args, workspace, q.device,
+             keep=(q, q_indptr, k_new, v_new, k_cache, v_cache, block_table, ctx_lens,
+                   block_version, req_version, out, lse))
     c.outputs = (out, lse)
     return c
 
@@ -315,9 +324,11 @@ def prepare_block_version_check(block_table, ctx_lens, block_version, req_versio
     if stale_pairs.shape[0] < cap:
         raise ValueError("stale_pairs must have at least cap rows")
     args = [_ptr(block_table), B, max_blocks, _ptr(ctx_lens), BLOCK_SIZE,
-            _ptr(block_version), _ptr(req_version), _ptr(stale_pairs), cap, _ptr(n_stale),
-            _ptr(valid_tokens)]
-    c = Call(lib.local_block_version_check, args, workspace, dev)
+            _ptr(block_version), block_version.numel(), _ptr(req_version), _ptr(stale_pairs),
+            cap, _ptr(n_stale), _ptr(valid_tokens)]
+    c = Call(lib.local_block_version_check, args, workspace, dev,
+             keep=(block_table, ctx_lens, block_version, req_version, stale_pairs, n_stale,
+                   valid_tokens))
     c.outputs = (stale_pairs, n_stale, valid_tokens)
     return c
 

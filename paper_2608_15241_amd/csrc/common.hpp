@@ -48,8 +48,20 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b,
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// v_mfma_f32_16x16x16_bf16: D[16x16] += A[16x16] * B[16x16], four k values
+// per lane (k-group l/16), same row/column/accumulator layout as above.
+__device__ __forceinline__ f32x4 mfma16x16x16(const bf16x4& a, const bf16x4& b, f32x4 c) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
+                                                   __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
   return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ bf16x4 as_bf16x4(u32x2 v) {
+  return __builtin_bit_cast(bf16x4, v);
 }
 
 // ---------------------------------------------------------------- loads
@@ -61,6 +73,24 @@ __device__ __forceinline__ T ld_global(const void* p) {
 template <typename T>
 __device__ __forceinline__ T ld_stream(const void* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
+}
+
+// Buffer loads: a descriptor covers [base, base + bytes); a load outside it
+// returns zeros and issues no memory request, so a zero-size descriptor is a
+// free "absent" load that keeps the instruction stream branch-free.
+constexpr int32_t kBufferConfig = 0x00020000;  // CDNA raw-buffer descriptor word 3
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), kBufferConfig);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(byte_off), 0, 0);
+}
+
+__device__ __forceinline__ u32x2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(byte_off), 0, 0);
 }
 
 // ---------------------------------------------------------------- math

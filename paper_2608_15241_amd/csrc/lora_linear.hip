@@ -1,36 +1,45 @@
-// local_lora_linear: y = x W^T + s_t (x A_a^T) B_a^T with a per-token adapter
-// a = adapter_idx[t] (§2.2 "LoRA adapters": one frozen base shared by many
-// low-rank adapters, every request routed to its own adapter).
+// local_lora_linear: y = res + x W^T + s_t (x A_a^T) B_a^T with a per-token
+// adapter a = adapter_idx[t] (§2.2 "LoRA adapters": one frozen base shared by
+// many low-rank adapters, every request routed to its own adapter).
 //
 // Design, SGMV-style but on the matrix cores end to end:
 //  * Shrink. U_s[t, a*r_max + j] = bf16(s_t * x_t . A[a,j,:]) for the token's
-//    own adapter a and j < rank(a), 0 elsewhere. It is one GEMM of x against
-//    all adapters' stacked A (rows a*r_max + j), whose epilogue keeps only the
-//    token's own adapter and rank. Its cost is a few percent of the main
-//    product; the gather of adapters per token is replaced by masking.
+//    own adapter a and j < rank(a), 0 elsewhere. It is one product of x with
+//    all adapters' stacked A (rows a*r_max + j) whose epilogue keeps only the
+//    token's own adapter and rank: the per-token gather of adapters becomes a
+//    mask, at a cost of a few percent of the base product.
 //  * Fused base + expand. The delta is U_s Btilde^T with
 //    Btilde[n, a*r_max + j] = B[a, n, j], i.e. extra K-steps of the base
-//    product over the columns of U_s. A K-step of 64 such columns is run only
-//    if an adapter it covers is used by some token of the tile, and only the
-//    columns below each adapter's rank are loaded; everything else is a zero
-//    fill that costs no memory traffic.
-//  * Tiles are computed transposed, Y^T = W X^T: features are MFMA rows
-//    (A operand, W rows), tokens are columns (B operand, x rows), so each
-//    lane ends with 4 consecutive features of one token and stores 8 bytes.
-//  * One kernel, two tilings. Prefill (many tokens): 128x128 tiles, 2x2
-//    waves, LDS double buffer, XCD-aware grouped tile order so each XCD's L2
-//    serves an 8x8 block of tiles. Decode (few tokens, HBM-bound on W):
-//    one token tile of <=128 rows, 64 features per workgroup, split-K to put
-//    >= 256 workgroups in flight, then a reduction kernel.
+//    product over the columns of U_s. A step over U_s columns runs only if an
+//    adapter it covers is used by a token of the tile, and only columns below
+//    each adapter's rank are loaded; the rest is a zero fill with no traffic.
+//  * Every tile is computed transposed, Y^T = W X^T: features are MFMA rows
+//    (A operand, rows of W), tokens are columns (B operand, rows of x), so a
+//    lane ends with 4 consecutive features of one token (an 8-byte store).
+//  * Two kernels for two regimes:
+//    - skinny (few tokens, or few features): decode projections are bound by
+//      streaming W once. A workgroup owns 16 features x up to 128 tokens and
+//      its 8 waves split K; each lane loads its MFMA operand slices straight
+//      from global memory several K-steps ahead (no LDS staging, no barrier
+//      in the main loop), and the 8 partial tiles are summed once through LDS
+//      in a fixed order. Also used for every shrink.
+//    - tiled (many tokens and features): prefill projections are bound by the
+//      matrix cores. 128x128 tiles, 2x2 waves, register prefetch into an LDS
+//      double buffer with padded rows, XCD-aware grouped tile order so each
+//      XCD's L2 serves an 8x8 block of tiles.
+//  Both sum the base K-steps in an order that does not depend on which
+//  adapters are present, so a zero up-projection leaves y bit-identical.
 #include "common.hpp"
 
 namespace localk {
 namespace {
 
-constexpr int kGemmThreads = 256;
+constexpr int kGemmThreads = 256;       // tiled kernel
+constexpr int kSkThreads = 512;         // skinny kernel (8 waves)
+constexpr int kSkWaves = kSkThreads / kWave;
 constexpr int kBK = 64;
 constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
-constexpr int kMaxLoraSteps = 512;      // R <= 256 * 128 columns / 64
+constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kNumXcd = 8;
 
 enum GemmMode { kModeMain = 0, kModeShrink = 1 };
@@ -45,37 +54,239 @@ struct GemmArgs {
   const int32_t* idx;    // [T] or null
   const float* scale;    // [T]
   int n_ad, r_max, R;
-  const uint16_t* res;  // optional residual [T][N] added before rounding (main mode)
-  uint16_t* y;           // bf16 output [T][N]   (split == 1)
-  float* part;           // fp32 partials [split][T][N] (split > 1)
-  int mode, split;
-  int gm, gn;            // tile grid
-  int swizzle;           // XCD-aware grouped order
+  const uint16_t* res;   // optional residual [T][N] (main mode)
+  uint16_t* y;           // bf16 output [T][N] (U_s in shrink mode)
+  int mode;
+  int gm, gn;            // tile grid of the tiled kernel
+  int swizzle;           // XCD-aware grouped order (tiled kernel)
 };
 
 __device__ __forceinline__ int rank_of(const GemmArgs& a, int ad) {
   return a.ranks ? a.ranks[ad] : a.r_max;
 }
 
+__device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad) {
+  return (present[ad >> 6] >> (ad & 63)) & 1ull;
+}
+
+// Store features n..n+3 of token t (bounds-checked): the shrink mask and
+// scale, or the residual, then one rounding to bf16.
+__device__ __forceinline__ void store4(const GemmArgs& a, int64_t t, int64_t n, f32x4 v) {
+  if (t >= a.T || n >= a.N) return;
+  float o[4] = {v[0], v[1], v[2], v[3]};
+  if (a.mode == kModeShrink) {
+    int ad = a.idx ? a.idx[t] : -1;
+    if (ad >= a.n_ad) ad = -1;  // indices outside [0, n_ad) mean no adapter
+    const float sc = ad >= 0 ? a.scale[t] : 0.f;
+    const int rk = ad >= 0 ? rank_of(a, ad) : 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = static_cast<int>(n) + e;
+      o[e] = (ad >= 0 && r / a.r_max == ad && r % a.r_max < rk) ? sc * o[e] : 0.f;
+    }
+  } else if (a.res) {
+    const u32x2 r = ld_global<u32x2>(a.res + t * a.N + n);
+    o[0] += __uint_as_float(r.x << 16);
+    o[1] += __uint_as_float(r.x & 0xffff0000u);
+    o[2] += __uint_as_float(r.y << 16);
+    o[3] += __uint_as_float(r.y & 0xffff0000u);
+  }
+  *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
+      u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+}
+
+// Marks the adapters used by tokens [t0, t0 + n_tok) and lists, in ascending
+// order, the chunks of `chunk` U_s columns that cover at least one of them.
+// Returns the number of chunks. All threads of the workgroup must call it.
+template <int THREADS>
+__device__ int lora_chunk_list(const GemmArgs& a, int64_t t0, int n_tok, int chunk,
+                               uint64_t* present, uint16_t* list, int* wave_cnt) {
+  constexpr int WAVES = THREADS / kWave;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  if (tid < 4) present[tid] = 0ull;
+  __syncthreads();
+  for (int t = tid; t < n_tok; t += THREADS) {
+    if (t0 + t < a.T) {
+      const int ad = a.idx[t0 + t];
+      if (ad >= 0 && ad < a.n_ad)
+        atomicOr(reinterpret_cast<unsigned long long*>(&present[ad >> 6]), 1ull << (ad & 63));
+    }
+  }
+  __syncthreads();
+  const int chunks = (a.R + chunk - 1) / chunk;
+  int n = 0;
+  for (int base = 0; base < chunks; base += THREADS) {
+    const int l = base + tid;
+    bool use = false;
+    if (l < chunks) {
+      const int a_lo = (l * chunk) / a.r_max;
+      const int a_hi = min((l * chunk + chunk - 1) / a.r_max, a.n_ad - 1);
+      for (int ad = a_lo; ad <= a_hi; ++ad) use |= adapter_present(present, ad);
+    }
+    const uint64_t m = __ballot(use);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[wave] = __popcll(m);
+    __syncthreads();
+    int off = n, tot = 0;
+    for (int w2 = 0; w2 < WAVES; ++w2) {
+      if (w2 < wave) off += wave_cnt[w2];
+      tot += wave_cnt[w2];
+    }
+    if (use) list[off + before] = static_cast<uint16_t>(l);
+    n += tot;
+    __syncthreads();
+  }
+  return n;
+}
+
+// 16-byte slice of Btilde row n at U_s column c (c % 8 == 0): zero when the
+// adapter is absent from the tile or the columns lie at or past its rank.
+__device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* present,
+                                             int64_t n, int c) {
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (c >= a.R || n >= a.N) return v;
+  const int ad = c / a.r_max, j = c % a.r_max;
+  const int rk = rank_of(a, ad);
+  if (j >= rk || !adapter_present(present, ad)) return v;
+  v = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(ad) * a.N + n) * a.r_max + j);
+  if (rk - j < 8) {  // clear columns at or past the rank
+    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (j + e >= rk) wv[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+    v = u32x4{wv[0], wv[1], wv[2], wv[3]};
+  }
+  return v;
+}
+
+// ------------------------------------------------------------------ skinny
+// Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM); wave w takes
+// a contiguous range of the K/32 base steps (U steps per batch of loads) and
+// every 8th U_s chunk; partial tiles are summed through LDS in wave order.
+template <int FN, int FM, int U>
+__global__ __launch_bounds__(kSkThreads) void lora_skinny_kernel(GemmArgs a) {
+  __shared__ uint64_t present[4];
+  __shared__ uint16_t chunks[kMaxLoraChunks];
+  __shared__ int wave_cnt[kSkWaves];
+  extern __shared__ f32x4 red[];  // [waves][FM][FN][64 lanes]
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int col = lane % 16, kgrp = lane / 16;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16 * FN;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.y) * 16 * FM;
+
+  int n_chunks = 0;
+  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr)
+    n_chunks = lora_chunk_list<kSkThreads>(a, t0, 16 * FM, 32, present, chunks, wave_cnt);
+
+  f32x4 acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // this lane's rows: feature rows of W, token rows of x
+  const uint16_t* wrow[FN];
+  bool wok[FN];
+#pragma unroll
+  for (int i = 0; i < FN; ++i) {
+    const int64_t n = n0 + 16 * i + col;
+    wok[i] = n < a.N;
+    wrow[i] = a.w + (wok[i] ? n : 0) * a.K + 8 * kgrp;
+  }
+  const uint16_t* xrow[FM];
+  bool xok[FM];
+#pragma unroll
+  for (int j = 0; j < FM; ++j) {
+    const int64_t t = t0 + 16 * j + col;
+    xok[j] = t < a.T;
+    xrow[j] = a.x + (xok[j] ? t : 0) * a.K + 8 * kgrp;
+  }
+
+  // Loads are unconditional (rows are clamped to a valid one above, steps
+  // past the wave's range to its last step) and invalid values are zeroed
+  // with selects, so the loop has no branch around a load and each batch of
+  // MFMAs waits only for its own loads.
+  const int ksteps = static_cast<int>(a.K / 32);
+  const int s_lo = (wave * ksteps) / kSkWaves;
+  const int s_hi = ((wave + 1) * ksteps) / kSkWaves;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  for (int s = s_lo; s < s_hi; s += U) {
+    u32x4 wv[U][FN], xv[U][FM];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 32;
+#pragma unroll
+      for (int i = 0; i < FN; ++i) wv[u][i] = ld_global<u32x4>(wrow[i] + k);
+#pragma unroll
+      for (int j = 0; j < FM; ++j) xv[u][j] = ld_global<u32x4>(xrow[j] + k);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool live = s + u < s_hi;
+#pragma unroll
+      for (int i = 0; i < FN; ++i) wv[u][i] = (live && wok[i]) ? wv[u][i] : zero4;
+#pragma unroll
+      for (int j = 0; j < FM; ++j) xv[u][j] = (live && xok[j]) ? xv[u][j] : zero4;
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j)
+          acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i]), as_bf16x8(xv[u][j]), acc[i][j]);
+    }
+  }
+  // adapter up-projection: chunks of 32 U_s columns, round-robin over waves
+  for (int q = wave; q < n_chunks; q += kSkWaves) {
+    const int c = chunks[q] * 32 + 8 * kgrp;
+    bf16x8 bv[FN], uv[FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i) bv[i] = as_bf16x8(load_btilde(a, present, n0 + 16 * i + col, c));
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const int64_t t = t0 + 16 * j + col;
+      uv[j] = as_bf16x8((t < a.T && c < a.R) ? ld_global<u32x4>(a.us + t * a.R + c)
+                                              : u32x4{0u, 0u, 0u, 0u});
+    }
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(bv[i], uv[j], acc[i][j]);
+  }
+
+  // ---- sum the waves' partial tiles in wave order, then store
+#pragma unroll
+  for (int j = 0; j < FM; ++j)
+#pragma unroll
+    for (int i = 0; i < FN; ++i) red[((wave * FM + j) * FN + i) * kWave + lane] = acc[i][j];
+  __syncthreads();
+  for (int e = tid; e < FM * FN * kWave; e += kSkThreads) {
+    const int l = e % kWave, i = (e / kWave) % FN, j = e / (kWave * FN);
+    f32x4 s = red[e];
+    for (int w = 1; w < kSkWaves; ++w) s += red[w * FM * FN * kWave + e];
+    store4(a, t0 + 16 * j + l % 16, n0 + 16 * i + 4 * (l / 16), s);
+  }
+}
+
+// ------------------------------------------------------------------ tiled
 template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(kGemmThreads) void lora_gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kGemmThreads) void lora_tiled_kernel(GemmArgs a) {
   constexpr int FN = BN / WN / 16;  // 16-row MFMA tiles per wave along features
   constexpr int FM = BM / WM / 16;  // 16-col MFMA tiles per wave along tokens
   constexpr int W_PIECES = BN * (kBK / 8) / kGemmThreads;
-  constexpr int X_PIECES = (BM * (kBK / 8) + kGemmThreads - 1) / kGemmThreads;
-  static_assert(W_PIECES >= 1 && WM * WN == 4, "tile shape");
+  constexpr int X_PIECES = BM * (kBK / 8) / kGemmThreads;
+  static_assert(W_PIECES >= 1 && X_PIECES >= 1 && WM * WN == 4, "tile shape");
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   // LDS: W tiles [2][BN][kLdsK], then x tiles [2][BM][kLdsK]
   auto w_lds = [&](int buf) { return smem + buf * (BN * kLdsK); };
   auto x_lds = [&](int buf) { return smem + 2 * BN * kLdsK + buf * (BM * kLdsK); };
   __shared__ uint64_t present[4];
-  __shared__ uint16_t lora_steps[kMaxLoraSteps];
+  __shared__ uint16_t chunks[kMaxLoraChunks];
   __shared__ int wave_cnt[4];
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
 
-  // ---- tile coordinates
+  // ---- tile coordinates (XCD-aware grouped order)
   int mt, nt;
   {
     const int id = blockIdx.x;
@@ -97,55 +308,12 @@ __global__ __launch_bounds__(kGemmThreads) void lora_gemm_kernel(GemmArgs a) {
   }
   const int64_t m0 = static_cast<int64_t>(mt) * BM;
   const int64_t n0 = static_cast<int64_t>(nt) * BN;
-  const int z = blockIdx.y;
 
-  // ---- adapters used by this token tile, and the LoRA K-steps to run
-  int n_lora = 0;
-  const bool lora = a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr;
-  if (lora) {
-    if (tid < 4) present[tid] = 0ull;
-    __syncthreads();
-    for (int t = tid; t < BM; t += kGemmThreads) {
-      if (m0 + t < a.T) {
-        const int ad = a.idx[m0 + t];
-        if (ad >= 0) atomicOr(reinterpret_cast<unsigned long long*>(&present[ad >> 6]),
-                              1ull << (ad & 63));
-      }
-    }
-    __syncthreads();
-    const int steps = (a.R + kBK - 1) / kBK;
-    for (int base = 0; base < steps; base += kGemmThreads) {
-      const int l = base + tid;
-      bool use = false;
-      if (l < steps) {
-        const int a_lo = (l * kBK) / a.r_max;
-        const int a_hi = min((l * kBK + kBK - 1) / a.r_max, a.n_ad - 1);
-        for (int ad = a_lo; ad <= a_hi; ++ad)
-          if ((present[ad >> 6] >> (ad & 63)) & 1ull) use = true;
-      }
-      const uint64_t m = __ballot(use);
-      const int before = __popcll(m & ((1ull << lane) - 1ull));
-      if (lane == 0) wave_cnt[wave] = __popcll(m);
-      __syncthreads();
-      int off = n_lora;
-      int tot = 0;
-      for (int w2 = 0; w2 < 4; ++w2) {
-        if (w2 < wave) off += wave_cnt[w2];
-        tot += wave_cnt[w2];
-      }
-      if (use) lora_steps[off + before] = static_cast<uint16_t>(l);
-      n_lora += tot;
-      __syncthreads();
-    }
-  }
-  // The base K-steps are split evenly; the LoRA steps go to the last split, so
-  // the base product is summed in the same order whether or not any adapter
-  // is present.
+  int n_chunks = 0;
+  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr)
+    n_chunks = lora_chunk_list<kGemmThreads>(a, m0, BM, kBK, present, chunks, wave_cnt);
   const int k_main = static_cast<int>(a.K / kBK);
-  const int s_begin = static_cast<int>((static_cast<int64_t>(z) * k_main) / a.split);
-  const int s_end = z == a.split - 1
-                        ? k_main + n_lora
-                        : static_cast<int>((static_cast<int64_t>(z + 1) * k_main) / a.split);
+  const int s_end = k_main + n_chunks;
 
   // ---- global -> register loaders for one K-step
   u32x4 wreg[W_PIECES], xreg[X_PIECES];
@@ -164,44 +332,22 @@ __global__ __launch_bounds__(kGemmThreads) void lora_gemm_kernel(GemmArgs a) {
         const int piece = tid + i * kGemmThreads;
         const int r = piece / 8, kp = piece % 8;
         const int64_t t = m0 + r;
-        xreg[i] = (piece < BM * 8 && t < a.T) ? ld_global<u32x4>(a.x + t * a.K + k0 + 8 * kp)
-                                              : u32x4{0u, 0u, 0u, 0u};
+        xreg[i] = t < a.T ? ld_global<u32x4>(a.x + t * a.K + k0 + 8 * kp) : u32x4{0u, 0u, 0u, 0u};
       }
     } else {
-      const int l = lora_steps[s - k_main];
-      const int c0 = l * kBK;
+      const int c0 = chunks[s - k_main] * kBK;
 #pragma unroll
       for (int i = 0; i < W_PIECES; ++i) {
         const int piece = tid + i * kGemmThreads;
-        const int r = piece / 8, kp = piece % 8;
-        const int64_t n = n0 + r;
-        const int c = c0 + 8 * kp;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (c < a.R && n < a.N) {
-          const int ad = c / a.r_max, j = c % a.r_max;
-          const int rk = rank_of(a, ad);
-          if (j < rk && ((present[ad >> 6] >> (ad & 63)) & 1ull)) {
-            v = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(ad) * a.N + n) * a.r_max + j);
-            if (rk - j < 8) {  // clear columns at or past the rank
-              uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-              for (int e = 0; e < 8; ++e)
-                if (j + e >= rk) wv[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-              v = u32x4{wv[0], wv[1], wv[2], wv[3]};
-            }
-          }
-        }
-        wreg[i] = v;
+        wreg[i] = load_btilde(a, present, n0 + piece / 8, c0 + 8 * (piece % 8));
       }
 #pragma unroll
       for (int i = 0; i < X_PIECES; ++i) {
         const int piece = tid + i * kGemmThreads;
-        const int r = piece / 8, kp = piece % 8;
-        const int64_t t = m0 + r;
-        const int c = c0 + 8 * kp;
-        xreg[i] = (piece < BM * 8 && t < a.T && c < a.R)
-                      ? ld_global<u32x4>(a.us + t * a.R + c)
-                      : u32x4{0u, 0u, 0u, 0u};
+        const int64_t t = m0 + piece / 8;
+        const int c = c0 + 8 * (piece % 8);
+        xreg[i] = (t < a.T && c < a.R) ? ld_global<u32x4>(a.us + t * a.R + c)
+                                       : u32x4{0u, 0u, 0u, 0u};
       }
     }
   };
@@ -214,8 +360,7 @@ __global__ __launch_bounds__(kGemmThreads) void lora_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < X_PIECES; ++i) {
       const int piece = tid + i * kGemmThreads;
-      if (piece < BM * 8)
-        *reinterpret_cast<u32x4*>(x_lds(buf) + (piece / 8) * kLdsK + 8 * (piece % 8)) = xreg[i];
+      *reinterpret_cast<u32x4*>(x_lds(buf) + (piece / 8) * kLdsK + 8 * (piece % 8)) = xreg[i];
     }
   };
 
@@ -229,143 +374,82 @@ __global__ __launch_bounds__(kGemmThreads) void lora_gemm_kernel(GemmArgs a) {
   const int wrow0 = wn * (BN / WN);  // this wave's first feature row in the tile
   const int wcol0 = wm * (BM / WM);  // this wave's first token column
 
-  if (s_begin < s_end) {
-    load_step(s_begin);
-    store_step(0);
+  load_step(0);
+  store_step(0);
+  __syncthreads();
+  int cur = 0;
+  for (int s = 0; s < s_end; ++s) {
+    const bool more = s + 1 < s_end;
+    if (more) load_step(s + 1);
+#pragma unroll
+    for (int kk = 0; kk < kBK / 32; ++kk) {
+      bf16x8 af[FN], bfr[FM];
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+        af[i] = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            w_lds(cur) + (wrow0 + 16 * i + col) * kLdsK + 32 * kk + 8 * kgrp));
+#pragma unroll
+      for (int j = 0; j < FM; ++j)
+        bfr[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            x_lds(cur) + (wcol0 + 16 * j + col) * kLdsK + 32 * kk + 8 * kgrp));
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+    }
+    if (more) store_step(cur ^ 1);
     __syncthreads();
-    int cur = 0;
-    for (int s = s_begin; s < s_end; ++s) {
-      const bool more = s + 1 < s_end;
-      if (more) load_step(s + 1);
-#pragma unroll
-      for (int kk = 0; kk < kBK / 32; ++kk) {
-        bf16x8 af[FN], bfr[FM];
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-          af[i] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-              w_lds(cur) + (wrow0 + 16 * i + col) * kLdsK + 32 * kk + 8 * kgrp));
-#pragma unroll
-        for (int j = 0; j < FM; ++j)
-          bfr[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-              x_lds(cur) + (wcol0 + 16 * j + col) * kLdsK + 32 * kk + 8 * kgrp));
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-#pragma unroll
-          for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
-      }
-      if (more) store_step(cur ^ 1);
-      __syncthreads();
-      cur ^= 1;
-    }
+    cur ^= 1;
   }
 
-  // ---- epilogue: lane holds features n..n+3 (rows) of token t (column)
 #pragma unroll
-  for (int j = 0; j < FM; ++j) {
-    const int64_t t = m0 + wcol0 + 16 * j + col;
-    if (t >= a.T) continue;
+  for (int j = 0; j < FM; ++j)
 #pragma unroll
-    for (int i = 0; i < FN; ++i) {
-      const int64_t n = n0 + wrow0 + 16 * i + 4 * kgrp;
-      if (n >= a.N) continue;
-      const f32x4 v = acc[i][j];
-      if (a.mode == kModeShrink) {
-        const int ad = a.idx ? a.idx[t] : -1;
-        const float sc = ad >= 0 ? a.scale[t] : 0.f;
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = static_cast<int>(n) + e;
-          const int rad = r / a.r_max, rj = r % a.r_max;
-          o[e] = (ad >= 0 && rad == ad && rj < rank_of(a, ad)) ? sc * v[e] : 0.f;
-        }
-        *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
-            u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-      } else if (a.split == 1) {
-        f32x4 o = v;
-        if (a.res) {
-          const u32x2 r = ld_global<u32x2>(a.res + t * a.N + n);
-          o[0] += __uint_as_float(r.x << 16);
-          o[1] += __uint_as_float(r.x & 0xffff0000u);
-          o[2] += __uint_as_float(r.y << 16);
-          o[3] += __uint_as_float(r.y & 0xffff0000u);
-        }
-        *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
-            u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-      } else {
-        *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = v;
-      }
-    }
-  }
+    for (int i = 0; i < FN; ++i)
+      store4(a, m0 + wcol0 + 16 * j + col, n0 + wrow0 + 16 * i + 4 * kgrp, acc[i][j]);
 }
 
-// y[t, n..n+3] = bf16(residual + sum over splits of the partials), summed in
-// split order.
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
-                                                            int split, int64_t TN,
-                                                            const uint16_t* __restrict__ res,
-                                                            uint16_t* __restrict__ y) {
-  const int64_t e4 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4;
-  if (e4 >= TN) return;
-  f32x4 s = *reinterpret_cast<const f32x4*>(part + e4);
-  for (int z = 1; z < split; ++z) s += *reinterpret_cast<const f32x4*>(part + z * TN + e4);
-  if (res) {
-    const u32x2 r = ld_global<u32x2>(res + e4);
-    s[0] += __uint_as_float(r.x << 16);
-    s[1] += __uint_as_float(r.x & 0xffff0000u);
-    s[2] += __uint_as_float(r.y << 16);
-    s[3] += __uint_as_float(r.y & 0xffff0000u);
+template <typename Kernel>
+void raise_lds_limit(Kernel k, size_t bytes, bool& done) {
+  if (!done) {  // benign race: every caller sets the same value
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              static_cast<int>(bytes));
+    done = true;
   }
-  *reinterpret_cast<u32x2*>(y + e4) = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
 }
-
-struct Tiling {
-  int bm, bn, split;
-};
 
 template <int BM, int BN, int WM, int WN>
-local_status_t launch_gemm(GemmArgs a, hipStream_t s) {
+local_status_t launch_tiled(GemmArgs a, hipStream_t s) {
   a.gm = static_cast<int>((a.T + BM - 1) / BM);
   a.gn = static_cast<int>((a.N + BN - 1) / BN);
+  a.swizzle = 1;
   const size_t lds = static_cast<size_t>(2 * (BN + BM) * kLdsK) * sizeof(uint16_t);
-  static bool attr_set = false;  // benign race: the attribute value is the same
-  if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(lora_gemm_kernel<BM, BN, WM, WN>),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-    attr_set = true;
-  }
-  dim3 grid(a.gm * a.gn, a.split);
-  lora_gemm_kernel<BM, BN, WM, WN><<<grid, kGemmThreads, lds, s>>>(a);
-  return local_check_launch("lora_linear (gemm)");
+  static bool done = false;
+  raise_lds_limit(lora_tiled_kernel<BM, BN, WM, WN>, lds, done);
+  lora_tiled_kernel<BM, BN, WM, WN><<<a.gm * a.gn, kGemmThreads, lds, s>>>(a);
+  return local_check_launch("lora_linear (tiled)");
 }
 
-// Choose the tile for a product of T tokens x N features over total_steps
-// K-steps of 64.
-local_status_t run_gemm(GemmArgs a, int total_steps_hint, hipStream_t s) {
-  if (a.T > 256) {
-    a.split = 1;
-    a.swizzle = 1;
-    return launch_gemm<128, 128, 2, 2>(a, s);
-  }
-  a.swizzle = 0;
-  const int64_t n_tiles = (a.N + 63) / 64;
-  const int64_t m_tiles = (a.T + 127) / 128;
-  int split = 1;
-  if (a.mode == kModeMain && a.part != nullptr) {
-    while (split < 8 && n_tiles * m_tiles * split < 256 && total_steps_hint / (2 * split) >= 4)
-      split *= 2;
-  }
-  a.split = split;
-  local_status_t st;
-  if (a.T <= 32) st = launch_gemm<32, 64, 1, 4>(a, s);
-  else if (a.T <= 64) st = launch_gemm<64, 64, 1, 4>(a, s);
-  else st = launch_gemm<128, 64, 1, 4>(a, s);
-  if (st != LOCAL_OK || split == 1) return st;
-  const int64_t TN = a.T * a.N;
-  const int64_t blocks = (TN / 4 + 255) / 256;
-  splitk_reduce_kernel<<<static_cast<unsigned>(blocks), 256, 0, s>>>(a.part, split, TN, a.res,
-                                                                    a.y);
-  return local_check_launch("lora_linear (split-K reduce)");
+template <int FN, int FM, int U>
+local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
+  const size_t lds = static_cast<size_t>(kSkWaves) * FM * FN * kWave * sizeof(f32x4);
+  static bool done = false;
+  raise_lds_limit(lora_skinny_kernel<FN, FM, U>, lds, done);
+  dim3 grid(static_cast<unsigned>((a.N + 16 * FN - 1) / (16 * FN)),
+            static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)));
+  lora_skinny_kernel<FN, FM, U><<<grid, kSkThreads, lds, s>>>(a);
+  return local_check_launch("lora_linear (skinny)");
+}
+
+local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.mode == kModeMain && a.T > 256) return launch_tiled<128, 128, 2, 2>(a, s);
+  // skinny: one token tile of <= 128 rows for decode; 32-row tiles when a
+  // shrink covers many tokens, so that enough workgroups run
+  if (a.T <= 16) return launch_skinny<1, 1, 8>(a, s);
+  if (a.T <= 32 || (a.mode == kModeShrink && a.T > 128)) return launch_skinny<1, 2, 8>(a, s);
+  if (a.T <= 64) return launch_skinny<1, 4, 4>(a, s);
+  return launch_skinny<1, 8, 4>(a, s);
 }
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -391,11 +475,7 @@ extern "C" local_status_t local_lora_linear(
                       "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
                       (long long)K, (long long)N, n_adapters, r_max);
   const int R = n_adapters > 0 ? n_adapters * r_max : 0;
-  // workspace: U_s [T][R] bf16, then split-K partials [8][T][N] fp32 for T <= 256
-  const size_t us_bytes = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
-  const size_t part_bytes =
-      T <= 256 ? align256(static_cast<size_t>(8) * T * N * sizeof(float)) : 0;
-  const size_t need = us_bytes + part_bytes;
+  const size_t need = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));  // U_s
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -408,7 +488,6 @@ extern "C" local_status_t local_lora_linear(
     return local_fail(LOCAL_ERR_NULL, "lora_linear: NULL adapter argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
-  float* part = part_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + us_bytes) : nullptr;
 
   if (n_adapters > 0) {
     GemmArgs sh{};
@@ -425,7 +504,7 @@ extern "C" local_status_t local_lora_linear(
     sh.R = R;
     sh.y = us;
     sh.mode = kModeShrink;
-    local_status_t st = run_gemm(sh, static_cast<int>(K / 64), s);
+    local_status_t st = run_gemm(sh, s);
     if (st != LOCAL_OK) return st;
   }
   GemmArgs m{};
@@ -444,7 +523,6 @@ extern "C" local_status_t local_lora_linear(
   m.R = R;
   m.res = residual;
   m.y = y;
-  m.part = part;
   m.mode = kModeMain;
-  return run_gemm(m, static_cast<int>(K / 64), s);
+  return run_gemm(m, s);
 }

@@ -4,34 +4,36 @@
 //
 // Design (HBM-bound: every valid KV byte is read once, stale blocks are never
 // read):
-//  * Split-KV. Workgroup (partition, kv head g, request b) owns 32 logical
-//    blocks (512 tokens); each of its 4 waves owns 8 of them. A wave reads the
-//    8 table entries and tags first, keeps the non-stale blocks and walks
-//    them two at a time.
+//  * Split-KV. A workgroup is one wave and owns a partition of 32 logical
+//    blocks (512 tokens) of one request and one KV head. It reads the 32
+//    table entries and tags first, keeps the non-stale blocks and walks them
+//    in order through a ring of DEPTH register sets, so that DEPTH-1 blocks'
+//    K/V loads are in flight while one block is computed. Block loads are
+//    buffer loads issued unconditionally (a block past the end gets a
+//    zero-size descriptor: zeros, no traffic) and the new token is merged in
+//    with selects, so the loop has no data-dependent branch and each block
+//    waits only for its own loads.
 //  * Matrix cores, transposed. Per block, S^T[16 keys x 16 cols] =
 //    K[16 x D] * Q^T[D x 16] on v_mfma_f32_16x16x32_bf16, where the columns
 //    are the Hq/Hkv query heads that share KV head g (zero-padded to 16).
 //    The K layout [D/8][16][8] makes each lane's 16-byte A-operand slice
 //    contiguous and each MFMA's 64 loads one contiguous kilobyte. The score
 //    tile's accumulator layout (lane: 4 keys of one column) is exactly the
-//    B-operand layout of the next product O^T[D x 16] += V^T[D x 32] P^T
-//    over a pair of blocks, whose A operand comes straight from the V layout
-//    [D][16] (each lane: 4 keys of one dim per block, 8 bytes).
-//  * Online softmax in the log2 domain per column; the wave's three
-//    quantities (max, sum, O) are merged across the 4 waves in LDS, and a
-//    second kernel merges partitions when a request has more than one.
+//    B-operand layout of the next product O^T[D x 16] += V^T[D x 16] P^T on
+//    v_mfma_f32_16x16x16_bf16, whose A operand comes straight from the V
+//    layout [D][16] (each lane: 4 keys of one dim, 8 bytes).
+//  * Online softmax in the log2 domain per column. A request that fits one
+//    partition is finished in place; otherwise each partition leaves its
+//    (max, sum, unnormalised O) and a second kernel merges them.
 //  * The new token's K/V are written at position L-1 by the wave that owns
-//    that block; the same wave substitutes them for the cache slot it reads,
-//    so no other workgroup and no second launch is involved.
+//    that block, which also substitutes them for the cache slot it reads, so
+//    no other workgroup and no second launch is involved.
 #include "common.hpp"
 
 namespace localk {
 namespace {
 
-constexpr int kDecWaves = 4;
-constexpr int kDecThreads = kDecWaves * kWave;
-constexpr int kBlocksPerWave = 8;
-constexpr int kBlocksPerPart = kDecWaves * kBlocksPerWave;  // 32 blocks = 512 tokens
+constexpr int kBlocksPerPart = 32;  // one wave, 512 tokens
 constexpr float kNegBig = -1.0e30f;
 
 struct DecodeArgs {
@@ -48,22 +50,28 @@ struct DecodeArgs {
   float* lse;
   float* part_o;   // [B][Hq][n_parts][D]
   float* part_ml;  // [B][Hq][n_parts][2]  (max in log2 units, sum)
+  int64_t num_blocks;
   int Hq, Hkv, group, max_blocks, n_parts;
   float scale_log2;  // sm_scale * log2(e)
 };
 
-// Replace the 4 V values a lane holds for one block (slots slot0..slot0+3)
-// where needed: slots past the last live one become 0 (their cache contents
-// are undefined and must not reach the product), the slot being appended
-// takes the new value.
-__device__ __forceinline__ u32x2 fix_v_last(u32x2 v, int slot0, int s_last, bool has_new,
-                                            uint32_t vnew) {
+// Logical blocks request b owns: ceil(L/16), at most the table's width.
+__device__ __forceinline__ int owned_blocks(int L, int max_blocks) {
+  return L <= 0 ? 0 : min((L + kBlockSize - 1) / kBlockSize, max_blocks);
+}
+
+// The 4 V values a lane holds for one block (slots slot0..slot0+3), with
+// slots past s_live set to 0 (their cache contents are undefined and must not
+// reach the product) and slot s_new replaced by vnew. For a block that is
+// neither the last nor the appended one, s_live = 15 and s_new = -1 leave it
+// unchanged; everything is a select.
+__device__ __forceinline__ u32x2 fix_v(u32x2 v, int slot0, int s_live, int s_new,
+                                       uint32_t vnew) {
   uint32_t h[4] = {v.x & 0xffffu, v.x >> 16, v.y & 0xffffu, v.y >> 16};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int slot = slot0 + e;
-    if (slot > s_last) h[e] = 0;
-    else if (has_new && slot == s_last) h[e] = vnew;
+    h[e] = slot > s_live ? 0u : (slot == s_new ? vnew : h[e]);
   }
   u32x2 r;
   r.x = h[0] | (h[1] << 16);
@@ -71,23 +79,40 @@ __device__ __forceinline__ u32x2 fix_v_last(u32x2 v, int slot0, int s_last, bool
   return r;
 }
 
+// K/V registers of one block.
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(DecodeArgs a) {
+struct BlockRegs {
+  u32x4 k[D / 32];
+  u32x2 v[D / 16];
+};
+
+template <int D, int DEPTH>
+__global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a) {
   constexpr int KC = D / 32;  // 32-dim chunks of the QK product
   constexpr int VT = D / 16;  // 16-dim tiles of the PV product
-  extern __shared__ float lds[];
 
   const int part = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int lane = threadIdx.x;
   const int col = lane % 16, kgrp = lane / 16;
   const int L = a.ctx_lens[b];
-  const int nb = (L + kBlockSize - 1) / kBlockSize;
-  const int first_block = part * kBlocksPerPart;
-  if (first_block >= nb) return;  // whole workgroup: nothing of b here
+  const int nb = owned_blocks(L, a.max_blocks);
+  const int j0 = part * kBlocksPerPart;
+  if (j0 >= nb) return;
   const int n_parts_b = (nb + kBlocksPerPart - 1) / kBlocksPerPart;
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
   const int G = a.group;
+
+  // This partition's blocks: table entries and tags, keep the non-stale ones.
+  const int jend = min(j0 + kBlocksPerPart, nb);
+  int my_phys = 0;
+  bool ok = false;
+  if (lane < kBlocksPerPart && j0 + lane < jend) {
+    my_phys = table[j0 + lane];
+    ok = my_phys >= 0 && my_phys < a.num_blocks && a.block_version[my_phys] == rv;
+    if (!ok) my_phys = 0;  // an id outside the pool is never dereferenced
+  }
+  uint64_t valid_mask = __ballot(ok);
 
   // Query heads of this KV head, as the B operand (column = head).
   bf16x8 qv[KC];
@@ -103,23 +128,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(DecodeArgs a) 
     }
   }
 
-  // This wave's blocks: read table entries and tags, keep the non-stale ones.
-  const int j0 = first_block + wave * kBlocksPerWave;
-  const int jend = min(j0 + kBlocksPerWave, nb);
-  int my_phys = 0;
-  bool ok = false;
-  if (lane < kBlocksPerWave && j0 + lane < jend) {
-    my_phys = table[j0 + lane];
-    ok = a.block_version[my_phys] == rv;
-  }
-  uint64_t valid_mask = __ballot(ok);
-
-  // Append of the new token (position L-1) by the wave that owns its block.
-  const int j_new = nb - 1, s_last = (L - 1) % kBlockSize;
+  // Append of the new token (position L-1) if its block is in this partition
+  // and its id lies in the pool.
+  const int j_new = (L - 1) / kBlockSize, s_last = (L - 1) % kBlockSize;
   const bool has_new = a.k_new != nullptr;
   const int64_t kvrow = (static_cast<int64_t>(b) * a.Hkv + g) * D;
   if (has_new && j_new >= j0 && j_new < jend) {
-    const int p = __shfl(my_phys, j_new - j0);
+    const int p = table[j_new];
+    if (p >= 0 && p < a.num_blocks) {
     const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
     if (lane < D / 8) {
       const u32x4 kv = ld_global<u32x4>(a.k_new + kvrow + 8 * lane);
@@ -127,6 +143,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(DecodeArgs a) 
     }
     for (int d = lane; d < D; d += kWave)
       a.v_cache[tile + d * kBlockSize + s_last] = a.v_new[kvrow + d];
+    }
   }
 
   f32x4 acc[VT];
@@ -134,139 +151,126 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(DecodeArgs a) 
   for (int t = 0; t < VT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegBig, l_run = 0.f;
 
-  while (valid_mask) {
-    const int iA = __builtin_ctzll(valid_mask);
-    valid_mask &= valid_mask - 1;
-    const int iB = valid_mask ? __builtin_ctzll(valid_mask) : -1;
-    if (valid_mask) valid_mask &= valid_mask - 1;
-    const int jA = j0 + iA, jB = j0 + iB;
-    const int pA = __shfl(my_phys, iA);
-    const int pB = __shfl(my_phys, iB < 0 ? iA : iB);
-    const int64_t tA = (static_cast<int64_t>(pA) * a.Hkv + g) * (kBlockSize * D);
-    const int64_t tB = (static_cast<int64_t>(pB) * a.Hkv + g) * (kBlockSize * D);
-
-    // ---- loads: K as the A operand, V^T as the A operand of the PV product
-    u32x4 kA[KC], kB[KC];
-    u32x2 vA[VT], vB[VT];
+  // the new token's K/V fragments, for the lanes that hold its slot
+  u32x4 kn[KC];
+  uint32_t vn[VT];
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const uint16_t* src = a.k_cache + tA + c * 512 + lane * 8;
-      if (has_new && jA == j_new && col == s_last) src = a.k_new + kvrow + 32 * c + 8 * kgrp;
-      kA[c] = ld_global<u32x4>(src);
-    }
+  for (int c = 0; c < KC; ++c) kn[c] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int t = 0; t < VT; ++t) vn[t] = 0u;
+  if (has_new && j_new >= j0 && j_new < jend) {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) kn[c] = ld_global<u32x4>(a.k_new + kvrow + 32 * c + 8 * kgrp);
+#pragma unroll
+    for (int t = 0; t < VT; ++t) vn[t] = a.v_new[kvrow + 16 * t + col];
+  }
+
+  // next valid block (partition-relative index), -1 when none is left
+  auto next_block = [&]() -> int {
+    if (!valid_mask) return -1;
+    const int i = __builtin_ctzll(valid_mask);
+    valid_mask &= valid_mask - 1;
+    return i;
+  };
+  constexpr uint32_t kTileBytes = kBlockSize * D * 2;
+  auto load_block = [&](BlockRegs<D>& R, int i) {
+    const bool live = i >= 0;
+    // the block id is the same in every lane: keep it (and the descriptors)
+    // in scalar registers
+    const int p = live ? __builtin_amdgcn_readfirstlane(__shfl(my_phys, i)) : 0;
+    const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(a.k_cache + tile, live ? kTileBytes : 0u);
+    const __amdgpu_buffer_rsrc_t rv2 = make_rsrc(a.v_cache + tile, live ? kTileBytes : 0u);
+#pragma unroll
+    for (int c = 0; c < KC; ++c) R.k[c] = buf_load16(rk, (c * 512 + lane * 8) * 2);
 #pragma unroll
     for (int t = 0; t < VT; ++t)
-      vA[t] = ld_global<u32x2>(a.v_cache + tA + (16 * t + col) * kBlockSize + 4 * kgrp);
-    if (iB >= 0) {
+      R.v[t] = buf_load8(rv2, ((16 * t + col) * kBlockSize + 4 * kgrp) * 2);
+  };
+  auto compute_block = [&](BlockRegs<D>& R, int i) {
+    const int j = j0 + i;
+    const bool last = j == j_new;
+    const int s_live = last ? s_last : kBlockSize - 1;
+    const int s_new = (last && has_new) ? s_last : -1;
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        const uint16_t* src = a.k_cache + tB + c * 512 + lane * 8;
-        if (has_new && jB == j_new && col == s_last) src = a.k_new + kvrow + 32 * c + 8 * kgrp;
-        kB[c] = ld_global<u32x4>(src);
-      }
+    for (int c = 0; c < KC; ++c) R.k[c] = col == s_new ? kn[c] : R.k[c];
 #pragma unroll
-      for (int t = 0; t < VT; ++t)
-        vB[t] = ld_global<u32x2>(a.v_cache + tB + (16 * t + col) * kBlockSize + 4 * kgrp);
-    } else {
+    for (int t = 0; t < VT; ++t) R.v[t] = fix_v(R.v[t], 4 * kgrp, s_live, s_new, vn[t]);
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < KC; ++c) kB[c] = u32x4{0u, 0u, 0u, 0u};
+    for (int c = 0; c < KC; ++c) sc = mfma16x16x32(as_bf16x8(R.k[c]), qv[c], sc);
+    float s[4];
 #pragma unroll
-      for (int t = 0; t < VT; ++t) vB[t] = u32x2{0u, 0u};
-    }
-    // last block: clear dead slots of V and put the new value in
-    if (jA == j_new) {
-#pragma unroll
-      for (int t = 0; t < VT; ++t)
-        vA[t] = fix_v_last(vA[t], 4 * kgrp, s_last, has_new,
-                           has_new ? a.v_new[kvrow + 16 * t + col] : 0u);
-    }
-    if (jB == j_new) {
-#pragma unroll
-      for (int t = 0; t < VT; ++t)
-        vB[t] = fix_v_last(vB[t], 4 * kgrp, s_last, has_new,
-                           has_new ? a.v_new[kvrow + 16 * t + col] : 0u);
-    }
-
-    // ---- scores S^T (rows = key slots 4*kgrp+i, column = head col)
-    f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      sA = mfma16x16x32(as_bf16x8(kA[c]), qv[c], sA);
-      sB = mfma16x16x32(as_bf16x8(kB[c]), qv[c], sB);
-    }
-    float s[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int posA = jA * kBlockSize + 4 * kgrp + i;
-      const int posB = jB * kBlockSize + 4 * kgrp + i;
-      s[i] = posA < L ? sA[i] * a.scale_log2 : -INFINITY;
-      s[4 + i] = (iB >= 0 && posB < L) ? sB[i] * a.scale_log2 : -INFINITY;
-    }
-    float mx = s[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, s[i]);
+    for (int e = 0; e < 4; ++e)
+      s[e] = j * kBlockSize + 4 * kgrp + e < L ? sc[e] * a.scale_log2 : -INFINITY;
+    float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
+    bf16x4 pb;
     float psum = 0.f;
-    bf16x8 pb;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float p = fast_exp2(s[i] - m_new);
+    for (int e = 0; e < 4; ++e) {
+      const float p = fast_exp2(s[e] - m_new);
       psum += p;
-      pb[i] = static_cast<__bf16>(p);
+      pb[e] = static_cast<__bf16>(p);
     }
     l_run = l_run * alpha + psum;
     m_run = m_new;
 #pragma unroll
     for (int t = 0; t < VT; ++t) {
       acc[t] *= alpha;
-      u32x4 v4 = {vA[t].x, vA[t].y, vB[t].x, vB[t].y};
-      acc[t] = mfma16x16x32(as_bf16x8(v4), pb, acc[t]);
+      acc[t] = mfma16x16x16(as_bf16x4(R.v[t]), pb, acc[t]);
+    }
+  };
+
+  // ring of DEPTH register sets: DEPTH-1 blocks load while one computes
+  BlockRegs<D> R[DEPTH];
+  int idx[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH - 1; ++d) {
+    idx[d] = next_block();
+    load_block(R[d], idx[d]);
+  }
+  bool done = false;
+  while (!done) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int fill = (d + DEPTH - 1) % DEPTH;
+      idx[fill] = next_block();
+      load_block(R[fill], idx[fill]);
+      if (idx[d] < 0) {
+        done = true;
+        break;
+      }
+      compute_block(R[d], idx[d]);
     }
   }
 
-  // ---- merge the 4 waves (per column: max, sum, O^T) in LDS
+  // ---- finish: the column's sum over the 4 lane groups, then write
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
-  float* o_lds = lds;                              // [waves][G][D]
-  float* ml_lds = lds + kDecWaves * G * D;         // [waves][G][2]
   if (col < G) {
-#pragma unroll
-    for (int t = 0; t < VT; ++t)
-      *reinterpret_cast<f32x4*>(o_lds + (wave * G + col) * D + 16 * t + 4 * kgrp) = acc[t];
-    if (kgrp == 0) {
-      ml_lds[(wave * G + col) * 2] = m_run;
-      ml_lds[(wave * G + col) * 2 + 1] = l_run;
-    }
-  }
-  __syncthreads();
-  const bool single = n_parts_b == 1;
-  for (int e = threadIdx.x; e < G * D; e += kDecThreads) {
-    const int n = e / D, d = e % D;
-    float M = kNegBig;
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, ml_lds[(w * G + n) * 2]);
-    float den = 0.f, num = 0.f;
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) {
-      const float f = fast_exp2(ml_lds[(w * G + n) * 2] - M);
-      den += ml_lds[(w * G + n) * 2 + 1] * f;
-      num += o_lds[(w * G + n) * D + d] * f;
-    }
-    const int h = g * G + n;
+    const int h = g * G + col;
     const int64_t bh = static_cast<int64_t>(b) * a.Hq + h;
-    if (single) {
-      a.out[bh * D + d] = f32_to_bf16(den > 0.f ? num / den : 0.f);
-      if (d == 0 && a.lse)
-        a.lse[bh] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
+    if (n_parts_b == 1) {
+      const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+#pragma unroll
+      for (int t = 0; t < VT; ++t)
+        *reinterpret_cast<u32x2*>(a.out + bh * D + 16 * t + 4 * kgrp) =
+            u32x2{pack_bf16x2(acc[t][0] * inv, acc[t][1] * inv),
+                  pack_bf16x2(acc[t][2] * inv, acc[t][3] * inv)};
+      if (kgrp == 0 && a.lse)
+        a.lse[bh] = l_run > 0.f ? (m_run + __log2f(l_run)) * kLn2 : -INFINITY;
     } else {
       const int64_t pi = bh * a.n_parts + part;
-      a.part_o[pi * D + d] = num;
-      if (d == 0) {
-        a.part_ml[pi * 2] = M;
-        a.part_ml[pi * 2 + 1] = den;
+#pragma unroll
+      for (int t = 0; t < VT; ++t)
+        *reinterpret_cast<f32x4*>(a.part_o + pi * D + 16 * t + 4 * kgrp) = acc[t];
+      if (kgrp == 0) {
+        a.part_ml[pi * 2] = m_run;
+        a.part_ml[pi * 2 + 1] = l_run;
       }
     }
   }
@@ -279,7 +283,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   const int b = bh / a.Hq;
   const int d = threadIdx.x;
   const int L = a.ctx_lens[b];
-  const int nb = (L + kBlockSize - 1) / kBlockSize;
+  const int nb = owned_blocks(L, a.max_blocks);
   const int np = (nb + kBlocksPerPart - 1) / kBlocksPerPart;
   if (np == 1) return;  // written by the main kernel
   float M = kNegBig;
@@ -296,11 +300,14 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   if (d == 0 && a.lse) a.lse[bh] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
 }
 
+#ifndef LOCAL_DECODE_DEPTH
+#define LOCAL_DECODE_DEPTH 3
+#endif
+
 template <int D>
 local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
-  const size_t lds = (kDecWaves * a.group * D + kDecWaves * a.group * 2) * sizeof(float);
   dim3 grid(a.n_parts, a.Hkv, B);
-  decode_attn_kernel<D><<<grid, kDecThreads, lds, s>>>(a);
+  decode_attn_kernel<D, LOCAL_DECODE_DEPTH><<<grid, kWave, 0, s>>>(a);
   if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
   return local_check_launch("paged_attn_decode");
 }
@@ -359,6 +366,7 @@ extern "C" local_status_t local_paged_attn_decode(
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.group = Hq / Hkv;
+  a.num_blocks = num_blocks;
   a.max_blocks = max_blocks;
   a.n_parts = n_parts;
   a.scale_log2 = sm_scale * kLog2e;

@@ -39,9 +39,14 @@ struct PrefillArgs {
   const int32_t* req_version;
   uint16_t* out;
   float* lse;
+  int64_t T, num_blocks;
   int B, Hq, Hkv, group, max_blocks;
   float scale_log2;
 };
+
+__device__ __forceinline__ bool id_ok(int p, int64_t num_blocks) {
+  return p >= 0 && p < num_blocks;
+}
 
 __device__ __forceinline__ int find_request(const int32_t* __restrict__ q_indptr, int B,
                                             int64_t t) {
@@ -62,7 +67,11 @@ __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
   while (b + 1 < a.B && a.q_indptr[b + 1] <= t) ++b;  // skip empty requests
   const int n_b = a.q_indptr[b + 1] - a.q_indptr[b];
   const int pos = a.ctx_lens[b] - n_b + static_cast<int>(t - a.q_indptr[b]);
+  // positions without a block, or blocks with an id outside the pool, are
+  // not written
+  if (pos < 0 || pos / kBlockSize >= a.max_blocks) return;
   const int p = a.block_table[static_cast<int64_t>(b) * a.max_blocks + pos / kBlockSize];
+  if (!id_ok(p, a.num_blocks)) return;
   const int slot = pos % kBlockSize;
   const int n16 = a.Hkv * (D / 8);
   for (int e = threadIdx.x; e < n16; e += blockDim.x) {
@@ -89,8 +98,9 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
   __shared__ int wave_cnt[kPfWaves];
 
   const int qtile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int r0 = a.q_indptr[b];
-  const int n_b = a.q_indptr[b + 1] - r0;
+  const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
+  if (r0 < 0 || r1 > a.T || r1 < r0) return;  // not a row range of q
+  const int n_b = r1 - r0;
   const int row0 = qtile * ROWS_PER_WG;
   if (row0 >= n_b) return;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -120,7 +130,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
   const int wave_last_row = min(row0 + (wave + 1) * 16 * QT, n_b) - 1;
   const int wave_limit = P + wave_last_row;  // largest key position this wave sees
   const int wg_limit = P + min(row0 + ROWS_PER_WG, n_b) - 1;
-  const int nb_lim = wg_limit / kBlockSize + 1;
+  const int nb_lim = wg_limit < 0 ? 0 : min(wg_limit / kBlockSize + 1, a.max_blocks);
 
   f32x4 acc[QT][VT];
   float m_run[QT], l_run[QT];
@@ -135,7 +145,11 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
   for (int w0 = 0; w0 < nb_lim; w0 += kPfWindow) {
     // ---- compact the non-stale blocks of this window (in ascending j)
     const int j = w0 + threadIdx.x;
-    const bool ok = j < nb_lim && a.block_version[table[min(j, nb_lim - 1)]] == rv;
+    bool ok = false;
+    if (j < nb_lim) {
+      const int p = table[j];
+      ok = id_ok(p, a.num_blocks) && a.block_version[p] == rv;
+    }
     const uint64_t mask = __ballot(ok);
     const int before = __popcll(mask & ((1ull << lane) - 1ull));
     if (lane == 0) wave_cnt[wave] = __popcll(mask);
@@ -330,6 +344,8 @@ extern "C" local_status_t local_paged_attn_prefill(
   a.req_version = req_version;
   a.out = out;
   a.lse = lse;
+  a.T = T;
+  a.num_blocks = num_blocks;
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;

@@ -18,10 +18,16 @@ namespace {
 constexpr int kVcThreads = 256;
 constexpr int kVcWaves = kVcThreads / kWave;
 
+// Stale: the tag differs, or the id is outside the pool (never read then).
 __device__ __forceinline__ bool is_stale(const int32_t* __restrict__ table_row,
                                          const int32_t* __restrict__ block_version,
-                                         int32_t rv, int j) {
-  return block_version[table_row[j]] != rv;
+                                         int64_t num_blocks, int32_t rv, int j) {
+  const int32_t p = table_row[j];
+  return p < 0 || p >= num_blocks || block_version[p] != rv;
+}
+
+__device__ __forceinline__ int owned_blocks(int L, int max_blocks) {
+  return L <= 0 ? 0 : min((L + kBlockSize - 1) / kBlockSize, max_blocks);
 }
 
 // Sums two ints over the workgroup; every thread gets the totals.
@@ -48,18 +54,18 @@ __device__ __forceinline__ void block_sum2(int& a, int& b, int* lds) {
 __global__ __launch_bounds__(kVcThreads) void version_count_kernel(
     const int32_t* __restrict__ block_table, int max_blocks,
     const int32_t* __restrict__ ctx_lens,
-    const int32_t* __restrict__ block_version,
+    const int32_t* __restrict__ block_version, int64_t num_blocks,
     const int32_t* __restrict__ req_version, int32_t* __restrict__ counts,
     int32_t* __restrict__ valid_tokens) {
   __shared__ int lds[2 * kVcWaves];
   const int b = blockIdx.x;
   const int L = ctx_lens[b];
-  const int nb = (L + kBlockSize - 1) / kBlockSize;
+  const int nb = owned_blocks(L, max_blocks);
   const int rv = req_version[b];
   const int32_t* row = block_table + static_cast<int64_t>(b) * max_blocks;
   int n_stale = 0, valid = 0;
   for (int j = threadIdx.x; j < nb; j += kVcThreads) {
-    if (is_stale(row, block_version, rv, j))
+    if (is_stale(row, block_version, num_blocks, rv, j))
       ++n_stale;
     else
       valid += min(kBlockSize, L - j * kBlockSize);
@@ -74,7 +80,7 @@ __global__ __launch_bounds__(kVcThreads) void version_count_kernel(
 __global__ __launch_bounds__(kVcThreads) void version_emit_kernel(
     const int32_t* __restrict__ block_table, int B, int max_blocks,
     const int32_t* __restrict__ ctx_lens,
-    const int32_t* __restrict__ block_version,
+    const int32_t* __restrict__ block_version, int64_t num_blocks,
     const int32_t* __restrict__ req_version,
     const int32_t* __restrict__ counts, int32_t* __restrict__ stale_pairs,
     int64_t cap, int32_t* __restrict__ n_stale_out) {
@@ -88,13 +94,13 @@ __global__ __launch_bounds__(kVcThreads) void version_emit_kernel(
   block_sum2(off, dummy, lds);
 
   const int L = ctx_lens[b];
-  const int nb = (L + kBlockSize - 1) / kBlockSize;
+  const int nb = owned_blocks(L, max_blocks);
   const int rv = req_version[b];
   const int32_t* row = block_table + static_cast<int64_t>(b) * max_blocks;
   int64_t running = off;
   for (int base = 0; base < nb; base += kVcThreads) {
     const int j = base + threadIdx.x;
-    const bool st = j < nb && is_stale(row, block_version, rv, j);
+    const bool st = j < nb && is_stale(row, block_version, num_blocks, rv, j);
     const uint64_t mask = __ballot(st);
     const int before = __popcll(mask & ((1ull << lane) - 1ull));
     if (lane == 0) wave_tot[wave] = __popcll(mask);
@@ -127,13 +133,14 @@ using namespace localk;
 extern "C" local_status_t local_block_version_check(
     const int32_t* block_table, int32_t B, int32_t max_blocks,
     const int32_t* ctx_lens, int32_t block_size,
-    const int32_t* block_version, const int32_t* req_version,
+    const int32_t* block_version, int64_t num_blocks, const int32_t* req_version,
     int32_t* stale_pairs, int64_t cap, int32_t* n_stale,
     int32_t* valid_tokens, void* ws, size_t* ws_bytes, void* stream) {
   if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "version_check: ws_bytes is NULL");
-  if (B < 0 || max_blocks < 1 || cap < 0)
-    return local_fail(LOCAL_ERR_SHAPE, "version_check: B=%d max_blocks=%d cap=%lld", B,
-                      max_blocks, (long long)cap);
+  if (B < 0 || max_blocks < 1 || num_blocks < 1 || cap < 0)
+    return local_fail(LOCAL_ERR_SHAPE,
+                      "version_check: B=%d max_blocks=%d num_blocks=%lld cap=%lld", B,
+                      max_blocks, (long long)num_blocks, (long long)cap);
   if (block_size != kBlockSize)
     return local_fail(LOCAL_ERR_UNSUPPORTED, "version_check: block_size %d (only 16)",
                       block_size);
@@ -156,10 +163,10 @@ extern "C" local_status_t local_block_version_check(
   }
   int32_t* counts = static_cast<int32_t*>(ws);
   version_count_kernel<<<B, kVcThreads, 0, s>>>(block_table, max_blocks, ctx_lens,
-                                                block_version, req_version, counts,
-                                                valid_tokens);
+                                                block_version, num_blocks, req_version,
+                                                counts, valid_tokens);
   version_emit_kernel<<<B, kVcThreads, 0, s>>>(block_table, B, max_blocks, ctx_lens,
-                                               block_version, req_version, counts,
-                                               stale_pairs, cap, n_stale);
+                                               block_version, num_blocks, req_version,
+                                               counts, stale_pairs, cap, n_stale);
   return local_check_launch("version_check");
 }

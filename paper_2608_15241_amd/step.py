@@ -65,6 +65,7 @@ class Step:
         D = head_dim
         self.kind = kind
         self.n_layers = len(weights)
+        self.inputs = (x, weights, meta, kv_pool)  # owned for the step's lifetime
         self.ws = bd.Workspace(dev)
         self.calls: List[bd.Call] = []
         self.buffers = {}
@@ -121,3 +122,18 @@ class Step:
         for c in self.calls:
             c()
         return self.out
+
+    def capture(self):
+        """Capture the step into a HIP graph; returns the torch.cuda.CUDAGraph.
+
+        Run the step eagerly at least once first (kernel attributes are set on
+        first launch). The library records no memset, so replays are exact.
+        """
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                self()
+        torch.cuda.current_stream().wait_stream(s)
+        return g

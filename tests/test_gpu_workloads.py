@@ -160,3 +160,32 @@ def test_prefill_7b_sampled():
     assert_lse(lse.cpu().numpy()[rows], rl, "prefill lse")
     del pool
     torch.cuda.empty_cache()
+
+
+def test_step_graph_replays_match_eager():
+    # The whole decode step captured into a HIP graph: every replay, with
+    # eager work and synchronisations in between, equals the eager step.
+    w = workloads.GQA_SKEW
+    meta, weights, pool, x = _setup(w, 3)
+    st = Step("decode", x, weights, meta_to_device(meta, "cuda"), pool, w.hq, w.hkv,
+              w.head_dim, residual=False)
+    st()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in st.buffers[0].items()}
+    ref_pairs = [t.clone() for t in st.version_check.outputs]
+    g = st.capture()
+    for rep in range(4):
+        for k in ("q", "o", "y", "lse"):
+            st.buffers[0][k].fill_(float("nan") if k == "lse" else 7.0)
+        st.version_check.outputs[2].fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(st.buffers[0][k].view(torch.int16) if v.dtype == torch.bfloat16
+                               else st.buffers[0][k], v.view(torch.int16)
+                               if v.dtype == torch.bfloat16 else v), (rep, k)
+        for a_, b_ in zip(st.version_check.outputs, ref_pairs):
+            assert torch.equal(a_, b_), rep
+    del st, pool, weights
+    torch.cuda.empty_cache()

@@ -322,3 +322,24 @@ def test_kv_append_writes_documented_slots():
             else:
                 assert np.array_equal(kd2[p, :, s], kd[p, :, s])
                 assert np.array_equal(vd2[p, :, s], vd[p, :, s])
+
+
+def test_out_of_range_id_equals_stale_block():
+    # An id outside the pool excludes its block exactly like a stale tag.
+    rng = np.random.default_rng(13)
+    Hq, Hkv, D = 4, 2, 64
+    ctx = np.array([40], np.int32)
+    table, num = make_table(rng, ctx)
+    rv = np.array([3], np.int32)
+    bv = _valid_tags(table, ctx, rv, num)
+    kd, vd = _pool(rng, num, Hkv, D)
+    q = rand_bf16(rng, (1, Hq, D))
+    qi = np.array([0, 1], np.int32)
+    bad = table.copy()
+    bad[0, 1] = num + 5
+    out1, lse1 = _run(q, qi, ctx, kd, vd, bad, bv, rv, Hq, Hkv, D, 0.125)
+    bv2 = bv.copy()
+    bv2[table[0, 1]] = 2
+    out2, lse2 = _run(q, qi, ctx, kd, vd, table, bv2, rv, Hq, Hkv, D, 0.125)
+    np.testing.assert_array_equal(out1, out2)
+    np.testing.assert_array_equal(lse1, lse2)

@@ -133,3 +133,11 @@ def test_residual_is_added_as_given():
     y0 = oracle.lora_linear(x, W, A, B, ranks, idx, s)
     y1 = oracle.lora_linear(x, W, A, B, ranks, idx, s, residual=res)
     np.testing.assert_allclose(y1 - y0, bits_to_f64(res), rtol=1e-12, atol=1e-12)
+
+
+def test_adapter_index_out_of_range_is_base():
+    rng = np.random.default_rng(9)
+    x, W, A, B, ranks = _setup(rng, T=3, K=64, N=16)
+    y = oracle.lora_linear(x, W, A, B, ranks, np.array([3, 7, -1], np.int32),
+                           np.full(3, 2.0, np.float32))
+    assert np.array_equal(y, oracle.lora_linear(x, W))

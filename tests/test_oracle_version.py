@@ -98,3 +98,13 @@ def test_churn_workload_matches_generator_record():
     assert np.array_equal(pairs, m.stale_entries)
     per_req = np.bincount(m.stale_entries[:, 0], minlength=m.B)
     assert np.array_equal(valid, m.ctx_lens - 16 * per_req)
+
+
+def test_out_of_range_ids_and_table_width():
+    # An id outside [0, num_blocks) is stale and never read; a request owns at
+    # most max_blocks blocks even if its context says more.
+    table = np.array([[0, 7, 1], [2, -3, 3]], np.int32)
+    bv = np.array([5, 5, 6, 6], np.int32)           # num_blocks = 4
+    pairs, n, valid = _check(table, [48, 64], bv, [5, 6])
+    assert pairs.tolist() == [[0, 1], [1, 1]] and n == 2
+    assert valid.tolist() == [32, 32]               # request 1 owns 3 of 4 blocks
