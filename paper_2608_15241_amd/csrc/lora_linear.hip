@@ -41,6 +41,17 @@ constexpr int kBK = 64;
 constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kNumXcd = 8;
+constexpr int kMaxShrinkSplit = 16;     // K slices of a decode-size shrink
+
+#ifndef LOCAL_SK_U32
+#define LOCAL_SK_U32 4     // K-steps of 64 per batch of loads, 32-token tiles
+#endif
+#ifndef LOCAL_SK_FN64
+#define LOCAL_SK_FN64 1    // 16-feature tiles per workgroup at 64 tokens
+#endif
+#ifndef LOCAL_SK_FN128
+#define LOCAL_SK_FN128 1   // 16-feature tiles per workgroup at 128 tokens
+#endif
 
 enum GemmMode { kModeMain = 0, kModeShrink = 1 };
 
@@ -56,6 +67,8 @@ struct GemmArgs {
   int n_ad, r_max, R;
   const uint16_t* res;   // optional residual [T][N] (main mode)
   uint16_t* y;           // bf16 output [T][N] (U_s in shrink mode)
+  float* part;           // split-K shrink: fp32 partial sums [ksplit][T][N]
+  int ksplit;            // K slices of the skinny kernel (grid.z)
   int mode;
   int gm, gn;            // tile grid of the tiled kernel
   int swizzle;           // XCD-aware grouped order (tiled kernel)
@@ -163,8 +176,12 @@ __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* 
 // Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM); wave w takes
 // a contiguous range of the K/32 base steps (U steps per batch of loads) and
 // every 8th U_s chunk; partial tiles are summed through LDS in wave order.
+// An 8-wave workgroup runs two waves per SIMD; telling the compiler so lets it
+// keep a whole batch of loads in registers instead of interleaving each load
+// with the MFMA that consumes it (which leaves one load in flight per wave).
 template <int FN, int FM, int U>
-__global__ __launch_bounds__(kSkThreads) void lora_skinny_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kSkThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void lora_skinny_kernel(GemmArgs a) {
   __shared__ uint64_t present[4];
   __shared__ uint16_t chunks[kMaxLoraChunks];
   __shared__ int wave_cnt[kSkWaves];
@@ -192,7 +209,7 @@ __global__ __launch_bounds__(kSkThreads) void lora_skinny_kernel(GemmArgs a) {
   for (int i = 0; i < FN; ++i) {
     const int64_t n = n0 + 16 * i + col;
     wok[i] = n < a.N;
-    wrow[i] = a.w + (wok[i] ? n : 0) * a.K + 8 * kgrp;
+    wrow[i] = a.w + (wok[i] ? n : 0) * a.K;
   }
   const uint16_t* xrow[FM];
   bool xok[FM];
@@ -200,39 +217,60 @@ __global__ __launch_bounds__(kSkThreads) void lora_skinny_kernel(GemmArgs a) {
   for (int j = 0; j < FM; ++j) {
     const int64_t t = t0 + 16 * j + col;
     xok[j] = t < a.T;
-    xrow[j] = a.x + (xok[j] ? t : 0) * a.K + 8 * kgrp;
+    xrow[j] = a.x + (xok[j] ? t : 0) * a.K;
   }
 
   // Loads are unconditional (rows are clamped to a valid one above, steps
   // past the wave's range to its last step) and invalid values are zeroed
   // with selects, so the loop has no branch around a load and each batch of
   // MFMAs waits only for its own loads.
-  const int ksteps = static_cast<int>(a.K / 32);
-  const int s_lo = (wave * ksteps) / kSkWaves;
-  const int s_hi = ((wave + 1) * ksteps) / kSkWaves;
+  //
+  // A step covers 64 k as two MFMAs. The k order inside a step is permuted
+  // (MFMA m, k-group g takes k = 16g + 8m .. +8), which is the same for both
+  // operands and so leaves the product unchanged, but lets every lane load 32
+  // contiguous bytes: each row of W and x is read as whole 128-byte lines.
+  // Every workgroup reads the same rows of x. Each one takes the 8 K ranges
+  // of its slice in a rotated order (wave w takes range (w + rot) mod 8), so
+  // that workgroups running together read different parts of x and spread
+  // over the L2 channels instead of all hitting the same lines at once.
+  const int ksteps = static_cast<int>(a.K / 64);
+  const int z = blockIdx.z;
+  const int z_lo = (z * ksteps) / a.ksplit, z_hi = ((z + 1) * ksteps) / a.ksplit;
+  const int rw = (wave + static_cast<int>(blockIdx.x + blockIdx.y)) % kSkWaves;
+  const int s_lo = z_lo + (rw * (z_hi - z_lo)) / kSkWaves;
+  const int s_hi = z_lo + ((rw + 1) * (z_hi - z_lo)) / kSkWaves;
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
   for (int s = s_lo; s < s_hi; s += U) {
-    u32x4 wv[U][FN], xv[U][FM];
+    u32x4 wv[U][FN][2], xv[U][FM][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 32;
+      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 64 + 16 * kgrp;
 #pragma unroll
-      for (int i = 0; i < FN; ++i) wv[u][i] = ld_global<u32x4>(wrow[i] + k);
+      for (int i = 0; i < FN; ++i) {
+        wv[u][i][0] = ld_global<u32x4>(wrow[i] + k);
+        wv[u][i][1] = ld_global<u32x4>(wrow[i] + k + 8);
+      }
 #pragma unroll
-      for (int j = 0; j < FM; ++j) xv[u][j] = ld_global<u32x4>(xrow[j] + k);
+      for (int j = 0; j < FM; ++j) {
+        xv[u][j][0] = ld_global<u32x4>(xrow[j] + k);
+        xv[u][j][1] = ld_global<u32x4>(xrow[j] + k + 8);
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool live = s + u < s_hi;
 #pragma unroll
-      for (int i = 0; i < FN; ++i) wv[u][i] = (live && wok[i]) ? wv[u][i] : zero4;
+      for (int m = 0; m < 2; ++m) {
 #pragma unroll
-      for (int j = 0; j < FM; ++j) xv[u][j] = (live && xok[j]) ? xv[u][j] : zero4;
+        for (int i = 0; i < FN; ++i) wv[u][i][m] = (live && wok[i]) ? wv[u][i][m] : zero4;
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
+        for (int j = 0; j < FM; ++j) xv[u][j][m] = (live && xok[j]) ? xv[u][j][m] : zero4;
 #pragma unroll
-        for (int j = 0; j < FM; ++j)
-          acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i]), as_bf16x8(xv[u][j]), acc[i][j]);
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+          for (int j = 0; j < FM; ++j)
+            acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i][m]), as_bf16x8(xv[u][j][m]), acc[i][j]);
+      }
     }
   }
   // adapter up-projection: chunks of 32 U_s columns, round-robin over waves
@@ -263,8 +301,31 @@ __global__ __launch_bounds__(kSkThreads) void lora_skinny_kernel(GemmArgs a) {
     const int l = e % kWave, i = (e / kWave) % FN, j = e / (kWave * FN);
     f32x4 s = red[e];
     for (int w = 1; w < kSkWaves; ++w) s += red[w * FM * FN * kWave + e];
-    store4(a, t0 + 16 * j + l % 16, n0 + 16 * i + 4 * (l / 16), s);
+    const int64_t t = t0 + 16 * j + l % 16, n = n0 + 16 * i + 4 * (l / 16);
+    if (a.part) {  // split-K: fp32 partial of this slice, finished by shrink_reduce
+      if (t < a.T && n < a.N)
+        *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
+    } else {
+      store4(a, t, n, s);
+    }
   }
+}
+
+// Finishes a split-K shrink: U_s[t, n..n+3] from the sum of the slices'
+// partials (in slice order), with the shrink's mask and scale.
+__global__ __launch_bounds__(256) void shrink_reduce_kernel(GemmArgs a) {
+  const int64_t e4 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4;
+  const int64_t TN = a.T * a.N;
+  if (e4 >= TN) return;
+  f32x4 v[kMaxShrinkSplit];
+#pragma unroll
+  for (int z = 0; z < kMaxShrinkSplit; ++z)
+    if (z < a.ksplit) v[z] = *reinterpret_cast<const f32x4*>(a.part + z * TN + e4);
+  f32x4 s = v[0];
+#pragma unroll
+  for (int z = 1; z < kMaxShrinkSplit; ++z)
+    if (z < a.ksplit) s += v[z];
+  store4(a, e4 / a.N, e4 % a.N, s);
 }
 
 // ------------------------------------------------------------------ tiled
@@ -437,19 +498,41 @@ local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
   static bool done = false;
   raise_lds_limit(lora_skinny_kernel<FN, FM, U>, lds, done);
   dim3 grid(static_cast<unsigned>((a.N + 16 * FN - 1) / (16 * FN)),
-            static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)));
+            static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)),
+            static_cast<unsigned>(a.ksplit));
   lora_skinny_kernel<FN, FM, U><<<grid, kSkThreads, lds, s>>>(a);
-  return local_check_launch("lora_linear (skinny)");
+  local_status_t st = local_check_launch("lora_linear (skinny)");
+  if (st != LOCAL_OK || a.part == nullptr) return st;
+  const int64_t quads = a.T * a.N / 4;
+  shrink_reduce_kernel<<<static_cast<unsigned>((quads + 255) / 256), 256, 0, s>>>(a);
+  return local_check_launch("lora_linear (shrink reduce)");
+}
+
+template <int FN, int FM, int U>
+local_status_t launch_skinny_tiles(GemmArgs a, hipStream_t s) {
+  // A decode-size shrink has few output tiles: split K so that about 256
+  // workgroups run, each wave still owning at least one K-step.
+  a.ksplit = 1;
+  if (a.mode == kModeShrink && a.part != nullptr) {
+    const int64_t tiles = ((a.N + 16 * FN - 1) / (16 * FN)) * ((a.T + 16 * FM - 1) / (16 * FM));
+    const int max_split = static_cast<int>(a.K / 64 / kSkWaves);
+    while (a.ksplit * 2 <= kMaxShrinkSplit && a.ksplit * 2 <= max_split &&
+           tiles * a.ksplit * 2 <= 256)
+      a.ksplit *= 2;
+  }
+  if (a.ksplit == 1) a.part = nullptr;
+  return launch_skinny<FN, FM, U>(a, s);
 }
 
 local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.mode == kModeMain && a.T > 256) return launch_tiled<128, 128, 2, 2>(a, s);
   // skinny: one token tile of <= 128 rows for decode; 32-row tiles when a
   // shrink covers many tokens, so that enough workgroups run
-  if (a.T <= 16) return launch_skinny<1, 1, 8>(a, s);
-  if (a.T <= 32 || (a.mode == kModeShrink && a.T > 128)) return launch_skinny<1, 2, 8>(a, s);
-  if (a.T <= 64) return launch_skinny<1, 4, 4>(a, s);
-  return launch_skinny<1, 8, 4>(a, s);
+  if (a.T <= 16) return launch_skinny_tiles<1, 1, 4>(a, s);
+  if (a.T <= 32 || (a.mode == kModeShrink && a.T > 128))
+    return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
+  if (a.T <= 64) return launch_skinny_tiles<LOCAL_SK_FN64, 4, 2>(a, s);
+  return launch_skinny_tiles<LOCAL_SK_FN128, 8, 2>(a, s);
 }
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -475,7 +558,12 @@ extern "C" local_status_t local_lora_linear(
                       "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
                       (long long)K, (long long)N, n_adapters, r_max);
   const int R = n_adapters > 0 ? n_adapters * r_max : 0;
-  const size_t need = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));  // U_s
+  // workspace: U_s [T][R] bf16, then (decode sizes) the shrink's split-K
+  // partial sums [<= 32][T][R] fp32
+  const size_t us_bytes = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
+  const size_t part_bytes =
+      T <= 128 ? align256(static_cast<size_t>(kMaxShrinkSplit) * T * R * sizeof(float)) : 0;
+  const size_t need = us_bytes + part_bytes;
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -503,6 +591,7 @@ extern "C" local_status_t local_lora_linear(
     sh.r_max = r_max;
     sh.R = R;
     sh.y = us;
+    sh.part = part_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + us_bytes) : nullptr;
     sh.mode = kModeShrink;
     local_status_t st = run_gemm(sh, s);
     if (st != LOCAL_OK) return st;

@@ -5,8 +5,12 @@
 // Design (HBM-bound: every valid KV byte is read once, stale blocks are never
 // read):
 //  * Split-KV. A workgroup is one wave and owns a partition of 32 logical
-//    blocks (512 tokens) of one request and one KV head. It reads the 32
-//    table entries and tags first, keeps the non-stale blocks and walks them
+//    blocks (512 tokens) of one request and one KV head. Partitions are
+//    counted from the end of the context and their index is the slowest grid
+//    dimension, so full partitions are dispatched first and each request's
+//    partial one (its oldest blocks) last, which shortens the tail when
+//    context lengths vary. A wave reads its 32 table entries and tags first,
+//    keeps the non-stale blocks and walks them
 //    in order through a ring of DEPTH register sets, so that DEPTH-1 blocks'
 //    K/V loads are in flight while one block is computed. Block loads are
 //    buffer loads issued unconditionally (a block past the end gets a
@@ -33,7 +37,10 @@
 namespace localk {
 namespace {
 
-constexpr int kBlocksPerPart = 32;  // one wave, 512 tokens
+#ifndef LOCAL_DECODE_PART_BLOCKS
+#define LOCAL_DECODE_PART_BLOCKS 32
+#endif
+constexpr int kBlocksPerPart = LOCAL_DECODE_PART_BLOCKS;  // one wave, 512 tokens
 constexpr float kNegBig = -1.0e30f;
 
 struct DecodeArgs {
@@ -91,20 +98,22 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a) {
   constexpr int KC = D / 32;  // 32-dim chunks of the QK product
   constexpr int VT = D / 16;  // 16-dim tiles of the PV product
 
-  const int part = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int g = blockIdx.x, b = blockIdx.y, part = blockIdx.z;
   const int lane = threadIdx.x;
   const int col = lane % 16, kgrp = lane / 16;
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  const int j0 = part * kBlocksPerPart;
-  if (j0 >= nb) return;
+  // partition `part` covers blocks [nb - 32(part+1), nb - 32 part) of b
+  const int j_end_part = nb - part * kBlocksPerPart;
+  if (j_end_part <= 0) return;
+  const int j0 = max(0, j_end_part - kBlocksPerPart);
   const int n_parts_b = (nb + kBlocksPerPart - 1) / kBlocksPerPart;
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
   const int G = a.group;
 
   // This partition's blocks: table entries and tags, keep the non-stale ones.
-  const int jend = min(j0 + kBlocksPerPart, nb);
+  const int jend = j_end_part;
   int my_phys = 0;
   bool ok = false;
   if (lane < kBlocksPerPart && j0 + lane < jend) {
@@ -306,7 +315,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
 
 template <int D>
 local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
-  dim3 grid(a.n_parts, a.Hkv, B);
+  dim3 grid(a.Hkv, B, a.n_parts);
   decode_attn_kernel<D, LOCAL_DECODE_DEPTH><<<grid, kWave, 0, s>>>(a);
   if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
   return local_check_launch("paged_attn_decode");
