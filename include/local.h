@@ -116,7 +116,8 @@ int32_t local_version(void);
  *   A            [n_adapters][r_max][K]  bf16, adapter down-projections
  *   B            [n_adapters][N][r_max]  bf16, adapter up-projections
  *   ranks        [n_adapters] int32 in [1, r_max], or NULL (every rank = r_max).
- *                Rows j >= rank of A and columns j >= rank of B are never used.
+ *                Rows j >= rank of A and columns j >= rank of B are never used;
+ *                a rank outside [0, r_max] is clamped to that range.
  *   adapter_idx  [T] int32 in [-1, n_adapters); -1 = base projection only
  *                (any value outside [0, n_adapters) is read as -1)
  *   scale        [T] float32, the per-token adapter scale s

@@ -82,6 +82,8 @@ void oracle_lora_linear(const uint16_t* x, int64_t T, int64_t K,
     double u[256];
     if (a >= 0) {
       rank = ranks ? ranks[a] : r_max;
+      if (rank < 0) rank = 0; /* clamped to [0, r_max] */
+      if (rank > r_max) rank = r_max;
       for (int j = 0; j < rank; ++j) {
         double acc = 0.0;
         for (int64_t k = 0; k < K; ++k)

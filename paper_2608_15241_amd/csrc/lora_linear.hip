@@ -22,7 +22,10 @@
 //      its 8 waves split K; each lane loads its MFMA operand slices straight
 //      from global memory several K-steps ahead (no LDS staging, no barrier
 //      in the main loop), and the 8 partial tiles are summed once through LDS
-//      in a fixed order. Also used for every shrink.
+//      in a fixed order. Also the shrink of a long prefill chunk.
+//    - SGMV shrink (decode sizes): one workgroup per adapter computes the
+//      shrink of the tokens routed to it on the matrix cores; each adapter's
+//      A is read once and no partial sums leave the workgroup.
 //    - tiled (many tokens and features): prefill projections are bound by the
 //      matrix cores. 128x128 tiles, 2x2 waves, register prefetch into an LDS
 //      double buffer with padded rows, XCD-aware grouped tile order so each
@@ -41,10 +44,12 @@ constexpr int kBK = 64;
 constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kNumXcd = 8;
-constexpr int kMaxShrinkSplit = 16;     // K slices of a decode-size shrink
 
 #ifndef LOCAL_SK_U32
 #define LOCAL_SK_U32 4     // K-steps of 64 per batch of loads, 32-token tiles
+#endif
+#ifndef LOCAL_SK_FN32
+#define LOCAL_SK_FN32 1    // 16-feature tiles per workgroup at 32 tokens
 #endif
 #ifndef LOCAL_SK_FN64
 #define LOCAL_SK_FN64 1    // 16-feature tiles per workgroup at 64 tokens
@@ -67,15 +72,16 @@ struct GemmArgs {
   int n_ad, r_max, R;
   const uint16_t* res;   // optional residual [T][N] (main mode)
   uint16_t* y;           // bf16 output [T][N] (U_s in shrink mode)
-  float* part;           // split-K shrink: fp32 partial sums [ksplit][T][N]
-  int ksplit;            // K slices of the skinny kernel (grid.z)
+  int ksplit;            // K slices of the skinny kernel (grid.z); 1 = whole K
   int mode;
   int gm, gn;            // tile grid of the tiled kernel
   int swizzle;           // XCD-aware grouped order (tiled kernel)
 };
 
+// Rank of adapter ad, clamped to [0, r_max] so that no rank reads past the
+// adapter's own rows.
 __device__ __forceinline__ int rank_of(const GemmArgs& a, int ad) {
-  return a.ranks ? a.ranks[ad] : a.r_max;
+  return a.ranks ? min(max(a.ranks[ad], 0), a.r_max) : a.r_max;
 }
 
 __device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad) {
@@ -301,31 +307,117 @@ void lora_skinny_kernel(GemmArgs a) {
     const int l = e % kWave, i = (e / kWave) % FN, j = e / (kWave * FN);
     f32x4 s = red[e];
     for (int w = 1; w < kSkWaves; ++w) s += red[w * FM * FN * kWave + e];
-    const int64_t t = t0 + 16 * j + l % 16, n = n0 + 16 * i + 4 * (l / 16);
-    if (a.part) {  // split-K: fp32 partial of this slice, finished by shrink_reduce
-      if (t < a.T && n < a.N)
-        *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
-    } else {
-      store4(a, t, n, s);
-    }
+    store4(a, t0 + 16 * j + l % 16, n0 + 16 * i + 4 * (l / 16), s);
   }
 }
 
-// Finishes a split-K shrink: U_s[t, n..n+3] from the sum of the slices'
-// partials (in slice order), with the shrink's mask and scale.
-__global__ __launch_bounds__(256) void shrink_reduce_kernel(GemmArgs a) {
-  const int64_t e4 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4;
-  const int64_t TN = a.T * a.N;
-  if (e4 >= TN) return;
-  f32x4 v[kMaxShrinkSplit];
+// ------------------------------------------------------------- SGMV shrink
+// Decode-size shrink, one workgroup per adapter a (segmented by adapter, as
+// in SGMV): the tokens routed to a are compacted (ascending) into groups of
+// 16 that become the columns of S^T = A_a X_g^T on the matrix cores, with the
+// adapter's rank rows as MFMA rows. The 16 waves split K, each issuing the
+// loads of U steps before their MFMAs, and their partial tiles are summed
+// through LDS in wave order. The workgroup owns U_s columns
+// [a*r_max, (a+1)*r_max) for every token: it first zero-fills them, then
+// writes bf16(s_t * u) for its tokens and rows below the rank, so every
+// adapter's A is read once and no partial sums leave the workgroup.
+constexpr int kSgThreads = 1024;
+constexpr int kSgWaves = kSgThreads / kWave;
+constexpr int kSgMaxTokens = 256;  // decode sizes only
+constexpr int kSgMaxTiles = 8;     // r_max <= 128
+
+template <int RT, int U>  // RT 16-row tiles of the rank dimension (r_max <= 16*RT)
+__global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a) {
+  __shared__ int toks[kSgMaxTokens];
+  __shared__ int wave_cnt[kSgWaves];
+  __shared__ f32x4 red[kSgWaves][kWave];
+  const int ad = blockIdx.x;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int col = lane % 16, kgrp = lane / 16;
+  const int rk = rank_of(a, ad);
+
+  // zero-fill this adapter's column block for every token
+  uint16_t* ublk = a.y + static_cast<int64_t>(ad) * a.r_max;
+  for (int64_t e = tid; e < a.T * a.r_max; e += kSgThreads)
+    ublk[(e / a.r_max) * a.R + e % a.r_max] = 0;
+
+  // tokens routed to this adapter, ascending (T <= kSgMaxTokens <= threads)
+  const int t = tid;
+  const bool mine = t < a.T && a.idx[t] == ad;
+  const uint64_t m = __ballot(mine);
+  if (lane == 0) wave_cnt[wave] = __popcll(m);
+  __syncthreads();  // also orders the zero-fill before the value writes below
+  int off = 0, n_tok = 0;
+  for (int w = 0; w < kSgWaves; ++w) {
+    if (w < wave) off += wave_cnt[w];
+    n_tok += wave_cnt[w];
+  }
+  if (mine) toks[off + __popcll(m & ((1ull << lane) - 1ull))] = t;
+  __syncthreads();
+  if (n_tok == 0 || rk == 0) return;  // uniform: nothing beyond the zero-fill
+
+  const int ksteps = static_cast<int>(a.K / 32);
+  const int s_lo = (wave * ksteps) / kSgWaves, s_hi = ((wave + 1) * ksteps) / kSgWaves;
+  const int tiles = (rk + 15) / 16;  // uniform: tiles past the rank are skipped
+  const uint16_t* abase = a.w + static_cast<int64_t>(ad) * a.r_max * a.K;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  for (int g0 = 0; g0 < n_tok; g0 += 16) {
+    // this lane's operand rows: rank row (A) and token (B) of each tile
+    const uint16_t* arow[RT];
+    bool aok[RT];
 #pragma unroll
-  for (int z = 0; z < kMaxShrinkSplit; ++z)
-    if (z < a.ksplit) v[z] = *reinterpret_cast<const f32x4*>(a.part + z * TN + e4);
-  f32x4 s = v[0];
+    for (int i = 0; i < RT; ++i) {
+      const int j = 16 * i + col;
+      aok[i] = j < rk;
+      arow[i] = abase + static_cast<int64_t>(aok[i] ? j : 0) * a.K + 8 * kgrp;
+    }
+    const bool xok = g0 + col < n_tok;
+    const uint16_t* xrow = a.x + static_cast<int64_t>(toks[xok ? g0 + col : g0]) * a.K + 8 * kgrp;
+    f32x4 acc[RT];
 #pragma unroll
-  for (int z = 1; z < kMaxShrinkSplit; ++z)
-    if (z < a.ksplit) s += v[z];
-  store4(a, e4 / a.N, e4 % a.N, s);
+    for (int i = 0; i < RT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = s_lo; s0 < s_hi; s0 += U) {
+      // steps past s_hi reload the last step and use a zero token operand
+      u32x4 xv[U], av[U][RT];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t k = static_cast<int64_t>(min(s0 + u, s_hi - 1)) * 32;
+        xv[u] = ld_global<u32x4>(xrow + k);
+#pragma unroll
+        for (int i = 0; i < RT; ++i)
+          av[u][i] = i < tiles ? ld_global<u32x4>(arow[i] + k) : zero4;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const u32x4 xb = (xok && s0 + u < s_hi) ? xv[u] : zero4;
+#pragma unroll
+        for (int i = 0; i < RT; ++i)
+          if (i < tiles)
+            acc[i] = mfma16x16x32(as_bf16x8(aok[i] ? av[u][i] : zero4), as_bf16x8(xb), acc[i]);
+      }
+    }
+    const int slot = g0 + col;
+    const int tok = slot < n_tok ? toks[slot] : 0;
+    const float sc = slot < n_tok ? a.scale[tok] : 0.f;
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+      if (i >= tiles) break;
+      red[wave][lane] = acc[i];
+      __syncthreads();
+      if (wave == 0) {
+        f32x4 v = red[0][lane];
+        for (int w = 1; w < kSgWaves; ++w) v += red[w][lane];
+        if (slot < n_tok) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int j = 16 * i + 4 * kgrp + q;  // rank row
+            if (j < rk) ublk[static_cast<int64_t>(tok) * a.R + j] = f32_to_bf16(sc * v[q]);
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
 }
 
 // ------------------------------------------------------------------ tiled
@@ -501,26 +593,12 @@ local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
             static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)),
             static_cast<unsigned>(a.ksplit));
   lora_skinny_kernel<FN, FM, U><<<grid, kSkThreads, lds, s>>>(a);
-  local_status_t st = local_check_launch("lora_linear (skinny)");
-  if (st != LOCAL_OK || a.part == nullptr) return st;
-  const int64_t quads = a.T * a.N / 4;
-  shrink_reduce_kernel<<<static_cast<unsigned>((quads + 255) / 256), 256, 0, s>>>(a);
-  return local_check_launch("lora_linear (shrink reduce)");
+  return local_check_launch("lora_linear (skinny)");
 }
 
 template <int FN, int FM, int U>
 local_status_t launch_skinny_tiles(GemmArgs a, hipStream_t s) {
-  // A decode-size shrink has few output tiles: split K so that about 256
-  // workgroups run, each wave still owning at least one K-step.
   a.ksplit = 1;
-  if (a.mode == kModeShrink && a.part != nullptr) {
-    const int64_t tiles = ((a.N + 16 * FN - 1) / (16 * FN)) * ((a.T + 16 * FM - 1) / (16 * FM));
-    const int max_split = static_cast<int>(a.K / 64 / kSkWaves);
-    while (a.ksplit * 2 <= kMaxShrinkSplit && a.ksplit * 2 <= max_split &&
-           tiles * a.ksplit * 2 <= 256)
-      a.ksplit *= 2;
-  }
-  if (a.ksplit == 1) a.part = nullptr;
   return launch_skinny<FN, FM, U>(a, s);
 }
 
@@ -529,8 +607,8 @@ local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
   // skinny: one token tile of <= 128 rows for decode; 32-row tiles when a
   // shrink covers many tokens, so that enough workgroups run
   if (a.T <= 16) return launch_skinny_tiles<1, 1, 4>(a, s);
-  if (a.T <= 32 || (a.mode == kModeShrink && a.T > 128))
-    return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
+  if (a.mode == kModeShrink && a.T > 128) return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
+  if (a.T <= 32) return launch_skinny_tiles<LOCAL_SK_FN32, 2, LOCAL_SK_U32>(a, s);
   if (a.T <= 64) return launch_skinny_tiles<LOCAL_SK_FN64, 4, 2>(a, s);
   return launch_skinny_tiles<LOCAL_SK_FN128, 8, 2>(a, s);
 }
@@ -558,12 +636,8 @@ extern "C" local_status_t local_lora_linear(
                       "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
                       (long long)K, (long long)N, n_adapters, r_max);
   const int R = n_adapters > 0 ? n_adapters * r_max : 0;
-  // workspace: U_s [T][R] bf16, then (decode sizes) the shrink's split-K
-  // partial sums [<= 32][T][R] fp32
-  const size_t us_bytes = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
-  const size_t part_bytes =
-      T <= 128 ? align256(static_cast<size_t>(kMaxShrinkSplit) * T * R * sizeof(float)) : 0;
-  const size_t need = us_bytes + part_bytes;
+  // workspace: U_s [T][R] bf16
+  const size_t need = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -591,9 +665,19 @@ extern "C" local_status_t local_lora_linear(
     sh.r_max = r_max;
     sh.R = R;
     sh.y = us;
-    sh.part = part_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + us_bytes) : nullptr;
     sh.mode = kModeShrink;
-    local_status_t st = run_gemm(sh, s);
+    local_status_t st;
+    if (T <= kSgMaxTokens) {  // decode sizes: one workgroup per adapter
+      const int rt = (r_max + 15) / 16;
+      const unsigned g = static_cast<unsigned>(n_adapters);
+      if (rt <= 1) lora_sgmv_shrink_kernel<1, 8><<<g, kSgThreads, 0, s>>>(sh);
+      else if (rt <= 2) lora_sgmv_shrink_kernel<2, 4><<<g, kSgThreads, 0, s>>>(sh);
+      else if (rt <= 4) lora_sgmv_shrink_kernel<4, 2><<<g, kSgThreads, 0, s>>>(sh);
+      else lora_sgmv_shrink_kernel<kSgMaxTiles, 1><<<g, kSgThreads, 0, s>>>(sh);
+      st = local_check_launch("lora_linear (SGMV shrink)");
+    } else {
+      st = run_gemm(sh, s);
+    }
     if (st != LOCAL_OK) return st;
   }
   GemmArgs m{};

@@ -57,6 +57,8 @@ CASES = [
     (257, 512, 256, 4, 16, None),
     (300, 512, 640, 4, 16, [16, 3, 9, 16]),
     (1000, 256, 512, 4, 16, None),
+    (256, 512, 256, 2, 128, [128, 57]),
+    (200, 1024, 256, 5, 32, [32, 1, 17, 32, 24]),
     (64, 512, 512, 0, 0, None),
     (700, 256, 384, 0, 0, None),
 ]
@@ -132,3 +134,33 @@ def test_empty_batch_launches_nothing():
     y = lk.local_lora_linear(x, W)
     torch.cuda.synchronize()
     assert y.shape == (0, 64)
+
+
+@pytest.mark.parametrize("T", [16, 256, 257])
+def test_one_adapter_for_every_token(T):
+    # All tokens on one adapter: the shrink's token groups for that adapter
+    # span many MFMA column tiles, the others get no tokens.
+    say("lora_linear one adapter", T)
+    rng = np.random.default_rng(500 + T)
+    K, N = 512, 256
+    x, W, A, B, rk, _, scale = _inputs(rng, T, K, N, 3, 16)
+    idx = np.full(T, 1, np.int32)
+    scale = rng.uniform(-2, 2, size=T).astype(np.float32)
+    y = _run_gpu(x, W, A, B, rk, idx, scale)
+    ref = oracle.lora_linear(x, W, A, B, rk, idx, scale)
+    assert_rel(f64(y), ref, "y")
+
+
+def test_out_of_range_adapter_and_rank():
+    # Adapter indices outside [0, n_adapters) mean no adapter; ranks outside
+    # [0, r_max] are clamped.
+    say("lora_linear out of range")
+    rng = np.random.default_rng(606)
+    for T in (40, 300):
+        K, N = 512, 256
+        x, W, A, B, _, _, scale = _inputs(rng, T, K, N, 4, 16)
+        rk = np.array([-3, 40, 16, 7], np.int32)
+        idx = rng.integers(-5, 9, size=T).astype(np.int32)
+        y = _run_gpu(x, W, A, B, rk, idx, scale)
+        ref = oracle.lora_linear(x, W, A, B, rk, idx, scale)
+        assert_rel(f64(y), ref, "y T=%d" % T)

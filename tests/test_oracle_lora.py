@@ -141,3 +141,17 @@ def test_adapter_index_out_of_range_is_base():
     y = oracle.lora_linear(x, W, A, B, ranks, np.array([3, 7, -1], np.int32),
                            np.full(3, 2.0, np.float32))
     assert np.array_equal(y, oracle.lora_linear(x, W))
+
+
+def test_rank_outside_range_is_clamped():
+    # A negative rank acts as rank 0 (the base projection); a rank above r_max
+    # as r_max.
+    rng = np.random.default_rng(10)
+    x, W, A, B, _ = _setup(rng, T=5, K=64, N=16, n_ad=2, r_max=8)
+    idx = np.array([0, 1, 1, 0, 1], np.int32)
+    s = np.full(5, 1.5, np.float32)
+    y = oracle.lora_linear(x, W, A, B, np.array([-4, 99], np.int32), idx, s)
+    base = bits_to_f64(x) @ bits_to_f64(W).T
+    full = oracle.lora_linear(x, W, A, B, None, idx, s)
+    np.testing.assert_allclose(y[idx == 0], base[idx == 0], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(y[idx == 1], full[idx == 1], rtol=1e-12, atol=1e-12)
