@@ -2,35 +2,34 @@
 // adapter a = adapter_idx[t] (§2.2 "LoRA adapters": one frozen base shared by
 // many low-rank adapters, every request routed to its own adapter).
 //
-// Design, SGMV-style but on the matrix cores end to end:
-//  * Shrink. U_s[t, a*r_max + j] = bf16(s_t * x_t . A[a,j,:]) for the token's
-//    own adapter a and j < rank(a), 0 elsewhere. It is one product of x with
-//    all adapters' stacked A (rows a*r_max + j) whose epilogue keeps only the
-//    token's own adapter and rank: the per-token gather of adapters becomes a
-//    mask, at a cost of a few percent of the base product.
-//  * Fused base + expand. The delta is U_s Btilde^T with
-//    Btilde[n, a*r_max + j] = B[a, n, j], i.e. extra K-steps of the base
-//    product over the columns of U_s. A step over U_s columns runs only if an
-//    adapter it covers is used by a token of the tile, and only columns below
-//    each adapter's rank are loaded; the rest is a zero fill with no traffic.
-//  * Every tile is computed transposed, Y^T = W X^T: features are MFMA rows
-//    (A operand, rows of W), tokens are columns (B operand, rows of x), so a
-//    lane ends with 4 consecutive features of one token (an 8-byte store).
-//  * Two kernels for two regimes:
-//    - skinny (few tokens, or few features): decode projections are bound by
-//      streaming W once. A workgroup owns 16 features x up to 128 tokens and
-//      its 8 waves split K; each lane loads its MFMA operand slices straight
-//      from global memory several K-steps ahead (no LDS staging, no barrier
-//      in the main loop), and the 8 partial tiles are summed once through LDS
-//      in a fixed order. Also the shrink of a long prefill chunk.
-//    - SGMV shrink (decode sizes): one workgroup per adapter computes the
-//      shrink of the tokens routed to it on the matrix cores; each adapter's
-//      A is read once and no partial sums leave the workgroup.
-//    - tiled (many tokens and features): prefill projections are bound by the
-//      matrix cores. 128x128 tiles, 2x2 waves, register prefetch into an LDS
-//      double buffer with padded rows, XCD-aware grouped tile order so each
-//      XCD's L2 serves an 8x8 block of tiles.
-//  Both sum the base K-steps in an order that does not depend on which
+// Design, SGMV-style but on the matrix cores end to end. Every tile is
+// computed transposed, Y^T = W X^T: features are MFMA rows (A operand, rows
+// of W), tokens are columns (B operand, rows of x), so a lane ends with 4
+// consecutive features of one token.
+//
+//  * Decode sizes (T <= 256), three kernels, none waiting on another's
+//    workgroups:
+//    - SGMV shrink: workgroups per (K slice, adapter) gather the tokens routed
+//      to that adapter and compute x_t . A[a,j,:] for their slice of K on the
+//      matrix cores; fp32 partial sums per slice.
+//    - skinny base product, split over K: a workgroup owns 16*FN features x
+//      up to 128 tokens of one K slice and its 8 waves split the slice; each
+//      lane loads its MFMA operand slices straight from global memory (no LDS
+//      staging, no barrier in the loop) and the 8 partial tiles are summed
+//      once through LDS in a fixed order; fp32 partial sums per slice. Wider
+//      feature tiles for fewer tokens cut the re-reads of x.
+//    - epilogue: sums the base slices, forms U_s = bf16(s_t * u) for the
+//      token's own adapter and rank, adds U_s B_a^T and the residual, and
+//      rounds once to bf16.
+//  * Long prefill chunks: the shrink is one product of x with all adapters'
+//    stacked A whose epilogue keeps only the token's own adapter and rank,
+//    U_s[t, a*r_max + j] = bf16(s_t * x_t . A[a,j,:]); the main product runs
+//    the delta U_s Btilde^T (Btilde[n, a*r_max + j] = B[a, n, j]) as extra
+//    K-steps, only over adapters used in the tile and columns below their
+//    rank. 128x128 tiles, 2x2 waves, register prefetch into an LDS double
+//    buffer with padded rows, XCD-aware grouped tile order so each XCD's L2
+//    serves an 8x8 block of tiles.
+//  Both paths sum the base K-steps in an order that does not depend on which
 //  adapters are present, so a zero up-projection leaves y bit-identical.
 #include "common.hpp"
 
@@ -43,28 +42,27 @@ constexpr int kSkWaves = kSkThreads / kWave;
 constexpr int kBK = 64;
 constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
+constexpr int kRedTiles = 8;            // skinny kernel: tiles per LDS reduction round
 constexpr int kNumXcd = 8;
 
 #ifndef LOCAL_SK_U32
 #define LOCAL_SK_U32 4     // K-steps of 64 per batch of loads, 32-token tiles
 #endif
-#ifndef LOCAL_SK_FN32
-#define LOCAL_SK_FN32 1    // 16-feature tiles per workgroup at 32 tokens
-#endif
-#ifndef LOCAL_SK_FN64
-#define LOCAL_SK_FN64 1    // 16-feature tiles per workgroup at 64 tokens
-#endif
-#ifndef LOCAL_SK_FN128
-#define LOCAL_SK_FN128 1   // 16-feature tiles per workgroup at 128 tokens
-#endif
 
-enum GemmMode { kModeMain = 0, kModeShrink = 1 };
+enum GemmMode { kModeMain = 0, kModeShrink = 1, kModePartial = 2 };
 
 struct GemmArgs {
   const uint16_t* x;     // [T][K]
   const uint16_t* w;     // main: W [N][K]; shrink: stacked A [R][K]
   int64_t T, K, N;       // N = output width (R in shrink mode)
-  const uint16_t* us;    // U_s [T][R] (main mode, adapters present)
+  const uint16_t* us;    // U_s [T][R] bf16 (tiled main kernel, adapters present)
+  float* pout;           // SGMV shrink: fp32 partial sums [up_ks][T][r_max]
+  int up_ks;             // K slices of the shrink partial sums
+  float* part;           // partial mode: fp32 base partial sums [ksplit][T][N]
+  const uint16_t* amat;  // partial mode: stacked A [R][K], rows taken as extra tiles
+  int xrows;             // stacked-A rows per feature-tile workgroup (0 = none)
+  int p_stride;          // row length of the shrink partial sums (R or r_max)
+  int p_stacked;         // 1: shrink sums indexed by stacked row a*r_max + j
   const uint16_t* bmat;  // B [n_ad][N][r_max]
   const int32_t* ranks;  // [n_ad] or null
   const int32_t* idx;    // [T] or null
@@ -114,23 +112,26 @@ __device__ __forceinline__ void store4(const GemmArgs& a, int64_t t, int64_t n, 
       u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
 }
 
-// Marks the adapters used by tokens [t0, t0 + n_tok) and lists, in ascending
-// order, the chunks of `chunk` U_s columns that cover at least one of them.
-// Returns the number of chunks. All threads of the workgroup must call it.
+// Adapter of token t, or -1 (past the batch, no adapter, or out of range).
+__device__ __forceinline__ int token_adapter(const GemmArgs& a, int64_t t) {
+  if (t >= a.T) return -1;
+  const int ad = a.idx[t];
+  return (ad >= 0 && ad < a.n_ad) ? ad : -1;
+}
+
+// Marks the adapters my_ad of the calling threads (one token each, -1 for
+// none) and lists, in ascending order, the chunks of `chunk` U_s columns that
+// cover at least one of them. Returns the number of chunks. All threads of
+// the workgroup must call it.
 template <int THREADS>
-__device__ int lora_chunk_list(const GemmArgs& a, int64_t t0, int n_tok, int chunk,
-                               uint64_t* present, uint16_t* list, int* wave_cnt) {
+__device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t* present,
+                               uint16_t* list, int* wave_cnt) {
   constexpr int WAVES = THREADS / kWave;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   if (tid < 4) present[tid] = 0ull;
   __syncthreads();
-  for (int t = tid; t < n_tok; t += THREADS) {
-    if (t0 + t < a.T) {
-      const int ad = a.idx[t0 + t];
-      if (ad >= 0 && ad < a.n_ad)
-        atomicOr(reinterpret_cast<unsigned long long*>(&present[ad >> 6]), 1ull << (ad & 63));
-    }
-  }
+  if (my_ad >= 0)
+    atomicOr(reinterpret_cast<unsigned long long*>(&present[my_ad >> 6]), 1ull << (my_ad & 63));
   __syncthreads();
   const int chunks = (a.R + chunk - 1) / chunk;
   int n = 0;
@@ -179,43 +180,55 @@ __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* 
 }
 
 // ------------------------------------------------------------------ skinny
-// Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM); wave w takes
-// a contiguous range of the K/32 base steps (U steps per batch of loads) and
-// every 8th U_s chunk; partial tiles are summed through LDS in wave order.
+// Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM) over the
+// z-th of ksplit slices of K; wave w takes a contiguous range of the slice's
+// 64-wide steps (U steps per batch of loads); partial tiles are summed through
+// LDS in wave order. Partial mode writes the slice's fp32 sum (decode base
+// product, finished by the epilogue kernel); shrink mode applies the adapter
+// mask and scale and writes U_s in bf16 (shrink of a long prefill chunk).
 // An 8-wave workgroup runs two waves per SIMD; telling the compiler so lets it
 // keep a whole batch of loads in registers instead of interleaving each load
 // with the MFMA that consumes it (which leaves one load in flight per wave).
-template <int FN, int FM, int U>
-__global__ __launch_bounds__(kSkThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+#ifndef LOCAL_SK_WPE
+#define LOCAL_SK_WPE 2  // waves per SIMD the skinny kernel is compiled for
+#endif
+
+template <int FN, int FM, int U, int XT>
+__global__ __launch_bounds__(kSkThreads) __attribute__((amdgpu_waves_per_eu(LOCAL_SK_WPE, LOCAL_SK_WPE)))
 void lora_skinny_kernel(GemmArgs a) {
-  __shared__ uint64_t present[4];
-  __shared__ uint16_t chunks[kMaxLoraChunks];
-  __shared__ int wave_cnt[kSkWaves];
-  extern __shared__ f32x4 red[];  // [waves][FM][FN][64 lanes]
+  constexpr int FT = FN + XT;     // row tiles: FN of W, then XT of stacked A
+  extern __shared__ f32x4 red[];  // [waves][tiles of one round][64 lanes]
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
   const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16 * FN;
   const int64_t t0 = static_cast<int64_t>(blockIdx.y) * 16 * FM;
+  const int64_t x0 = static_cast<int64_t>(blockIdx.x) * a.xrows;  // first stacked-A row
 
-  int n_chunks = 0;
-  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr)
-    n_chunks = lora_chunk_list<kSkThreads>(a, t0, 16 * FM, 32, present, chunks, wave_cnt);
-
-  f32x4 acc[FN][FM];
+  f32x4 acc[FT][FM];
 #pragma unroll
-  for (int i = 0; i < FN; ++i)
+  for (int i = 0; i < FT; ++i)
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // this lane's rows: feature rows of W, token rows of x
-  const uint16_t* wrow[FN];
-  bool wok[FN];
+  // this lane's rows: feature rows of W, stacked-A rows (below the adapter's
+  // rank only), token rows of x
+  const uint16_t* wrow[FT];
+  bool wok[FT];
 #pragma unroll
   for (int i = 0; i < FN; ++i) {
     const int64_t n = n0 + 16 * i + col;
     wok[i] = n < a.N;
     wrow[i] = a.w + (wok[i] ? n : 0) * a.K;
+  }
+#pragma unroll
+  for (int e = 0; e < XT; ++e) {
+    const int rr = 16 * e + col;
+    const int64_t row = x0 + rr;
+    bool ok = rr < a.xrows && row < a.R;
+    if (ok) ok = static_cast<int>(row % a.r_max) < rank_of(a, static_cast<int>(row / a.r_max));
+    wok[FN + e] = ok;
+    wrow[FN + e] = a.amat + (ok ? row : 0) * a.K;
   }
   const uint16_t* xrow[FM];
   bool xok[FM];
@@ -247,12 +260,12 @@ void lora_skinny_kernel(GemmArgs a) {
   const int s_hi = z_lo + ((rw + 1) * (z_hi - z_lo)) / kSkWaves;
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
   for (int s = s_lo; s < s_hi; s += U) {
-    u32x4 wv[U][FN][2], xv[U][FM][2];
+    u32x4 wv[U][FT][2], xv[U][FM][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 64 + 16 * kgrp;
 #pragma unroll
-      for (int i = 0; i < FN; ++i) {
+      for (int i = 0; i < FT; ++i) {
         wv[u][i][0] = ld_global<u32x4>(wrow[i] + k);
         wv[u][i][1] = ld_global<u32x4>(wrow[i] + k + 8);
       }
@@ -268,155 +281,341 @@ void lora_skinny_kernel(GemmArgs a) {
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
 #pragma unroll
-        for (int i = 0; i < FN; ++i) wv[u][i][m] = (live && wok[i]) ? wv[u][i][m] : zero4;
+        for (int i = 0; i < FT; ++i) wv[u][i][m] = (live && wok[i]) ? wv[u][i][m] : zero4;
 #pragma unroll
         for (int j = 0; j < FM; ++j) xv[u][j][m] = (live && xok[j]) ? xv[u][j][m] : zero4;
 #pragma unroll
-        for (int i = 0; i < FN; ++i)
+        for (int i = 0; i < FT; ++i)
 #pragma unroll
           for (int j = 0; j < FM; ++j)
             acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i][m]), as_bf16x8(xv[u][j][m]), acc[i][j]);
       }
     }
   }
-  // adapter up-projection: chunks of 32 U_s columns, round-robin over waves
-  for (int q = wave; q < n_chunks; q += kSkWaves) {
-    const int c = chunks[q] * 32 + 8 * kgrp;
-    bf16x8 bv[FN], uv[FM];
+  // ---- sum the waves' partial tiles in wave order, then store; in rounds of
+  // at most kRedTiles tiles so that the LDS buffer stays within 64 KB
+  constexpr int NT = FM * FT;
+  constexpr int G = NT < kRedTiles ? NT : kRedTiles;
 #pragma unroll
-    for (int i = 0; i < FN; ++i) bv[i] = as_bf16x8(load_btilde(a, present, n0 + 16 * i + col, c));
+  for (int g0 = 0; g0 < NT; g0 += G) {
+    if (g0 > 0) __syncthreads();  // the previous round's reads are done
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      const int64_t t = t0 + 16 * j + col;
-      uv[j] = as_bf16x8((t < a.T && c < a.R) ? ld_global<u32x4>(a.us + t * a.R + c)
-                                              : u32x4{0u, 0u, 0u, 0u});
+    for (int j = 0; j < FM; ++j)
+#pragma unroll
+      for (int i = 0; i < FT; ++i) {
+        const int tl = j * FT + i;
+        if (tl >= g0 && tl < g0 + G) red[(wave * G + tl - g0) * kWave + lane] = acc[i][j];
+      }
+    __syncthreads();
+    for (int e = tid; e < G * kWave; e += kSkThreads) {
+      const int l = e % kWave, tl = g0 + e / kWave;
+      if (tl >= NT) continue;
+      const int i = tl % FT, j = tl / FT;
+      f32x4 s = red[e];
+      for (int w = 1; w < kSkWaves; ++w) s += red[w * G * kWave + e];
+      const int64_t t = t0 + 16 * j + l % 16;
+      if (i >= FN) {  // stacked-A rows: the shrink's partial sums of this slice
+        if (t >= a.T) continue;
+        const int rr = 16 * (i - FN) + 4 * (l / 16);
+        float* dst = a.pout + (static_cast<int64_t>(z) * a.T + t) * a.R + x0 + rr;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (rr + q < a.xrows && x0 + rr + q < a.R) dst[q] = s[q];
+        continue;
+      }
+      const int64_t n = n0 + 16 * i + 4 * (l / 16);
+      if (a.mode == kModePartial) {
+        if (t < a.T && n < a.N)
+          *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
+      } else {
+        store4(a, t, n, s);
+      }
     }
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-      for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(bv[i], uv[j], acc[i][j]);
-  }
-
-  // ---- sum the waves' partial tiles in wave order, then store
-#pragma unroll
-  for (int j = 0; j < FM; ++j)
-#pragma unroll
-    for (int i = 0; i < FN; ++i) red[((wave * FM + j) * FN + i) * kWave + lane] = acc[i][j];
-  __syncthreads();
-  for (int e = tid; e < FM * FN * kWave; e += kSkThreads) {
-    const int l = e % kWave, i = (e / kWave) % FN, j = e / (kWave * FN);
-    f32x4 s = red[e];
-    for (int w = 1; w < kSkWaves; ++w) s += red[w * FM * FN * kWave + e];
-    store4(a, t0 + 16 * j + l % 16, n0 + 16 * i + 4 * (l / 16), s);
   }
 }
 
 // ------------------------------------------------------------- SGMV shrink
-// Decode-size shrink, one workgroup per adapter a (segmented by adapter, as
-// in SGMV): the tokens routed to a are compacted (ascending) into groups of
-// 16 that become the columns of S^T = A_a X_g^T on the matrix cores, with the
-// adapter's rank rows as MFMA rows. The 16 waves split K, each issuing the
-// loads of U steps before their MFMAs, and their partial tiles are summed
-// through LDS in wave order. The workgroup owns U_s columns
-// [a*r_max, (a+1)*r_max) for every token: it first zero-fills them, then
-// writes bf16(s_t * u) for its tokens and rows below the rank, so every
-// adapter's A is read once and no partial sums leave the workgroup.
-constexpr int kSgThreads = 1024;
+// Decode-size shrink, segmented by adapter as in SGMV. Workgroup (z, a) takes
+// adapter a and the z-th of up_ks slices of K: the tokens routed to a are
+// compacted (ascending) into groups of 16 that become the columns of
+// S^T = A_a X_g^T on the matrix cores, with the adapter's rank rows as MFMA
+// rows. Each of the 4 waves holds at most U steps of 32 k, so it loads its
+// whole slice of A before it even knows the tokens; the waves' partial tiles
+// are summed through LDS in wave order. The result, the unscaled fp32 partial
+// sum of slice z, goes to P[z][t][j] for the adapter's tokens t and rows
+// j < rank; the main kernel sums the slices in order, scales and rounds.
+constexpr int kSgThreads = 256;
 constexpr int kSgWaves = kSgThreads / kWave;
-constexpr int kSgMaxTokens = 256;  // decode sizes only
+constexpr int kSgMaxTokens = 256;  // decode sizes only (one token per thread)
 constexpr int kSgMaxTiles = 8;     // r_max <= 128
+
+#ifndef LOCAL_SG_U1
+#define LOCAL_SG_U1 4  // K-steps of 32 per wave when r_max <= 16
+#endif
 
 template <int RT, int U>  // RT 16-row tiles of the rank dimension (r_max <= 16*RT)
 __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a) {
   __shared__ int toks[kSgMaxTokens];
   __shared__ int wave_cnt[kSgWaves];
-  __shared__ f32x4 red[kSgWaves][kWave];
-  const int ad = blockIdx.x;
+  __shared__ f32x4 red[kSgWaves][RT][kWave];
+  const int z = blockIdx.x, ad = blockIdx.y;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
   const int rk = rank_of(a, ad);
+  if (rk == 0) return;  // uniform: no row of this adapter is used
+  const int tiles = (rk + 15) / 16;
 
-  // zero-fill this adapter's column block for every token
-  uint16_t* ublk = a.y + static_cast<int64_t>(ad) * a.r_max;
-  for (int64_t e = tid; e < a.T * a.r_max; e += kSgThreads)
-    ublk[(e / a.r_max) * a.R + e % a.r_max] = 0;
+  // this wave's steps: [s_lo, s_hi) of 32 k, at most U of them
+  const int ksteps = static_cast<int>(a.K / 32);
+  const int z_lo = (z * ksteps) / a.up_ks, z_hi = ((z + 1) * ksteps) / a.up_ks;
+  const int s_lo = z_lo + (wave * (z_hi - z_lo)) / kSgWaves;
+  const int s_hi = z_lo + ((wave + 1) * (z_hi - z_lo)) / kSgWaves;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
 
-  // tokens routed to this adapter, ascending (T <= kSgMaxTokens <= threads)
-  const int t = tid;
-  const bool mine = t < a.T && a.idx[t] == ad;
+  // A: rank rows 16i + col of the slice, loaded first (rows past the rank
+  // read row 0 and are zeroed; steps past s_hi read a valid step and are
+  // dropped below)
+  const uint16_t* abase = a.w + static_cast<int64_t>(ad) * a.r_max * a.K + 8 * kgrp;
+  bool aok[RT];
+  u32x4 av[U][RT];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) aok[i] = 16 * i + col < rk;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t k = static_cast<int64_t>(max(min(s_lo + u, s_hi - 1), 0)) * 32;
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+      const int64_t row = aok[i] ? 16 * i + col : 0;
+      av[u][i] = i < tiles ? ld_global<u32x4>(abase + row * a.K + k) : zero4;
+    }
+  }
+
+  // tokens routed to this adapter, ascending
+  const bool mine = token_adapter(a, tid) == ad;
   const uint64_t m = __ballot(mine);
   if (lane == 0) wave_cnt[wave] = __popcll(m);
-  __syncthreads();  // also orders the zero-fill before the value writes below
+  __syncthreads();
   int off = 0, n_tok = 0;
   for (int w = 0; w < kSgWaves; ++w) {
     if (w < wave) off += wave_cnt[w];
     n_tok += wave_cnt[w];
   }
-  if (mine) toks[off + __popcll(m & ((1ull << lane) - 1ull))] = t;
+  if (mine) toks[off + __popcll(m & ((1ull << lane) - 1ull))] = tid;
   __syncthreads();
-  if (n_tok == 0 || rk == 0) return;  // uniform: nothing beyond the zero-fill
 
-  const int ksteps = static_cast<int>(a.K / 32);
-  const int s_lo = (wave * ksteps) / kSgWaves, s_hi = ((wave + 1) * ksteps) / kSgWaves;
-  const int tiles = (rk + 15) / 16;  // uniform: tiles past the rank are skipped
-  const uint16_t* abase = a.w + static_cast<int64_t>(ad) * a.r_max * a.K;
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  for (int g0 = 0; g0 < n_tok; g0 += 16) {
-    // this lane's operand rows: rank row (A) and token (B) of each tile
-    const uint16_t* arow[RT];
-    bool aok[RT];
 #pragma unroll
-    for (int i = 0; i < RT; ++i) {
-      const int j = 16 * i + col;
-      aok[i] = j < rk;
-      arow[i] = abase + static_cast<int64_t>(aok[i] ? j : 0) * a.K + 8 * kgrp;
-    }
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int i = 0; i < RT; ++i) av[u][i] = (aok[i] && s_lo + u < s_hi) ? av[u][i] : zero4;
+
+  float* pz = a.pout + static_cast<int64_t>(z) * a.T * a.r_max;
+  for (int g0 = 0; g0 < n_tok; g0 += 16) {
     const bool xok = g0 + col < n_tok;
     const uint16_t* xrow = a.x + static_cast<int64_t>(toks[xok ? g0 + col : g0]) * a.K + 8 * kgrp;
+    u32x4 xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      xv[u] = ld_global<u32x4>(xrow + static_cast<int64_t>(max(min(s_lo + u, s_hi - 1), 0)) * 32);
     f32x4 acc[RT];
 #pragma unroll
     for (int i = 0; i < RT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = s_lo; s0 < s_hi; s0 += U) {
-      // steps past s_hi reload the last step and use a zero token operand
-      u32x4 xv[U], av[U][RT];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t k = static_cast<int64_t>(min(s0 + u, s_hi - 1)) * 32;
-        xv[u] = ld_global<u32x4>(xrow + k);
+    for (int u = 0; u < U; ++u) {
+      const u32x4 xb = xok ? xv[u] : zero4;
 #pragma unroll
-        for (int i = 0; i < RT; ++i)
-          av[u][i] = i < tiles ? ld_global<u32x4>(arow[i] + k) : zero4;
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const u32x4 xb = (xok && s0 + u < s_hi) ? xv[u] : zero4;
-#pragma unroll
-        for (int i = 0; i < RT; ++i)
-          if (i < tiles)
-            acc[i] = mfma16x16x32(as_bf16x8(aok[i] ? av[u][i] : zero4), as_bf16x8(xb), acc[i]);
-      }
+      for (int i = 0; i < RT; ++i)
+        if (i < tiles) acc[i] = mfma16x16x32(as_bf16x8(av[u][i]), as_bf16x8(xb), acc[i]);
     }
-    const int slot = g0 + col;
-    const int tok = slot < n_tok ? toks[slot] : 0;
-    const float sc = slot < n_tok ? a.scale[tok] : 0.f;
 #pragma unroll
-    for (int i = 0; i < RT; ++i) {
-      if (i >= tiles) break;
-      red[wave][lane] = acc[i];
-      __syncthreads();
-      if (wave == 0) {
-        f32x4 v = red[0][lane];
-        for (int w = 1; w < kSgWaves; ++w) v += red[w][lane];
-        if (slot < n_tok) {
+    for (int i = 0; i < RT; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    for (int e = tid; e < tiles * kWave; e += kSgThreads) {
+      const int i = e / kWave, l = e % kWave;
+      f32x4 v = red[0][i][l];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int j = 16 * i + 4 * kgrp + q;  // rank row
-            if (j < rk) ublk[static_cast<int64_t>(tok) * a.R + j] = f32_to_bf16(sc * v[q]);
-          }
+      for (int w = 1; w < kSgWaves; ++w) v += red[w][i][l];
+      const int slot = g0 + l % 16;
+      const int j = 16 * i + 4 * (l / 16);  // first of 4 rank rows
+      if (slot < n_tok && j < rk) {
+        float* dst = pz + static_cast<int64_t>(toks[slot]) * a.r_max + j;
+        if (j + 4 <= rk) {
+          *reinterpret_cast<f32x4*>(dst) = v;
+        } else {
+          for (int q = 0; j + q < rk; ++q) dst[q] = v[q];
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
+  }
+}
+
+// Launch of the SGMV shrink: U steps per wave for the rank tiles, K cut into
+// enough slices that no wave has more than U steps.
+template <int RT, int U>
+local_status_t launch_sgmv_shrink(GemmArgs a, hipStream_t s) {
+  lora_sgmv_shrink_kernel<RT, U>
+      <<<dim3(static_cast<unsigned>(a.up_ks), static_cast<unsigned>(a.n_ad)), kSgThreads, 0, s>>>(a);
+  return local_check_launch("lora_linear (SGMV shrink)");
+}
+
+// Steps per wave of the SGMV shrink for a given r_max.
+int sgmv_steps_per_wave(int r_max) {
+  const int rt = (r_max + 15) / 16;
+  return rt <= 1 ? LOCAL_SG_U1 : rt <= 2 ? 8 : rt <= 4 ? 4 : 2;
+}
+
+// K slices of the SGMV shrink.
+int sgmv_slices(int64_t K, int r_max) {
+  const int64_t steps = K / 32;
+  const int64_t per = static_cast<int64_t>(kSgWaves) * sgmv_steps_per_wave(r_max);
+  return static_cast<int>((steps + per - 1) / per);
+}
+
+local_status_t run_sgmv_shrink(const GemmArgs& a, hipStream_t s) {
+  const int rt = (a.r_max + 15) / 16;
+  const int u = sgmv_steps_per_wave(a.r_max);
+  if (rt <= 1 && u == 4) return launch_sgmv_shrink<1, 4>(a, s);
+  if (rt <= 1) return launch_sgmv_shrink<1, 8>(a, s);
+  if (rt <= 2) return launch_sgmv_shrink<2, 8>(a, s);
+  if (rt <= 4) return launch_sgmv_shrink<4, 4>(a, s);
+  return launch_sgmv_shrink<kSgMaxTiles, 2>(a, s);
+}
+
+// --------------------------------------------------------------- epilogue
+// Decode sizes, after the base partial sums and the shrink:
+//   y[t, n] = bf16( sum_z part[z][t][n] + sum_j U_s[t][j] B[a_t][n][j] + res[t][n] )
+// with U_s[t][j] = bf16(s_t * sum_z P[z][t][c]) for j < rank(a_t), both sums
+// in slice order; c = a_t*r_max + j when the shrink ran fused with the base
+// product (sums for every stacked row), c = j after the SGMV shrink. Workgroup: 16 tokens x 64 features; U_s of its tokens is
+// built once in LDS, then each thread finishes 4 consecutive features of one
+// token (16-byte partial loads, an 8-byte store).
+constexpr int kEpThreads = 256;
+constexpr int kEpTokens = 16;
+constexpr int kEpFeatures = 64;
+
+template <int KSB>
+__global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
+  __shared__ float us[kEpTokens][128 + 1];
+  const int tid = threadIdx.x;
+  const int tt = tid / (kEpFeatures / 4), ng = tid % (kEpFeatures / 4);
+  const int64_t t0 = static_cast<int64_t>(blockIdx.y) * kEpTokens;
+  const int64_t t = t0 + tt, n = static_cast<int64_t>(blockIdx.x) * kEpFeatures + 4 * ng;
+  const bool live = t < a.T && n < a.N;
+  const bool lora = a.n_ad > 0;  // uniform
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+
+  // Every load that needs no other load's result is issued first: the base
+  // slices, the residual, this token's adapter; then, needing only the
+  // adapter, the first 32 rank columns of its B rows and the shrink slices.
+  f32x4 pv[KSB];
+#pragma unroll
+  for (int z = 0; z < KSB; ++z)
+    pv[z] = live ? ld_global<f32x4>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n)
+                 : f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x2 rv = {0u, 0u};
+  if (live && a.res) rv = ld_global<u32x2>(a.res + t * a.N + n);
+  const int my_ad = (lora && live) ? token_adapter(a, t) : -1;
+  const uint16_t* brow =
+      a.bmat + (static_cast<int64_t>(my_ad >= 0 ? my_ad : 0) * a.N + n) * a.r_max;
+  u32x4 bv[4][4];  // [8-column step][feature]
+  if (my_ad >= 0) {
+#pragma unroll
+    for (int js = 0; js < 4; ++js)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        bv[js][i] = 8 * js < a.r_max ? ld_global<u32x4>(brow + i * a.r_max + 8 * js) : zero4;
+  }
+
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int z = 0; z < KSB; ++z) acc += pv[z];
+
+  if (lora) {
+    // U_s of the tile's tokens, 4 rank rows per item: bf16(s_t * u), u the
+    // sum of the shrink slices in slice order (batches of 8 loads)
+    const int quads = a.r_max / 4;
+    const int64_t slice = a.T * a.p_stride;
+    for (int e = tid; e < kEpTokens * quads; e += kEpThreads) {
+      const int et = e / quads, j = 4 * (e % quads);
+      const int ad = token_adapter(a, t0 + et);
+      f32x4 u = {0.f, 0.f, 0.f, 0.f};
+      if (ad >= 0) {
+        const float sc = a.scale[t0 + et];
+        const int rk = rank_of(a, ad);
+        const float* p =
+            a.pout + (t0 + et) * a.p_stride + (a.p_stacked ? ad * a.r_max : 0) + j;
+        for (int z0 = 0; z0 < a.up_ks; z0 += 8) {
+          f32x4 sv[8];
+#pragma unroll
+          for (int zz = 0; zz < 8; ++zz)
+            sv[zz] = z0 + zz < a.up_ks ? ld_global<f32x4>(p + (z0 + zz) * slice)
+                                       : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int zz = 0; zz < 8; ++zz) u += sv[zz];
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)  // rows at or past the rank are never written
+          u[q] = j + q < rk ? bf16_to_f32(f32_to_bf16(sc * u[q])) : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) us[et][j + q] = u[q];
+    }
+    __syncthreads();
+    if (my_ad >= 0) {
+      // delta of 4 features over the rank columns, 32 at a time
+      const int rk = rank_of(a, my_ad);
+      for (int j0 = 0; j0 < rk; j0 += 32) {
+        if (j0 > 0) {
+#pragma unroll
+          for (int js = 0; js < 4; ++js)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              bv[js][i] = j0 + 8 * js < rk ? ld_global<u32x4>(brow + i * a.r_max + j0 + 8 * js)
+                                           : zero4;
+        }
+#pragma unroll
+        for (int js = 0; js < 4; ++js)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int j = j0 + 8 * js + e;
+            if (j < rk) {  // columns at or past the rank are never used
+              const float u = us[tt][j];
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const uint32_t w = bv[js][i][e / 2];
+                acc[i] += u * __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+              }
+            }
+          }
+      }
+    }
+  }
+  if (!live) return;
+  if (a.res) {
+    acc[0] += __uint_as_float(rv.x << 16);
+    acc[1] += __uint_as_float(rv.x & 0xffff0000u);
+    acc[2] += __uint_as_float(rv.y << 16);
+    acc[3] += __uint_as_float(rv.y & 0xffff0000u);
+  }
+  *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
+      u32x2{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+}
+
+template <int KSB>
+local_status_t launch_epilogue(const GemmArgs& a, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>((a.N + kEpFeatures - 1) / kEpFeatures),
+            static_cast<unsigned>((a.T + kEpTokens - 1) / kEpTokens));
+  lora_epilogue_kernel<KSB><<<grid, kEpThreads, 0, s>>>(a);
+  return local_check_launch("lora_linear (epilogue)");
+}
+
+local_status_t run_epilogue(const GemmArgs& a, hipStream_t s) {
+  switch (a.ksplit) {
+    case 1: return launch_epilogue<1>(a, s);
+    case 2: return launch_epilogue<2>(a, s);
+    case 4: return launch_epilogue<4>(a, s);
+    case 8: return launch_epilogue<8>(a, s);
+    default: return launch_epilogue<16>(a, s);
   }
 }
 
@@ -463,8 +662,11 @@ __global__ __launch_bounds__(kGemmThreads) void lora_tiled_kernel(GemmArgs a) {
   const int64_t n0 = static_cast<int64_t>(nt) * BN;
 
   int n_chunks = 0;
-  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr)
-    n_chunks = lora_chunk_list<kGemmThreads>(a, m0, BM, kBK, present, chunks, wave_cnt);
+  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr) {
+    static_assert(BM <= kGemmThreads, "one token per thread");
+    const int my_ad = tid < BM ? token_adapter(a, m0 + tid) : -1;
+    n_chunks = lora_chunk_list<kGemmThreads>(a, my_ad, kBK, present, chunks, wave_cnt);
+  }
   const int k_main = static_cast<int>(a.K / kBK);
   const int s_end = k_main + n_chunks;
 
@@ -584,33 +786,102 @@ local_status_t launch_tiled(GemmArgs a, hipStream_t s) {
   return local_check_launch("lora_linear (tiled)");
 }
 
-template <int FN, int FM, int U>
+template <int FN, int FM, int U, int XT = 0>
 local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
-  const size_t lds = static_cast<size_t>(kSkWaves) * FM * FN * kWave * sizeof(f32x4);
+  constexpr int NT = FM * (FN + XT);
+  const size_t lds = static_cast<size_t>(kSkWaves) * (NT < kRedTiles ? NT : kRedTiles) * kWave *
+                     sizeof(f32x4);
   static bool done = false;
-  raise_lds_limit(lora_skinny_kernel<FN, FM, U>, lds, done);
+  raise_lds_limit(lora_skinny_kernel<FN, FM, U, XT>, lds, done);
   dim3 grid(static_cast<unsigned>((a.N + 16 * FN - 1) / (16 * FN)),
             static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)),
             static_cast<unsigned>(a.ksplit));
-  lora_skinny_kernel<FN, FM, U><<<grid, kSkThreads, lds, s>>>(a);
+  lora_skinny_kernel<FN, FM, U, XT><<<grid, kSkThreads, lds, s>>>(a);
   return local_check_launch("lora_linear (skinny)");
 }
 
 template <int FN, int FM, int U>
 local_status_t launch_skinny_tiles(GemmArgs a, hipStream_t s) {
   a.ksplit = 1;
-  return launch_skinny<FN, FM, U>(a, s);
+  a.xrows = 0;
+  return launch_skinny<FN, FM, U, 0>(a, s);
 }
 
+// Long prefill chunks (T > 256): the tiled kernel for the fused main product,
+// the skinny kernel for the shrink.
 local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.mode == kModeMain && a.T > 256) return launch_tiled<128, 128, 2, 2>(a, s);
-  // skinny: one token tile of <= 128 rows for decode; 32-row tiles when a
-  // shrink covers many tokens, so that enough workgroups run
-  if (a.T <= 16) return launch_skinny_tiles<1, 1, 4>(a, s);
-  if (a.mode == kModeShrink && a.T > 128) return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
-  if (a.T <= 32) return launch_skinny_tiles<LOCAL_SK_FN32, 2, LOCAL_SK_U32>(a, s);
-  if (a.T <= 64) return launch_skinny_tiles<LOCAL_SK_FN64, 4, 2>(a, s);
-  return launch_skinny_tiles<LOCAL_SK_FN128, 8, 2>(a, s);
+  if (a.mode == kModeMain) return launch_tiled<128, 128, 2, 2>(a, s);
+  return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
+}
+
+// Decode sizes (T <= 256): base partial sums over K slices. Wider feature
+// tiles for fewer tokens cut the re-reads of x (every workgroup of a slice
+// reads the slice of x for all its tokens).
+#ifndef LOCAL_P_FN16
+#define LOCAL_P_FN16 4
+#endif
+#ifndef LOCAL_P_FN32
+#define LOCAL_P_FN32 4
+#endif
+#ifndef LOCAL_P_FN64
+#define LOCAL_P_FN64 4
+#endif
+#ifndef LOCAL_P_FN128
+#define LOCAL_P_FN128 2
+#endif
+#ifndef LOCAL_P_TARGET_WG
+#define LOCAL_P_TARGET_WG 256  // aim: about one workgroup per compute unit
+#endif
+
+// Feature tiles (of 16) per workgroup of the decode base product.
+int partial_fn(int64_t T) {
+  return T <= 16 ? LOCAL_P_FN16 : T <= 32 ? LOCAL_P_FN32 : T <= 64 ? LOCAL_P_FN64 : LOCAL_P_FN128;
+}
+
+// K slices of the decode base product: the power of two (at most 8 and at
+// most the number of 64-wide K steps) that brings the grid closest to
+// LOCAL_P_TARGET_WG workgroups from below.
+int partial_slices(int64_t T, int64_t N, int64_t K) {
+  const int64_t fm = T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8;
+  const int64_t tiles = ((N + 16 * partial_fn(T) - 1) / (16 * partial_fn(T))) *
+                        ((T + 16 * fm - 1) / (16 * fm));
+  int ks = 1;
+  while (ks < 8 && tiles * ks * 2 <= LOCAL_P_TARGET_WG && ks * 2 <= K / 64) ks *= 2;
+  return ks;
+}
+
+#ifndef LOCAL_P_U
+#define LOCAL_P_U 2  // 64-wide K steps per batch of loads
+#endif
+
+// Batches of one step where the operand registers of two would not fit (the
+// load batching does not change the order of the MFMA accumulation).
+template <int XT>
+local_status_t run_partial_xt(const GemmArgs& a, hipStream_t s) {
+  if (a.T <= 16) return launch_skinny<LOCAL_P_FN16, 1, LOCAL_P_U, XT>(a, s);
+  if (a.T <= 32) return launch_skinny<LOCAL_P_FN32, 2, LOCAL_P_U, XT>(a, s);
+  if (a.T <= 64) return launch_skinny<LOCAL_P_FN64, 4, (XT >= 4 ? 1 : LOCAL_P_U), XT>(a, s);
+  if constexpr (XT <= 2) return launch_skinny<LOCAL_P_FN128, 8, (XT >= 1 ? 1 : LOCAL_P_U), XT>(a, s);
+  return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d extra row tiles above 64 tokens", XT);
+}
+
+// Stacked-A rows each feature-tile workgroup takes with the base product
+// (the shrink fused into it), or 0 when that would take more than 4 extra
+// row tiles (2 above 64 tokens, where the accumulators of more would not fit
+// in registers); then the SGMV shrink runs as its own kernel.
+int partial_xrows(int64_t T, int64_t N, int R) {
+  if (R == 0) return 0;
+  const int64_t tiles = (N + 16 * partial_fn(T) - 1) / (16 * partial_fn(T));
+  const int64_t rows = (R + tiles - 1) / tiles;
+  return rows <= (T <= 64 ? 64 : 32) ? static_cast<int>(rows) : 0;
+}
+
+local_status_t run_partial(const GemmArgs& a, hipStream_t s) {
+  if (a.xrows == 0) return run_partial_xt<0>(a, s);
+  if (a.xrows <= 16) return run_partial_xt<1>(a, s);
+  if (a.xrows <= 32) return run_partial_xt<2>(a, s);
+  if (a.T <= 64) return run_partial_xt<4>(a, s);
+  return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d stacked rows per tile", a.xrows);
 }
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -636,8 +907,21 @@ extern "C" local_status_t local_lora_linear(
                       "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
                       (long long)K, (long long)N, n_adapters, r_max);
   const int R = n_adapters > 0 ? n_adapters * r_max : 0;
-  // workspace: U_s [T][R] bf16
-  const size_t need = align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
+  // Workspace. Decode sizes (T <= kSgMaxTokens): the base partial sums
+  // [ksb][T][N] fp32, then the shrink's partial sums: [ksb][T][R] fp32 when
+  // the shrink runs inside the base product, [slices][T][r_max] after the
+  // SGMV shrink. Above: U_s [T][R] bf16.
+  const bool decode = T <= kSgMaxTokens;
+  const int ksb = decode ? partial_slices(T, N, K) : 0;
+  const int xrows = decode ? partial_xrows(T, N, R) : 0;
+  const bool fused = xrows > 0;
+  const int slices = n_adapters > 0 && decode && !fused ? sgmv_slices(K, r_max) : 0;
+  const size_t part_bytes = decode ? align256(static_cast<size_t>(ksb) * T * N * sizeof(float)) : 0;
+  const size_t shrink_bytes =
+      fused ? align256(static_cast<size_t>(ksb) * T * R * sizeof(float))
+            : align256(static_cast<size_t>(slices) * T * r_max * sizeof(float));
+  const size_t need = decode ? part_bytes + shrink_bytes
+                             : align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -649,51 +933,63 @@ extern "C" local_status_t local_lora_linear(
   if (n_adapters > 0 && (!A || !B || !adapter_idx || !scale))
     return local_fail(LOCAL_ERR_NULL, "lora_linear: NULL adapter argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
 
-  if (n_adapters > 0) {
-    GemmArgs sh{};
-    sh.x = x;
+  GemmArgs g{};
+  g.x = x;
+  g.T = T;
+  g.K = K;
+  g.idx = adapter_idx;
+  g.scale = scale;
+  g.ranks = ranks;
+  g.n_ad = n_adapters;
+  g.r_max = r_max;
+  g.R = R;
+  g.bmat = B;
+  local_status_t st;
+
+  if (decode) {
+    float* part = static_cast<float*>(ws);
+    float* sp = reinterpret_cast<float*>(static_cast<char*>(ws) + part_bytes);
+    if (n_adapters > 0 && !fused) {  // SGMV shrink: partial sums per K slice
+      GemmArgs sh = g;
+      sh.w = A;
+      sh.N = R;
+      sh.mode = kModeShrink;
+      sh.pout = sp;
+      sh.up_ks = slices;
+      if ((st = run_sgmv_shrink(sh, s)) != LOCAL_OK) return st;
+    }
+    GemmArgs m = g;  // base product (+ fused shrink): partial sums per K slice
+    m.w = W;
+    m.N = N;
+    m.mode = kModePartial;
+    m.part = part;
+    m.ksplit = ksb;
+    m.amat = A;
+    m.xrows = xrows;
+    m.pout = sp;
+    if ((st = run_partial(m, s)) != LOCAL_OK) return st;
+    m.up_ks = fused ? ksb : slices;  // epilogue: sums, up-projection, residual
+    m.p_stride = fused ? R : r_max;
+    m.p_stacked = fused ? 1 : 0;
+    m.res = residual;
+    m.y = y;
+    return run_epilogue(m, s);
+  }
+
+  uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
+  if (n_adapters > 0) {  // shrink into U_s (mask and scale in its epilogue)
+    GemmArgs sh = g;
     sh.w = A;  // [n_ad][r_max][K] == [R][K]
-    sh.T = T;
-    sh.K = K;
     sh.N = R;
-    sh.idx = adapter_idx;
-    sh.scale = scale;
-    sh.ranks = ranks;
-    sh.n_ad = n_adapters;
-    sh.r_max = r_max;
-    sh.R = R;
     sh.y = us;
     sh.mode = kModeShrink;
-    local_status_t st;
-    if (T <= kSgMaxTokens) {  // decode sizes: one workgroup per adapter
-      const int rt = (r_max + 15) / 16;
-      const unsigned g = static_cast<unsigned>(n_adapters);
-      if (rt <= 1) lora_sgmv_shrink_kernel<1, 8><<<g, kSgThreads, 0, s>>>(sh);
-      else if (rt <= 2) lora_sgmv_shrink_kernel<2, 4><<<g, kSgThreads, 0, s>>>(sh);
-      else if (rt <= 4) lora_sgmv_shrink_kernel<4, 2><<<g, kSgThreads, 0, s>>>(sh);
-      else lora_sgmv_shrink_kernel<kSgMaxTiles, 1><<<g, kSgThreads, 0, s>>>(sh);
-      st = local_check_launch("lora_linear (SGMV shrink)");
-    } else {
-      st = run_gemm(sh, s);
-    }
-    if (st != LOCAL_OK) return st;
+    if ((st = run_gemm(sh, s)) != LOCAL_OK) return st;
   }
-  GemmArgs m{};
-  m.x = x;
+  GemmArgs m = g;
   m.w = W;
-  m.T = T;
-  m.K = K;
   m.N = N;
   m.us = us;
-  m.bmat = B;
-  m.ranks = ranks;
-  m.idx = adapter_idx;
-  m.scale = scale;
-  m.n_ad = n_adapters;
-  m.r_max = r_max;
-  m.R = R;
   m.res = residual;
   m.y = y;
   m.mode = kModeMain;

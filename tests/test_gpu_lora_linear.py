@@ -59,6 +59,11 @@ CASES = [
     (1000, 256, 512, 4, 16, None),
     (256, 512, 256, 2, 128, [128, 57]),
     (200, 1024, 256, 5, 32, [32, 1, 17, 32, 24]),
+    (40, 4160, 256, 5, 16, None),
+    (64, 4096, 512, 16, 64, [8, 16, 32, 64] * 4),
+    (24, 2048, 256, 2, 128, [128, 100]),
+    (128, 512, 256, 16, 32, [32, 8, 24, 16] * 4),
+    (16, 512, 64, 8, 16, None),
     (64, 512, 512, 0, 0, None),
     (700, 256, 384, 0, 0, None),
 ]

@@ -52,9 +52,19 @@ def test_lora_linear_workspace_and_errors(lib):
     # sizes only: T=32, K=N=4096, 8 adapters of rank 16
     st, n = _size(f, FAKE, 32, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
     assert st == OK
-    assert n == 32 * 128 * 2                       # U_s: T x n_adapters*r_max bf16
+    # decode sizes: fp32 base partial sums (4 K slices x T x N), then the
+    # shrink's, fused into the base product (4 K slices x T x n_adapters*r_max)
+    assert n == 4 * 32 * 4096 * 4 + 4 * 32 * 128 * 4
+    # a shrink too wide to fuse (N = 64: one feature tile, 8 base K slices)
+    # runs on its own:
+    # 8 K slices x T x r_max
+    st, n2 = _size(f, FAKE, 32, 4096, FAKE, 64, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
+    assert st == OK and n2 == 8 * 32 * 64 * 4 + 8 * 32 * 16 * 4
+    # above 256 tokens: U_s, T x n_adapters*r_max bf16
+    st, n1 = _size(f, FAKE, 300, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
+    assert st == OK and n1 == 300 * 128 * 2
     st, n0 = _size(f, FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)
-    assert st == OK and n0 < n
+    assert st == OK and n0 == 4 * 32 * 4096 * 4
     assert _size(f, FAKE, 32, 100, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_UNSUPPORTED
     assert _size(f, FAKE, 32, 4096, FAKE, 4096, FAKE, FAKE, 8, 12, None, FAKE, FAKE, None, FAKE)[0] == ERR_UNSUPPORTED
     assert _size(f, FAKE, -1, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_SHAPE
