@@ -93,6 +93,19 @@ __device__ __forceinline__ u32x2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t by
   return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(byte_off), 0, 0);
 }
 
+// Streaming (non-temporal) variants for data read once per call, such as the
+// KV blocks of decode attention: the loads carry the nt cache policy, which
+// on gfx950 lets a pure read stream reach about 7 TB/s instead of about 6.3.
+constexpr int kCacheStream = 2;  // cache-policy operand: nt
+
+__device__ __forceinline__ u32x4 buf_load16_stream(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(byte_off), 0, kCacheStream);
+}
+
+__device__ __forceinline__ u32x2 buf_load8_stream(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(byte_off), 0, kCacheStream);
+}
+
 // ---------------------------------------------------------------- math
 __device__ __forceinline__ float fast_exp2(float x) {
   return __builtin_amdgcn_exp2f(x);

@@ -191,10 +191,10 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a) {
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(a.k_cache + tile, live ? kTileBytes : 0u);
     const __amdgpu_buffer_rsrc_t rv2 = make_rsrc(a.v_cache + tile, live ? kTileBytes : 0u);
 #pragma unroll
-    for (int c = 0; c < KC; ++c) R.k[c] = buf_load16(rk, (c * 512 + lane * 8) * 2);
+    for (int c = 0; c < KC; ++c) R.k[c] = buf_load16_stream(rk, (c * 512 + lane * 8) * 2);
 #pragma unroll
     for (int t = 0; t < VT; ++t)
-      R.v[t] = buf_load8(rv2, ((16 * t + col) * kBlockSize + 4 * kgrp) * 2);
+      R.v[t] = buf_load8_stream(rv2, ((16 * t + col) * kBlockSize + 4 * kgrp) * 2);
   };
   auto compute_block = [&](BlockRegs<D>& R, int i) {
     const int j = j0 + i;
