@@ -145,9 +145,8 @@ def main():
         st = sets[i % len(sets)][0]
         st.version_check()
         lc = st.layer_calls[0]
-        lc["q"]()
-        lc["k"]()
-        lc["v"]()
+        for c in lc["in"]:
+            c()
         ev_a[i].record(stream)
         lc["attn"]()
         ev_b[i].record(stream)

@@ -144,6 +144,37 @@ local_status_t local_lora_linear(
     void* ws, size_t* ws_bytes, void* stream);
 
 /*
+ * local_lora_linear_grouped — G (1..4) mixed-adapter LoRA projections of the
+ * same activations, e.g. the q, k and v projections of a layer (§2.2 "LoRA
+ * adapters"): for every g, y[g] equals what local_lora_linear computes from
+ * (x, W[g], N[g], A[g], B[g], n_adapters, r_max, ranks[g], adapter_idx,
+ * scale) with no residual, up to float32 summation order.
+ *
+ *   W, N, A, B, ranks, y   HOST arrays of G entries: device pointers (or, for
+ *                          N, the sizes) of each projection, with the layouts
+ *                          of local_lora_linear. A, B and ranks may be NULL
+ *                          when n_adapters = 0; ranks or an entry of it may be
+ *                          NULL (every rank = r_max). The arrays are read
+ *                          during the call only.
+ *
+ *  All projections share x, T, K, adapter_idx, scale, n_adapters and r_max;
+ *  sizes as for local_lora_linear, for every N[g]. At decode sizes (T <= 256)
+ *  the projections run as one virtual weight of sum N[g] rows, so one pass
+ *  of launches serves all of them; above, they run one after another.
+ *  Errors as for local_lora_linear; LOCAL_ERR_UNSUPPORTED for G outside 1..4,
+ *  LOCAL_ERR_NULL for a NULL array.
+ */
+local_status_t local_lora_linear_grouped(
+    const uint16_t* x, int64_t T, int64_t K, int32_t G,
+    const uint16_t* const* W, const int64_t* N,
+    const uint16_t* const* A, const uint16_t* const* B,
+    int32_t n_adapters, int32_t r_max,
+    const int32_t* const* ranks,
+    const int32_t* adapter_idx, const float* scale,
+    uint16_t* const* y,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
  * local_paged_attn_decode — one new token per request attends over its paged
  * KV cache with the per-block version mask (§2.2 "KV cache and prefix
  * caching"; §5.1 validity key; stale coverage is rejected, never reused).

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "liblocal.so")
 BLOCK_SIZE = 16
 
 EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
-           "local_paged_attn_decode", "local_paged_attn_prefill",
+           "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
            "local_block_version_check")
 
 _STATUS = {0: "LOCAL_OK", 1: "LOCAL_ERR_NULL", 2: "LOCAL_ERR_SHAPE",
@@ -56,6 +56,9 @@ def load_library(path: str = LIB_PATH):
     lib.local_lora_linear.restype = ctypes.c_int
     lib.local_lora_linear.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
                                       P, SZ, P]
+    lib.local_lora_linear_grouped.restype = ctypes.c_int
+    lib.local_lora_linear_grouped.argtypes = [P, i64, i64, i32, P, P, P, P, i32, i32, P, P, P,
+                                              P, P, SZ, P]
     lib.local_paged_attn_decode.restype = ctypes.c_int
     lib.local_paged_attn_decode.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64, i32, P,
                                             i32, P, P, P, f32, P, P, P, SZ, P]
@@ -191,6 +194,77 @@ def prepare_lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scal
 def local_lora_linear(*args, **kwargs):
     """y = residual + x W^T + scale_t (x A_a^T) B_a^T per token (bf16 in and out)."""
     return prepare_lora_linear(*args, **kwargs)()
+
+
+def _ptr_array(ts):
+    """A host array of device pointers (NULL for None)."""
+    arr = (ctypes.c_void_p * len(ts))(*[t.data_ptr() if t is not None else None for t in ts])
+    return arr, ctypes.cast(arr, ctypes.c_void_p)
+
+
+def prepare_lora_linear_grouped(x, Ws, As=None, Bs=None, ranks=None, adapter_idx=None,
+                                scale=None, outs=None,
+                                workspace: Optional[Workspace] = None) -> Call:
+    """Prepared y_g = x W_g^T + scale_t (x A_g,a^T) B_g,a^T for up to 4 projections g that
+    share x and the adapter routing (one adapter set shape for all of them)."""
+    lib = load_library()
+    _req(x, "x", torch.bfloat16, 2)
+    T, K = x.shape
+    G = len(Ws)
+    if not 1 <= G <= 4:
+        raise ValueError("1 to 4 projections, got %d" % G)
+    for W in Ws:
+        _req(W, "W", torch.bfloat16, 2)
+        if W.shape[1] != K:
+            raise ValueError("every W must be [N, K=%d], got %s" % (K, tuple(W.shape)))
+    Ns = [W.shape[0] for W in Ws]
+    n_ad, r_max = 0, 0
+    if As is not None:
+        if len(As) != G or len(Bs) != G:
+            raise ValueError("one A and one B per projection")
+        n_ad, r_max = As[0].shape[0], As[0].shape[1]
+        for A, B, N in zip(As, Bs, Ns):
+            _req(A, "A", torch.bfloat16, 3)
+            _req(B, "B", torch.bfloat16, 3)
+            if tuple(A.shape) != (n_ad, r_max, K) or tuple(B.shape) != (n_ad, N, r_max):
+                raise ValueError("A must be [n_ad, r_max, K] and B [n_ad, N, r_max], with one "
+                                 "n_ad and r_max for every projection")
+        _req(adapter_idx, "adapter_idx", torch.int32, 1)
+        _req(scale, "scale", torch.float32, 1)
+        if adapter_idx.shape[0] != T or scale.shape[0] != T:
+            raise ValueError("adapter_idx and scale must have T=%d entries" % T)
+        if ranks is not None:
+            if len(ranks) != G:
+                raise ValueError("one ranks tensor (or None) per projection")
+            for r in ranks:
+                if r is not None:
+                    _req(r, "ranks", torch.int32, 1)
+                    if r.shape[0] != n_ad:
+                        raise ValueError("ranks must have n_adapters entries")
+    if outs is None:
+        outs = [torch.empty((T, N), dtype=torch.bfloat16, device=x.device) for N in Ns]
+    for o, N in zip(outs, Ns):
+        _req(o, "out", torch.bfloat16, 2)
+        if tuple(o.shape) != (T, N):
+            raise ValueError("each out must be [T, N_g]")
+    w_arr, w_p = _ptr_array(Ws)
+    n_arr = (ctypes.c_int64 * G)(*Ns)
+    a_arr, a_p = _ptr_array(As) if As is not None else (None, None)
+    b_arr, b_p = _ptr_array(Bs) if Bs is not None else (None, None)
+    r_arr, r_p = _ptr_array(ranks) if ranks is not None else (None, None)
+    y_arr, y_p = _ptr_array(outs)
+    args = [_ptr(x), T, K, G, w_p, ctypes.cast(n_arr, ctypes.c_void_p), a_p, b_p, n_ad, r_max,
+            r_p, _ptr(adapter_idx), _ptr(scale), y_p]
+    keep = (x, adapter_idx, scale, w_arr, n_arr, a_arr, b_arr, r_arr, y_arr) + tuple(Ws) + \
+        tuple(As or ()) + tuple(Bs or ()) + tuple(ranks or ()) + tuple(outs)
+    c = Call(lib.local_lora_linear_grouped, args, workspace, x.device, keep=keep)
+    c.outputs = tuple(outs)
+    return c
+
+
+def local_lora_linear_grouped(*args, **kwargs):
+    """Outputs of up to 4 LoRA projections of one x (see prepare_lora_linear_grouped)."""
+    return prepare_lora_linear_grouped(*args, **kwargs)()
 
 
 def _pool_checks(k_cache, v_cache, Hkv, D):

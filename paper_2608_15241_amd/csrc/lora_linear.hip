@@ -43,6 +43,7 @@ constexpr int kBK = 64;
 constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kRedTiles = 8;            // skinny kernel: tiles per LDS reduction round
+constexpr int kMaxGroup = 4;            // projections sharing x in one grouped call
 constexpr int kNumXcd = 8;
 
 #ifndef LOCAL_SK_U32
@@ -59,8 +60,19 @@ struct GemmArgs {
   float* pout;           // SGMV shrink: fp32 partial sums [up_ks][T][r_max]
   int up_ks;             // K slices of the shrink partial sums
   float* part;           // partial mode: fp32 base partial sums [ksplit][T][N]
-  const uint16_t* amat;  // partial mode: stacked A [R][K], rows taken as extra tiles
   int xrows;             // stacked-A rows per feature-tile workgroup (0 = none)
+  // Skinny kernel and epilogue: G projections that share x, taken as one
+  // virtual weight whose rows [gstart[g], gstart[g+1]) are the rows of W_g
+  // (N = gstart[G]); their stacked A rows are likewise concatenated, R rows
+  // per projection.
+  int G;
+  int64_t gstart[kMaxGroup + 1];
+  const uint16_t* gw[kMaxGroup];     // W_g [N_g][K] (skinny shrink mode: stacked A)
+  const uint16_t* ga[kMaxGroup];     // A_g [n_ad][r_max][K]
+  const uint16_t* gb[kMaxGroup];     // B_g [n_ad][N_g][r_max]
+  const int32_t* granks[kMaxGroup];  // ranks_g [n_ad] or null
+  const uint16_t* gres[kMaxGroup];   // residual_g [T][N_g] or null
+  uint16_t* gy[kMaxGroup];           // y_g [T][N_g]
   int p_stride;          // row length of the shrink partial sums (R or r_max)
   int p_stacked;         // 1: shrink sums indexed by stacked row a*r_max + j
   const uint16_t* bmat;  // B [n_ad][N][r_max]
@@ -80,6 +92,38 @@ struct GemmArgs {
 // adapter's own rows.
 __device__ __forceinline__ int rank_of(const GemmArgs& a, int ad) {
   return a.ranks ? min(max(a.ranks[ad], 0), a.r_max) : a.r_max;
+}
+
+// Entry g of a per-projection argument array. Compare-and-select over the
+// array (instead of indexing it) keeps the by-value argument in registers.
+template <typename T>
+__device__ __forceinline__ T pick(const T (&v)[kMaxGroup], int g) {
+  T r = v[0];
+#pragma unroll
+  for (int i = 1; i < kMaxGroup; ++i) r = g == i ? v[i] : r;
+  return r;
+}
+
+// Projection of virtual row n of a grouped call.
+__device__ __forceinline__ int group_of(const GemmArgs& a, int64_t n) {
+  int g = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroup; ++i) g += (i < a.G && n >= a.gstart[i]) ? 1 : 0;
+  return g;
+}
+
+// First virtual row of projection g (g may be G: the end of the last one).
+__device__ __forceinline__ int64_t gstart_of(const GemmArgs& a, int g) {
+  int64_t r = a.gstart[0];
+#pragma unroll
+  for (int i = 1; i <= kMaxGroup; ++i) r = g == i ? a.gstart[i] : r;
+  return r;
+}
+
+// Rank of adapter ad of projection g, clamped to [0, r_max].
+__device__ __forceinline__ int rank_g(const GemmArgs& a, int g, int ad) {
+  const int32_t* r = pick(a.granks, g);
+  return r ? min(max(r[ad], 0), a.r_max) : a.r_max;
 }
 
 __device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad) {
@@ -216,19 +260,22 @@ void lora_skinny_kernel(GemmArgs a) {
   const uint16_t* wrow[FT];
   bool wok[FT];
 #pragma unroll
-  for (int i = 0; i < FN; ++i) {
+  for (int i = 0; i < FN; ++i) {  // a 16-row tile lies in one projection
+    const int g = group_of(a, n0 + 16 * i);
     const int64_t n = n0 + 16 * i + col;
     wok[i] = n < a.N;
-    wrow[i] = a.w + (wok[i] ? n : 0) * a.K;
+    wrow[i] = pick(a.gw, g) + (wok[i] ? n - gstart_of(a, g) : 0) * a.K;
   }
 #pragma unroll
   for (int e = 0; e < XT; ++e) {
     const int rr = 16 * e + col;
-    const int64_t row = x0 + rr;
-    bool ok = rr < a.xrows && row < a.R;
-    if (ok) ok = static_cast<int>(row % a.r_max) < rank_of(a, static_cast<int>(row / a.r_max));
+    const int64_t row = x0 + rr;  // virtual stacked row: projection row / R
+    bool ok = rr < a.xrows && row < static_cast<int64_t>(a.G) * a.R;
+    const int g = ok ? static_cast<int>(row / a.R) : 0;
+    const int64_t rl = ok ? row % a.R : 0;
+    if (ok) ok = static_cast<int>(rl % a.r_max) < rank_g(a, g, static_cast<int>(rl / a.r_max));
     wok[FN + e] = ok;
-    wrow[FN + e] = a.amat + (ok ? row : 0) * a.K;
+    wrow[FN + e] = pick(a.ga, g) + (ok ? rl : 0) * a.K;
   }
   const uint16_t* xrow[FM];
   bool xok[FM];
@@ -317,10 +364,11 @@ void lora_skinny_kernel(GemmArgs a) {
       if (i >= FN) {  // stacked-A rows: the shrink's partial sums of this slice
         if (t >= a.T) continue;
         const int rr = 16 * (i - FN) + 4 * (l / 16);
-        float* dst = a.pout + (static_cast<int64_t>(z) * a.T + t) * a.R + x0 + rr;
+        const int64_t rows = static_cast<int64_t>(a.G) * a.R;
+        float* dst = a.pout + (static_cast<int64_t>(z) * a.T + t) * rows + x0 + rr;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          if (rr + q < a.xrows && x0 + rr + q < a.R) dst[q] = s[q];
+          if (rr + q < a.xrows && x0 + rr + q < rows) dst[q] = s[q];
         continue;
       }
       const int64_t n = n0 + 16 * i + 4 * (l / 16);
@@ -499,10 +547,15 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
   const int tid = threadIdx.x;
   const int tt = tid / (kEpFeatures / 4), ng = tid % (kEpFeatures / 4);
   const int64_t t0 = static_cast<int64_t>(blockIdx.y) * kEpTokens;
-  const int64_t t = t0 + tt, n = static_cast<int64_t>(blockIdx.x) * kEpFeatures + 4 * ng;
-  const bool live = t < a.T && n < a.N;
+  const int64_t nv0 = static_cast<int64_t>(blockIdx.x) * kEpFeatures;  // virtual row
+  const int64_t t = t0 + tt, nv = nv0 + 4 * ng;
+  const bool live = t < a.T && nv < a.N;
   const bool lora = a.n_ad > 0;  // uniform
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  // the tile's projection (a 64-row tile lies in one) and its own row index
+  const int g = group_of(a, nv0);
+  const int64_t Ng = gstart_of(a, g + 1) - gstart_of(a, g);
+  const int64_t n = nv - gstart_of(a, g);
 
   // Every load that needs no other load's result is issued first: the base
   // slices, the residual, this token's adapter; then, needing only the
@@ -510,13 +563,14 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
   f32x4 pv[KSB];
 #pragma unroll
   for (int z = 0; z < KSB; ++z)
-    pv[z] = live ? ld_global<f32x4>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n)
+    pv[z] = live ? ld_global<f32x4>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + nv)
                  : f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* res = pick(a.gres, g);
   u32x2 rv = {0u, 0u};
-  if (live && a.res) rv = ld_global<u32x2>(a.res + t * a.N + n);
+  if (live && res) rv = ld_global<u32x2>(res + t * Ng + n);
   const int my_ad = (lora && live) ? token_adapter(a, t) : -1;
   const uint16_t* brow =
-      a.bmat + (static_cast<int64_t>(my_ad >= 0 ? my_ad : 0) * a.N + n) * a.r_max;
+      pick(a.gb, g) + (static_cast<int64_t>(my_ad >= 0 ? my_ad : 0) * Ng + n) * a.r_max;
   u32x4 bv[4][4];  // [8-column step][feature]
   if (my_ad >= 0) {
 #pragma unroll
@@ -541,9 +595,9 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
       f32x4 u = {0.f, 0.f, 0.f, 0.f};
       if (ad >= 0) {
         const float sc = a.scale[t0 + et];
-        const int rk = rank_of(a, ad);
-        const float* p =
-            a.pout + (t0 + et) * a.p_stride + (a.p_stacked ? ad * a.r_max : 0) + j;
+        const int rk = rank_g(a, g, ad);
+        const float* p = a.pout + (t0 + et) * a.p_stride +
+                         (a.p_stacked ? static_cast<int64_t>(g) * a.R + ad * a.r_max : 0) + j;
         for (int z0 = 0; z0 < a.up_ks; z0 += 8) {
           f32x4 sv[8];
 #pragma unroll
@@ -563,7 +617,7 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
     __syncthreads();
     if (my_ad >= 0) {
       // delta of 4 features over the rank columns, 32 at a time
-      const int rk = rank_of(a, my_ad);
+      const int rk = rank_g(a, g, my_ad);
       for (int j0 = 0; j0 < rk; j0 += 32) {
         if (j0 > 0) {
 #pragma unroll
@@ -591,13 +645,13 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
     }
   }
   if (!live) return;
-  if (a.res) {
+  if (res) {
     acc[0] += __uint_as_float(rv.x << 16);
     acc[1] += __uint_as_float(rv.x & 0xffff0000u);
     acc[2] += __uint_as_float(rv.y << 16);
     acc[3] += __uint_as_float(rv.y & 0xffff0000u);
   }
-  *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
+  *reinterpret_cast<u32x2*>(pick(a.gy, g) + t * Ng + n) =
       u32x2{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
 }
 
@@ -815,76 +869,297 @@ local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
 }
 
 // Decode sizes (T <= 256): base partial sums over K slices. Wider feature
-// tiles for fewer tokens cut the re-reads of x (every workgroup of a slice
-// reads the slice of x for all its tokens).
-#ifndef LOCAL_P_FN16
-#define LOCAL_P_FN16 4
-#endif
-#ifndef LOCAL_P_FN32
-#define LOCAL_P_FN32 4
-#endif
-#ifndef LOCAL_P_FN64
-#define LOCAL_P_FN64 4
-#endif
-#ifndef LOCAL_P_FN128
-#define LOCAL_P_FN128 2
-#endif
+// tiles cut the re-reads of x (every workgroup of a slice reads the slice of
+// x for all its tokens); the shape is the widest tile (of 4, 3 or 2 MFMA
+// tiles; 2 above 64 tokens) and K split that bring the grid closest to
+// LOCAL_P_TARGET_WG workgroups from below.
 #ifndef LOCAL_P_TARGET_WG
 #define LOCAL_P_TARGET_WG 256  // aim: about one workgroup per compute unit
 #endif
-
-// Feature tiles (of 16) per workgroup of the decode base product.
-int partial_fn(int64_t T) {
-  return T <= 16 ? LOCAL_P_FN16 : T <= 32 ? LOCAL_P_FN32 : T <= 64 ? LOCAL_P_FN64 : LOCAL_P_FN128;
-}
-
-// K slices of the decode base product: the power of two (at most 8 and at
-// most the number of 64-wide K steps) that brings the grid closest to
-// LOCAL_P_TARGET_WG workgroups from below.
-int partial_slices(int64_t T, int64_t N, int64_t K) {
-  const int64_t fm = T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8;
-  const int64_t tiles = ((N + 16 * partial_fn(T) - 1) / (16 * partial_fn(T))) *
-                        ((T + 16 * fm - 1) / (16 * fm));
-  int ks = 1;
-  while (ks < 8 && tiles * ks * 2 <= LOCAL_P_TARGET_WG && ks * 2 <= K / 64) ks *= 2;
-  return ks;
-}
-
 #ifndef LOCAL_P_U
 #define LOCAL_P_U 2  // 64-wide K steps per batch of loads
 #endif
 
+struct PartialShape {
+  int fn;   // 16-row MFMA tiles per workgroup
+  int ksb;  // K slices
+};
+
+int token_tiles(int64_t T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
+
+PartialShape partial_shape(int64_t T, int64_t N, int64_t K) {
+  const int64_t fm = token_tiles(T);
+  const int64_t ttiles = (T + 16 * fm - 1) / (16 * fm);
+  PartialShape best{T <= 64 ? 4 : 2, 1};
+  int64_t best_wg = -1;
+  const int fns[3] = {4, 3, 2};
+  for (int fn : fns) {
+    if (T > 64 && fn != 2) continue;
+    const int64_t tiles = (N + 16 * fn - 1) / (16 * fn) * ttiles;
+    for (int ks = 1; ks <= 8 && ks <= K / 64; ks *= 2) {
+      const int64_t wg = tiles * ks;
+      if (wg <= LOCAL_P_TARGET_WG && wg > best_wg) {
+        best = {fn, ks};
+        best_wg = wg;
+      }
+    }
+  }
+  return best;
+}
+
 // Batches of one step where the operand registers of two would not fit (the
 // load batching does not change the order of the MFMA accumulation).
+template <int FN, int XT>
+local_status_t run_partial_fn(const GemmArgs& a, hipStream_t s) {
+  if (a.T <= 16) return launch_skinny<FN, 1, LOCAL_P_U, XT>(a, s);
+  if (a.T <= 32) return launch_skinny<FN, 2, LOCAL_P_U, XT>(a, s);
+  return launch_skinny<FN, 4, (XT >= 4 || (FN >= 4 && XT >= 2) ? 1 : LOCAL_P_U), XT>(a, s);
+}
+
 template <int XT>
-local_status_t run_partial_xt(const GemmArgs& a, hipStream_t s) {
-  if (a.T <= 16) return launch_skinny<LOCAL_P_FN16, 1, LOCAL_P_U, XT>(a, s);
-  if (a.T <= 32) return launch_skinny<LOCAL_P_FN32, 2, LOCAL_P_U, XT>(a, s);
-  if (a.T <= 64) return launch_skinny<LOCAL_P_FN64, 4, (XT >= 4 ? 1 : LOCAL_P_U), XT>(a, s);
-  if constexpr (XT <= 2) return launch_skinny<LOCAL_P_FN128, 8, (XT >= 1 ? 1 : LOCAL_P_U), XT>(a, s);
-  return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d extra row tiles above 64 tokens", XT);
+local_status_t run_partial_xt(const GemmArgs& a, int fn, hipStream_t s) {
+  if (a.T > 64) {
+    if constexpr (XT <= 2) return launch_skinny<2, 8, (XT >= 1 ? 1 : LOCAL_P_U), XT>(a, s);
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d extra row tiles above 64 tokens", XT);
+  }
+  if (fn == 4) return run_partial_fn<4, XT>(a, s);
+  if (fn == 3) return run_partial_fn<3, XT>(a, s);
+  return run_partial_fn<2, XT>(a, s);
 }
 
 // Stacked-A rows each feature-tile workgroup takes with the base product
 // (the shrink fused into it), or 0 when that would take more than 4 extra
 // row tiles (2 above 64 tokens, where the accumulators of more would not fit
 // in registers); then the SGMV shrink runs as its own kernel.
-int partial_xrows(int64_t T, int64_t N, int R) {
-  if (R == 0) return 0;
-  const int64_t tiles = (N + 16 * partial_fn(T) - 1) / (16 * partial_fn(T));
-  const int64_t rows = (R + tiles - 1) / tiles;
-  return rows <= (T <= 64 ? 64 : 32) ? static_cast<int>(rows) : 0;
+int partial_xrows(int64_t T, int64_t ftiles, int64_t rows) {
+  if (rows == 0) return 0;
+  const int64_t per = (rows + ftiles - 1) / ftiles;
+  return per <= (T <= 64 ? 64 : 32) ? static_cast<int>(per) : 0;
 }
 
-local_status_t run_partial(const GemmArgs& a, hipStream_t s) {
-  if (a.xrows == 0) return run_partial_xt<0>(a, s);
-  if (a.xrows <= 16) return run_partial_xt<1>(a, s);
-  if (a.xrows <= 32) return run_partial_xt<2>(a, s);
-  if (a.T <= 64) return run_partial_xt<4>(a, s);
+local_status_t run_partial(const GemmArgs& a, int fn, hipStream_t s) {
+  if (a.xrows == 0) return run_partial_xt<0>(a, fn, s);
+  if (a.xrows <= 16) return run_partial_xt<1>(a, fn, s);
+  if (a.xrows <= 32) return run_partial_xt<2>(a, fn, s);
+  if (a.T <= 64) return run_partial_xt<4>(a, fn, s);
   return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d stacked rows per tile", a.xrows);
 }
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+// One projection of a (grouped) call.
+struct Proj {
+  const uint16_t* W;
+  int64_t N;
+  const uint16_t* A;
+  const uint16_t* B;
+  const int32_t* ranks;
+  const uint16_t* res;
+  uint16_t* y;
+};
+
+// Sets the group fields of `a` for projections p[0..G).
+void set_groups(GemmArgs& a, int G, const Proj* p) {
+  a.G = G;
+  int64_t n = 0;
+  for (int g = 0; g <= kMaxGroup; ++g) {
+    a.gstart[g] = n;
+    if (g < G) n += p[g].N;
+  }
+  for (int g = 0; g < kMaxGroup; ++g) {
+    const Proj& q = p[g < G ? g : 0];
+    a.gw[g] = q.W;
+    a.ga[g] = q.A;
+    a.gb[g] = q.B;
+    a.granks[g] = q.ranks;
+    a.gres[g] = q.res;
+    a.gy[g] = q.y;
+  }
+  a.N = n;
+}
+
+// Decode-size plan of a call: tile shape, fused shrink rows, workspace.
+struct DecodePlan {
+  PartialShape shape;
+  int xrows;      // stacked-A rows per workgroup (shrink fused), or 0
+  int slices;     // SGMV shrink K slices (shrink not fused), or 0
+  bool split;     // a grouped call that runs its projections one by one
+  size_t part_bytes, shrink_bytes;
+};
+
+DecodePlan plan_decode(int64_t T, int64_t K, int G, const Proj* p, int n_ad, int r_max) {
+  DecodePlan d{};
+  int64_t n_total = 0;
+  for (int g = 0; g < G; ++g) n_total += p[g].N;
+  const int64_t R = n_ad > 0 ? static_cast<int64_t>(n_ad) * r_max : 0;
+  d.shape = partial_shape(T, n_total, K);
+  const int64_t ftiles = (n_total + 16 * d.shape.fn - 1) / (16 * d.shape.fn);
+  d.xrows = partial_xrows(T, ftiles, G * R);
+  if (n_ad > 0 && d.xrows == 0) {
+    if (G > 1) {
+      d.split = true;
+      return d;
+    }
+    d.slices = sgmv_slices(K, r_max);
+  }
+  d.part_bytes = align256(static_cast<size_t>(d.shape.ksb) * T * n_total * sizeof(float));
+  d.shrink_bytes =
+      d.xrows > 0 ? align256(static_cast<size_t>(d.shape.ksb) * T * G * R * sizeof(float))
+                  : align256(static_cast<size_t>(d.slices) * T * r_max * sizeof(float));
+  return d;
+}
+
+local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const Proj* p,
+                         int32_t n_adapters, int32_t r_max, const int32_t* adapter_idx,
+                         const float* scale, void* ws, size_t* ws_bytes, hipStream_t s);
+
+// Workspace need of a call that runs projections p[0..G) one after another.
+local_status_t one_by_one(const uint16_t* x, int64_t T, int64_t K, int G, const Proj* p,
+                          int32_t n_adapters, int32_t r_max, const int32_t* adapter_idx,
+                          const float* scale, void* ws, size_t* ws_bytes, hipStream_t s) {
+  if (!ws) {
+    size_t need = 0;
+    for (int g = 0; g < G; ++g) {
+      size_t n = 0;
+      const local_status_t st = lora_impl(x, T, K, 1, p + g, n_adapters, r_max, adapter_idx,
+                                          scale, nullptr, &n, s);
+      if (st != LOCAL_OK) return st;
+      need = need > n ? need : n;
+    }
+    *ws_bytes = need;
+    return LOCAL_OK;
+  }
+  for (int g = 0; g < G; ++g) {
+    size_t n = *ws_bytes;
+    const local_status_t st =
+        lora_impl(x, T, K, 1, p + g, n_adapters, r_max, adapter_idx, scale, ws, &n, s);
+    if (st != LOCAL_OK) return st;
+  }
+  return LOCAL_OK;
+}
+
+local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const Proj* p,
+                         int32_t n_adapters, int32_t r_max, const int32_t* adapter_idx,
+                         const float* scale, void* ws, size_t* ws_bytes, hipStream_t s) {
+  const int R = n_adapters > 0 ? n_adapters * r_max : 0;
+  const bool decode = T <= kSgMaxTokens;
+  if (G > 1 && !decode)
+    return one_by_one(x, T, K, G, p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes, s);
+  DecodePlan d{};
+  if (decode) {
+    d = plan_decode(T, K, G, p, n_adapters, r_max);
+    if (d.split)
+      return one_by_one(x, T, K, G, p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes, s);
+  }
+  // Workspace. Decode sizes (T <= kSgMaxTokens): the base partial sums
+  // [ksb][T][N] fp32 (N over all projections), then the shrink's partial
+  // sums: [ksb][T][G*R] fp32 when the shrink runs inside the base product,
+  // [slices][T][r_max] after the SGMV shrink. Above: U_s [T][R] bf16.
+  const size_t need = decode ? d.part_bytes + d.shrink_bytes
+                             : align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
+  if (!ws) {
+    *ws_bytes = need;
+    return LOCAL_OK;
+  }
+  if (*ws_bytes < need)
+    return local_fail(LOCAL_ERR_WORKSPACE, "lora_linear: workspace %zu < %zu", *ws_bytes, need);
+  if (T == 0) return LOCAL_OK;
+
+  GemmArgs g{};
+  g.x = x;
+  g.T = T;
+  g.K = K;
+  g.idx = adapter_idx;
+  g.scale = scale;
+  g.n_ad = n_adapters;
+  g.r_max = r_max;
+  g.R = R;
+  local_status_t st;
+
+  if (decode) {
+    float* part = static_cast<float*>(ws);
+    float* sp = reinterpret_cast<float*>(static_cast<char*>(ws) + d.part_bytes);
+    const bool fused = d.xrows > 0;
+    if (n_adapters > 0 && !fused) {  // SGMV shrink (one projection): partial sums
+      GemmArgs sh = g;
+      sh.w = p[0].A;
+      sh.ranks = p[0].ranks;
+      sh.N = R;
+      sh.mode = kModeShrink;
+      sh.pout = sp;
+      sh.up_ks = d.slices;
+      if ((st = run_sgmv_shrink(sh, s)) != LOCAL_OK) return st;
+    }
+    GemmArgs m = g;  // base product (+ fused shrink): partial sums per K slice
+    set_groups(m, G, p);
+    m.mode = kModePartial;
+    m.part = part;
+    m.ksplit = d.shape.ksb;
+    m.xrows = d.xrows;
+    m.pout = sp;
+    if ((st = run_partial(m, d.shape.fn, s)) != LOCAL_OK) return st;
+    m.up_ks = fused ? d.shape.ksb : d.slices;  // epilogue: sums, up-projection, residual
+    m.p_stride = fused ? G * R : r_max;
+    m.p_stacked = fused ? 1 : 0;
+    m.ksplit = d.shape.ksb;
+    return run_epilogue(m, s);
+  }
+
+  const Proj& q = p[0];
+  uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
+  if (n_adapters > 0) {  // shrink into U_s (mask and scale in its epilogue)
+    GemmArgs sh = g;
+    const Proj stacked{q.A, R, nullptr, nullptr, q.ranks, nullptr, us};
+    set_groups(sh, 1, &stacked);
+    sh.w = q.A;  // [n_ad][r_max][K] == [R][K]
+    sh.ranks = q.ranks;
+    sh.y = us;
+    sh.mode = kModeShrink;
+    if ((st = run_gemm(sh, s)) != LOCAL_OK) return st;
+  }
+  GemmArgs m = g;
+  m.w = q.W;
+  m.N = q.N;
+  m.bmat = q.B;
+  m.ranks = q.ranks;
+  m.us = us;
+  m.res = q.res;
+  m.y = q.y;
+  m.mode = kModeMain;
+  return run_gemm(m, s);
+}
+
+// Argument checks shared by the entry points (before any launch).
+local_status_t check_args(const char* who, const uint16_t* x, int64_t T, int64_t K, int G,
+                          const Proj* p, int32_t n_adapters, int32_t r_max,
+                          const int32_t* adapter_idx, const float* scale, size_t* ws_bytes,
+                          bool sizes_only) {
+  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "%s: ws_bytes is NULL", who);
+  if (T < 0 || K <= 0 || n_adapters < 0)
+    return local_fail(LOCAL_ERR_SHAPE, "%s: T=%lld K=%lld n_adapters=%d", who, (long long)T,
+                      (long long)K, n_adapters);
+  for (int g = 0; g < G; ++g)
+    if (p[g].N <= 0)
+      return local_fail(LOCAL_ERR_SHAPE, "%s: N=%lld (projection %d)", who, (long long)p[g].N, g);
+  bool shapes_ok = K % 64 == 0 && n_adapters <= 256 &&
+                   (n_adapters == 0 || (r_max >= 8 && r_max <= 128 && r_max % 8 == 0));
+  for (int g = 0; g < G; ++g) shapes_ok = shapes_ok && p[g].N % 64 == 0;
+  if (!shapes_ok)
+    return local_fail(LOCAL_ERR_UNSUPPORTED,
+                      "%s: K=%lld n_adapters=%d r_max=%d (need K and every N %% 64 == 0, "
+                      "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
+                      who, (long long)K, n_adapters, r_max);
+  if (sizes_only || T == 0) return LOCAL_OK;
+  if (!x) return local_fail(LOCAL_ERR_NULL, "%s: NULL x", who);
+  for (int g = 0; g < G; ++g) {
+    if (!p[g].W || !p[g].y) return local_fail(LOCAL_ERR_NULL, "%s: NULL W or y", who);
+    if (n_adapters > 0 && (!p[g].A || !p[g].B))
+      return local_fail(LOCAL_ERR_NULL, "%s: NULL adapter argument", who);
+  }
+  if (n_adapters > 0 && (!adapter_idx || !scale))
+    return local_fail(LOCAL_ERR_NULL, "%s: NULL adapter argument", who);
+  return LOCAL_OK;
+}
 
 }  // namespace
 }  // namespace localk
@@ -896,102 +1171,31 @@ extern "C" local_status_t local_lora_linear(
     const uint16_t* B, int32_t n_adapters, int32_t r_max, const int32_t* ranks,
     const int32_t* adapter_idx, const float* scale, const uint16_t* residual, uint16_t* y,
     void* ws, size_t* ws_bytes, void* stream) {
-  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "lora_linear: ws_bytes is NULL");
-  if (T < 0 || K <= 0 || N <= 0 || n_adapters < 0)
-    return local_fail(LOCAL_ERR_SHAPE, "lora_linear: T=%lld K=%lld N=%lld n_adapters=%d",
-                      (long long)T, (long long)K, (long long)N, n_adapters);
-  if (K % 64 != 0 || N % 64 != 0 || n_adapters > 256 ||
-      (n_adapters > 0 && (r_max < 8 || r_max > 128 || r_max % 8 != 0)))
-    return local_fail(LOCAL_ERR_UNSUPPORTED,
-                      "lora_linear: K=%lld N=%lld n_adapters=%d r_max=%d (need K,N %% 64 == 0, "
-                      "n_adapters <= 256, r_max in [8,128] and %% 8 == 0)",
-                      (long long)K, (long long)N, n_adapters, r_max);
-  const int R = n_adapters > 0 ? n_adapters * r_max : 0;
-  // Workspace. Decode sizes (T <= kSgMaxTokens): the base partial sums
-  // [ksb][T][N] fp32, then the shrink's partial sums: [ksb][T][R] fp32 when
-  // the shrink runs inside the base product, [slices][T][r_max] after the
-  // SGMV shrink. Above: U_s [T][R] bf16.
-  const bool decode = T <= kSgMaxTokens;
-  const int ksb = decode ? partial_slices(T, N, K) : 0;
-  const int xrows = decode ? partial_xrows(T, N, R) : 0;
-  const bool fused = xrows > 0;
-  const int slices = n_adapters > 0 && decode && !fused ? sgmv_slices(K, r_max) : 0;
-  const size_t part_bytes = decode ? align256(static_cast<size_t>(ksb) * T * N * sizeof(float)) : 0;
-  const size_t shrink_bytes =
-      fused ? align256(static_cast<size_t>(ksb) * T * R * sizeof(float))
-            : align256(static_cast<size_t>(slices) * T * r_max * sizeof(float));
-  const size_t need = decode ? part_bytes + shrink_bytes
-                             : align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
-  if (!ws) {
-    *ws_bytes = need;
-    return LOCAL_OK;
-  }
-  if (*ws_bytes < need)
-    return local_fail(LOCAL_ERR_WORKSPACE, "lora_linear: workspace %zu < %zu", *ws_bytes, need);
-  if (T == 0) return LOCAL_OK;
-  if (!x || !W || !y) return local_fail(LOCAL_ERR_NULL, "lora_linear: NULL x, W or y");
-  if (n_adapters > 0 && (!A || !B || !adapter_idx || !scale))
-    return local_fail(LOCAL_ERR_NULL, "lora_linear: NULL adapter argument");
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Proj p{W, N, A, B, ranks, residual, y};
+  local_status_t st = check_args("lora_linear", x, T, K, 1, &p, n_adapters, r_max, adapter_idx,
+                                 scale, ws_bytes, ws == nullptr);
+  if (st != LOCAL_OK) return st;
+  return lora_impl(x, T, K, 1, &p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream));
+}
 
-  GemmArgs g{};
-  g.x = x;
-  g.T = T;
-  g.K = K;
-  g.idx = adapter_idx;
-  g.scale = scale;
-  g.ranks = ranks;
-  g.n_ad = n_adapters;
-  g.r_max = r_max;
-  g.R = R;
-  g.bmat = B;
-  local_status_t st;
-
-  if (decode) {
-    float* part = static_cast<float*>(ws);
-    float* sp = reinterpret_cast<float*>(static_cast<char*>(ws) + part_bytes);
-    if (n_adapters > 0 && !fused) {  // SGMV shrink: partial sums per K slice
-      GemmArgs sh = g;
-      sh.w = A;
-      sh.N = R;
-      sh.mode = kModeShrink;
-      sh.pout = sp;
-      sh.up_ks = slices;
-      if ((st = run_sgmv_shrink(sh, s)) != LOCAL_OK) return st;
-    }
-    GemmArgs m = g;  // base product (+ fused shrink): partial sums per K slice
-    m.w = W;
-    m.N = N;
-    m.mode = kModePartial;
-    m.part = part;
-    m.ksplit = ksb;
-    m.amat = A;
-    m.xrows = xrows;
-    m.pout = sp;
-    if ((st = run_partial(m, s)) != LOCAL_OK) return st;
-    m.up_ks = fused ? ksb : slices;  // epilogue: sums, up-projection, residual
-    m.p_stride = fused ? R : r_max;
-    m.p_stacked = fused ? 1 : 0;
-    m.res = residual;
-    m.y = y;
-    return run_epilogue(m, s);
-  }
-
-  uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
-  if (n_adapters > 0) {  // shrink into U_s (mask and scale in its epilogue)
-    GemmArgs sh = g;
-    sh.w = A;  // [n_ad][r_max][K] == [R][K]
-    sh.N = R;
-    sh.y = us;
-    sh.mode = kModeShrink;
-    if ((st = run_gemm(sh, s)) != LOCAL_OK) return st;
-  }
-  GemmArgs m = g;
-  m.w = W;
-  m.N = N;
-  m.us = us;
-  m.res = residual;
-  m.y = y;
-  m.mode = kModeMain;
-  return run_gemm(m, s);
+extern "C" local_status_t local_lora_linear_grouped(
+    const uint16_t* x, int64_t T, int64_t K, int32_t G, const uint16_t* const* W,
+    const int64_t* N, const uint16_t* const* A, const uint16_t* const* B, int32_t n_adapters,
+    int32_t r_max, const int32_t* const* ranks, const int32_t* adapter_idx, const float* scale,
+    uint16_t* const* y, void* ws, size_t* ws_bytes, void* stream) {
+  if (G < 1 || G > kMaxGroup)
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear_grouped: G=%d (need 1..%d)", G,
+                      kMaxGroup);
+  if (!W || !N || !y || (n_adapters > 0 && (!A || !B)))
+    return local_fail(LOCAL_ERR_NULL, "lora_linear_grouped: NULL argument array");
+  Proj p[kMaxGroup];
+  for (int g = 0; g < G; ++g)
+    p[g] = Proj{W[g], N[g], n_adapters > 0 ? A[g] : nullptr, n_adapters > 0 ? B[g] : nullptr,
+                (n_adapters > 0 && ranks) ? ranks[g] : nullptr, nullptr, y[g]};
+  local_status_t st = check_args("lora_linear_grouped", x, T, K, G, p, n_adapters, r_max,
+                                 adapter_idx, scale, ws_bytes, ws == nullptr);
+  if (st != LOCAL_OK) return st;
+  return lora_impl(x, T, K, G, p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream));
 }

@@ -9,12 +9,10 @@ followed, per layer, by
               residual x added when layers are chained)
 and the next layer's input is y. Nothing here computes: it only lays out the
 buffers and replays the prepared calls, in order on the current stream, so
-the whole step can also be captured into a HIP graph. A graph may instead be
-captured with what does not depend on each other on parallel branches: the
-version check (its stale list is for the host; attention checks the tags
-itself) beside the whole step, and the k and v projections beside the q
-projection. On the 7B decode step the joins cost more than the overlap
-gains, so the in-order graph is the default.
+the whole step can also be captured into a HIP graph by the caller. The q, k
+and v projections read the same x, so those with the same adapter setup run
+as one grouped call (local_lora_linear_grouped): one pass of launches over
+their concatenated weights.
 """
 from __future__ import annotations
 
@@ -72,14 +70,12 @@ class Step:
         self.n_layers = len(weights)
         self.inputs = (x, weights, meta, kv_pool)  # owned for the step's lifetime
         self.ws = bd.Workspace(dev)
-        # calls that may run concurrently get workspaces of their own
-        self.ws_k, self.ws_v, self.ws_vc = (bd.Workspace(dev) for _ in range(3))
         self.calls: List[bd.Call] = []
         self.buffers = {}
         cap = stale_cap if stale_cap is not None else meta.block_table.numel()
         self.version_check = bd.prepare_block_version_check(
             meta.block_table, meta.ctx_lens, meta.block_version, meta.req_version, cap=cap,
-            workspace=self.ws_vc)
+            workspace=self.ws)
         self.calls.append(self.version_check)
         sm_scale = 1.0 / math.sqrt(D)
         xs = [x]
@@ -92,10 +88,7 @@ class Step:
             o = torch.empty((T, hq * D), dtype=torch.bfloat16, device=dev)
             y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
             lse = torch.empty((T, hq), dtype=torch.float32, device=dev)
-            lc = {}
-            for name, inp, outp, ws in (("q", xin, q, self.ws), ("k", xin, k, self.ws_k),
-                                        ("v", xin, v, self.ws_v)):
-                lc[name] = self._proj(lw, name, inp, outp, meta, None, ws)
+            lc = {"in": self._in_proj(lw, xin, {"q": q, "k": k, "v": v}, meta)}
             kc, vc = kv_pool[l, 0], kv_pool[l, 1]
             if kind == "decode":
                 lc["attn"] = bd.prepare_paged_attn_decode(
@@ -109,68 +102,65 @@ class Step:
                     meta.block_version, meta.req_version, sm_scale,
                     k_new=k.view(T, hkv, D), v_new=v.view(T, hkv, D), Hkv=hkv,
                     out=o.view(T, hq, D), lse=lse, workspace=self.ws)
-            lc["o"] = self._proj(lw, "o", o, y, meta, xin if residual else None, self.ws)
-            for name in ("q", "k", "v", "attn", "o"):
-                self.calls.append(lc[name])
+            lc["o"] = self._proj(lw, "o", o, y, meta, xin if residual else None)
+            self.calls += lc["in"] + [lc["attn"], lc["o"]]
             self.layer_calls.append(lc)
             self.buffers[l] = dict(x=xin, q=q, k=k, v=v, o=o, y=y, lse=lse)
             xs.append(y)
         self.out = xs[-1]
 
-    def _proj(self, lw, name, inp, outp, meta, residual, ws):
+    def _proj(self, lw, name, inp, outp, meta, residual):
         if ("A_" + name) in lw:
             return bd.prepare_lora_linear(
                 inp, lw["W_" + name], lw["A_" + name], lw["B_" + name], lw["ranks_" + name],
                 meta.token_adapter, meta.token_scale, residual=residual, out=outp,
-                workspace=ws)
+                workspace=self.ws)
         return bd.prepare_lora_linear(inp, lw["W_" + name], residual=residual, out=outp,
-                                      workspace=ws)
+                                      workspace=self.ws)
+
+    def _in_proj(self, lw, x, outs, meta) -> List[bd.Call]:
+        """Calls for the q, k, v projections of x: one grouped call per set of
+        projections with the same adapter setup."""
+        calls = []
+        with_ad = [n for n in ("q", "k", "v") if ("A_" + n) in lw]
+        without = [n for n in ("q", "k", "v") if ("A_" + n) not in lw]
+        if len({tuple(lw["A_" + n].shape[:2]) for n in with_ad}) > 1:
+            # adapter sets of different shapes: those projections one by one
+            calls += [self._proj(lw, n, x, outs[n], meta, None) for n in with_ad]
+            with_ad = []
+        for names, ad in ((with_ad, True), (without, False)):
+            if not names:
+                continue
+            if len(names) == 1:
+                calls.append(self._proj(lw, names[0], x, outs[names[0]], meta, None))
+            elif ad:
+                calls.append(bd.prepare_lora_linear_grouped(
+                    x, [lw["W_" + n] for n in names], [lw["A_" + n] for n in names],
+                    [lw["B_" + n] for n in names], [lw["ranks_" + n] for n in names],
+                    meta.token_adapter, meta.token_scale, outs=[outs[n] for n in names],
+                    workspace=self.ws))
+            else:
+                calls.append(bd.prepare_lora_linear_grouped(
+                    x, [lw["W_" + n] for n in names], outs=[outs[n] for n in names],
+                    workspace=self.ws))
+        return calls
 
     def __call__(self):
         for c in self.calls:
             c()
         return self.out
 
-    def _run_branched(self, side):
-        """The step with its independent calls on the side streams (capture)."""
-        cur = torch.cuda.current_stream()
-        s_vc, s_k, s_v = side
-        s_vc.wait_stream(cur)
-        with torch.cuda.stream(s_vc):
-            self.version_check()
-        for lc in self.layer_calls:
-            s_k.wait_stream(cur)
-            s_v.wait_stream(cur)
-            lc["q"]()
-            with torch.cuda.stream(s_k):
-                lc["k"]()
-            with torch.cuda.stream(s_v):
-                lc["v"]()
-            cur.wait_stream(s_k)
-            cur.wait_stream(s_v)
-            lc["attn"]()
-            lc["o"]()
-        cur.wait_stream(s_vc)
-
-    def capture(self, parallel: bool = False):
+    def capture(self):
         """Capture the step into a HIP graph; returns the torch.cuda.CUDAGraph.
 
-        With `parallel`, independent calls become parallel branches of the
-        graph (see the module docstring); otherwise the graph is the eager
-        order. Run the step eagerly at least once first (kernel attributes are
-        set on first launch). The library records no memset, so replays are
-        exact.
+        Run the step eagerly at least once first (kernel attributes are set on
+        first launch). The library records no memset, so replays are exact.
         """
         g = torch.cuda.CUDAGraph()
         s = torch.cuda.Stream()
-        side = [torch.cuda.Stream() for _ in range(3)]
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
             with torch.cuda.graph(g, stream=s):
-                if parallel:
-                    self._run_branched(side)
-                else:
-                    self()
+                self()
         torch.cuda.current_stream().wait_stream(s)
-        self._side = side  # the graph's branches were recorded on these
         return g

@@ -63,7 +63,9 @@ CASES = [
     (64, 4096, 512, 16, 64, [8, 16, 32, 64] * 4),
     (24, 2048, 256, 2, 128, [128, 100]),
     (128, 512, 256, 16, 32, [32, 8, 24, 16] * 4),
-    (16, 512, 64, 8, 16, None),
+    (16, 512, 64, 16, 16, None),
+    (32, 1024, 4096, 8, 16, None),
+    (64, 512, 3072, 16, 32, None),
     (64, 512, 512, 0, 0, None),
     (700, 256, 384, 0, 0, None),
 ]
@@ -169,3 +171,68 @@ def test_out_of_range_adapter_and_rank():
         y = _run_gpu(x, W, A, B, rk, idx, scale)
         ref = oracle.lora_linear(x, W, A, B, rk, idx, scale)
         assert_rel(f64(y), ref, "y T=%d" % T)
+
+
+def _grouped_gpu(x, Ws, As, Bs, ranks, idx, scale):
+    kw = {}
+    if As is not None:
+        kw = dict(As=[dev_u16(a) for a in As], Bs=[dev_u16(b) for b in Bs],
+                  ranks=[dev(r) for r in ranks], adapter_idx=dev(idx),
+                  scale=dev(scale, torch.float32))
+    ys = lk.local_lora_linear_grouped(dev_u16(x), [dev_u16(w) for w in Ws], **kw)
+    torch.cuda.synchronize()
+    return ys
+
+
+GROUPED = [
+    # T, K, N per projection, n_ad, r_max, ranks
+    (32, 1024, (1024, 256, 256), 8, 16, None),
+    (64, 512, (2048, 512, 512), 16, 64, [8, 16, 32, 64] * 4),
+    (128, 512, (1024, 256, 256), 32, 16, None),
+    (4, 256, (256, 256), 3, 8, None),
+    (300, 512, (512, 256), 4, 16, None),       # long chunk: one projection at a time
+    (16, 512, (64, 64), 16, 16, None),          # shrink too wide to fuse: one at a time
+    (32, 512, (512, 512, 512), 0, 0, None),
+    (200, 256, (256, 256, 512, 256), 5, 32, [32, 1, 17, 32, 24]),
+]
+
+
+@pytest.mark.parametrize("case", GROUPED, ids=lambda c: "T%d_K%d_G%d_ad%d" % (c[0], c[1], len(c[2]), c[3]))
+def test_grouped_matches_oracle(case):
+    T, K, Ns, n_ad, r_max, ranks = case
+    say("lora_linear_grouped", case)
+    rng = np.random.default_rng(T + K + sum(Ns) + n_ad)
+    x = rand_bf16(rng, (T, K))
+    Ws, As, Bs, Rs = [], [], [], []
+    idx = scale = None
+    for N in Ns:
+        _, W, A, B, rk, idx_g, scale_g = _inputs(rng, T, K, N, n_ad, r_max, ranks)
+        Ws.append(W)
+        As.append(A)
+        Bs.append(B)
+        Rs.append(rk)
+        if idx is None:
+            idx, scale = idx_g, scale_g
+    if n_ad:
+        scale = rng.uniform(-2, 2, size=T).astype(np.float32)
+    ys = _grouped_gpu(x, Ws, As if n_ad else None, Bs, Rs, idx, scale)
+    for g, (W, A, B, rk) in enumerate(zip(Ws, As, Bs, Rs)):
+        ref = oracle.lora_linear(x, W, A, B, rk, idx, scale) if n_ad else \
+            oracle.lora_linear(x, W)
+        assert_rel(f64(ys[g]), ref, "y[%d]" % g)
+
+
+def test_grouped_zero_up_projection_is_bitwise_base():
+    rng = np.random.default_rng(808)
+    T, K, Ns = 32, 1024, (1024, 256, 256)
+    x = rand_bf16(rng, (T, K))
+    parts = [_inputs(rng, T, K, N, 6, 16, neg_frac=0.0) for N in Ns]
+    Ws = [p[1] for p in parts]
+    As = [p[2] for p in parts]
+    Bz = [np.zeros_like(p[3]) for p in parts]
+    Rs = [p[4] for p in parts]
+    idx, scale = parts[0][5], parts[0][6]
+    y_zero = _grouped_gpu(x, Ws, As, Bz, Rs, idx, scale)
+    y_base = _grouped_gpu(x, Ws, None, None, None, None, None)
+    for a, b in zip(y_zero, y_base):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))

@@ -162,12 +162,10 @@ def test_prefill_7b_sampled():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("parallel", [False, True])
-def test_step_graph_replays_match_eager(parallel):
-    # The whole decode step captured into a HIP graph (in eager order, or with
-    # independent calls on parallel branches): every replay, with eager work
-    # and synchronisations in between, equals the eager step.
-    say("step graph", parallel)
+def test_step_graph_replays_match_eager():
+    # The whole decode step captured into a HIP graph: every replay, with
+    # eager work and synchronisations in between, equals the eager step.
+    say("step graph")
     w = workloads.GQA_SKEW
     meta, weights, pool, x = _setup(w, 3)
     st = Step("decode", x, weights, meta_to_device(meta, "cuda"), pool, w.hq, w.hkv,
@@ -176,7 +174,7 @@ def test_step_graph_replays_match_eager(parallel):
     torch.cuda.synchronize()
     ref = {k: v.clone() for k, v in st.buffers[0].items()}
     ref_pairs = [t.clone() for t in st.version_check.outputs]
-    g = st.capture(parallel)
+    g = st.capture()
     for rep in range(4):
         for k in ("q", "o", "y", "lse"):
             st.buffers[0][k].fill_(float("nan") if k == "lse" else 7.0)

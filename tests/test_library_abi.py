@@ -55,10 +55,9 @@ def test_lora_linear_workspace_and_errors(lib):
     # decode sizes: fp32 base partial sums (4 K slices x T x N), then the
     # shrink's, fused into the base product (4 K slices x T x n_adapters*r_max)
     assert n == 4 * 32 * 4096 * 4 + 4 * 32 * 128 * 4
-    # a shrink too wide to fuse (N = 64: one feature tile, 8 base K slices)
-    # runs on its own:
-    # 8 K slices x T x r_max
-    st, n2 = _size(f, FAKE, 32, 4096, FAKE, 64, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
+    # a shrink too wide to fuse (N = 64: two 48-row feature tiles for 256
+    # stacked rows, 8 base K slices) runs on its own: 8 K slices x T x r_max
+    st, n2 = _size(f, FAKE, 32, 4096, FAKE, 64, FAKE, FAKE, 16, 16, None, FAKE, FAKE, None, FAKE)
     assert st == OK and n2 == 8 * 32 * 64 * 4 + 8 * 32 * 16 * 4
     # above 256 tokens: U_s, T x n_adapters*r_max bf16
     st, n1 = _size(f, FAKE, 300, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
@@ -128,3 +127,27 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros((4, 64), dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU"):
         lk.local_lora_linear(x, torch.zeros((64, 64), dtype=torch.bfloat16))
+
+
+def test_lora_linear_grouped_workspace_and_errors(lib):
+    f = lib.local_lora_linear_grouped
+    P = ctypes.c_void_p
+    ptrs = lambda n: (P * n)(*([FAKE] * n))
+    Ns = (ctypes.c_int64 * 3)(4096, 4096, 4096)
+    # q, k, v of a 7B layer at T=32 with 8 rank-16 adapters: one virtual weight
+    # of 12288 rows in 48-row tiles (256 workgroups, K not split), the shrink
+    # fused (3 x 128 stacked rows): base sums 32 x 12288 fp32, shrink sums
+    # 32 x 384 fp32
+    st, n = _size(f, FAKE, 32, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 8, 16, None, FAKE,
+                  FAKE, ptrs(3))
+    assert st == OK and n == 32 * 12288 * 4 + 32 * 384 * 4
+    assert _size(f, FAKE, 32, 4096, 0, ptrs(1), Ns, None, None, 0, 0, None, None, None,
+                 ptrs(1))[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 32, 4096, 5, ptrs(5), Ns, None, None, 0, 0, None, None, None,
+                 ptrs(5))[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 32, 4096, 3, None, Ns, None, None, 0, 0, None, None, None,
+                 ptrs(3))[0] == ERR_NULL
+    bad = (ctypes.c_int64 * 3)(4096, 100, 4096)
+    assert _size(f, FAKE, 32, 4096, 3, ptrs(3), bad, None, None, 0, 0, None, None, None,
+                 ptrs(3))[0] == ERR_UNSUPPORTED
+    assert b"grouped" in lib.local_last_error()
