@@ -40,7 +40,48 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-prefill", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--traffic-probe", action="store_true",
+                   help="only run, eagerly, a 256 MiB device copy (the calibration of the "
+                        "HBM byte counters) and 5 decode attention launches of the workload; "
+                        "for rocprofv3 --pmc runs")
     return p.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "decode_attn_traffic_decode_7b_mha_b32.md")
+DECODE_SOURCES = ("paper_2608_15241_amd/csrc/paged_attn_decode.hip",
+                  "paper_2608_15241_amd/csrc/common.hpp")
+
+
+def decode_source_hash():
+    """sha256 over the sources of the decode attention kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for rel in DECODE_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode attention launch from the committed counter summary,
+    or None when it is missing or was taken on other kernel sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("source_sha256") != decode_source_hash():
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def decode_bytes(w, meta):
@@ -102,6 +143,9 @@ def main():
     w = workloads.DECODE_7B
     meta = workloads.make_meta(w, seed=0)
     md = meta_to_device(meta, dev)
+    if args.traffic_probe:
+        traffic_probe(torch, workloads, w, meta, md, dev)
+        return
     sets = []
     for s in range(args.sets):
         weights = [workloads.make_layer_weights(w, 0, dev, seed=100 + s)]
@@ -181,7 +225,7 @@ def main():
                    "input_sets": args.sets},
         "roofline": {"kernel": "local_paged_attn_decode", "bound": "hbm",
                      "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
                      "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5)},
         "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
                      "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
@@ -196,6 +240,33 @@ def main():
 
     del sets
     print(json.dumps(result), flush=True)
+
+
+def traffic_probe(torch, workloads, w, meta, md, dev):
+    """A plain copy of known size, then decode attention launches, eagerly."""
+    from paper_2608_15241_amd.step import Step
+    weights = [workloads.make_layer_weights(w, 0, dev, seed=100)]
+    pool = workloads.make_kv_pool(w, meta, dev, seed=100)
+    x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=200)
+    st = Step("decode", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
+    st()
+    torch.cuda.synchronize()
+    n = 256 << 20
+    src = torch.ones(n // 2, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)       # elementwise kernel: reads n bytes, writes n
+    torch.cuda.synchronize()
+    for _ in range(5):
+        st.layer_calls[0]["attn"]()
+    torch.cuda.synchronize()
+    attn_bytes, _, _ = decode_bytes(w, meta)
+    print(json.dumps({"traffic_probe": {"copy_read_bytes": n, "copy_write_bytes": n,
+                                        "copy_kernel": "torch.mul(src, 1.0, out=dst), bf16",
+                                        "attn_launches": 5,
+                                        "attn_algorithmic_bytes": attn_bytes,
+                                        "decode_source_sha256": decode_source_hash()}}),
+          flush=True)
 
 
 def bench_prefill(torch, workloads, lk, dev, reps=20):

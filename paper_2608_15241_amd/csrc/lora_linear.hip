@@ -237,6 +237,11 @@ __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* 
 #define LOCAL_SK_WPE 2  // waves per SIMD the skinny kernel is compiled for
 #endif
 
+// k offsets of a lane's two 16-byte loads within a 64-wide step: k-group g of
+// MFMA m takes k = kLaneK*g + kHalfK*m .. +8.
+constexpr int kLaneK = 16;
+constexpr int kHalfK = 8;
+
 template <int FN, int FM, int U, int XT>
 __global__ __launch_bounds__(kSkThreads) __attribute__((amdgpu_waves_per_eu(LOCAL_SK_WPE, LOCAL_SK_WPE)))
 void lora_skinny_kernel(GemmArgs a) {
@@ -306,22 +311,25 @@ void lora_skinny_kernel(GemmArgs a) {
   const int s_lo = z_lo + (rw * (z_hi - z_lo)) / kSkWaves;
   const int s_hi = z_lo + ((rw + 1) * (z_hi - z_lo)) / kSkWaves;
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  for (int s = s_lo; s < s_hi; s += U) {
-    u32x4 wv[U][FT][2], xv[U][FM][2];
+  // one batch: the loads of U steps from step s (past s_hi: the last step)
+  auto load_batch = [&](int s, u32x4 (&wv)[U][FT][2], u32x4 (&xv)[U][FM][2]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 64 + 16 * kgrp;
+      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 64 + kLaneK * kgrp;
 #pragma unroll
       for (int i = 0; i < FT; ++i) {
         wv[u][i][0] = ld_global<u32x4>(wrow[i] + k);
-        wv[u][i][1] = ld_global<u32x4>(wrow[i] + k + 8);
+        wv[u][i][1] = ld_global<u32x4>(wrow[i] + k + kHalfK);
       }
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
         xv[u][j][0] = ld_global<u32x4>(xrow[j] + k);
-        xv[u][j][1] = ld_global<u32x4>(xrow[j] + k + 8);
+        xv[u][j][1] = ld_global<u32x4>(xrow[j] + k + kHalfK);
       }
     }
+  };
+  // its MFMAs, with invalid rows and steps past s_hi zeroed
+  auto mfma_batch = [&](int s, u32x4 (&wv)[U][FT][2], u32x4 (&xv)[U][FM][2]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool live = s + u < s_hi;
@@ -338,6 +346,11 @@ void lora_skinny_kernel(GemmArgs a) {
             acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i][m]), as_bf16x8(xv[u][j][m]), acc[i][j]);
       }
     }
+  };
+  for (int s = s_lo; s < s_hi; s += U) {
+    u32x4 wv[U][FT][2], xv[U][FM][2];
+    load_batch(s, wv, xv);
+    mfma_batch(s, wv, xv);
   }
   // ---- sum the waves' partial tiles in wave order, then store; in rounds of
   // at most kRedTiles tiles so that the LDS buffer stays within 64 KB
@@ -877,7 +890,13 @@ local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
 #define LOCAL_P_TARGET_WG 256  // aim: about one workgroup per compute unit
 #endif
 #ifndef LOCAL_P_U
-#define LOCAL_P_U 2  // 64-wide K steps per batch of loads
+#define LOCAL_P_U 2  // 64-wide K steps per batch of loads, up to 32 tokens
+#endif
+#ifndef LOCAL_P_U64
+#define LOCAL_P_U64 2  // the same, up to 64 tokens
+#endif
+#ifndef LOCAL_P_WIDE
+#define LOCAL_P_WIDE 6  // widest feature tile (MFMA tiles) up to 32 tokens; 0 = none
 #endif
 
 struct PartialShape {
@@ -887,14 +906,14 @@ struct PartialShape {
 
 int token_tiles(int64_t T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 
-PartialShape partial_shape(int64_t T, int64_t N, int64_t K) {
+PartialShape partial_shape(int64_t T, int64_t N, int64_t K, bool allow_wide) {
   const int64_t fm = token_tiles(T);
   const int64_t ttiles = (T + 16 * fm - 1) / (16 * fm);
   PartialShape best{T <= 64 ? 4 : 2, 1};
   int64_t best_wg = -1;
-  const int fns[3] = {4, 3, 2};
+  const int fns[4] = {LOCAL_P_WIDE, 4, 3, 2};
   for (int fn : fns) {
-    if (T > 64 && fn != 2) continue;
+    if (fn == 0 || (T > 64 && fn != 2) || (fn > 4 && (T > 32 || !allow_wide))) continue;
     const int64_t tiles = (N + 16 * fn - 1) / (16 * fn) * ttiles;
     for (int ks = 1; ks <= 8 && ks <= K / 64; ks *= 2) {
       const int64_t wg = tiles * ks;
@@ -913,7 +932,7 @@ template <int FN, int XT>
 local_status_t run_partial_fn(const GemmArgs& a, hipStream_t s) {
   if (a.T <= 16) return launch_skinny<FN, 1, LOCAL_P_U, XT>(a, s);
   if (a.T <= 32) return launch_skinny<FN, 2, LOCAL_P_U, XT>(a, s);
-  return launch_skinny<FN, 4, (XT >= 4 || (FN >= 4 && XT >= 2) ? 1 : LOCAL_P_U), XT>(a, s);
+  return launch_skinny<FN, 4, (XT >= 4 || (FN >= 4 && XT >= 2) ? 1 : LOCAL_P_U64), XT>(a, s);
 }
 
 template <int XT>
@@ -922,6 +941,15 @@ local_status_t run_partial_xt(const GemmArgs& a, int fn, hipStream_t s) {
     if constexpr (XT <= 2) return launch_skinny<2, 8, (XT >= 1 ? 1 : LOCAL_P_U), XT>(a, s);
     return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d extra row tiles above 64 tokens", XT);
   }
+#if LOCAL_P_WIDE > 4
+  if (fn == LOCAL_P_WIDE) {  // the planner keeps it to T <= 32 and XT <= 2
+    if constexpr (XT <= 2) {
+      if (a.T <= 16) return launch_skinny<LOCAL_P_WIDE, 1, LOCAL_P_U, XT>(a, s);
+      return launch_skinny<LOCAL_P_WIDE, 2, (XT >= 2 ? 1 : LOCAL_P_U), XT>(a, s);
+    }
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: wide tile with %d row tiles", XT);
+  }
+#endif
   if (fn == 4) return run_partial_fn<4, XT>(a, s);
   if (fn == 3) return run_partial_fn<3, XT>(a, s);
   return run_partial_fn<2, XT>(a, s);
@@ -992,9 +1020,14 @@ DecodePlan plan_decode(int64_t T, int64_t K, int G, const Proj* p, int n_ad, int
   int64_t n_total = 0;
   for (int g = 0; g < G; ++g) n_total += p[g].N;
   const int64_t R = n_ad > 0 ? static_cast<int64_t>(n_ad) * r_max : 0;
-  d.shape = partial_shape(T, n_total, K);
-  const int64_t ftiles = (n_total + 16 * d.shape.fn - 1) / (16 * d.shape.fn);
+  d.shape = partial_shape(T, n_total, K, true);
+  int64_t ftiles = (n_total + 16 * d.shape.fn - 1) / (16 * d.shape.fn);
   d.xrows = partial_xrows(T, ftiles, G * R);
+  if (d.shape.fn > 4 && d.xrows > 32) {  // the wide tile takes at most 2 extra row tiles
+    d.shape = partial_shape(T, n_total, K, false);
+    ftiles = (n_total + 16 * d.shape.fn - 1) / (16 * d.shape.fn);
+    d.xrows = partial_xrows(T, ftiles, G * R);
+  }
   if (n_ad > 0 && d.xrows == 0) {
     if (G > 1) {
       d.split = true;

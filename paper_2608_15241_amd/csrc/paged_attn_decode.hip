@@ -98,16 +98,29 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a) {
   constexpr int KC = D / 32;  // 32-dim chunks of the QK product
   constexpr int VT = D / 16;  // 16-dim tiles of the PV product
 
-  const int g = blockIdx.x, b = blockIdx.y, part = blockIdx.z;
+  const int g = blockIdx.x, b = blockIdx.y;
   const int lane = threadIdx.x;
   const int col = lane % 16, kgrp = lane / 16;
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  // partition `part` covers blocks [nb - 32(part+1), nb - 32 part) of b
+  // Partition p covers blocks [nb - 32(p+1), nb - 32p) of b: the full ones
+  // first, counted from the end of the context, then at most one partial one
+  // at the start. blockIdx.z < n_parts takes full partition z, blockIdx.z =
+  // n_parts the partial one, so every full partition is dispatched before any
+  // partial one and the last waves to start are short. An empty context runs
+  // partition 0 with no block (zero output, lse = -inf).
+  const int n_full = nb / kBlocksPerPart, rem = nb % kBlocksPerPart;
+  int part;
+  if (blockIdx.z < static_cast<unsigned>(a.n_parts)) {
+    part = blockIdx.z;
+    if (part >= n_full && !(nb == 0 && part == 0)) return;
+  } else {
+    if (rem == 0) return;
+    part = n_full;
+  }
   const int j_end_part = nb - part * kBlocksPerPart;
-  if (j_end_part <= 0) return;
   const int j0 = max(0, j_end_part - kBlocksPerPart);
-  const int n_parts_b = (nb + kBlocksPerPart - 1) / kBlocksPerPart;
+  const int n_parts_b = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
   const int G = a.group;
@@ -293,7 +306,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   const int d = threadIdx.x;
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  const int np = (nb + kBlocksPerPart - 1) / kBlocksPerPart;
+  const int np = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
   if (np == 1) return;  // written by the main kernel
   float M = kNegBig;
   const float* ml = a.part_ml + static_cast<int64_t>(bh) * a.n_parts * 2;
@@ -315,7 +328,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
 
 template <int D>
 local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
-  dim3 grid(a.Hkv, B, a.n_parts);
+  dim3 grid(a.Hkv, B, a.n_parts + 1);  // full partitions, then the partial ones
   decode_attn_kernel<D, LOCAL_DECODE_DEPTH><<<grid, kWave, 0, s>>>(a);
   if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
   return local_check_launch("paged_attn_decode");

@@ -121,6 +121,25 @@ def test_decode_degenerate_cases():
     assert np.array_equal(host_u16(out)[2], vn[2].reshape(Hkv, D))
 
 
+@pytest.mark.parametrize("max_blocks", [4, 80])
+def test_decode_empty_context(max_blocks):
+    # An empty context has no key: zero output and lse = -inf, also when the
+    # table is narrow enough for a single partition (no merge pass), and no
+    # append (the token position L-1 does not exist).
+    say("decode empty context", max_blocks)
+    rng = np.random.default_rng(40 + max_blocks)
+    c = _decode_case(rng, [0, 33, 0, 50], 8, 2, 128, stale_frac=0.0,
+                     max_blocks=max_blocks)
+    out, lse, kc_d, vc_d = _run_decode(c)
+    ro, rl, rkc, rvc = _oracle_decode(c)
+    o, l = f64(out), lse.cpu().numpy()
+    for b in (0, 2):
+        assert np.all(o[b] == 0.0) and np.all(np.isneginf(l[b]))
+    assert_rel(o, ro, "out")
+    assert_lse(l, rl, "lse")
+    assert np.array_equal(host_u16(kc_d), rkc) and np.array_equal(host_u16(vc_d), rvc)
+
+
 def test_decode_wide_block_table_and_batch():
     rng = np.random.default_rng(8)
     ctx = rng.integers(1, 700, size=97)

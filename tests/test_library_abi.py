@@ -135,12 +135,12 @@ def test_lora_linear_grouped_workspace_and_errors(lib):
     ptrs = lambda n: (P * n)(*([FAKE] * n))
     Ns = (ctypes.c_int64 * 3)(4096, 4096, 4096)
     # q, k, v of a 7B layer at T=32 with 8 rank-16 adapters: one virtual weight
-    # of 12288 rows in 48-row tiles (256 workgroups, K not split), the shrink
-    # fused (3 x 128 stacked rows): base sums 32 x 12288 fp32, shrink sums
-    # 32 x 384 fp32
+    # of 12288 rows in 96-row tiles, K in 2 slices (256 workgroups), the shrink
+    # fused (3 x 128 stacked rows): base sums 2 x 32 x 12288 fp32, shrink sums
+    # 2 x 32 x 384 fp32
     st, n = _size(f, FAKE, 32, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 8, 16, None, FAKE,
                   FAKE, ptrs(3))
-    assert st == OK and n == 32 * 12288 * 4 + 32 * 384 * 4
+    assert st == OK and n == 2 * 32 * 12288 * 4 + 2 * 32 * 384 * 4
     assert _size(f, FAKE, 32, 4096, 0, ptrs(1), Ns, None, None, 0, 0, None, None, None,
                  ptrs(1))[0] == ERR_UNSUPPORTED
     assert _size(f, FAKE, 32, 4096, 5, ptrs(5), Ns, None, None, 0, 0, None, None, None,
