@@ -10,6 +10,9 @@
 //          wavefront ballots. The order is the canonical (b, j) order for
 //          any number of workgroups, so the result is exact and
 //          deterministic without atomics.
+// (One launch for small tables, as a single workgroup scanning stale flags in
+// table order or as per-request workgroups recounting the earlier requests,
+// measured no faster: the check is bound by its chain of dependent loads.)
 #include "common.hpp"
 
 namespace localk {
@@ -31,6 +34,7 @@ __device__ __forceinline__ int owned_blocks(int L, int max_blocks) {
 }
 
 // Sums two ints over the workgroup; every thread gets the totals.
+template <int WAVES = kVcWaves>
 __device__ __forceinline__ void block_sum2(int& a, int& b, int* lds) {
   for (int off = kWave / 2; off > 0; off >>= 1) {
     a += __shfl_xor(a, off);
@@ -44,11 +48,44 @@ __device__ __forceinline__ void block_sum2(int& a, int& b, int* lds) {
   __syncthreads();
   a = 0;
   b = 0;
-  for (int w = 0; w < kVcWaves; ++w) {
+  for (int w = 0; w < WAVES; ++w) {
     a += lds[2 * w];
     b += lds[2 * w + 1];
   }
   __syncthreads();
+}
+
+// Stale pairs of request b in ascending j from `running` on (capped), with
+// wavefront ballots; returns the new running count. All threads must call it.
+template <int THREADS>
+__device__ int64_t emit_request(const int32_t* row, int nb, const int32_t* block_version,
+                                int64_t num_blocks, int rv, int b, int64_t running,
+                                int32_t* stale_pairs, int64_t cap, int* wave_tot) {
+  constexpr int WAVES = THREADS / kWave;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int base = 0; base < nb; base += THREADS) {
+    const int j = base + threadIdx.x;
+    const bool st = j < nb && is_stale(row, block_version, num_blocks, rv, j);
+    const uint64_t mask = __ballot(st);
+    const int before = __popcll(mask & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_tot[wave] = __popcll(mask);
+    __syncthreads();
+    int wave_off = 0, total = 0;
+    for (int w = 0; w < WAVES; ++w) {
+      if (w < wave) wave_off += wave_tot[w];
+      total += wave_tot[w];
+    }
+    if (st) {
+      const int64_t idx = running + wave_off + before;
+      if (idx < cap) {
+        stale_pairs[2 * idx] = b;
+        stale_pairs[2 * idx + 1] = j;
+      }
+    }
+    running += total;
+    __syncthreads();
+  }
+  return running;
 }
 
 __global__ __launch_bounds__(kVcThreads) void version_count_kernel(
@@ -87,7 +124,6 @@ __global__ __launch_bounds__(kVcThreads) void version_emit_kernel(
   __shared__ int lds[2 * kVcWaves];
   __shared__ int wave_tot[kVcWaves];
   const int b = blockIdx.x;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   // offset of request b = counts[0] + ... + counts[b-1]
   int off = 0, dummy = 0;
   for (int i = threadIdx.x; i < b; i += kVcThreads) off += counts[i];
@@ -97,29 +133,8 @@ __global__ __launch_bounds__(kVcThreads) void version_emit_kernel(
   const int nb = owned_blocks(L, max_blocks);
   const int rv = req_version[b];
   const int32_t* row = block_table + static_cast<int64_t>(b) * max_blocks;
-  int64_t running = off;
-  for (int base = 0; base < nb; base += kVcThreads) {
-    const int j = base + threadIdx.x;
-    const bool st = j < nb && is_stale(row, block_version, num_blocks, rv, j);
-    const uint64_t mask = __ballot(st);
-    const int before = __popcll(mask & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_tot[wave] = __popcll(mask);
-    __syncthreads();
-    int wave_off = 0, total = 0;
-    for (int w = 0; w < kVcWaves; ++w) {
-      if (w < wave) wave_off += wave_tot[w];
-      total += wave_tot[w];
-    }
-    if (st) {
-      const int64_t idx = running + wave_off + before;
-      if (idx < cap) {
-        stale_pairs[2 * idx] = b;
-        stale_pairs[2 * idx + 1] = j;
-      }
-    }
-    running += total;
-    __syncthreads();
-  }
+  const int64_t running = emit_request<kVcThreads>(row, nb, block_version, num_blocks, rv, b,
+                                                   off, stale_pairs, cap, wave_tot);
   if (b == B - 1 && threadIdx.x == 0) *n_stale_out = static_cast<int32_t>(running);
 }
 

@@ -88,3 +88,23 @@ def test_tags_are_never_written():
     lk.local_block_version_check(dev(m.block_table), dev(m.ctx_lens), bv, dev(m.req_version))
     torch.cuda.synchronize()
     assert torch.equal(bv, before)
+
+
+def test_small_tables():
+    # Small tables: random stale tags, empty contexts, truncated lists.
+    rng = np.random.default_rng(77)
+    for trial in range(10):
+        B = int(rng.integers(1, 33))
+        mb = int(rng.integers(1, 8192 // B + 1))
+        ctx = rng.integers(0, 16 * mb + 1, size=B).astype(np.int32)
+        ctx[rng.random(B) < 0.15] = 0
+        table, num = make_table(rng, ctx, extra_blocks=3, max_blocks=mb)
+        rv = (rng.integers(1, 20, size=B) * 1000).astype(np.int32)
+        bv = np.zeros(num, np.int32)
+        for b in range(B):
+            nb = (ctx[b] + 15) // 16
+            bv[table[b, :nb]] = rv[b] + rng.choice([0, 0, 0, -1, 1], size=nb)
+        say("version check small table", trial, "B", B, "mb", mb)
+        n = _compare(table, ctx, bv, rv)
+        for cap in (0, 1, max(0, n // 2)):
+            _compare(table, ctx, bv, rv, cap=cap)
