@@ -21,14 +21,16 @@
 //    - epilogue: sums the base slices, forms U_s = bf16(s_t * u) for the
 //      token's own adapter and rank, adds U_s B_a^T and the residual, and
 //      rounds once to bf16.
-//  * Long prefill chunks: the shrink is one product of x with all adapters'
-//    stacked A whose epilogue keeps only the token's own adapter and rank,
-//    U_s[t, a*r_max + j] = bf16(s_t * x_t . A[a,j,:]); the main product runs
-//    the delta U_s Btilde^T (Btilde[n, a*r_max + j] = B[a, n, j]) as extra
-//    K-steps, only over adapters used in the tile and columns below their
-//    rank. 128x128 tiles, 2x2 waves, register prefetch into an LDS double
-//    buffer with padded rows, XCD-aware grouped tile order so each XCD's L2
-//    serves an 8x8 block of tiles.
+//  * Long prefill chunks (T > 256), two kernels:
+//    - shrink: workgroups of 32 tokens x one K slice compute, for each
+//      adapter routed in the tile, x_t . A[a,j,:] of its tokens on the matrix
+//      cores; fp32 partial sums per slice.
+//    - main product: 128 tokens x 256 features per workgroup, both operands
+//      brought to LDS by direct global-to-LDS loads in a three-stage ring;
+//      the delta U_s Btilde^T (U_s[t, a*r_max + j] = bf16(s_t * sum of the
+//      slices), zero unless a is t's adapter; Btilde[n, a*r_max + j] =
+//      B[a, n, j]) runs as extra K-steps, only over adapters used in the tile
+//      and columns below their rank.
 //  Both paths sum the base K-steps in an order that does not depend on which
 //  adapters are present, so a zero up-projection leaves y bit-identical.
 #include "common.hpp"
@@ -36,28 +38,18 @@
 namespace localk {
 namespace {
 
-constexpr int kGemmThreads = 256;       // tiled kernel
 constexpr int kSkThreads = 512;         // skinny kernel (8 waves)
 constexpr int kSkWaves = kSkThreads / kWave;
-constexpr int kBK = 64;
-constexpr int kLdsK = kBK + 8;          // padded LDS row (144 bytes): conflict-free reads
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kRedTiles = 8;            // skinny kernel: tiles per LDS reduction round
 constexpr int kMaxGroup = 4;            // projections sharing x in one grouped call
 constexpr int kNumXcd = 8;
 
-#ifndef LOCAL_SK_U32
-#define LOCAL_SK_U32 4     // K-steps of 64 per batch of loads, 32-token tiles
-#endif
-
-enum GemmMode { kModeMain = 0, kModeShrink = 1, kModePartial = 2 };
-
 struct GemmArgs {
   const uint16_t* x;     // [T][K]
   const uint16_t* w;     // main: W [N][K]; shrink: stacked A [R][K]
-  int64_t T, K, N;       // N = output width (R in shrink mode)
-  const uint16_t* us;    // U_s [T][R] bf16 (tiled main kernel, adapters present)
-  float* pout;           // SGMV shrink: fp32 partial sums [up_ks][T][r_max]
+  int64_t T, K, N;       // N = output width
+  float* pout;           // shrink: fp32 partial sums [up_ks][T][p_stride]
   int up_ks;             // K slices of the shrink partial sums
   float* part;           // partial mode: fp32 base partial sums [ksplit][T][N]
   int xrows;             // stacked-A rows per feature-tile workgroup (0 = none)
@@ -67,7 +59,7 @@ struct GemmArgs {
   // per projection.
   int G;
   int64_t gstart[kMaxGroup + 1];
-  const uint16_t* gw[kMaxGroup];     // W_g [N_g][K] (skinny shrink mode: stacked A)
+  const uint16_t* gw[kMaxGroup];     // W_g [N_g][K]
   const uint16_t* ga[kMaxGroup];     // A_g [n_ad][r_max][K]
   const uint16_t* gb[kMaxGroup];     // B_g [n_ad][N_g][r_max]
   const int32_t* granks[kMaxGroup];  // ranks_g [n_ad] or null
@@ -81,11 +73,9 @@ struct GemmArgs {
   const float* scale;    // [T]
   int n_ad, r_max, R;
   const uint16_t* res;   // optional residual [T][N] (main mode)
-  uint16_t* y;           // bf16 output [T][N] (U_s in shrink mode)
+  uint16_t* y;           // bf16 output [T][N]
   int ksplit;            // K slices of the skinny kernel (grid.z); 1 = whole K
-  int mode;
-  int gm, gn;            // tile grid of the tiled kernel
-  int swizzle;           // XCD-aware grouped order (tiled kernel)
+  int gm, gn;            // tile grid of the long-chunk main product
 };
 
 // Rank of adapter ad, clamped to [0, r_max] so that no rank reads past the
@@ -130,22 +120,12 @@ __device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad)
   return (present[ad >> 6] >> (ad & 63)) & 1ull;
 }
 
-// Store features n..n+3 of token t (bounds-checked): the shrink mask and
-// scale, or the residual, then one rounding to bf16.
+// Store features n..n+3 of token t (bounds-checked): the residual, then one
+// rounding to bf16.
 __device__ __forceinline__ void store4(const GemmArgs& a, int64_t t, int64_t n, f32x4 v) {
   if (t >= a.T || n >= a.N) return;
   float o[4] = {v[0], v[1], v[2], v[3]};
-  if (a.mode == kModeShrink) {
-    int ad = a.idx ? a.idx[t] : -1;
-    if (ad >= a.n_ad) ad = -1;  // indices outside [0, n_ad) mean no adapter
-    const float sc = ad >= 0 ? a.scale[t] : 0.f;
-    const int rk = ad >= 0 ? rank_of(a, ad) : 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = static_cast<int>(n) + e;
-      o[e] = (ad >= 0 && r / a.r_max == ad && r % a.r_max < rk) ? sc * o[e] : 0.f;
-    }
-  } else if (a.res) {
+  if (a.res) {
     const u32x2 r = ld_global<u32x2>(a.res + t * a.N + n);
     o[0] += __uint_as_float(r.x << 16);
     o[1] += __uint_as_float(r.x & 0xffff0000u);
@@ -203,6 +183,15 @@ __device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t
   return n;
 }
 
+// The first `keep` (clamped to 0..8) of 8 packed bf16 values; the rest zero.
+__device__ __forceinline__ u32x4 keep_first8(u32x4 v, int keep) {
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (e >= keep) w[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
 // 16-byte slice of Btilde row n at U_s column c (c % 8 == 0): zero when the
 // adapter is absent from the tile or the columns lie at or past its rank.
 __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* present,
@@ -227,9 +216,8 @@ __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* 
 // Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM) over the
 // z-th of ksplit slices of K; wave w takes a contiguous range of the slice's
 // 64-wide steps (U steps per batch of loads); partial tiles are summed through
-// LDS in wave order. Partial mode writes the slice's fp32 sum (decode base
-// product, finished by the epilogue kernel); shrink mode applies the adapter
-// mask and scale and writes U_s in bf16 (shrink of a long prefill chunk).
+// LDS in wave order and written as the slice's fp32 sum (decode base
+// product, finished by the epilogue kernel).
 // An 8-wave workgroup runs two waves per SIMD; telling the compiler so lets it
 // keep a whole batch of loads in registers instead of interleaving each load
 // with the MFMA that consumes it (which leaves one load in flight per wave).
@@ -385,12 +373,8 @@ void lora_skinny_kernel(GemmArgs a) {
         continue;
       }
       const int64_t n = n0 + 16 * i + 4 * (l / 16);
-      if (a.mode == kModePartial) {
-        if (t < a.T && n < a.N)
-          *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
-      } else {
-        store4(a, t, n, s);
-      }
+      if (t < a.T && n < a.N)
+        *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
     }
   }
 }
@@ -686,149 +670,477 @@ local_status_t run_epilogue(const GemmArgs& a, hipStream_t s) {
   }
 }
 
-// ------------------------------------------------------------------ tiled
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(kGemmThreads) void lora_tiled_kernel(GemmArgs a) {
-  constexpr int FN = BN / WN / 16;  // 16-row MFMA tiles per wave along features
-  constexpr int FM = BM / WM / 16;  // 16-col MFMA tiles per wave along tokens
-  constexpr int W_PIECES = BN * (kBK / 8) / kGemmThreads;
-  constexpr int X_PIECES = BM * (kBK / 8) / kGemmThreads;
-  static_assert(W_PIECES >= 1 && X_PIECES >= 1 && WM * WN == 4, "tile shape");
-  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  // LDS: W tiles [2][BN][kLdsK], then x tiles [2][BM][kLdsK]
-  auto w_lds = [&](int buf) { return smem + buf * (BN * kLdsK); };
-  auto x_lds = [&](int buf) { return smem + 2 * BN * kLdsK + buf * (BM * kLdsK); };
+// ----------------------------------------------------------------- prefill
+// Long chunks (T > 256), the fused main product. Workgroup: tokens
+// [m0, m0 + 128) x features [n0, n0 + 256); wave w owns features
+// n0 + 64w .. +64 for all 128 tokens (4 x 8 MFMA tiles, 128 fp32 accumulators
+// per lane). Both operands reach LDS by direct global-to-LDS loads (no
+// staging registers, no LDS store instructions): a K-step of 64 is one 48 KB
+// stage (x: 128 rows, W: 256 rows, 128 bytes each), three stages in a ring,
+// so the loads of step s + 2 are in flight while step s computes. Each load
+// instruction moves 8 whole 128-byte rows (64 lanes x 16 bytes), so the
+// vector memory path sees fully used lines. Inside a row the eight 16-byte
+// chunks are stored XOR-swizzled by the row index (chunk c of row r at
+// position c ^ (r % 8)): the MFMA operand reads (16 rows, one chunk column)
+// then touch distinct banks. The loads name their own waits (the library
+// waits on the load counter itself before each barrier). The LoRA delta
+// follows as extra K-steps over the U_s columns of the adapters used in the
+// token tile.
+constexpr int kPfM = 128;
+constexpr int kPfN = 256;
+constexpr int kPfThreads = 256;
+constexpr int kPfWaves = kPfThreads / kWave;
+constexpr int kPfFT = 4;   // 16-feature MFMA tiles per wave
+constexpr int kPfTT = 8;   // 16-token MFMA tiles
+constexpr int kPfRow = 128;                       // bytes of one row of a stage
+constexpr int kPfXBytes = kPfM * kPfRow;          // 16 KB
+constexpr int kPfStageBytes = (kPfM + kPfN) * kPfRow;  // 48 KB
+constexpr int kPfStages = 3;
+constexpr int kPfURow = 80;                       // bytes of a U_s tile row: 32 bf16 + pad
+constexpr int kPfUBytes = kPfM * kPfURow;         // 10 KB
+constexpr int kPfLdsBytes = kPfStages * kPfStageBytes + kPfUBytes;  // 154 KB
+constexpr int kPfXDma = kPfM / 8 / kPfWaves;      // 1 KB loads of x per wave and step (4)
+constexpr int kPfWDma = kPfN / 8 / kPfWaves;      // ... of W (8)
+constexpr int kPfDma = kPfXDma + kPfWDma;         // 12
+
+// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
+// operations are outstanding / until all LDS operations are done.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkm0_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t pf_lds[];
   __shared__ uint64_t present[4];
   __shared__ uint16_t chunks[kMaxLoraChunks];
-  __shared__ int wave_cnt[4];
+  __shared__ int wave_cnt[kPfWaves];
 
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: LDS bases in SGPRs
   const int col = lane % 16, kgrp = lane / 16;
 
-  // ---- tile coordinates (XCD-aware grouped order)
+  // ---- tile coordinates: XCD-aware grouped order (the blocks of one XCD
+  // take an 8-tall column of tiles, so its L2 serves x and W rows in common)
   int mt, nt;
   {
     const int id = blockIdx.x;
     const int total = a.gm * a.gn;
     int lid = id;
-    if (a.swizzle && total % kNumXcd == 0) lid = (id % kNumXcd) * (total / kNumXcd) + id / kNumXcd;
-    if (a.swizzle) {
-      constexpr int GM = 8;
-      const int group = lid / (GM * a.gn);
-      const int first_m = group * GM;
-      const int gsize = min(a.gm - first_m, GM);
-      const int r = lid % (GM * a.gn);
-      mt = first_m + r % gsize;
-      nt = r / gsize;
-    } else {
-      mt = lid % a.gm;
-      nt = lid / a.gm;
-    }
+    if (total % kNumXcd == 0) lid = (id % kNumXcd) * (total / kNumXcd) + id / kNumXcd;
+    constexpr int GM = 8;
+    const int group = lid / (GM * a.gn);
+    const int first_m = group * GM;
+    const int gsize = min(a.gm - first_m, GM);
+    const int r = lid % (GM * a.gn);
+    mt = first_m + r % gsize;
+    nt = r / gsize;
   }
-  const int64_t m0 = static_cast<int64_t>(mt) * BM;
-  const int64_t n0 = static_cast<int64_t>(nt) * BN;
+  const int64_t m0 = static_cast<int64_t>(mt) * kPfM;
+  const int64_t n0 = static_cast<int64_t>(nt) * kPfN;
+  const int64_t fw0 = n0 + 64 * wave;  // this wave's first feature
 
   int n_chunks = 0;
-  if (a.mode == kModeMain && a.n_ad > 0 && a.us != nullptr) {
-    static_assert(BM <= kGemmThreads, "one token per thread");
-    const int my_ad = tid < BM ? token_adapter(a, m0 + tid) : -1;
-    n_chunks = lora_chunk_list<kGemmThreads>(a, my_ad, kBK, present, chunks, wave_cnt);
+  if (a.n_ad > 0 && a.pout != nullptr) {
+    const int my_ad = tid < kPfM ? token_adapter(a, m0 + tid) : -1;
+    n_chunks = lora_chunk_list<kPfThreads>(a, my_ad, 32, present, chunks, wave_cnt);
   }
-  const int k_main = static_cast<int>(a.K / kBK);
-  const int s_end = k_main + n_chunks;
 
-  // ---- global -> register loaders for one K-step
-  u32x4 wreg[W_PIECES], xreg[X_PIECES];
-  auto load_step = [&](int s) {
-    if (s < k_main) {
-      const int64_t k0 = static_cast<int64_t>(s) * kBK;
+  // ---- direct loads. Wave w moves x rows 32w .. +32 and W rows 64w .. +64
+  // (its own features) of every stage; lane l writes 16 bytes at
+  // block + 16 l, i.e. row 8q + l/8, position l%8, which holds chunk
+  // (l%8) ^ (l/8) of that row. Rows past T (N) repeat row m0 (row 0): their
+  // accumulators are never stored.
+  const int dchunk = (lane % 8) ^ (lane / 8);
+  const uint16_t* xg[kPfXDma];
+  const uint16_t* wg[kPfWDma];
 #pragma unroll
-      for (int i = 0; i < W_PIECES; ++i) {
-        const int piece = tid + i * kGemmThreads;
-        const int r = piece / 8, kp = piece % 8;
-        const int64_t n = n0 + r;
-        wreg[i] = n < a.N ? ld_global<u32x4>(a.w + n * a.K + k0 + 8 * kp) : u32x4{0u, 0u, 0u, 0u};
-      }
+  for (int q = 0; q < kPfXDma; ++q) {
+    const int64_t t = m0 + 32 * wave + 8 * q + lane / 8;
+    xg[q] = a.x + (t < a.T ? t : m0) * a.K + 8 * dchunk;
+  }
 #pragma unroll
-      for (int i = 0; i < X_PIECES; ++i) {
-        const int piece = tid + i * kGemmThreads;
-        const int r = piece / 8, kp = piece % 8;
-        const int64_t t = m0 + r;
-        xreg[i] = t < a.T ? ld_global<u32x4>(a.x + t * a.K + k0 + 8 * kp) : u32x4{0u, 0u, 0u, 0u};
-      }
-    } else {
-      const int c0 = chunks[s - k_main] * kBK;
+  for (int q = 0; q < kPfWDma; ++q) {
+    const int64_t n = fw0 + 8 * q + lane / 8;
+    wg[q] = a.w + (n < a.N ? n : 0) * a.K + 8 * dchunk;
+  }
+  // loads of K-step s into stage `stage`
+  auto issue = [&](int stage, int s) {
+    uint8_t* st = pf_lds + stage * kPfStageBytes;
+    const int64_t k = static_cast<int64_t>(s) * 64;
 #pragma unroll
-      for (int i = 0; i < W_PIECES; ++i) {
-        const int piece = tid + i * kGemmThreads;
-        wreg[i] = load_btilde(a, present, n0 + piece / 8, c0 + 8 * (piece % 8));
-      }
+    for (int q = 0; q < kPfXDma; ++q)
+      __builtin_amdgcn_global_load_lds(xg[q] + k, st + (32 * wave + 8 * q) * kPfRow, 16, 0, 0);
 #pragma unroll
-      for (int i = 0; i < X_PIECES; ++i) {
-        const int piece = tid + i * kGemmThreads;
-        const int64_t t = m0 + piece / 8;
-        const int c = c0 + 8 * (piece % 8);
-        xreg[i] = (t < a.T && c < a.R) ? ld_global<u32x4>(a.us + t * a.R + c)
-                                       : u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  };
-  auto store_step = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < W_PIECES; ++i) {
-      const int piece = tid + i * kGemmThreads;
-      *reinterpret_cast<u32x4*>(w_lds(buf) + (piece / 8) * kLdsK + 8 * (piece % 8)) = wreg[i];
-    }
-#pragma unroll
-    for (int i = 0; i < X_PIECES; ++i) {
-      const int piece = tid + i * kGemmThreads;
-      *reinterpret_cast<u32x4*>(x_lds(buf) + (piece / 8) * kLdsK + 8 * (piece % 8)) = xreg[i];
-    }
+    for (int q = 0; q < kPfWDma; ++q)
+      __builtin_amdgcn_global_load_lds(wg[q] + k, st + kPfXBytes + (64 * wave + 8 * q) * kPfRow,
+                                       16, 0, 0);
   };
 
-  f32x4 acc[FN][FM];
+  f32x4 acc[kPfFT][kPfTT];
 #pragma unroll
-  for (int i = 0; i < FN; ++i)
+  for (int i = 0; i < kPfFT; ++i)
 #pragma unroll
-    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < kPfTT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int wn = wave % WN, wm = wave / WN;
-  const int wrow0 = wn * (BN / WN);  // this wave's first feature row in the tile
-  const int wcol0 = wm * (BM / WM);  // this wave's first token column
-
-  load_step(0);
-  store_step(0);
-  __syncthreads();
-  int cur = 0;
-  for (int s = 0; s < s_end; ++s) {
-    const bool more = s + 1 < s_end;
-    if (more) load_step(s + 1);
+  // MFMA operand reads. K-group g of MFMA m holds k = 32m + 8g .. +8 of the
+  // step (chunk 4m + g), the same for W and x; chunk c of row r sits at
+  // position c ^ (r % 8), and r % 8 = col % 8 for every row a lane reads.
+  const int rd0 = col * kPfRow + 16 * (kgrp ^ (col % 8));  // chunk kgrp
+  const int rd1 = rd0 ^ 64;                                 // chunk 4 + kgrp
+  u32x4 xf[2][kPfTT], wf[2][kPfFT];
+  auto read_half = [&](int stage, int m) {
+    const uint8_t* st = pf_lds + stage * kPfStageBytes + (m ? rd1 : rd0);
 #pragma unroll
-    for (int kk = 0; kk < kBK / 32; ++kk) {
-      bf16x8 af[FN], bfr[FM];
+    for (int i = 0; i < kPfFT; ++i)
+      wf[m][i] = *reinterpret_cast<const u32x4*>(st + kPfXBytes + (64 * wave + 16 * i) * kPfRow);
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
-        af[i] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            w_lds(cur) + (wrow0 + 16 * i + col) * kLdsK + 32 * kk + 8 * kgrp));
+    for (int j = 0; j < kPfTT; ++j) xf[m][j] = *reinterpret_cast<const u32x4*>(st + 16 * j * kPfRow);
+  };
+  // MFMAs [b, e) of half m, in the order tile (i, j) = (idx / 8, idx % 8)
+  auto mfma_range = [&](int m, int b, int e) {
 #pragma unroll
-      for (int j = 0; j < FM; ++j)
-        bfr[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            x_lds(cur) + (wcol0 + 16 * j + col) * kLdsK + 32 * kk + 8 * kgrp));
-#pragma unroll
-      for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+    for (int idx = b; idx < e; ++idx) {
+      const int i = idx / kPfTT, j = idx % kPfTT;
+      acc[i][j] = mfma16x16x32(as_bf16x8(wf[m][i]), as_bf16x8(xf[m][j]), acc[i][j]);
     }
-    if (more) store_step(cur ^ 1);
+  };
+  // instruction-group masks of the scheduler's group barriers
+  constexpr int kSgMfma = 0x8, kSgVmem = 0x10, kSgDsRead = 0x100;
+
+  // Step s (stage s % 3), first half: the m = 1 operands are read under the
+  // m = 0 MFMAs. Then each wave waits for its own loads of step s + 1 (those
+  // of step s + 2 may stay in flight) and for its reads of stage s % 3; after
+  // the barrier every wave's loads of step s + 1 are visible and stage s % 3
+  // is free, so the loads of step s + 3 refill it. Second half: the m = 0
+  // operands of step s + 1 are read under the m = 1 MFMAs of step s. The
+  // body has no branch (a branch between the two halves makes the compiler
+  // copy the 128 accumulators around it): past the last step the loads
+  // repeat the last step into the free stage and the reads fetch operands
+  // that are never used, so every wait count holds at every step.
+  const int steps = static_cast<int>(a.K / 64);
+  const int last = steps - 1;
+  auto prologue_loads = [&]() {
+    issue(0, 0);
+    issue(1, min(1, last));
+    issue(2, min(2, last));
+  };
+
+  // ---- LoRA delta first, chunk by chunk (32 stacked columns
+  // c = a*r_max + j): U_s[t][c] = bf16(s_t * sum_z P[z][t][j]) (slices in
+  // order) when a is token t's adapter, else 0, formed by the whole
+  // workgroup into an LDS tile; Btilde is zero at or past the rank. The
+  // first chunk's loads are issued before the stage loads of the main
+  // product, so their latency overlaps. Adding the delta first leaves a zero
+  // up-projection's result bit-identical (the MFMAs add +0).
+  __builtin_amdgcn_s_waitcnt(0);
+  bool staged = false;
+  if (n_chunks > 0) {
+    uint8_t* ut = pf_lds + kPfStages * kPfStageBytes;  // [128 tokens][kPfURow]
+    const int ftl = tid / 2, fh = tid % 2;            // forming: token, 16-column half
+    const int64_t ft = m0 + ftl;
+    const int64_t ftc = ft < a.T ? ft : m0;
+    const int fidx = a.idx[ftc];
+    const float fscl = a.scale[ftc];
+    const int64_t slice = a.T * a.r_max;
+    // Every load of a chunk is issued unconditionally (clamped to valid
+    // addresses) and masked afterwards, so that all of them are in flight
+    // together.
+    for (int q = 0; q < n_chunks; ++q) {
+      const int c0 = chunks[q] * 32;
+      // Btilde operand: features fw0 + 16i + col, columns cb .. cb+8
+      const int cb = c0 + 8 * kgrp;
+      const int bad = min(cb / a.r_max, a.n_ad - 1), bj = cb % a.r_max;
+      const int brk = a.ranks ? a.ranks[bad] : a.r_max;
+      u32x4 bw[kPfFT];
+#pragma unroll
+      for (int i = 0; i < kPfFT; ++i) {
+        const int64_t n = fw0 + 16 * i + col;
+        bw[i] = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(bad) * a.N + (n < a.N ? n : 0)) *
+                                              a.r_max + bj);
+      }
+      // forming: columns c0 + 16 fh + 8g, g = 0, 1 (8 columns of one adapter)
+      int frk[2];
+      int64_t off[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int c = c0 + 16 * fh + 8 * g;
+        frk[g] = a.ranks ? a.ranks[min(c / a.r_max, a.n_ad - 1)] : a.r_max;
+        off[g] = (ft < a.T ? ft : m0) * a.r_max + c % a.r_max;
+      }
+      f32x4 sum[2][2] = {};
+      for (int z0 = 0; z0 < a.up_ks; z0 += 4) {
+        f32x4 v[4][2][2];
+#pragma unroll
+        for (int dz = 0; dz < 4; ++dz)
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+            const int64_t o = static_cast<int64_t>(min(z0 + dz, a.up_ks - 1)) * slice + off[g];
+            v[dz][g][0] = ld_global<f32x4>(a.pout + o);
+            v[dz][g][1] = ld_global<f32x4>(a.pout + o + 4);
+          }
+        if (!staged) {  // the main product's first stages, behind these loads
+          prologue_loads();
+          staged = true;
+        }
+#pragma unroll
+        for (int dz = 0; dz < 4; ++dz)
+          if (z0 + dz < a.up_ks)
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+              sum[g][0] += v[dz][g][0];
+              sum[g][1] += v[dz][g][1];
+            }
+      }
+      // U_s: zero unless the columns' adapter is the token's, and at or past
+      // its rank (padding rows of A may hold anything)
+      const int fad = (ft < a.T && fidx >= 0 && fidx < a.n_ad) ? fidx : -1;
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int c = c0 + 16 * fh + 8 * g;
+        const bool own = c < a.R && fad == c / a.r_max;
+        const int keep = own ? min(max(frk[g], 0), a.r_max) - c % a.r_max : 0;
+        float u[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sv = e < 4 ? sum[g][0][e] : sum[g][1][e - 4];
+          u[e] = e < keep ? fscl * sv : 0.f;
+        }
+        *reinterpret_cast<u32x4*>(ut + ftl * kPfURow + 32 * fh + 16 * g) =
+            u32x4{pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]), pack_bf16x2(u[4], u[5]),
+                  pack_bf16x2(u[6], u[7])};
+      }
+      // Btilde: zero for an adapter not routed in the tile, and at or past
+      // the rank
+      const int bkeep = (cb < a.R && adapter_present(present, bad))
+                            ? min(max(brk, 0), a.r_max) - bj : 0;
+      bf16x8 bv[kPfFT];
+#pragma unroll
+      for (int i = 0; i < kPfFT; ++i) bv[i] = as_bf16x8(keep_first8(bw[i], bkeep));
+      wait_lgkm0_barrier();
+      bf16x8 uv[kPfTT];
+#pragma unroll
+      for (int j = 0; j < kPfTT; ++j)
+        uv[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(ut + (16 * j + col) * kPfURow + 16 * kgrp));
+#pragma unroll
+      for (int i = 0; i < kPfFT; ++i)
+#pragma unroll
+        for (int j = 0; j < kPfTT; ++j) acc[i][j] = mfma16x16x32(bv[i], uv[j], acc[i][j]);
+      wait_lgkm0_barrier();  // the tile is rewritten by the next chunk
+    }
+  }
+  if (!staged) prologue_loads();
+  wait_vmcnt<0>();
+  wait_lgkm0_barrier();
+  read_half(0, 0);
+  // unrolled over the stage ring so that stage offsets are constants; the
+  // tail leaves the loop (a branch out of the loop, not around work in it)
+  for (int s0 = 0; s0 < steps; s0 += kPfStages) {
+#pragma unroll
+    for (int u = 0; u < kPfStages; ++u) {
+      const int s = s0 + u;
+      if (s >= steps) break;
+      // first half: one operand read (m = 1) beside each of the first 12
+      // MFMAs (m = 0)
+      read_half(u, 1);
+      mfma_range(0, 0, 32);
+#pragma unroll
+      for (int g = 0; g < 12; ++g) {
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, 20, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      // second half: 8 MFMAs (m = 1) before the barrier, then the operand
+      // reads of the next step and the loads of step s + 3 beside the rest
+      mfma_range(1, 0, 8);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<kPfDma>();
+      wait_lgkm0_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      read_half((u + 1) % kPfStages, 0);
+      issue(u, min(s + 3, last));
+      mfma_range(1, 8, 32);
+#pragma unroll
+      for (int g = 0; g < 12; ++g) {
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 1);
+      }
+#pragma unroll
+      for (int g = 0; g < 12; ++g) {
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(kSgVmem, 1, 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  wait_vmcnt<0>();
+
+#pragma unroll
+  for (int j = 0; j < kPfTT; ++j)
+#pragma unroll
+    for (int i = 0; i < kPfFT; ++i)
+      store4(a, m0 + 16 * j + col, fw0 + 16 * i + 4 * kgrp, acc[i][j]);
+}
+
+// ------------------------------------------------------------ long shrink
+// Long chunks (T > 256): the shrink as SGMV partial sums over K slices,
+//   P[z][t][j] = sum over slice z of x[t][k] A[a_t][j][k],   j < r_max,
+// for the token's own adapter a_t only. Workgroup: 32 tokens x one K slice
+// of sps 64-k steps. The x slice (32 rows) and then, adapter by adapter
+// (those routed in the token tile), the A slice (r_max rows padded to 16)
+// are brought to LDS by direct loads in one go, in the 128-byte rows and
+// chunk swizzle of the main product; the four waves take every fourth
+// 64-k step and their partial tiles are summed through LDS in wave order.
+constexpr int kShTok = 32;
+constexpr int kShThreads = 256;
+constexpr int kShWaves = kShThreads / kWave;
+constexpr size_t kShLdsMax = 147456;
+
+struct ShrinkShape {
+  int ks;      // K slices (grid.y)
+  int sps;     // 64-k steps per slice
+  int rpad;    // r_max rounded up to 16
+  size_t lds;  // dynamic LDS bytes
+};
+
+size_t shrink_lds(int sps, int rpad) {
+  return static_cast<size_t>(kShTok + rpad) * sps * 128 +
+         static_cast<size_t>(kShWaves) * (2 * rpad / 16) * kWave * sizeof(f32x4);
+}
+
+// Fewest K slices (a divisor of the step count) that fit LDS and give at
+// least one workgroup per compute unit, at most kShMaxSlices of them unless
+// LDS needs more (the main product sums the slices for every U_s value it
+// uses).
+constexpr int kShMaxSlices = 8;
+ShrinkShape shrink_shape(int64_t T, int64_t K, int r_max) {
+  const int steps = static_cast<int>(K / 64);
+  const int rpad = (r_max + 15) / 16 * 16;
+  const int64_t tiles = (T + kShTok - 1) / kShTok;
+  ShrinkShape best{steps, 1, rpad, shrink_lds(1, rpad)};
+  for (int ks = 1; ks <= steps; ++ks) {
+    if (steps % ks) continue;
+    const int sps = steps / ks;
+    const size_t lds = shrink_lds(sps, rpad);
+    if (lds > kShLdsMax) continue;
+    best = ShrinkShape{ks, sps, rpad, lds};
+    if (tiles * ks >= 256 || ks >= kShMaxSlices) break;
+  }
+  return best;
+}
+
+template <int RT>
+__global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a, int sps) {
+  constexpr int rpad = 16 * RT;
+  extern __shared__ __attribute__((aligned(16))) uint8_t sh_lds[];
+  __shared__ int ad_list[kShTok];
+  __shared__ int n_list;
+
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int col = lane % 16, kgrp = lane / 16;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kShTok;
+  const int z = blockIdx.y;
+  const int64_t k0 = static_cast<int64_t>(z) * sps * 64;
+  uint8_t* xl = sh_lds;                                   // [sps][32][128 B]
+  uint8_t* al = sh_lds + static_cast<size_t>(sps) * kShTok * 128;  // [sps][rpad][128 B]
+  f32x4* red = reinterpret_cast<f32x4*>(al + static_cast<size_t>(sps) * rpad * 128);
+
+  // adapters routed in the tile, in order of first appearance
+  if (wave == 0) {
+    const int my = lane < kShTok ? token_adapter(a, t0 + lane) : -1;
+    uint64_t pending = __ballot(my >= 0);
+    int n = 0;
+    while (pending) {
+      const int ad = __shfl(my, __ffsll(static_cast<long long>(pending)) - 1);
+      if (lane == 0) ad_list[n] = ad;
+      ++n;
+      pending &= ~__ballot(my == ad);
+    }
+    if (lane == 0) n_list = n;
+  }
+
+  // direct loads as in the main product: lane l writes 16 bytes at
+  // block + 16 l = row 8b + l/8, position l%8, holding chunk (l%8) ^ (l/8)
+  const int dchunk = (lane % 8) ^ (lane / 8);
+  {
+    const int64_t t = t0 + 8 * wave + lane / 8;  // wave w moves rows 8w .. +8 of every step
+    const uint16_t* src = a.x + (t < a.T ? t : t0) * a.K + k0 + 8 * dchunk;
+    for (int st = 0; st < sps; ++st)
+      __builtin_amdgcn_global_load_lds(src + 64 * st, xl + (st * kShTok + 8 * wave) * 128, 16, 0,
+                                       0);
+  }
+  wait_vmcnt<0>();
+  wait_lgkm0_barrier();
+  const int n_ad_tile = n_list;
+
+  const int rd0 = col * 128 + 16 * (kgrp ^ (col % 8));
+  const int rd1 = rd0 ^ 64;
+  const int64_t slice = a.T * a.r_max;
+  for (int q = 0; q < n_ad_tile; ++q) {
+    const int ad = ad_list[q];
+    // A rows of the adapter (rows past r_max repeat its last row: never stored)
+    for (int b = wave; b < sps * (rpad / 8); b += kShWaves) {
+      const int st = b / (rpad / 8), rb = b % (rpad / 8);
+      const int j = min(8 * rb + lane / 8, a.r_max - 1);
+      __builtin_amdgcn_global_load_lds(
+          a.w + (static_cast<int64_t>(ad) * a.r_max + j) * a.K + k0 + 64 * st + 8 * dchunk,
+          al + (st * rpad + 8 * rb) * 128, 16, 0, 0);
+    }
+    wait_vmcnt<0>();
+    wait_lgkm0_barrier();
+
+    f32x4 acc[2][RT];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[tt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int st = wave; st < sps; st += kShWaves) {
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const int rd = m ? rd1 : rd0;
+        u32x4 xf[2], af[RT];
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+          xf[tt] = *reinterpret_cast<const u32x4*>(xl + (st * kShTok + 16 * tt) * 128 + rd);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+          af[rt] = *reinterpret_cast<const u32x4*>(al + (st * rpad + 16 * rt) * 128 + rd);
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+            acc[tt][rt] = mfma16x16x32(as_bf16x8(af[rt]), as_bf16x8(xf[tt]), acc[tt][rt]);
+      }
+    }
+    // sum the four waves' tiles in wave order; lane l of tile (tt, rt) holds
+    // rank rows 16rt + 4(l/16) .. +4 of token 16tt + l%16
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) red[((wave * 2 + tt) * RT + rt) * kWave + lane] = acc[tt][rt];
     __syncthreads();
-    cur ^= 1;
+    for (int item = tid; item < 2 * RT * kWave; item += kShThreads) {
+      const int tile = item / kWave, ln = item % kWave;
+      f32x4 v = red[tile * kWave + ln];
+#pragma unroll
+      for (int w = 1; w < kShWaves; ++w) v += red[(w * 2 * RT + tile) * kWave + ln];
+      const int tt = tile / RT, rt = tile % RT;
+      const int64_t t = t0 + 16 * tt + ln % 16;
+      const int j = 16 * rt + 4 * (ln / 16);
+      if (j < a.r_max && token_adapter(a, t) == ad)
+        *reinterpret_cast<f32x4*>(a.pout + z * slice + t * a.r_max + j) = v;
+    }
+    __syncthreads();  // A and the reduction area are reused by the next adapter
   }
-
-#pragma unroll
-  for (int j = 0; j < FM; ++j)
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-      store4(a, m0 + wcol0 + 16 * j + col, n0 + wrow0 + 16 * i + 4 * kgrp, acc[i][j]);
 }
 
 template <typename Kernel>
@@ -841,16 +1153,35 @@ void raise_lds_limit(Kernel k, size_t bytes, bool& done) {
   }
 }
 
-template <int BM, int BN, int WM, int WN>
-local_status_t launch_tiled(GemmArgs a, hipStream_t s) {
-  a.gm = static_cast<int>((a.T + BM - 1) / BM);
-  a.gn = static_cast<int>((a.N + BN - 1) / BN);
-  a.swizzle = 1;
-  const size_t lds = static_cast<size_t>(2 * (BN + BM) * kLdsK) * sizeof(uint16_t);
+local_status_t launch_prefill(GemmArgs a, hipStream_t s) {
+  a.gm = static_cast<int>((a.T + kPfM - 1) / kPfM);
+  a.gn = static_cast<int>((a.N + kPfN - 1) / kPfN);
   static bool done = false;
-  raise_lds_limit(lora_tiled_kernel<BM, BN, WM, WN>, lds, done);
-  lora_tiled_kernel<BM, BN, WM, WN><<<a.gm * a.gn, kGemmThreads, lds, s>>>(a);
-  return local_check_launch("lora_linear (tiled)");
+  raise_lds_limit(lora_prefill_kernel, kPfLdsBytes, done);
+  lora_prefill_kernel<<<a.gm * a.gn, kPfThreads, kPfLdsBytes, s>>>(a);
+  return local_check_launch("lora_linear (prefill)");
+}
+
+template <int RT>
+local_status_t launch_shrink_rt(GemmArgs a, const ShrinkShape& sh, hipStream_t s) {
+  static bool done = false;
+  raise_lds_limit(lora_shrink_long_kernel<RT>, kShLdsMax, done);
+  const dim3 grid(static_cast<unsigned>((a.T + kShTok - 1) / kShTok), static_cast<unsigned>(sh.ks));
+  lora_shrink_long_kernel<RT><<<grid, kShThreads, sh.lds, s>>>(a, sh.sps);
+  return local_check_launch("lora_linear (shrink)");
+}
+
+local_status_t launch_shrink_long(const GemmArgs& a, const ShrinkShape& sh, hipStream_t s) {
+  switch (sh.rpad / 16) {
+    case 1: return launch_shrink_rt<1>(a, sh, s);
+    case 2: return launch_shrink_rt<2>(a, sh, s);
+    case 3: return launch_shrink_rt<3>(a, sh, s);
+    case 4: return launch_shrink_rt<4>(a, sh, s);
+    case 5: return launch_shrink_rt<5>(a, sh, s);
+    case 6: return launch_shrink_rt<6>(a, sh, s);
+    case 7: return launch_shrink_rt<7>(a, sh, s);
+    default: return launch_shrink_rt<8>(a, sh, s);
+  }
 }
 
 template <int FN, int FM, int U, int XT = 0>
@@ -865,20 +1196,6 @@ local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
             static_cast<unsigned>(a.ksplit));
   lora_skinny_kernel<FN, FM, U, XT><<<grid, kSkThreads, lds, s>>>(a);
   return local_check_launch("lora_linear (skinny)");
-}
-
-template <int FN, int FM, int U>
-local_status_t launch_skinny_tiles(GemmArgs a, hipStream_t s) {
-  a.ksplit = 1;
-  a.xrows = 0;
-  return launch_skinny<FN, FM, U, 0>(a, s);
-}
-
-// Long prefill chunks (T > 256): the tiled kernel for the fused main product,
-// the skinny kernel for the shrink.
-local_status_t run_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.mode == kModeMain) return launch_tiled<128, 128, 2, 2>(a, s);
-  return launch_skinny_tiles<1, 2, LOCAL_SK_U32>(a, s);
 }
 
 // Decode sizes (T <= 256): base partial sums over K slices. Wider feature
@@ -1087,9 +1404,13 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   // Workspace. Decode sizes (T <= kSgMaxTokens): the base partial sums
   // [ksb][T][N] fp32 (N over all projections), then the shrink's partial
   // sums: [ksb][T][G*R] fp32 when the shrink runs inside the base product,
-  // [slices][T][r_max] after the SGMV shrink. Above: U_s [T][R] bf16.
-  const size_t need = decode ? d.part_bytes + d.shrink_bytes
-                             : align256(static_cast<size_t>(T) * R * sizeof(uint16_t));
+  // [slices][T][r_max] after the SGMV shrink. Above: the long shrink's
+  // partial sums [ks][T][r_max] fp32.
+  const ShrinkShape shs = decode ? ShrinkShape{} : shrink_shape(T, K, r_max);
+  const size_t need =
+      decode ? d.part_bytes + d.shrink_bytes
+             : (n_adapters > 0 ? align256(static_cast<size_t>(shs.ks) * T * r_max * sizeof(float))
+                               : 0);
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -1118,14 +1439,12 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
       sh.w = p[0].A;
       sh.ranks = p[0].ranks;
       sh.N = R;
-      sh.mode = kModeShrink;
       sh.pout = sp;
       sh.up_ks = d.slices;
       if ((st = run_sgmv_shrink(sh, s)) != LOCAL_OK) return st;
     }
     GemmArgs m = g;  // base product (+ fused shrink): partial sums per K slice
     set_groups(m, G, p);
-    m.mode = kModePartial;
     m.part = part;
     m.ksplit = d.shape.ksb;
     m.xrows = d.xrows;
@@ -1139,27 +1458,25 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   }
 
   const Proj& q = p[0];
-  uint16_t* us = n_adapters > 0 ? static_cast<uint16_t*>(ws) : nullptr;
-  if (n_adapters > 0) {  // shrink into U_s (mask and scale in its epilogue)
+  float* P = n_adapters > 0 ? static_cast<float*>(ws) : nullptr;
+  if (n_adapters > 0) {  // shrink: per-slice partial sums for each token's own adapter
     GemmArgs sh = g;
-    const Proj stacked{q.A, R, nullptr, nullptr, q.ranks, nullptr, us};
-    set_groups(sh, 1, &stacked);
-    sh.w = q.A;  // [n_ad][r_max][K] == [R][K]
+    sh.w = q.A;  // [n_ad][r_max][K]
     sh.ranks = q.ranks;
-    sh.y = us;
-    sh.mode = kModeShrink;
-    if ((st = run_gemm(sh, s)) != LOCAL_OK) return st;
+    sh.pout = P;
+    sh.up_ks = shs.ks;
+    if ((st = launch_shrink_long(sh, shs, s)) != LOCAL_OK) return st;
   }
   GemmArgs m = g;
   m.w = q.W;
   m.N = q.N;
   m.bmat = q.B;
   m.ranks = q.ranks;
-  m.us = us;
+  m.pout = P;
+  m.up_ks = shs.ks;
   m.res = q.res;
   m.y = q.y;
-  m.mode = kModeMain;
-  return run_gemm(m, s);
+  return launch_prefill(m, s);
 }
 
 // Argument checks shared by the entry points (before any launch).

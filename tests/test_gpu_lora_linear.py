@@ -24,7 +24,7 @@ def _inputs(rng, T, K, N, n_ad, r_max, ranks=None, neg_frac=0.15):
     A = np.zeros((n_ad, r_max, K), np.uint16)
     B = np.zeros((n_ad, N, r_max), np.uint16)
     for a, r in enumerate(ranks):
-        A[a, :r] = rand_bf16(rng, (r, K), 1 / math.sqrt(r))
+        A[a, :r] = rand_bf16(rng, (r, K), 1 / math.sqrt(max(r, 1)))
         B[a, :, :r] = rand_bf16(rng, (N, r), 0.01)
     idx = rng.integers(0, n_ad, size=T).astype(np.int32)
     idx[rng.random(T) < neg_frac] = -1
@@ -68,6 +68,12 @@ CASES = [
     (64, 512, 3072, 16, 32, None),
     (64, 512, 512, 0, 0, None),
     (700, 256, 384, 0, 0, None),
+    # long chunks: the shrink's rank tiles (r_max 8 padded to 16, 24, 128),
+    # a K of 65 steps (5 slices), many adapters inside one 32-token tile
+    (513, 512, 512, 3, 8, None),
+    (300, 256, 256, 5, 24, [24, 1, 17, 0, 24]),
+    (400, 1024, 256, 2, 128, [128, 57]),
+    (600, 4160, 256, 16, 64, [8, 16, 32, 64] * 4),
 ]
 
 
@@ -120,10 +126,12 @@ def test_zero_up_projection_is_bitwise_base(T):
     assert torch.equal(y_none.view(torch.int16), y_base.view(torch.int16))
 
 
-def test_padding_beyond_rank_is_never_read():
-    # NaN beyond each adapter's rank: any read of it would poison the output.
+@pytest.mark.parametrize("T", [80, 300])
+def test_padding_beyond_rank_is_never_read(T):
+    # NaN beyond each adapter's rank: any read of it would poison the output
+    # (T = 300: the long-chunk shrink reads A rows up to r_max, U_s masks them).
     rng = np.random.default_rng(77)
-    T, K, N = 80, 512, 256
+    K, N = 512, 256
     ranks = [3, 8, 13, 16]
     x, W, A, B, rk, idx, scale = _inputs(rng, T, K, N, 4, 16, ranks)
     nan = np.uint16(0x7FC0)

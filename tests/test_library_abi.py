@@ -59,9 +59,13 @@ def test_lora_linear_workspace_and_errors(lib):
     # stacked rows, 8 base K slices) runs on its own: 8 K slices x T x r_max
     st, n2 = _size(f, FAKE, 32, 4096, FAKE, 64, FAKE, FAKE, 16, 16, None, FAKE, FAKE, None, FAKE)
     assert st == OK and n2 == 8 * 32 * 64 * 4 + 8 * 32 * 16 * 4
-    # above 256 tokens: U_s, T x n_adapters*r_max bf16
+    # above 256 tokens: the shrink's fp32 partial sums for each token's own
+    # adapter, 8 K slices (the most; 10 token tiles) x T x r_max
     st, n1 = _size(f, FAKE, 300, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
-    assert st == OK and n1 == 300 * 128 * 2
+    assert st == OK and n1 == 8 * 300 * 16 * 4
+    # 2048 tokens (64 tiles): 4 slices fill the chip
+    st, n2k = _size(f, FAKE, 2048, 4096, FAKE, 4096, FAKE, FAKE, 4, 16, None, FAKE, FAKE, None, FAKE)
+    assert st == OK and n2k == 4 * 2048 * 16 * 4
     st, n0 = _size(f, FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)
     assert st == OK and n0 == 4 * 32 * 4096 * 4
     assert _size(f, FAKE, 32, 100, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_UNSUPPORTED
