@@ -688,10 +688,15 @@ local_status_t run_epilogue(const GemmArgs& a, hipStream_t s) {
 // token tile.
 constexpr int kPfM = 128;
 constexpr int kPfN = 256;
-constexpr int kPfThreads = 256;
-constexpr int kPfWaves = kPfThreads / kWave;
-constexpr int kPfFT = 4;   // 16-feature MFMA tiles per wave
-constexpr int kPfTT = 8;   // 16-token MFMA tiles
+#ifndef LOCAL_PF_WM
+#define LOCAL_PF_WM 2      // waves along tokens (x 4 along features)
+#endif
+constexpr int kPfWM = LOCAL_PF_WM;
+constexpr int kPfWN = 4;
+constexpr int kPfWaves = kPfWM * kPfWN;
+constexpr int kPfThreads = kPfWaves * kWave;
+constexpr int kPfFT = kPfN / kPfWN / 16;   // 16-feature MFMA tiles per wave (4)
+constexpr int kPfTT = kPfM / kPfWM / 16;   // 16-token MFMA tiles per wave
 constexpr int kPfRow = 128;                       // bytes of one row of a stage
 constexpr int kPfXBytes = kPfM * kPfRow;          // 16 KB
 constexpr int kPfStageBytes = (kPfM + kPfN) * kPfRow;  // 48 KB
@@ -699,9 +704,10 @@ constexpr int kPfStages = 3;
 constexpr int kPfURow = 80;                       // bytes of a U_s tile row: 32 bf16 + pad
 constexpr int kPfUBytes = kPfM * kPfURow;         // 10 KB
 constexpr int kPfLdsBytes = kPfStages * kPfStageBytes + kPfUBytes;  // 154 KB
-constexpr int kPfXDma = kPfM / 8 / kPfWaves;      // 1 KB loads of x per wave and step (4)
-constexpr int kPfWDma = kPfN / 8 / kPfWaves;      // ... of W (8)
-constexpr int kPfDma = kPfXDma + kPfWDma;         // 12
+constexpr int kPfXDma = kPfM / 8 / kPfWaves;      // 1 KB loads of x per wave and step
+constexpr int kPfWDma = kPfN / 8 / kPfWaves;      // ... of W
+constexpr int kPfDma = kPfXDma + kPfWDma;
+constexpr int kPfMfma = kPfFT * kPfTT;            // MFMAs per wave and half step
 
 // s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
 // operations are outstanding / until all LDS operations are done.
@@ -745,7 +751,9 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   }
   const int64_t m0 = static_cast<int64_t>(mt) * kPfM;
   const int64_t n0 = static_cast<int64_t>(nt) * kPfN;
-  const int64_t fw0 = n0 + 64 * wave;  // this wave's first feature
+  const int wm = wave / kPfWN, wn = wave % kPfWN;
+  const int64_t fw0 = n0 + 16 * kPfFT * wn;  // this wave's first feature
+  const int tw0 = 16 * kPfTT * wm;           // ... and first token of the tile
 
   int n_chunks = 0;
   if (a.n_ad > 0 && a.pout != nullptr) {
@@ -763,12 +771,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   const uint16_t* wg[kPfWDma];
 #pragma unroll
   for (int q = 0; q < kPfXDma; ++q) {
-    const int64_t t = m0 + 32 * wave + 8 * q + lane / 8;
+    const int64_t t = m0 + (kPfM / kPfWaves) * wave + 8 * q + lane / 8;
     xg[q] = a.x + (t < a.T ? t : m0) * a.K + 8 * dchunk;
   }
 #pragma unroll
   for (int q = 0; q < kPfWDma; ++q) {
-    const int64_t n = fw0 + 8 * q + lane / 8;
+    const int64_t n = n0 + (kPfN / kPfWaves) * wave + 8 * q + lane / 8;
     wg[q] = a.w + (n < a.N ? n : 0) * a.K + 8 * dchunk;
   }
   // loads of K-step s into stage `stage`
@@ -777,11 +785,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
     const int64_t k = static_cast<int64_t>(s) * 64;
 #pragma unroll
     for (int q = 0; q < kPfXDma; ++q)
-      __builtin_amdgcn_global_load_lds(xg[q] + k, st + (32 * wave + 8 * q) * kPfRow, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(xg[q] + k, st + ((kPfM / kPfWaves) * wave + 8 * q) * kPfRow,
+                                       16, 0, 0);
 #pragma unroll
     for (int q = 0; q < kPfWDma; ++q)
-      __builtin_amdgcn_global_load_lds(wg[q] + k, st + kPfXBytes + (64 * wave + 8 * q) * kPfRow,
-                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          wg[q] + k, st + kPfXBytes + ((kPfN / kPfWaves) * wave + 8 * q) * kPfRow, 16, 0, 0);
   };
 
   f32x4 acc[kPfFT][kPfTT];
@@ -800,11 +809,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
     const uint8_t* st = pf_lds + stage * kPfStageBytes + (m ? rd1 : rd0);
 #pragma unroll
     for (int i = 0; i < kPfFT; ++i)
-      wf[m][i] = *reinterpret_cast<const u32x4*>(st + kPfXBytes + (64 * wave + 16 * i) * kPfRow);
+      wf[m][i] = *reinterpret_cast<const u32x4*>(st + kPfXBytes + (16 * kPfFT * wn + 16 * i) * kPfRow);
 #pragma unroll
-    for (int j = 0; j < kPfTT; ++j) xf[m][j] = *reinterpret_cast<const u32x4*>(st + 16 * j * kPfRow);
+    for (int j = 0; j < kPfTT; ++j)
+      xf[m][j] = *reinterpret_cast<const u32x4*>(st + (tw0 + 16 * j) * kPfRow);
   };
-  // MFMAs [b, e) of half m, in the order tile (i, j) = (idx / 8, idx % 8)
+  // MFMAs [b, e) of half m, in the order tile (i, j) = (idx / TT, idx % TT)
   auto mfma_range = [&](int m, int b, int e) {
 #pragma unroll
     for (int idx = b; idx < e; ++idx) {
@@ -812,8 +822,13 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       acc[i][j] = mfma16x16x32(as_bf16x8(wf[m][i]), as_bf16x8(xf[m][j]), acc[i][j]);
     }
   };
-  // instruction-group masks of the scheduler's group barriers
+  // instruction-group masks of the scheduler's group barriers, and the
+  // group sizes of a step: R operand reads per half, Q MFMAs of the second
+  // half before the barrier, the loads paired with MFMAs after the reads
   constexpr int kSgMfma = 0x8, kSgVmem = 0x10, kSgDsRead = 0x100;
+  constexpr int kR = kPfFT + kPfTT, kQ = kPfMfma / 4;
+  constexpr int kVPair = kPfDma < kPfMfma - kQ - kR ? kPfDma : kPfMfma - kQ - kR;
+  static_assert(kPfMfma - kQ >= kR && kVPair >= 0, "step schedule");
 
   // Step s (stage s % 3), first half: the m = 1 operands are read under the
   // m = 0 MFMAs. Then each wave waits for its own loads of step s + 1 (those
@@ -844,7 +859,9 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   bool staged = false;
   if (n_chunks > 0) {
     uint8_t* ut = pf_lds + kPfStages * kPfStageBytes;  // [128 tokens][kPfURow]
-    const int ftl = tid / 2, fh = tid % 2;            // forming: token, 16-column half
+    // forming: kFTpt threads per token, kFG groups of 8 columns each
+    constexpr int kFTpt = kPfThreads / kPfM, kFG = 4 / kFTpt;
+    const int ftl = tid / kFTpt, fh = tid % kFTpt;
     const int64_t ft = m0 + ftl;
     const int64_t ftc = ft < a.T ? ft : m0;
     const int fidx = a.idx[ftc];
@@ -866,22 +883,22 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
         bw[i] = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(bad) * a.N + (n < a.N ? n : 0)) *
                                               a.r_max + bj);
       }
-      // forming: columns c0 + 16 fh + 8g, g = 0, 1 (8 columns of one adapter)
-      int frk[2];
-      int64_t off[2];
+      // forming: columns c0 + 8 (kFG fh + g), g < kFG (8 columns of one adapter)
+      int frk[kFG];
+      int64_t off[kFG];
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const int c = c0 + 16 * fh + 8 * g;
+      for (int g = 0; g < kFG; ++g) {
+        const int c = c0 + 8 * (kFG * fh + g);
         frk[g] = a.ranks ? a.ranks[min(c / a.r_max, a.n_ad - 1)] : a.r_max;
         off[g] = (ft < a.T ? ft : m0) * a.r_max + c % a.r_max;
       }
-      f32x4 sum[2][2] = {};
+      f32x4 sum[kFG][2] = {};
       for (int z0 = 0; z0 < a.up_ks; z0 += 4) {
-        f32x4 v[4][2][2];
+        f32x4 v[4][kFG][2];
 #pragma unroll
         for (int dz = 0; dz < 4; ++dz)
 #pragma unroll
-          for (int g = 0; g < 2; ++g) {
+          for (int g = 0; g < kFG; ++g) {
             const int64_t o = static_cast<int64_t>(min(z0 + dz, a.up_ks - 1)) * slice + off[g];
             v[dz][g][0] = ld_global<f32x4>(a.pout + o);
             v[dz][g][1] = ld_global<f32x4>(a.pout + o + 4);
@@ -894,7 +911,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
         for (int dz = 0; dz < 4; ++dz)
           if (z0 + dz < a.up_ks)
 #pragma unroll
-            for (int g = 0; g < 2; ++g) {
+            for (int g = 0; g < kFG; ++g) {
               sum[g][0] += v[dz][g][0];
               sum[g][1] += v[dz][g][1];
             }
@@ -903,8 +920,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       // its rank (padding rows of A may hold anything)
       const int fad = (ft < a.T && fidx >= 0 && fidx < a.n_ad) ? fidx : -1;
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const int c = c0 + 16 * fh + 8 * g;
+      for (int g = 0; g < kFG; ++g) {
+        const int c = c0 + 8 * (kFG * fh + g);
         const bool own = c < a.R && fad == c / a.r_max;
         const int keep = own ? min(max(frk[g], 0), a.r_max) - c % a.r_max : 0;
         float u[8];
@@ -913,7 +930,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
           const float sv = e < 4 ? sum[g][0][e] : sum[g][1][e - 4];
           u[e] = e < keep ? fscl * sv : 0.f;
         }
-        *reinterpret_cast<u32x4*>(ut + ftl * kPfURow + 32 * fh + 16 * g) =
+        *reinterpret_cast<u32x4*>(ut + ftl * kPfURow + 16 * (kFG * fh + g)) =
             u32x4{pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]), pack_bf16x2(u[4], u[5]),
                   pack_bf16x2(u[6], u[7])};
       }
@@ -928,7 +945,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       bf16x8 uv[kPfTT];
 #pragma unroll
       for (int j = 0; j < kPfTT; ++j)
-        uv[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(ut + (16 * j + col) * kPfURow + 16 * kgrp));
+        uv[j] = as_bf16x8(
+            *reinterpret_cast<const u32x4*>(ut + (tw0 + 16 * j + col) * kPfURow + 16 * kgrp));
 #pragma unroll
       for (int i = 0; i < kPfFT; ++i)
 #pragma unroll
@@ -947,37 +965,40 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
     for (int u = 0; u < kPfStages; ++u) {
       const int s = s0 + u;
       if (s >= steps) break;
-      // first half: one operand read (m = 1) beside each of the first 12
+      // first half: one operand read (m = 1) beside each of the first kR
       // MFMAs (m = 0)
       read_half(u, 1);
-      mfma_range(0, 0, 32);
+      mfma_range(0, 0, kPfMfma);
 #pragma unroll
-      for (int g = 0; g < 12; ++g) {
+      for (int g = 0; g < kR; ++g) {
         __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
         __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(kSgMfma, 20, 0);
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, kPfMfma - kR, 0);
       __builtin_amdgcn_sched_barrier(0);
-      // second half: 8 MFMAs (m = 1) before the barrier, then the operand
+      // second half: kQ MFMAs (m = 1) before the barrier, then the operand
       // reads of the next step and the loads of step s + 3 beside the rest
-      mfma_range(1, 0, 8);
+      mfma_range(1, 0, kQ);
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<kPfDma>();
       wait_lgkm0_barrier();
       __builtin_amdgcn_sched_barrier(0);
       read_half((u + 1) % kPfStages, 0);
       issue(u, min(s + 3, last));
-      mfma_range(1, 8, 32);
+      mfma_range(1, kQ, kPfMfma);
 #pragma unroll
-      for (int g = 0; g < 12; ++g) {
+      for (int g = 0; g < kR; ++g) {
         __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 1);
         __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 1);
       }
 #pragma unroll
-      for (int g = 0; g < 12; ++g) {
+      for (int g = 0; g < kVPair; ++g) {
         __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 1);
         __builtin_amdgcn_sched_group_barrier(kSgVmem, 1, 1);
       }
+      if (kPfDma > kVPair) __builtin_amdgcn_sched_group_barrier(kSgVmem, kPfDma - kVPair, 1);
+      if (kPfMfma - kQ - kR > kVPair)
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, kPfMfma - kQ - kR - kVPair, 1);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -987,7 +1008,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   for (int j = 0; j < kPfTT; ++j)
 #pragma unroll
     for (int i = 0; i < kPfFT; ++i)
-      store4(a, m0 + 16 * j + col, fw0 + 16 * i + 4 * kgrp, acc[i][j]);
+      store4(a, m0 + tw0 + 16 * j + col, fw0 + 16 * i + 4 * kgrp, acc[i][j]);
 }
 
 // ------------------------------------------------------------ long shrink
