@@ -7,17 +7,17 @@
 // of W), tokens are columns (B operand, rows of x), so a lane ends with 4
 // consecutive features of one token.
 //
-//  * Decode sizes (T <= 256), three kernels, none waiting on another's
-//    workgroups:
-//    - SGMV shrink: workgroups per (K slice, adapter) gather the tokens routed
-//      to that adapter and compute x_t . A[a,j,:] for their slice of K on the
-//      matrix cores; fp32 partial sums per slice.
-//    - skinny base product, split over K: a workgroup owns 16*FN features x
-//      up to 128 tokens of one K slice and its 8 waves split the slice; each
-//      lane loads its MFMA operand slices straight from global memory (no LDS
-//      staging, no barrier in the loop) and the 8 partial tiles are summed
-//      once through LDS in a fixed order; fp32 partial sums per slice. Wider
-//      feature tiles for fewer tokens cut the re-reads of x.
+//  * Decode sizes (T <= 256), none waiting on another kernel's workgroups:
+//    - base product split over K, streamed: a workgroup owns 16*FN features
+//      x up to 128 tokens of one K slice; its W rows (with the shrink's
+//      stacked-A rows as extra row tiles when they fit) and x rows stream
+//      through an LDS ring by direct global-to-LDS loads, whole 128-byte rows
+//      per load instruction; fp32 partial sums per slice. Wider feature
+//      tiles for fewer tokens cut the re-reads of x.
+//    - SGMV shrink, when the stacked rows are too many to ride along:
+//      workgroups per (K slice, adapter) gather the tokens routed to that
+//      adapter and compute x_t . A[a,j,:] for their slice of K on the matrix
+//      cores; fp32 partial sums per slice.
 //    - epilogue: sums the base slices, forms U_s = bf16(s_t * u) for the
 //      token's own adapter and rank, adds U_s B_a^T and the residual, and
 //      rounds once to bf16.
@@ -38,10 +38,7 @@
 namespace localk {
 namespace {
 
-constexpr int kSkThreads = 512;         // skinny kernel (8 waves)
-constexpr int kSkWaves = kSkThreads / kWave;
 constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
-constexpr int kRedTiles = 8;            // skinny kernel: tiles per LDS reduction round
 constexpr int kMaxGroup = 4;            // projections sharing x in one grouped call
 constexpr int kNumXcd = 8;
 
@@ -74,7 +71,7 @@ struct GemmArgs {
   int n_ad, r_max, R;
   const uint16_t* res;   // optional residual [T][N] (main mode)
   uint16_t* y;           // bf16 output [T][N]
-  int ksplit;            // K slices of the skinny kernel (grid.z); 1 = whole K
+  int ksplit;            // K slices of the decode base product (grid.z)
   int gm, gn;            // tile grid of the long-chunk main product
 };
 
@@ -212,170 +209,179 @@ __device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* 
   return v;
 }
 
-// ------------------------------------------------------------------ skinny
-// Workgroup: features [n0, n0 + 16*FN) x tokens [t0, t0 + 16*FM) over the
-// z-th of ksplit slices of K; wave w takes a contiguous range of the slice's
-// 64-wide steps (U steps per batch of loads); partial tiles are summed through
-// LDS in wave order and written as the slice's fp32 sum (decode base
-// product, finished by the epilogue kernel).
-// An 8-wave workgroup runs two waves per SIMD; telling the compiler so lets it
-// keep a whole batch of loads in registers instead of interleaving each load
-// with the MFMA that consumes it (which leaves one load in flight per wave).
-#ifndef LOCAL_SK_WPE
-#define LOCAL_SK_WPE 2  // waves per SIMD the skinny kernel is compiled for
-#endif
+// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
+// operations are outstanding / until all LDS operations are done.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkm0_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
-// k offsets of a lane's two 16-byte loads within a 64-wide step: k-group g of
-// MFMA m takes k = kLaneK*g + kHalfK*m .. +8.
-constexpr int kLaneK = 16;
-constexpr int kHalfK = 8;
+// Direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at
+// lds + 16 l (lds is the wave's common base). A plain function: the builtin
+// called with template-dependent arguments fails the host compilation pass
+// of a kernel template.
+__device__ __forceinline__ void lds_load16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
 
-template <int FN, int FM, int U, int XT>
-__global__ __launch_bounds__(kSkThreads) __attribute__((amdgpu_waves_per_eu(LOCAL_SK_WPE, LOCAL_SK_WPE)))
-void lora_skinny_kernel(GemmArgs a) {
-  constexpr int FT = FN + XT;     // row tiles: FN of W, then XT of stacked A
-  extern __shared__ f32x4 red[];  // [waves][tiles of one round][64 lanes]
+// ------------------------------------------------------------------ stream
+// Decode sizes (T <= 256): the base product, with the shrink's stacked-A rows
+// as extra row tiles, of one K slice, streamed through LDS. Workgroup:
+// features [n0, n0 + 16 FN) (+ XT tiles of stacked-A rows) x tokens
+// [t0, t0 + 16 FM) over the z-th of ksplit K slices. Each 64-k step of the
+// slice is one LDS stage holding the tile's W and A rows and its x rows
+// (128-byte rows, chunk-swizzled as in the long-chunk product), brought in
+// by direct global-to-LDS loads: every load instruction moves 8 whole rows,
+// and a ring of S stages keeps S - 2 steps in flight while one is computed.
+// Each wave owns every fourth output tile, so there is no reduction across
+// waves. Rows past N or T and stacked-A rows past the adapter's rank read
+// clamped rows; their outputs are never stored (rows past the rank are
+// masked by the epilogue). Workgroups start their slice at different steps
+// (by feature tile), so that those running together read different parts
+// of x; the order depends on the feature tile only, as with the K slices.
+constexpr int kStThreads = 256;
+constexpr int kStWaves = kStThreads / kWave;
+constexpr int kStLdsMax = 147456;
 
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+template <int FN, int FM, int XT>
+struct StreamShape {
+  static constexpr int FT = FN + XT;                                // W and A row tiles
+  static constexpr int ROWS = 16 * (FT + FM);                       // rows of a stage
+  static constexpr int DMA = (ROWS / 8 + kStWaves - 1) / kStWaves;  // loads per wave and stage
+  static constexpr int STAGE = 8 * DMA * kStWaves * 128;            // bytes, padded
+  static constexpr int S = kStLdsMax / STAGE < 8 ? kStLdsMax / STAGE : 8;
+  static constexpr int NT = (FT * FM + kStWaves - 1) / kStWaves;    // tiles per wave
+  static_assert(S >= 3 && DMA * (S - 2) < 64, "stream ring");
+};
+
+template <int FN, int FM, int XT>
+__global__ __launch_bounds__(kStThreads) void lora_stream_kernel(GemmArgs a) {
+  using SS = StreamShape<FN, FM, XT>;
+  constexpr int FT = SS::FT, S = SS::S, D = SS::DMA, NT = SS::NT;
+  extern __shared__ __attribute__((aligned(16))) uint8_t st_lds[];
+
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane % 16, kgrp = lane / 16;
   const int64_t n0 = static_cast<int64_t>(blockIdx.x) * 16 * FN;
   const int64_t t0 = static_cast<int64_t>(blockIdx.y) * 16 * FM;
   const int64_t x0 = static_cast<int64_t>(blockIdx.x) * a.xrows;  // first stacked-A row
-
-  f32x4 acc[FT][FM];
-#pragma unroll
-  for (int i = 0; i < FT; ++i)
-#pragma unroll
-    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // this lane's rows: feature rows of W, stacked-A rows (below the adapter's
-  // rank only), token rows of x
-  const uint16_t* wrow[FT];
-  bool wok[FT];
-#pragma unroll
-  for (int i = 0; i < FN; ++i) {  // a 16-row tile lies in one projection
-    const int g = group_of(a, n0 + 16 * i);
-    const int64_t n = n0 + 16 * i + col;
-    wok[i] = n < a.N;
-    wrow[i] = pick(a.gw, g) + (wok[i] ? n - gstart_of(a, g) : 0) * a.K;
-  }
-#pragma unroll
-  for (int e = 0; e < XT; ++e) {
-    const int rr = 16 * e + col;
-    const int64_t row = x0 + rr;  // virtual stacked row: projection row / R
-    bool ok = rr < a.xrows && row < static_cast<int64_t>(a.G) * a.R;
-    const int g = ok ? static_cast<int>(row / a.R) : 0;
-    const int64_t rl = ok ? row % a.R : 0;
-    if (ok) ok = static_cast<int>(rl % a.r_max) < rank_g(a, g, static_cast<int>(rl / a.r_max));
-    wok[FN + e] = ok;
-    wrow[FN + e] = pick(a.ga, g) + (ok ? rl : 0) * a.K;
-  }
-  const uint16_t* xrow[FM];
-  bool xok[FM];
-#pragma unroll
-  for (int j = 0; j < FM; ++j) {
-    const int64_t t = t0 + 16 * j + col;
-    xok[j] = t < a.T;
-    xrow[j] = a.x + (xok[j] ? t : 0) * a.K;
-  }
-
-  // Loads are unconditional (rows are clamped to a valid one above, steps
-  // past the wave's range to its last step) and invalid values are zeroed
-  // with selects, so the loop has no branch around a load and each batch of
-  // MFMAs waits only for its own loads.
-  //
-  // A step covers 64 k as two MFMAs. The k order inside a step is permuted
-  // (MFMA m, k-group g takes k = 16g + 8m .. +8), which is the same for both
-  // operands and so leaves the product unchanged, but lets every lane load 32
-  // contiguous bytes: each row of W and x is read as whole 128-byte lines.
-  // Every workgroup reads the same rows of x. Each one takes the 8 K ranges
-  // of its slice in a rotated order (wave w takes range (w + rot) mod 8), so
-  // that workgroups running together read different parts of x and spread
-  // over the L2 channels instead of all hitting the same lines at once.
-  const int ksteps = static_cast<int>(a.K / 64);
   const int z = blockIdx.z;
+  const int ksteps = static_cast<int>(a.K / 64);
   const int z_lo = (z * ksteps) / a.ksplit, z_hi = ((z + 1) * ksteps) / a.ksplit;
-  const int rw = (wave + static_cast<int>(blockIdx.x + blockIdx.y)) % kSkWaves;
-  const int s_lo = z_lo + (rw * (z_hi - z_lo)) / kSkWaves;
-  const int s_hi = z_lo + ((rw + 1) * (z_hi - z_lo)) / kSkWaves;
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  // one batch: the loads of U steps from step s (past s_hi: the last step)
-  auto load_batch = [&](int s, u32x4 (&wv)[U][FT][2], u32x4 (&xv)[U][FM][2]) {
+  const int nsteps = z_hi - z_lo;
+  const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nsteps));
+
+  // the lane's rows of its loads: stage row 8 (wave + 4q) + lane/8
+  const int dchunk = (lane % 8) ^ (lane / 8);
+  const uint16_t* src[D];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t k = static_cast<int64_t>(min(s + u, s_hi - 1)) * 64 + kLaneK * kgrp;
-#pragma unroll
-      for (int i = 0; i < FT; ++i) {
-        wv[u][i][0] = ld_global<u32x4>(wrow[i] + k);
-        wv[u][i][1] = ld_global<u32x4>(wrow[i] + k + kHalfK);
-      }
-#pragma unroll
-      for (int j = 0; j < FM; ++j) {
-        xv[u][j][0] = ld_global<u32x4>(xrow[j] + k);
-        xv[u][j][1] = ld_global<u32x4>(xrow[j] + k + kHalfK);
-      }
+  for (int q = 0; q < D; ++q) {
+    const int r = 8 * (wave + kStWaves * q) + lane / 8;
+    const uint16_t* p;
+    if (r < 16 * FN) {  // W row (a 16-row tile lies in one projection)
+      const int g = group_of(a, n0 + 16 * (r / 16));
+      const int64_t n = n0 + r;
+      p = pick(a.gw, g) + (n < a.N ? n - gstart_of(a, g) : 0) * a.K;
+    } else if (r < 16 * FT) {  // stacked-A row
+      const int64_t row = x0 + (r - 16 * FN);
+      const bool ok = r - 16 * FN < a.xrows && row < static_cast<int64_t>(a.G) * a.R;
+      const int g = ok ? static_cast<int>(row / a.R) : 0;
+      p = pick(a.ga, g) + (ok ? row % a.R : 0) * a.K;
+    } else {  // x row (also the padding rows, never read)
+      const int64_t t = t0 + (r < 16 * (FT + FM) ? r - 16 * FT : 0);
+      p = a.x + (t < a.T ? t : t0) * a.K;
     }
-  };
-  // its MFMAs, with invalid rows and steps past s_hi zeroed
-  auto mfma_batch = [&](int s, u32x4 (&wv)[U][FT][2], u32x4 (&xv)[U][FM][2]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const bool live = s + u < s_hi;
-#pragma unroll
-      for (int m = 0; m < 2; ++m) {
-#pragma unroll
-        for (int i = 0; i < FT; ++i) wv[u][i][m] = (live && wok[i]) ? wv[u][i][m] : zero4;
-#pragma unroll
-        for (int j = 0; j < FM; ++j) xv[u][j][m] = (live && xok[j]) ? xv[u][j][m] : zero4;
-#pragma unroll
-        for (int i = 0; i < FT; ++i)
-#pragma unroll
-          for (int j = 0; j < FM; ++j)
-            acc[i][j] = mfma16x16x32(as_bf16x8(wv[u][i][m]), as_bf16x8(xv[u][j][m]), acc[i][j]);
-      }
-    }
-  };
-  for (int s = s_lo; s < s_hi; s += U) {
-    u32x4 wv[U][FT][2], xv[U][FM][2];
-    load_batch(s, wv, xv);
-    mfma_batch(s, wv, xv);
+    src[q] = p + 8 * dchunk;
   }
-  // ---- sum the waves' partial tiles in wave order, then store; in rounds of
-  // at most kRedTiles tiles so that the LDS buffer stays within 64 KB
-  constexpr int NT = FM * FT;
-  constexpr int G = NT < kRedTiles ? NT : kRedTiles;
+  // k offset of relative step rs (rotated, clamped into the slice)
+  auto step_k = [&](int rs) {
+    int as = rs < nsteps ? rs + rot : rot;
+    as = z_lo + (as >= nsteps ? as - nsteps : as);
+    return static_cast<int64_t>(as) * 64;
+  };
+
+  // this wave's tiles (past the last tile: the last tile again, not stored)
+  int woff[NT], xoff[NT];
 #pragma unroll
-  for (int g0 = 0; g0 < NT; g0 += G) {
-    if (g0 > 0) __syncthreads();  // the previous round's reads are done
+  for (int k = 0; k < NT; ++k) {
+    const int tl = min(wave + kStWaves * k, FT * FM - 1);
+    woff[k] = 16 * (tl / FM) * 128;
+    xoff[k] = 16 * (FT + tl % FM) * 128;
+  }
+  const int rd0 = col * 128 + 16 * (kgrp ^ (col % 8));  // chunk kgrp of row col
+  const int rd1 = rd0 ^ 64;                              // chunk 4 + kgrp
+  f32x4 acc[NT];
 #pragma unroll
-    for (int j = 0; j < FM; ++j)
+  for (int k = 0; k < NT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Step rs: each wave waits for its own loads of stage rs % S (those of the
+  // S - 2 later steps may stay in flight); after the barrier every wave's
+  // loads of the step are visible and stage (rs - 1) % S is free for the
+  // loads of step rs + S - 1.
 #pragma unroll
-      for (int i = 0; i < FT; ++i) {
-        const int tl = j * FT + i;
-        if (tl >= g0 && tl < g0 + G) red[(wave * G + tl - g0) * kWave + lane] = acc[i][j];
-      }
-    __syncthreads();
-    for (int e = tid; e < G * kWave; e += kSkThreads) {
-      const int l = e % kWave, tl = g0 + e / kWave;
-      if (tl >= NT) continue;
-      const int i = tl % FT, j = tl / FT;
-      f32x4 s = red[e];
-      for (int w = 1; w < kSkWaves; ++w) s += red[w * G * kWave + e];
-      const int64_t t = t0 + 16 * j + l % 16;
-      if (i >= FN) {  // stacked-A rows: the shrink's partial sums of this slice
-        if (t >= a.T) continue;
-        const int rr = 16 * (i - FN) + 4 * (l / 16);
-        const int64_t rows = static_cast<int64_t>(a.G) * a.R;
-        float* dst = a.pout + (static_cast<int64_t>(z) * a.T + t) * rows + x0 + rr;
+  for (int p = 0; p < S - 1; ++p) {
+    const int64_t k = step_k(p);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (rr + q < a.xrows && x0 + rr + q < rows) dst[q] = s[q];
-        continue;
-      }
-      const int64_t n = n0 + 16 * i + 4 * (l / 16);
-      if (t < a.T && n < a.N)
-        *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = s;
+    for (int q = 0; q < D; ++q)
+      lds_load16(src[q] + k, st_lds + p * SS::STAGE + 8 * (wave + kStWaves * q) * 128);
+  }
+  for (int rs = 0; rs < nsteps; ++rs) {
+    const int cur = rs % S;
+    wait_vmcnt<D * (S - 2)>();
+    wait_lgkm0_barrier();
+    {
+      const int64_t k = step_k(rs + S - 1);
+      uint8_t* st = st_lds + (cur == 0 ? S - 1 : cur - 1) * SS::STAGE;
+#pragma unroll
+      for (int q = 0; q < D; ++q)
+        lds_load16(src[q] + k, st + 8 * (wave + kStWaves * q) * 128);
     }
+    const uint8_t* st = st_lds + cur * SS::STAGE;
+    u32x4 wv[2][NT], xv[2][NT];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int k = 0; k < NT; ++k) {
+        wv[m][k] = *reinterpret_cast<const u32x4*>(st + woff[k] + (m ? rd1 : rd0));
+        xv[m][k] = *reinterpret_cast<const u32x4*>(st + xoff[k] + (m ? rd1 : rd0));
+      }
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int k = 0; k < NT; ++k)
+        acc[k] = mfma16x16x32(as_bf16x8(wv[m][k]), as_bf16x8(xv[m][k]), acc[k]);
+  }
+  wait_vmcnt<0>();
+
+  // partial sums of the slice: lane holds rows 4 (l/16) .. +4 of tile row i,
+  // token column l % 16 of tile j
+#pragma unroll
+  for (int k = 0; k < NT; ++k) {
+    const int tl = wave + kStWaves * k;
+    if (tl >= FT * FM) continue;
+    const int i = tl / FM, j = tl % FM;
+    const int64_t t = t0 + 16 * j + col;
+    if (t >= a.T) continue;
+    if (i >= FN) {  // stacked-A rows: the shrink's partial sums of this slice
+      const int rr = 16 * (i - FN) + 4 * kgrp;
+      const int64_t rows = static_cast<int64_t>(a.G) * a.R;
+      float* dst = a.pout + (static_cast<int64_t>(z) * a.T + t) * rows + x0 + rr;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (rr + q < a.xrows && x0 + rr + q < rows) dst[q] = acc[k][q];
+      continue;
+    }
+    const int64_t n = n0 + 16 * i + 4 * kgrp;
+    if (n < a.N)
+      *reinterpret_cast<f32x4*>(a.part + (static_cast<int64_t>(z) * a.T + t) * a.N + n) = acc[k];
   }
 }
 
@@ -708,20 +714,6 @@ constexpr int kPfXDma = kPfM / 8 / kPfWaves;      // 1 KB loads of x per wave an
 constexpr int kPfWDma = kPfN / 8 / kPfWaves;      // ... of W
 constexpr int kPfDma = kPfXDma + kPfWDma;
 constexpr int kPfMfma = kPfFT * kPfTT;            // MFMAs per wave and half step
-
-// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
-// operations are outstanding / until all LDS operations are done.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-__device__ __forceinline__ void wait_lgkm0_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t pf_lds[];
@@ -1205,18 +1197,16 @@ local_status_t launch_shrink_long(const GemmArgs& a, const ShrinkShape& sh, hipS
   }
 }
 
-template <int FN, int FM, int U, int XT = 0>
-local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
-  constexpr int NT = FM * (FN + XT);
-  const size_t lds = static_cast<size_t>(kSkWaves) * (NT < kRedTiles ? NT : kRedTiles) * kWave *
-                     sizeof(f32x4);
+template <int FN, int FM, int XT>
+local_status_t launch_stream(GemmArgs a, hipStream_t s) {
+  using SS = StreamShape<FN, FM, XT>;
   static bool done = false;
-  raise_lds_limit(lora_skinny_kernel<FN, FM, U, XT>, lds, done);
+  raise_lds_limit(lora_stream_kernel<FN, FM, XT>, kStLdsMax, done);
   dim3 grid(static_cast<unsigned>((a.N + 16 * FN - 1) / (16 * FN)),
             static_cast<unsigned>((a.T + 16 * FM - 1) / (16 * FM)),
             static_cast<unsigned>(a.ksplit));
-  lora_skinny_kernel<FN, FM, U, XT><<<grid, kSkThreads, lds, s>>>(a);
-  return local_check_launch("lora_linear (skinny)");
+  lora_stream_kernel<FN, FM, XT><<<grid, kStThreads, SS::S * SS::STAGE, s>>>(a);
+  return local_check_launch("lora_linear (stream)");
 }
 
 // Decode sizes (T <= 256): base partial sums over K slices. Wider feature
@@ -1226,12 +1216,6 @@ local_status_t launch_skinny(GemmArgs a, hipStream_t s) {
 // LOCAL_P_TARGET_WG workgroups from below.
 #ifndef LOCAL_P_TARGET_WG
 #define LOCAL_P_TARGET_WG 256  // aim: about one workgroup per compute unit
-#endif
-#ifndef LOCAL_P_U
-#define LOCAL_P_U 2  // 64-wide K steps per batch of loads, up to 32 tokens
-#endif
-#ifndef LOCAL_P_U64
-#define LOCAL_P_U64 2  // the same, up to 64 tokens
 #endif
 #ifndef LOCAL_P_WIDE
 #define LOCAL_P_WIDE 6  // widest feature tile (MFMA tiles) up to 32 tokens; 0 = none
@@ -1264,29 +1248,26 @@ PartialShape partial_shape(int64_t T, int64_t N, int64_t K, bool allow_wide) {
   return best;
 }
 
-// Batches of one step where the operand registers of two would not fit (the
-// load batching does not change the order of the MFMA accumulation).
+// The stream kernel for the planned shape: FM token tiles by batch size
+// (16 / 32 / 64 / 256 tokens), only the combinations the planner produces.
 template <int FN, int XT>
 local_status_t run_partial_fn(const GemmArgs& a, hipStream_t s) {
-  if (a.T <= 16) return launch_skinny<FN, 1, LOCAL_P_U, XT>(a, s);
-  if (a.T <= 32) return launch_skinny<FN, 2, LOCAL_P_U, XT>(a, s);
-  return launch_skinny<FN, 4, (XT >= 4 || (FN >= 4 && XT >= 2) ? 1 : LOCAL_P_U64), XT>(a, s);
+  if (a.T <= 16) return launch_stream<FN, 1, XT>(a, s);
+  if constexpr (FN <= 4) {
+    if (a.T <= 32) return launch_stream<FN, 2, XT>(a, s);
+    if (a.T <= 64) return launch_stream<FN, 4, XT>(a, s);
+    if constexpr (FN == 2 && XT <= 2) return launch_stream<2, 8, XT>(a, s);
+  } else if constexpr (XT <= 2) {
+    if (a.T <= 32) return launch_stream<FN, 2, XT>(a, s);
+  }
+  return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: tile of %d features, %d extra row tiles, "
+                    "%lld tokens", 16 * FN, XT, static_cast<long long>(a.T));
 }
 
 template <int XT>
 local_status_t run_partial_xt(const GemmArgs& a, int fn, hipStream_t s) {
-  if (a.T > 64) {
-    if constexpr (XT <= 2) return launch_skinny<2, 8, (XT >= 1 ? 1 : LOCAL_P_U), XT>(a, s);
-    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: %d extra row tiles above 64 tokens", XT);
-  }
 #if LOCAL_P_WIDE > 4
-  if (fn == LOCAL_P_WIDE) {  // the planner keeps it to T <= 32 and XT <= 2
-    if constexpr (XT <= 2) {
-      if (a.T <= 16) return launch_skinny<LOCAL_P_WIDE, 1, LOCAL_P_U, XT>(a, s);
-      return launch_skinny<LOCAL_P_WIDE, 2, (XT >= 2 ? 1 : LOCAL_P_U), XT>(a, s);
-    }
-    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_linear: wide tile with %d row tiles", XT);
-  }
+  if (fn == LOCAL_P_WIDE) return run_partial_fn<LOCAL_P_WIDE, XT>(a, s);
 #endif
   if (fn == 4) return run_partial_fn<4, XT>(a, s);
   if (fn == 3) return run_partial_fn<3, XT>(a, s);
