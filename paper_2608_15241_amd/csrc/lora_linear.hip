@@ -64,7 +64,6 @@ struct GemmArgs {
   uint16_t* gy[kMaxGroup];           // y_g [T][N_g]
   int p_stride;          // row length of the shrink partial sums (R or r_max)
   int p_stacked;         // 1: shrink sums indexed by stacked row a*r_max + j
-  const uint16_t* bmat;  // B [n_ad][N][r_max]
   const int32_t* ranks;  // [n_ad] or null
   const int32_t* idx;    // [T] or null
   const float* scale;    // [T]
@@ -117,20 +116,20 @@ __device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad)
   return (present[ad >> 6] >> (ad & 63)) & 1ull;
 }
 
-// Store features n..n+3 of token t (bounds-checked): the residual, then one
-// rounding to bf16.
-__device__ __forceinline__ void store4(const GemmArgs& a, int64_t t, int64_t n, f32x4 v) {
-  if (t >= a.T || n >= a.N) return;
+// Store features n..n+3 of token t of a [T][N] output (bounds-checked): the
+// residual, then one rounding to bf16.
+__device__ __forceinline__ void store4_out(uint16_t* y, const uint16_t* res, int64_t T, int64_t N,
+                                           int64_t t, int64_t n, f32x4 v) {
+  if (t >= T || n >= N) return;
   float o[4] = {v[0], v[1], v[2], v[3]};
-  if (a.res) {
-    const u32x2 r = ld_global<u32x2>(a.res + t * a.N + n);
+  if (res) {
+    const u32x2 r = ld_global<u32x2>(res + t * N + n);
     o[0] += __uint_as_float(r.x << 16);
     o[1] += __uint_as_float(r.x & 0xffff0000u);
     o[2] += __uint_as_float(r.y << 16);
     o[3] += __uint_as_float(r.y & 0xffff0000u);
   }
-  *reinterpret_cast<u32x2*>(a.y + t * a.N + n) =
-      u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+  *reinterpret_cast<u32x2*>(y + t * N + n) = u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
 }
 
 // Adapter of token t, or -1 (past the batch, no adapter, or out of range).
@@ -189,25 +188,6 @@ __device__ __forceinline__ u32x4 keep_first8(u32x4 v, int keep) {
   return u32x4{w[0], w[1], w[2], w[3]};
 }
 
-// 16-byte slice of Btilde row n at U_s column c (c % 8 == 0): zero when the
-// adapter is absent from the tile or the columns lie at or past its rank.
-__device__ __forceinline__ u32x4 load_btilde(const GemmArgs& a, const uint64_t* present,
-                                             int64_t n, int c) {
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (c >= a.R || n >= a.N) return v;
-  const int ad = c / a.r_max, j = c % a.r_max;
-  const int rk = rank_of(a, ad);
-  if (j >= rk || !adapter_present(present, ad)) return v;
-  v = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(ad) * a.N + n) * a.r_max + j);
-  if (rk - j < 8) {  // clear columns at or past the rank
-    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (j + e >= rk) wv[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-    v = u32x4{wv[0], wv[1], wv[2], wv[3]};
-  }
-  return v;
-}
 
 // s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
 // operations are outstanding / until all LDS operations are done.
@@ -743,12 +723,20 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   }
   const int64_t m0 = static_cast<int64_t>(mt) * kPfM;
   const int64_t n0 = static_cast<int64_t>(nt) * kPfN;
+  // projection of the tile (a 256-feature tile lies in one projection) and
+  // its operands; feature indices below are virtual rows n0 + ...
+  const int gq = group_of(a, n0);
+  const int64_t gbase = gstart_of(a, gq), Ng = gstart_of(a, gq + 1) - gbase;
+  const uint16_t* Wg = pick(a.gw, gq);
+  const uint16_t* Bg = pick(a.gb, gq);
+  const int32_t* ranksg = pick(a.granks, gq);
+  const float* Pg = a.pout ? a.pout + static_cast<int64_t>(gq) * a.up_ks * a.T * a.r_max : nullptr;
   const int wm = wave / kPfWN, wn = wave % kPfWN;
   const int64_t fw0 = n0 + 16 * kPfFT * wn;  // this wave's first feature
   const int tw0 = 16 * kPfTT * wm;           // ... and first token of the tile
 
   int n_chunks = 0;
-  if (a.n_ad > 0 && a.pout != nullptr) {
+  if (a.n_ad > 0 && Pg != nullptr) {
     const int my_ad = tid < kPfM ? token_adapter(a, m0 + tid) : -1;
     n_chunks = lora_chunk_list<kPfThreads>(a, my_ad, 32, present, chunks, wave_cnt);
   }
@@ -768,8 +756,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   }
 #pragma unroll
   for (int q = 0; q < kPfWDma; ++q) {
-    const int64_t n = n0 + (kPfN / kPfWaves) * wave + 8 * q + lane / 8;
-    wg[q] = a.w + (n < a.N ? n : 0) * a.K + 8 * dchunk;
+    const int64_t nl = n0 - gbase + (kPfN / kPfWaves) * wave + 8 * q + lane / 8;
+    wg[q] = Wg + (nl < Ng ? nl : 0) * a.K + 8 * dchunk;
   }
   // loads of K-step s into stage `stage`
   auto issue = [&](int stage, int s) {
@@ -867,13 +855,13 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       // Btilde operand: features fw0 + 16i + col, columns cb .. cb+8
       const int cb = c0 + 8 * kgrp;
       const int bad = min(cb / a.r_max, a.n_ad - 1), bj = cb % a.r_max;
-      const int brk = a.ranks ? a.ranks[bad] : a.r_max;
+      const int brk = ranksg ? ranksg[bad] : a.r_max;
       u32x4 bw[kPfFT];
 #pragma unroll
       for (int i = 0; i < kPfFT; ++i) {
-        const int64_t n = fw0 + 16 * i + col;
-        bw[i] = ld_global<u32x4>(a.bmat + (static_cast<int64_t>(bad) * a.N + (n < a.N ? n : 0)) *
-                                              a.r_max + bj);
+        const int64_t nl = fw0 - gbase + 16 * i + col;
+        bw[i] = ld_global<u32x4>(Bg + (static_cast<int64_t>(bad) * Ng + (nl < Ng ? nl : 0)) *
+                                          a.r_max + bj);
       }
       // forming: columns c0 + 8 (kFG fh + g), g < kFG (8 columns of one adapter)
       int frk[kFG];
@@ -881,7 +869,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
 #pragma unroll
       for (int g = 0; g < kFG; ++g) {
         const int c = c0 + 8 * (kFG * fh + g);
-        frk[g] = a.ranks ? a.ranks[min(c / a.r_max, a.n_ad - 1)] : a.r_max;
+        frk[g] = ranksg ? ranksg[min(c / a.r_max, a.n_ad - 1)] : a.r_max;
         off[g] = (ft < a.T ? ft : m0) * a.r_max + c % a.r_max;
       }
       f32x4 sum[kFG][2] = {};
@@ -892,8 +880,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
 #pragma unroll
           for (int g = 0; g < kFG; ++g) {
             const int64_t o = static_cast<int64_t>(min(z0 + dz, a.up_ks - 1)) * slice + off[g];
-            v[dz][g][0] = ld_global<f32x4>(a.pout + o);
-            v[dz][g][1] = ld_global<f32x4>(a.pout + o + 4);
+            v[dz][g][0] = ld_global<f32x4>(Pg + o);
+            v[dz][g][1] = ld_global<f32x4>(Pg + o + 4);
           }
         if (!staged) {  // the main product's first stages, behind these loads
           prologue_loads();
@@ -1000,7 +988,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   for (int j = 0; j < kPfTT; ++j)
 #pragma unroll
     for (int i = 0; i < kPfFT; ++i)
-      store4(a, m0 + tw0 + 16 * j + col, fw0 + 16 * i + 4 * kgrp, acc[i][j]);
+      store4_out(pick(a.gy, gq), pick(a.gres, gq), a.T, Ng, m0 + tw0 + 16 * j + col,
+                 fw0 - gbase + 16 * i + 4 * kgrp, acc[i][j]);
 }
 
 // ------------------------------------------------------------ long shrink
@@ -1062,6 +1051,9 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
   const int col = lane % 16, kgrp = lane / 16;
   const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kShTok;
   const int z = blockIdx.y;
+  const int gz = blockIdx.z;  // projection
+  const uint16_t* Ag = pick(a.ga, gz);
+  float* Pz = a.pout + static_cast<int64_t>(gz) * a.up_ks * a.T * a.r_max;
   const int64_t k0 = static_cast<int64_t>(z) * sps * 64;
   uint8_t* xl = sh_lds;                                   // [sps][32][128 B]
   uint8_t* al = sh_lds + static_cast<size_t>(sps) * kShTok * 128;  // [sps][rpad][128 B]
@@ -1105,7 +1097,7 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
       const int st = b / (rpad / 8), rb = b % (rpad / 8);
       const int j = min(8 * rb + lane / 8, a.r_max - 1);
       __builtin_amdgcn_global_load_lds(
-          a.w + (static_cast<int64_t>(ad) * a.r_max + j) * a.K + k0 + 64 * st + 8 * dchunk,
+          Ag + (static_cast<int64_t>(ad) * a.r_max + j) * a.K + k0 + 64 * st + 8 * dchunk,
           al + (st * rpad + 8 * rb) * 128, 16, 0, 0);
     }
     wait_vmcnt<0>();
@@ -1150,7 +1142,7 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
       const int64_t t = t0 + 16 * tt + ln % 16;
       const int j = 16 * rt + 4 * (ln / 16);
       if (j < a.r_max && token_adapter(a, t) == ad)
-        *reinterpret_cast<f32x4*>(a.pout + z * slice + t * a.r_max + j) = v;
+        *reinterpret_cast<f32x4*>(Pz + z * slice + t * a.r_max + j) = v;
     }
     __syncthreads();  // A and the reduction area are reused by the next adapter
   }
@@ -1179,7 +1171,8 @@ template <int RT>
 local_status_t launch_shrink_rt(GemmArgs a, const ShrinkShape& sh, hipStream_t s) {
   static bool done = false;
   raise_lds_limit(lora_shrink_long_kernel<RT>, kShLdsMax, done);
-  const dim3 grid(static_cast<unsigned>((a.T + kShTok - 1) / kShTok), static_cast<unsigned>(sh.ks));
+  const dim3 grid(static_cast<unsigned>((a.T + kShTok - 1) / kShTok), static_cast<unsigned>(sh.ks),
+                  static_cast<unsigned>(a.G));
   lora_shrink_long_kernel<RT><<<grid, kShThreads, sh.lds, s>>>(a, sh.sps);
   return local_check_launch("lora_linear (shrink)");
 }
@@ -1395,8 +1388,11 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
                          const float* scale, void* ws, size_t* ws_bytes, hipStream_t s) {
   const int R = n_adapters > 0 ? n_adapters * r_max : 0;
   const bool decode = T <= kSgMaxTokens;
-  if (G > 1 && !decode)
-    return one_by_one(x, T, K, G, p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes, s);
+  if (G > 1 && !decode) {  // one launch over all projections when no tile straddles two
+    for (int q = 0; q < G; ++q)
+      if (p[q].N % kPfN != 0)
+        return one_by_one(x, T, K, G, p, n_adapters, r_max, adapter_idx, scale, ws, ws_bytes, s);
+  }
   DecodePlan d{};
   if (decode) {
     d = plan_decode(T, K, G, p, n_adapters, r_max);
@@ -1411,8 +1407,9 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   const ShrinkShape shs = decode ? ShrinkShape{} : shrink_shape(T, K, r_max);
   const size_t need =
       decode ? d.part_bytes + d.shrink_bytes
-             : (n_adapters > 0 ? align256(static_cast<size_t>(shs.ks) * T * r_max * sizeof(float))
-                               : 0);
+             : (n_adapters > 0
+                    ? align256(static_cast<size_t>(G) * shs.ks * T * r_max * sizeof(float))
+                    : 0);
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -1459,25 +1456,14 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
     return run_epilogue(m, s);
   }
 
-  const Proj& q = p[0];
+  // long chunks: the shrink's partial sums [G][ks][T][r_max], then the main
+  // product over the projections' tiles
   float* P = n_adapters > 0 ? static_cast<float*>(ws) : nullptr;
-  if (n_adapters > 0) {  // shrink: per-slice partial sums for each token's own adapter
-    GemmArgs sh = g;
-    sh.w = q.A;  // [n_ad][r_max][K]
-    sh.ranks = q.ranks;
-    sh.pout = P;
-    sh.up_ks = shs.ks;
-    if ((st = launch_shrink_long(sh, shs, s)) != LOCAL_OK) return st;
-  }
   GemmArgs m = g;
-  m.w = q.W;
-  m.N = q.N;
-  m.bmat = q.B;
-  m.ranks = q.ranks;
+  set_groups(m, G, p);
   m.pout = P;
   m.up_ks = shs.ks;
-  m.res = q.res;
-  m.y = q.y;
+  if (n_adapters > 0 && (st = launch_shrink_long(m, shs, s)) != LOCAL_OK) return st;
   return launch_prefill(m, s);
 }
 

@@ -198,7 +198,9 @@ GROUPED = [
     (64, 512, (2048, 512, 512), 16, 64, [8, 16, 32, 64] * 4),
     (128, 512, (1024, 256, 256), 32, 16, None),
     (4, 256, (256, 256), 3, 8, None),
-    (300, 512, (512, 256), 4, 16, None),       # long chunk: one projection at a time
+    (300, 512, (512, 256), 4, 16, None),       # long chunk: one launch over both
+    (520, 512, (256, 768, 512), 5, 16, [16, 3, 9, 16, 0]),  # long chunk, three projections
+    (300, 256, (320, 256), 3, 8, None),        # long chunk, N % 256 != 0: one at a time
     (16, 512, (64, 64), 16, 16, None),          # shrink too wide to fuse: one at a time
     (32, 512, (512, 512, 512), 0, 0, None),
     (200, 256, (256, 256, 512, 256), 5, 32, [32, 1, 17, 32, 24]),

@@ -145,6 +145,11 @@ def test_lora_linear_grouped_workspace_and_errors(lib):
     st, n = _size(f, FAKE, 32, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 8, 16, None, FAKE,
                   FAKE, ptrs(3))
     assert st == OK and n == 2 * 32 * 12288 * 4 + 2 * 32 * 384 * 4
+    # a 2048-token chunk: one launch over the three projections, the shrink's
+    # partial sums per projection (4 K slices x T x r_max fp32 each)
+    st, n = _size(f, FAKE, 2048, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 4, 16, None, FAKE,
+                  FAKE, ptrs(3))
+    assert st == OK and n == 3 * 4 * 2048 * 16 * 4
     assert _size(f, FAKE, 32, 4096, 0, ptrs(1), Ns, None, None, 0, 0, None, None, None,
                  ptrs(1))[0] == ERR_UNSUPPORTED
     assert _size(f, FAKE, 32, 4096, 5, ptrs(5), Ns, None, None, 0, 0, None, None, None,
