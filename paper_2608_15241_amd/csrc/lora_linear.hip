@@ -139,20 +139,50 @@ __device__ __forceinline__ int token_adapter(const GemmArgs& a, int64_t t) {
   return (ad >= 0 && ad < a.n_ad) ? ad : -1;
 }
 
+// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
+// operations are outstanding / until all LDS operations are done.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkm0_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Marks the adapters my_ad of the calling threads (one token each, -1 for
-// none) and lists, in ascending order, the chunks of `chunk` U_s columns that
-// cover at least one of them. Returns the number of chunks. All threads of
-// the workgroup must call it.
+// none) in present[0..3] and lists, in ascending order, the chunks of `chunk`
+// U_s columns that cover at least one of them. Returns the number of chunks.
+// All threads of the workgroup must call it; `present` holds 4 * (1 + waves)
+// words (the bitmap, then one partial bitmap per wave). The bitmap is built
+// with wavefront OR reductions and plain LDS stores, not LDS atomics: an
+// atomic would make the compiler wait for the direct-to-LDS loads the caller
+// has in flight.
 template <int THREADS>
 __device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t* present,
                                uint16_t* list, int* wave_cnt) {
   constexpr int WAVES = THREADS / kWave;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  if (tid < 4) present[tid] = 0ull;
-  __syncthreads();
-  if (my_ad >= 0)
-    atomicOr(reinterpret_cast<unsigned long long*>(&present[my_ad >> 6]), 1ull << (my_ad & 63));
-  __syncthreads();
+  uint64_t mine = 0ull;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint64_t bits = (my_ad >= 0 && (my_ad >> 6) == w) ? 1ull << (my_ad & 63) : 0ull;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) bits |= __shfl_xor(bits, off);
+    mine = lane == w ? bits : mine;
+  }
+  if (lane < 4) present[4 + 4 * wave + lane] = mine;
+  wait_lgkm0_barrier();
+  if (tid < 4) {
+    uint64_t all = 0ull;
+#pragma unroll
+    for (int w2 = 0; w2 < WAVES; ++w2) all |= present[4 + 4 * w2 + tid];
+    present[tid] = all;
+  }
+  wait_lgkm0_barrier();
   const int chunks = (a.R + chunk - 1) / chunk;
   int n = 0;
   for (int base = 0; base < chunks; base += THREADS) {
@@ -166,7 +196,7 @@ __device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t
     const uint64_t m = __ballot(use);
     const int before = __popcll(m & ((1ull << lane) - 1ull));
     if (lane == 0) wave_cnt[wave] = __popcll(m);
-    __syncthreads();
+    wait_lgkm0_barrier();
     int off = n, tot = 0;
     for (int w2 = 0; w2 < WAVES; ++w2) {
       if (w2 < wave) off += wave_cnt[w2];
@@ -174,7 +204,7 @@ __device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t
     }
     if (use) list[off + before] = static_cast<uint16_t>(l);
     n += tot;
-    __syncthreads();
+    wait_lgkm0_barrier();
   }
   return n;
 }
@@ -189,19 +219,6 @@ __device__ __forceinline__ u32x4 keep_first8(u32x4 v, int keep) {
 }
 
 
-// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
-// operations are outstanding / until all LDS operations are done.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-__device__ __forceinline__ void wait_lgkm0_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 // Direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at
 // lds + 16 l (lds is the wave's common base). A plain function: the builtin
@@ -697,7 +714,7 @@ constexpr int kPfMfma = kPfFT * kPfTT;            // MFMAs per wave and half ste
 
 __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t pf_lds[];
-  __shared__ uint64_t present[4];
+  __shared__ uint64_t present[4 * (1 + kPfWaves)];
   __shared__ uint16_t chunks[kMaxLoraChunks];
   __shared__ int wave_cnt[kPfWaves];
 
@@ -735,11 +752,11 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   const int64_t fw0 = n0 + 16 * kPfFT * wn;  // this wave's first feature
   const int tw0 = 16 * kPfTT * wm;           // ... and first token of the tile
 
-  int n_chunks = 0;
-  if (a.n_ad > 0 && Pg != nullptr) {
-    const int my_ad = tid < kPfM ? token_adapter(a, m0 + tid) : -1;
-    n_chunks = lora_chunk_list<kPfThreads>(a, my_ad, 32, present, chunks, wave_cnt);
-  }
+  // the tile's token adapters are loaded before the stage loads (the load
+  // counter drains in order, so a load issued after them would wait for them)
+  const bool lora = a.n_ad > 0 && Pg != nullptr;
+  const int my_ad = (lora && tid < kPfM) ? token_adapter(a, m0 + tid) : -1;
+  asm volatile("" ::: "memory");
 
   // ---- direct loads. Wave w moves x rows 32w .. +32 and W rows 64w .. +64
   // (its own features) of every stage; lane l writes 16 bytes at
@@ -822,21 +839,19 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   // that are never used, so every wait count holds at every step.
   const int steps = static_cast<int>(a.K / 64);
   const int last = steps - 1;
-  auto prologue_loads = [&]() {
-    issue(0, 0);
-    issue(1, min(1, last));
-    issue(2, min(2, last));
-  };
+  // the first three stages' loads go out before anything else waits
+  issue(0, 0);
+  issue(1, min(1, last));
+  issue(2, min(2, last));
 
   // ---- LoRA delta first, chunk by chunk (32 stacked columns
   // c = a*r_max + j): U_s[t][c] = bf16(s_t * sum_z P[z][t][j]) (slices in
   // order) when a is token t's adapter, else 0, formed by the whole
-  // workgroup into an LDS tile; Btilde is zero at or past the rank. The
-  // first chunk's loads are issued before the stage loads of the main
-  // product, so their latency overlaps. Adding the delta first leaves a zero
-  // up-projection's result bit-identical (the MFMAs add +0).
-  __builtin_amdgcn_s_waitcnt(0);
-  bool staged = false;
+  // workgroup into an LDS tile; Btilde is zero at or past the rank. Its
+  // chain of loads runs while the first stages load. Adding the delta first
+  // leaves a zero up-projection's result bit-identical (the MFMAs add +0).
+  int n_chunks = 0;
+  if (lora) n_chunks = lora_chunk_list<kPfThreads>(a, my_ad, 32, present, chunks, wave_cnt);
   if (n_chunks > 0) {
     uint8_t* ut = pf_lds + kPfStages * kPfStageBytes;  // [128 tokens][kPfURow]
     // forming: kFTpt threads per token, kFG groups of 8 columns each
@@ -883,10 +898,6 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
             v[dz][g][0] = ld_global<f32x4>(Pg + o);
             v[dz][g][1] = ld_global<f32x4>(Pg + o + 4);
           }
-        if (!staged) {  // the main product's first stages, behind these loads
-          prologue_loads();
-          staged = true;
-        }
 #pragma unroll
         for (int dz = 0; dz < 4; ++dz)
           if (z0 + dz < a.up_ks)
@@ -934,7 +945,6 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       wait_lgkm0_barrier();  // the tile is rewritten by the next chunk
     }
   }
-  if (!staged) prologue_loads();
   wait_vmcnt<0>();
   wait_lgkm0_barrier();
   read_half(0, 0);
