@@ -15,6 +15,10 @@ dominant kernel (decode attention), timed with HIP events around its launches
 inside the timed region. `prefill` reports the matrix-core utilisation of the
 LoRA-fused projections of the chunked-prefill workload, timed the same way.
 `cpu_baseline` is the CPU oracle timed on this host on the same workload.
+
+`--workload gqa_skew_b64 | churn_32l_b128 | tiny_decode` times the decode step
+of another workload the same way (without the prefill and CPU legs; the
+32-layer one with a single input set, since its KV pool is 146 GB).
 """
 from __future__ import annotations
 
@@ -31,6 +35,11 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix cores
 
 
+def say(*a):
+    """Progress on stderr (the JSON line alone goes to stdout)."""
+    print("bench:", *a, file=sys.stderr, flush=True)
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -40,6 +49,12 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-prefill", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--workload", default="decode_7b_mha_b32",
+                   choices=("tiny_decode", "decode_7b_mha_b32", "gqa_skew_b64",
+                            "churn_32l_b128"),
+                   help="decode workload of the step; prefill and cpu_baseline are reported "
+                        "with the default one only. The 32-layer workload uses one input set "
+                        "(its KV pool is 146 GB)")
     p.add_argument("--traffic-probe", action="store_true",
                    help="only run, eagerly, a 256 MiB device copy (the calibration of the "
                         "HBM byte counters) and 5 decode attention launches of the workload; "
@@ -85,7 +100,8 @@ def measured_traffic():
 
 
 def decode_bytes(w, meta):
-    """Algorithmic HBM bytes of one decode step and of its attention launch."""
+    """Algorithmic HBM bytes of one layer's attention launch and of one decode
+    step over all layers (each layer reads its own KV pool and weights)."""
     D, hq, hkv, H = w.head_dim, w.hq, w.hkv, w.hidden
     B = meta.B
     nb = (meta.ctx_lens.astype(np.int64) + 15) // 16
@@ -110,7 +126,20 @@ def decode_bytes(w, meta):
                 r = w.ranks[a]
                 proj += r * K * 2 + N * r * 2
     vc = int(nb.sum()) * 8 + B * 4 * 3
-    return attn, attn + proj + vc, valid_tokens
+    return attn, w.n_layers * (attn + proj) + vc, valid_tokens
+
+
+def context_text(w):
+    kind = w.ctx[0]
+    if kind == "fixed":
+        return "fixed %s" % (list(w.ctx[1]),)
+    return "%s[%d,%d]" % ({"uniform": "U", "loguniform": "logU"}[kind], w.ctx[1], w.ctx[2])
+
+
+def adapters_text(w):
+    ranks = sorted(set(w.ranks))
+    r = "rank %d" % ranks[0] if len(ranks) == 1 else "ranks %s" % ranks
+    return "%d x %s on %s (%s)" % (w.n_adapters, r, "/".join(w.lora_targets), w.assignment)
 
 
 def prefill_gemm_flops(w, meta):
@@ -140,15 +169,19 @@ def main():
     lk.load_library()
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    w = workloads.DECODE_7B
+    w = workloads.BY_NAME[args.workload]
+    primary = w.name == workloads.DECODE_7B.name
     meta = workloads.make_meta(w, seed=0)
     md = meta_to_device(meta, dev)
     if args.traffic_probe:
         traffic_probe(torch, workloads, w, meta, md, dev)
         return
+    n_sets = args.sets if w.n_layers == 1 else 1
     sets = []
-    for s in range(args.sets):
-        weights = [workloads.make_layer_weights(w, 0, dev, seed=100 + s)]
+    for s in range(n_sets):
+        say("input set", s, "of", w.name)
+        weights = [workloads.make_layer_weights(w, l, dev, seed=100 + s)
+                   for l in range(w.n_layers)]
         pool = workloads.make_kv_pool(w, meta, dev, seed=100 + s)
         x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=200 + s)
         st = Step("decode", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
@@ -166,6 +199,7 @@ def main():
         graphs[i % len(graphs)].replay()
     torch.cuda.synchronize()
 
+    say("timed steps")
     K = args.steps
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -179,22 +213,22 @@ def main():
     ms_per_step = total_ms / K
 
     # the dominant kernel (decode attention), timed with HIP events around
-    # each of its launches in K eager steps on the same stream
-    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    # each of its launches (every layer) in K eager steps on the same stream
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K * w.n_layers)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K * w.n_layers)]
     e_start = torch.cuda.Event(enable_timing=True)
     e_end = torch.cuda.Event(enable_timing=True)
     e_start.record(stream)
     for i in range(K):
         st = sets[i % len(sets)][0]
         st.version_check()
-        lc = st.layer_calls[0]
-        for c in lc["in"]:
-            c()
-        ev_a[i].record(stream)
-        lc["attn"]()
-        ev_b[i].record(stream)
-        lc["o"]()
+        for l, lc in enumerate(st.layer_calls):
+            for c in lc["in"]:
+                c()
+            ev_a[i * w.n_layers + l].record(stream)
+            lc["attn"]()
+            ev_b[i * w.n_layers + l].record(stream)
+            lc["o"]()
     e_end.record(stream)
     torch.cuda.synchronize()
     eager_ms = e_start.elapsed_time(e_end) / K
@@ -220,22 +254,25 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "layers": w.n_layers, "hidden": w.hidden,
                    "heads": "%dq/%dkv x %d" % (w.hq, w.hkv, w.head_dim), "batch": meta.B,
-                   "context": "U[256,4096]", "sum_context": int(meta.ctx_lens.sum()),
-                   "adapters": "%d x rank %d on q/k/v/o" % (w.n_adapters, w.r_max),
-                   "input_sets": args.sets},
+                   "context": context_text(w), "sum_context": int(meta.ctx_lens.sum()),
+                   "valid_kv_tokens": valid_tokens, "stale_frac": w.stale_frac,
+                   "adapters": adapters_text(w), "input_sets": n_sets},
         "roofline": {"kernel": "local_paged_attn_decode", "bound": "hbm",
                      "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": measured_traffic() if primary else None,
                      "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5)},
         "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
                      "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
         "step_launch": {"mode": "hip_graph_replay", "eager_ms_per_step": round(eager_ms, 5)},
     }
 
-    if not args.no_prefill:
+    if primary and not args.no_prefill:
+        say("prefill projections")
         result["prefill"] = bench_prefill(torch, workloads, lk, dev)
 
-    if not args.no_cpu_baseline:
+    if primary and not args.no_cpu_baseline:
+        say("cpu baseline")
         result["cpu_baseline"] = cpu_baseline(torch, workloads, w, meta, sets[0], args)
 
     del sets

@@ -22,9 +22,10 @@
 //      token's own adapter and rank, adds U_s B_a^T and the residual, and
 //      rounds once to bf16.
 //  * Long prefill chunks (T > 256), two kernels:
-//    - shrink: workgroups of 32 tokens x one K slice compute, for each
-//      adapter routed in the tile, x_t . A[a,j,:] of its tokens on the matrix
-//      cores; fp32 partial sums per slice.
+//    - shrink: workgroups of 64 tokens x one K slice compute, for each
+//      adapter routed in the tile and every projection of the call,
+//      x_t . A[a,j,:] of its tokens on the matrix cores; fp32 partial sums
+//      per slice.
 //    - main product: 128 tokens x 256 features per workgroup, both operands
 //      brought to LDS by direct global-to-LDS loads in a three-stage ring;
 //      the delta U_s Btilde^T (U_s[t, a*r_max + j] = bf16(s_t * sum of the
@@ -1004,14 +1005,15 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
 
 // ------------------------------------------------------------ long shrink
 // Long chunks (T > 256): the shrink as SGMV partial sums over K slices,
-//   P[z][t][j] = sum over slice z of x[t][k] A[a_t][j][k],   j < r_max,
-// for the token's own adapter a_t only. Workgroup: 32 tokens x one K slice
-// of sps 64-k steps. The x slice (32 rows) and then, adapter by adapter
-// (those routed in the token tile), the A slice (r_max rows padded to 16)
-// are brought to LDS by direct loads in one go, in the 128-byte rows and
-// chunk swizzle of the main product; the four waves take every fourth
-// 64-k step and their partial tiles are summed through LDS in wave order.
-constexpr int kShTok = 32;
+//   P[g][z][t][j] = sum over slice z of x[t][k] A_g[a_t][j][k],   j < r_max,
+// for the token's own adapter a_t only and every projection g of the call.
+// Workgroup: 64 tokens x one K slice of sps 64-k steps; wave w owns tokens
+// 16w .. 16w + 15 over the whole slice, so nothing is reduced across waves.
+// The x slice is brought to LDS by direct loads while wave 0 lists the
+// adapters routed in the tile; then, adapter by adapter, the A slices of
+// every projection (r_max rows padded to 16) follow, in the 128-byte rows and
+// chunk swizzle of the main product. x is read once for all projections.
+constexpr int kShTok = 64;
 constexpr int kShThreads = 256;
 constexpr int kShWaves = kShThreads / kWave;
 constexpr size_t kShLdsMax = 147456;
@@ -1023,25 +1025,24 @@ struct ShrinkShape {
   size_t lds;  // dynamic LDS bytes
 };
 
-size_t shrink_lds(int sps, int rpad) {
-  return static_cast<size_t>(kShTok + rpad) * sps * 128 +
-         static_cast<size_t>(kShWaves) * (2 * rpad / 16) * kWave * sizeof(f32x4);
+size_t shrink_lds(int sps, int rpad, int G) {
+  return static_cast<size_t>(kShTok + G * rpad) * sps * 128;
 }
 
 // Fewest K slices (a divisor of the step count) that fit LDS and give at
 // least one workgroup per compute unit, at most kShMaxSlices of them unless
 // LDS needs more (the main product sums the slices for every U_s value it
-// uses).
+// uses). One slice step always fits: (64 + 4 * 128) rows of 128 bytes.
 constexpr int kShMaxSlices = 8;
-ShrinkShape shrink_shape(int64_t T, int64_t K, int r_max) {
+ShrinkShape shrink_shape(int64_t T, int64_t K, int r_max, int G) {
   const int steps = static_cast<int>(K / 64);
   const int rpad = (r_max + 15) / 16 * 16;
   const int64_t tiles = (T + kShTok - 1) / kShTok;
-  ShrinkShape best{steps, 1, rpad, shrink_lds(1, rpad)};
+  ShrinkShape best{steps, 1, rpad, shrink_lds(1, rpad, G)};
   for (int ks = 1; ks <= steps; ++ks) {
     if (steps % ks) continue;
     const int sps = steps / ks;
-    const size_t lds = shrink_lds(sps, rpad);
+    const size_t lds = shrink_lds(sps, rpad, G);
     if (lds > kShLdsMax) continue;
     best = ShrinkShape{ks, sps, rpad, lds};
     if (tiles * ks >= 256 || ks >= kShMaxSlices) break;
@@ -1054,6 +1055,7 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
   constexpr int rpad = 16 * RT;
   extern __shared__ __attribute__((aligned(16))) uint8_t sh_lds[];
   __shared__ int ad_list[kShTok];
+  __shared__ int tok_ad[kShTok];
   __shared__ int n_list;
 
   const int tid = threadIdx.x, lane = tid % kWave;
@@ -1061,17 +1063,33 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
   const int col = lane % 16, kgrp = lane / 16;
   const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kShTok;
   const int z = blockIdx.y;
-  const int gz = blockIdx.z;  // projection
-  const uint16_t* Ag = pick(a.ga, gz);
-  float* Pz = a.pout + static_cast<int64_t>(gz) * a.up_ks * a.T * a.r_max;
+  const int G = a.G;
+  static_assert(kShTok == kWave, "wave 0 reads one token per lane");
   const int64_t k0 = static_cast<int64_t>(z) * sps * 64;
-  uint8_t* xl = sh_lds;                                   // [sps][32][128 B]
-  uint8_t* al = sh_lds + static_cast<size_t>(sps) * kShTok * 128;  // [sps][rpad][128 B]
-  f32x4* red = reinterpret_cast<f32x4*>(al + static_cast<size_t>(sps) * rpad * 128);
+  uint8_t* xl = sh_lds;                                            // [sps][64][128 B]
+  uint8_t* al = sh_lds + static_cast<size_t>(sps) * kShTok * 128;  // [G][sps][rpad][128 B]
 
-  // adapters routed in the tile, in order of first appearance
-  if (wave == 0) {
-    const int my = lane < kShTok ? token_adapter(a, t0 + lane) : -1;
+  // wave 0 reads the tile's adapters before it issues any x load, so that
+  // listing them waits for that load alone; the other waves read theirs from
+  // LDS after the list is made
+  const int my = wave == 0 ? token_adapter(a, t0 + lane) : -1;
+  const int64_t t = t0 + 16 * wave + col;  // this lane's token (MFMA column)
+
+  // direct loads as in the main product: lane l writes 16 bytes at
+  // block + 16 l = row 8b + l/8, position l%8, holding chunk (l%8) ^ (l/8);
+  // wave w moves rows 8w .. +8 and 32 + 8w .. +8 of every step
+  const int dchunk = (lane % 8) ^ (lane / 8);
+  auto load_x = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r0 = 8 * (wave + kShWaves * i);
+      const int64_t tr = t0 + r0 + lane / 8;
+      const uint16_t* src = a.x + (tr < a.T ? tr : t0) * a.K + k0 + 8 * dchunk;
+      for (int st = 0; st < sps; ++st)
+        lds_load16(src + 64 * st, xl + (static_cast<size_t>(st) * kShTok + r0) * 128);
+    }
+  };
+  if (wave == 0) {  // adapters routed in the tile, in order of first appearance
     uint64_t pending = __ballot(my >= 0);
     int n = 0;
     while (pending) {
@@ -1081,81 +1099,64 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
       pending &= ~__ballot(my == ad);
     }
     if (lane == 0) n_list = n;
+    tok_ad[lane] = my;
   }
-
-  // direct loads as in the main product: lane l writes 16 bytes at
-  // block + 16 l = row 8b + l/8, position l%8, holding chunk (l%8) ^ (l/8)
-  const int dchunk = (lane % 8) ^ (lane / 8);
-  {
-    const int64_t t = t0 + 8 * wave + lane / 8;  // wave w moves rows 8w .. +8 of every step
-    const uint16_t* src = a.x + (t < a.T ? t : t0) * a.K + k0 + 8 * dchunk;
-    for (int st = 0; st < sps; ++st)
-      __builtin_amdgcn_global_load_lds(src + 64 * st, xl + (st * kShTok + 8 * wave) * 128, 16, 0,
-                                       0);
-  }
-  wait_vmcnt<0>();
-  wait_lgkm0_barrier();
+  load_x();
+  wait_lgkm0_barrier();  // the list; the x loads stay in flight
   const int n_ad_tile = n_list;
+  const int t_ad = tok_ad[16 * wave + col];
 
   const int rd0 = col * 128 + 16 * (kgrp ^ (col % 8));
   const int rd1 = rd0 ^ 64;
   const int64_t slice = a.T * a.r_max;
+  const int a_blocks = sps * (rpad / 8);  // 8-row load blocks per projection
   for (int q = 0; q < n_ad_tile; ++q) {
     const int ad = ad_list[q];
-    // A rows of the adapter (rows past r_max repeat its last row: never stored)
-    for (int b = wave; b < sps * (rpad / 8); b += kShWaves) {
-      const int st = b / (rpad / 8), rb = b % (rpad / 8);
+    if (q > 0) wait_lgkm0_barrier();  // every wave is done with the previous A
+    // A rows of the adapter, every projection (rows past r_max repeat its
+    // last row: never stored)
+    for (int b = wave; b < G * a_blocks; b += kShWaves) {
+      const int g = b / a_blocks, st = (b % a_blocks) / (rpad / 8), rb = b % (rpad / 8);
       const int j = min(8 * rb + lane / 8, a.r_max - 1);
-      __builtin_amdgcn_global_load_lds(
-          Ag + (static_cast<int64_t>(ad) * a.r_max + j) * a.K + k0 + 64 * st + 8 * dchunk,
-          al + (st * rpad + 8 * rb) * 128, 16, 0, 0);
+      lds_load16(pick(a.ga, g) + (static_cast<int64_t>(ad) * a.r_max + j) * a.K + k0 + 64 * st +
+                     8 * dchunk,
+                 al + ((static_cast<size_t>(g) * sps + st) * rpad + 8 * rb) * 128);
     }
     wait_vmcnt<0>();
     wait_lgkm0_barrier();
 
-    f32x4 acc[2][RT];
+    for (int g = 0; g < G; ++g) {
+      f32x4 acc[RT];
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const uint8_t* ag = al + static_cast<size_t>(g) * sps * rpad * 128;
+      for (int st = 0; st < sps; ++st) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[tt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int st = wave; st < sps; st += kShWaves) {
-#pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const int rd = m ? rd1 : rd0;
-        u32x4 xf[2], af[RT];
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-          xf[tt] = *reinterpret_cast<const u32x4*>(xl + (st * kShTok + 16 * tt) * 128 + rd);
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          af[rt] = *reinterpret_cast<const u32x4*>(al + (st * rpad + 16 * rt) * 128 + rd);
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+        for (int m = 0; m < 2; ++m) {
+          const int rd = m ? rd1 : rd0;
+          const u32x4 xf =
+              *reinterpret_cast<const u32x4*>(xl + (st * kShTok + 16 * wave) * 128 + rd);
+          u32x4 af[RT];
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
-            acc[tt][rt] = mfma16x16x32(as_bf16x8(af[rt]), as_bf16x8(xf[tt]), acc[tt][rt]);
+            af[rt] = *reinterpret_cast<const u32x4*>(ag + (st * rpad + 16 * rt) * 128 + rd);
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+            acc[rt] = mfma16x16x32(as_bf16x8(af[rt]), as_bf16x8(xf), acc[rt]);
+        }
+      }
+      // lane l of tile rt holds rank rows 16 rt + 4 (l/16) .. +4 of token t
+      if (t_ad == ad) {
+        float* Pz = a.pout + (static_cast<int64_t>(g) * a.up_ks + z) * slice + t * a.r_max;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const int j = 16 * rt + 4 * kgrp;
+          if (j < a.r_max) *reinterpret_cast<f32x4*>(Pz + j) = acc[rt];
+        }
       }
     }
-    // sum the four waves' tiles in wave order; lane l of tile (tt, rt) holds
-    // rank rows 16rt + 4(l/16) .. +4 of token 16tt + l%16
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) red[((wave * 2 + tt) * RT + rt) * kWave + lane] = acc[tt][rt];
-    __syncthreads();
-    for (int item = tid; item < 2 * RT * kWave; item += kShThreads) {
-      const int tile = item / kWave, ln = item % kWave;
-      f32x4 v = red[tile * kWave + ln];
-#pragma unroll
-      for (int w = 1; w < kShWaves; ++w) v += red[(w * 2 * RT + tile) * kWave + ln];
-      const int tt = tile / RT, rt = tile % RT;
-      const int64_t t = t0 + 16 * tt + ln % 16;
-      const int j = 16 * rt + 4 * (ln / 16);
-      if (j < a.r_max && token_adapter(a, t) == ad)
-        *reinterpret_cast<f32x4*>(Pz + z * slice + t * a.r_max + j) = v;
-    }
-    __syncthreads();  // A and the reduction area are reused by the next adapter
   }
+  wait_vmcnt<0>();  // no direct load may still be writing LDS when the workgroup ends
 }
 
 template <typename Kernel>
@@ -1181,8 +1182,7 @@ template <int RT>
 local_status_t launch_shrink_rt(GemmArgs a, const ShrinkShape& sh, hipStream_t s) {
   static bool done = false;
   raise_lds_limit(lora_shrink_long_kernel<RT>, kShLdsMax, done);
-  const dim3 grid(static_cast<unsigned>((a.T + kShTok - 1) / kShTok), static_cast<unsigned>(sh.ks),
-                  static_cast<unsigned>(a.G));
+  const dim3 grid(static_cast<unsigned>((a.T + kShTok - 1) / kShTok), static_cast<unsigned>(sh.ks));
   lora_shrink_long_kernel<RT><<<grid, kShThreads, sh.lds, s>>>(a, sh.sps);
   return local_check_launch("lora_linear (shrink)");
 }
@@ -1414,7 +1414,7 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   // sums: [ksb][T][G*R] fp32 when the shrink runs inside the base product,
   // [slices][T][r_max] after the SGMV shrink. Above: the long shrink's
   // partial sums [ks][T][r_max] fp32.
-  const ShrinkShape shs = decode ? ShrinkShape{} : shrink_shape(T, K, r_max);
+  const ShrinkShape shs = decode ? ShrinkShape{} : shrink_shape(T, K, r_max, G);
   const size_t need =
       decode ? d.part_bytes + d.shrink_bytes
              : (n_adapters > 0
