@@ -39,7 +39,6 @@
 namespace localk {
 namespace {
 
-constexpr int kMaxLoraChunks = 1024;    // R <= 256 * 128 columns, in chunks of 32
 constexpr int kMaxGroup = 4;            // projections sharing x in one grouped call
 constexpr int kNumXcd = 8;
 
@@ -73,6 +72,8 @@ struct GemmArgs {
   uint16_t* y;           // bf16 output [T][N]
   int ksplit;            // K slices of the decode base product (grid.z)
   int gm, gn;            // tile grid of the long-chunk main product
+  uint64_t* tile_present;  // long chunks: bitmap of the adapters routed in each
+                           // 64-token tile, [ceil(T/64)][4], written by the shrink
 };
 
 // Rank of adapter ad, clamped to [0, r_max] so that no rank reads past the
@@ -113,10 +114,6 @@ __device__ __forceinline__ int rank_g(const GemmArgs& a, int g, int ad) {
   return r ? min(max(r[ad], 0), a.r_max) : a.r_max;
 }
 
-__device__ __forceinline__ bool adapter_present(const uint64_t* present, int ad) {
-  return (present[ad >> 6] >> (ad & 63)) & 1ull;
-}
-
 // Store features n..n+3 of token t of a [T][N] output (bounds-checked): the
 // residual, then one rounding to bf16.
 __device__ __forceinline__ void store4_out(uint16_t* y, const uint16_t* res, int64_t T, int64_t N,
@@ -152,62 +149,6 @@ __device__ __forceinline__ void wait_lgkm0_barrier() {
   __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-}
-
-// Marks the adapters my_ad of the calling threads (one token each, -1 for
-// none) in present[0..3] and lists, in ascending order, the chunks of `chunk`
-// U_s columns that cover at least one of them. Returns the number of chunks.
-// All threads of the workgroup must call it; `present` holds 4 * (1 + waves)
-// words (the bitmap, then one partial bitmap per wave). The bitmap is built
-// with wavefront OR reductions and plain LDS stores, not LDS atomics: an
-// atomic would make the compiler wait for the direct-to-LDS loads the caller
-// has in flight.
-template <int THREADS>
-__device__ int lora_chunk_list(const GemmArgs& a, int my_ad, int chunk, uint64_t* present,
-                               uint16_t* list, int* wave_cnt) {
-  constexpr int WAVES = THREADS / kWave;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  uint64_t mine = 0ull;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    uint64_t bits = (my_ad >= 0 && (my_ad >> 6) == w) ? 1ull << (my_ad & 63) : 0ull;
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) bits |= __shfl_xor(bits, off);
-    mine = lane == w ? bits : mine;
-  }
-  if (lane < 4) present[4 + 4 * wave + lane] = mine;
-  wait_lgkm0_barrier();
-  if (tid < 4) {
-    uint64_t all = 0ull;
-#pragma unroll
-    for (int w2 = 0; w2 < WAVES; ++w2) all |= present[4 + 4 * w2 + tid];
-    present[tid] = all;
-  }
-  wait_lgkm0_barrier();
-  const int chunks = (a.R + chunk - 1) / chunk;
-  int n = 0;
-  for (int base = 0; base < chunks; base += THREADS) {
-    const int l = base + tid;
-    bool use = false;
-    if (l < chunks) {
-      const int a_lo = (l * chunk) / a.r_max;
-      const int a_hi = min((l * chunk + chunk - 1) / a.r_max, a.n_ad - 1);
-      for (int ad = a_lo; ad <= a_hi; ++ad) use |= adapter_present(present, ad);
-    }
-    const uint64_t m = __ballot(use);
-    const int before = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_cnt[wave] = __popcll(m);
-    wait_lgkm0_barrier();
-    int off = n, tot = 0;
-    for (int w2 = 0; w2 < WAVES; ++w2) {
-      if (w2 < wave) off += wave_cnt[w2];
-      tot += wave_cnt[w2];
-    }
-    if (use) list[off + before] = static_cast<uint16_t>(l);
-    n += tot;
-    wait_lgkm0_barrier();
-  }
-  return n;
 }
 
 // The first `keep` (clamped to 0..8) of 8 packed bf16 values; the rest zero.
@@ -715,9 +656,6 @@ constexpr int kPfMfma = kPfFT * kPfTT;            // MFMAs per wave and half ste
 
 __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t pf_lds[];
-  __shared__ uint64_t present[4 * (1 + kPfWaves)];
-  __shared__ uint16_t chunks[kMaxLoraChunks];
-  __shared__ int wave_cnt[kPfWaves];
 
   const int tid = threadIdx.x, lane = tid % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: LDS bases in SGPRs
@@ -753,11 +691,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   const int64_t fw0 = n0 + 16 * kPfFT * wn;  // this wave's first feature
   const int tw0 = 16 * kPfTT * wm;           // ... and first token of the tile
 
-  // the tile's token adapters are loaded before the stage loads (the load
-  // counter drains in order, so a load issued after them would wait for them)
-  const bool lora = a.n_ad > 0 && Pg != nullptr;
-  const int my_ad = (lora && tid < kPfM) ? token_adapter(a, m0 + tid) : -1;
-  asm volatile("" ::: "memory");
+  const bool lora = a.n_ad > 0 && Pg != nullptr && a.tile_present != nullptr;  // uniform
 
   // ---- direct loads. Wave w moves x rows 32w .. +32 and W rows 64w .. +64
   // (its own features) of every stage; lane l writes 16 bytes at
@@ -851,9 +785,41 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   // workgroup into an LDS tile; Btilde is zero at or past the rank. Its
   // chain of loads runs while the first stages load. Adding the delta first
   // leaves a zero up-projection's result bit-identical (the MFMAs add +0).
-  int n_chunks = 0;
-  if (lora) n_chunks = lora_chunk_list<kPfThreads>(a, my_ad, 32, present, chunks, wave_cnt);
-  if (n_chunks > 0) {
+  // The adapters routed in the tile come from the bitmaps the shrink wrote
+  // for its two 64-token tiles, read by scalar loads, which do not wait for
+  // the stage loads.
+  uint64_t pm[4] = {0ull, 0ull, 0ull, 0ull};
+  if (lora) {
+    const int n64 = static_cast<int>((a.T + 63) / 64);
+    using const_u64 = const __attribute__((address_space(4))) uint64_t;  // scalar loads
+    const_u64* tp = (const_u64*)a.tile_present;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (2 * mt + h < n64)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) pm[w] |= tp[4 * (2 * mt + h) + w];
+  }
+  // the first chunk after chunk c that covers a routed adapter, or -1
+  auto next_chunk = [&](int c) {
+    const int amin = ((c + 1) * 32) / a.r_max;  // adapters with columns past chunk c
+    int found = -1;
+#pragma unroll
+    for (int w = 3; w >= 0; --w) {
+      uint64_t m = pm[w];
+      if (64 * w + 63 < amin)
+        m = 0ull;
+      else if (64 * w < amin)
+        m &= ~0ull << (amin - 64 * w);
+      if (m) found = 64 * w + __builtin_ctzll(m);
+    }
+    return found < 0 ? -1 : max(c + 1, found * a.r_max / 32);
+  };
+  auto routed = [&](int ad) {  // per lane: adapter ad is routed in the tile
+    const int w = ad >> 6;
+    const uint64_t m = w == 0 ? pm[0] : w == 1 ? pm[1] : w == 2 ? pm[2] : pm[3];
+    return ((m >> (ad & 63)) & 1ull) != 0ull;
+  };
+  if (lora) {
     uint8_t* ut = pf_lds + kPfStages * kPfStageBytes;  // [128 tokens][kPfURow]
     // forming: kFTpt threads per token, kFG groups of 8 columns each
     constexpr int kFTpt = kPfThreads / kPfM, kFG = 4 / kFTpt;
@@ -866,8 +832,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
     // Every load of a chunk is issued unconditionally (clamped to valid
     // addresses) and masked afterwards, so that all of them are in flight
     // together.
-    for (int q = 0; q < n_chunks; ++q) {
-      const int c0 = chunks[q] * 32;
+    for (int c = next_chunk(-1); c >= 0; c = next_chunk(c)) {
+      const int c0 = c * 32;
       // Btilde operand: features fw0 + 16i + col, columns cb .. cb+8
       const int cb = c0 + 8 * kgrp;
       const int bad = min(cb / a.r_max, a.n_ad - 1), bj = cb % a.r_max;
@@ -889,18 +855,26 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
         off[g] = (ft < a.T ? ft : m0) * a.r_max + c % a.r_max;
       }
       f32x4 sum[kFG][2] = {};
-      for (int z0 = 0; z0 < a.up_ks; z0 += 4) {
-        f32x4 v[4][kFG][2];
+      constexpr int kZB = 8;  // slices loaded together
+      for (int z0 = 0; z0 < a.up_ks; z0 += kZB) {
+        f32x4 v[kZB][kFG][2];
 #pragma unroll
-        for (int dz = 0; dz < 4; ++dz)
+        for (int dz = 0; dz < kZB; ++dz)
 #pragma unroll
           for (int g = 0; g < kFG; ++g) {
             const int64_t o = static_cast<int64_t>(min(z0 + dz, a.up_ks - 1)) * slice + off[g];
             v[dz][g][0] = ld_global<f32x4>(Pg + o);
             v[dz][g][1] = ld_global<f32x4>(Pg + o + 4);
           }
+        // every slice's loads are issued before the first sum (the compiler
+        // would otherwise move some into the conditional sums below, one
+        // memory round trip after the others)
 #pragma unroll
-        for (int dz = 0; dz < 4; ++dz)
+        for (int dz = 0; dz < kZB; ++dz)
+#pragma unroll
+          for (int g = 0; g < kFG; ++g) asm volatile("" : "+v"(v[dz][g][0]), "+v"(v[dz][g][1]));
+#pragma unroll
+        for (int dz = 0; dz < kZB; ++dz)
           if (z0 + dz < a.up_ks)
 #pragma unroll
             for (int g = 0; g < kFG; ++g) {
@@ -909,8 +883,14 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
             }
       }
       // U_s: zero unless the columns' adapter is the token's, and at or past
-      // its rank (padding rows of A may hold anything)
-      const int fad = (ft < a.T && fidx >= 0 && fidx < a.n_ad) ? fidx : -1;
+      // its rank (padding rows of A may hold anything). The token's adapter
+      // and scale are passed through an empty asm here so that the compiler
+      // cannot test them (and wait for their loads, which the stage loads
+      // precede) before the chunk's loads are issued.
+      int fidx_c = fidx;
+      float fscl_c = fscl;
+      asm volatile("" : "+v"(fidx_c), "+v"(fscl_c));
+      const int fad = (ft < a.T && fidx_c >= 0 && fidx_c < a.n_ad) ? fidx_c : -1;
 #pragma unroll
       for (int g = 0; g < kFG; ++g) {
         const int c = c0 + 8 * (kFG * fh + g);
@@ -920,7 +900,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float sv = e < 4 ? sum[g][0][e] : sum[g][1][e - 4];
-          u[e] = e < keep ? fscl * sv : 0.f;
+          u[e] = e < keep ? fscl_c * sv : 0.f;
         }
         *reinterpret_cast<u32x4*>(ut + ftl * kPfURow + 16 * (kFG * fh + g)) =
             u32x4{pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]), pack_bf16x2(u[4], u[5]),
@@ -928,7 +908,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
       }
       // Btilde: zero for an adapter not routed in the tile, and at or past
       // the rank
-      const int bkeep = (cb < a.R && adapter_present(present, bad))
+      const int bkeep = (cb < a.R && routed(bad))
                             ? min(max(brk, 0), a.r_max) - bj : 0;
       bf16x8 bv[kPfFT];
 #pragma unroll
@@ -1092,14 +1072,17 @@ __global__ __launch_bounds__(kShThreads) void lora_shrink_long_kernel(GemmArgs a
   if (wave == 0) {  // adapters routed in the tile, in order of first appearance
     uint64_t pending = __ballot(my >= 0);
     int n = 0;
+    uint64_t bits = 0ull;  // lane w < 4: word w of the tile's adapter bitmap
     while (pending) {
       const int ad = __shfl(my, __ffsll(static_cast<long long>(pending)) - 1);
       if (lane == 0) ad_list[n] = ad;
       ++n;
+      if (lane == (ad >> 6)) bits |= 1ull << (ad & 63);
       pending &= ~__ballot(my == ad);
     }
     if (lane == 0) n_list = n;
     tok_ad[lane] = my;
+    if (z == 0 && lane < 4) a.tile_present[4 * blockIdx.x + lane] = bits;
   }
   load_x();
   wait_lgkm0_barrier();  // the list; the x loads stay in flight
@@ -1413,13 +1396,14 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   // [ksb][T][N] fp32 (N over all projections), then the shrink's partial
   // sums: [ksb][T][G*R] fp32 when the shrink runs inside the base product,
   // [slices][T][r_max] after the SGMV shrink. Above: the long shrink's
-  // partial sums [ks][T][r_max] fp32.
+  // partial sums [G][ks][T][r_max] fp32, then its adapter bitmaps
+  // [ceil(T/64)][4] uint64.
   const ShrinkShape shs = decode ? ShrinkShape{} : shrink_shape(T, K, r_max, G);
-  const size_t need =
-      decode ? d.part_bytes + d.shrink_bytes
-             : (n_adapters > 0
-                    ? align256(static_cast<size_t>(G) * shs.ks * T * r_max * sizeof(float))
-                    : 0);
+  const size_t long_p =
+      align256(static_cast<size_t>(G) * shs.ks * T * r_max * sizeof(float));
+  const size_t long_bits = align256(static_cast<size_t>((T + 63) / 64) * 4 * sizeof(uint64_t));
+  const size_t need = decode ? d.part_bytes + d.shrink_bytes
+                             : (n_adapters > 0 ? long_p + long_bits : 0);
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -1472,6 +1456,8 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
   GemmArgs m = g;
   set_groups(m, G, p);
   m.pout = P;
+  m.tile_present =
+      n_adapters > 0 ? reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + long_p) : nullptr;
   m.up_ks = shs.ks;
   if (n_adapters > 0 && (st = launch_shrink_long(m, shs, s)) != LOCAL_OK) return st;
   return launch_prefill(m, s);

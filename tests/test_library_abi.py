@@ -60,12 +60,13 @@ def test_lora_linear_workspace_and_errors(lib):
     st, n2 = _size(f, FAKE, 32, 4096, FAKE, 64, FAKE, FAKE, 16, 16, None, FAKE, FAKE, None, FAKE)
     assert st == OK and n2 == 8 * 32 * 64 * 4 + 8 * 32 * 16 * 4
     # above 256 tokens: the shrink's fp32 partial sums for each token's own
-    # adapter, 8 K slices (the most; 5 tiles of 64 tokens) x T x r_max
+    # adapter, 8 K slices (the most; 5 tiles of 64 tokens) x T x r_max, then
+    # a 32-byte adapter bitmap per 64-token tile, each part 256-byte aligned
     st, n1 = _size(f, FAKE, 300, 4096, FAKE, 4096, FAKE, FAKE, 8, 16, None, FAKE, FAKE, None, FAKE)
-    assert st == OK and n1 == 8 * 300 * 16 * 4
+    assert st == OK and n1 == 8 * 300 * 16 * 4 + 256
     # 2048 tokens (32 tiles of 64): 8 slices fill the chip (fewer do not fit LDS)
     st, n2k = _size(f, FAKE, 2048, 4096, FAKE, 4096, FAKE, FAKE, 4, 16, None, FAKE, FAKE, None, FAKE)
-    assert st == OK and n2k == 8 * 2048 * 16 * 4
+    assert st == OK and n2k == 8 * 2048 * 16 * 4 + 32 * 32
     st, n0 = _size(f, FAKE, 32, 4096, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)
     assert st == OK and n0 == 4 * 32 * 4096 * 4
     assert _size(f, FAKE, 32, 100, FAKE, 4096, None, None, 0, 0, None, None, None, None, FAKE)[0] == ERR_UNSUPPORTED
@@ -146,10 +147,11 @@ def test_lora_linear_grouped_workspace_and_errors(lib):
                   FAKE, ptrs(3))
     assert st == OK and n == 2 * 32 * 12288 * 4 + 2 * 32 * 384 * 4
     # a 2048-token chunk: one launch over the three projections, the shrink's
-    # partial sums per projection (8 K slices x T x r_max fp32 each)
+    # partial sums per projection (8 K slices x T x r_max fp32 each), then the
+    # adapter bitmaps (32 bytes per 64-token tile)
     st, n = _size(f, FAKE, 2048, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 4, 16, None, FAKE,
                   FAKE, ptrs(3))
-    assert st == OK and n == 3 * 8 * 2048 * 16 * 4
+    assert st == OK and n == 3 * 8 * 2048 * 16 * 4 + 32 * 32
     assert _size(f, FAKE, 32, 4096, 0, ptrs(1), Ns, None, None, 0, 0, None, None, None,
                  ptrs(1))[0] == ERR_UNSUPPORTED
     assert _size(f, FAKE, 32, 4096, 5, ptrs(5), Ns, None, None, 0, 0, None, None, None,
