@@ -114,22 +114,6 @@ __device__ __forceinline__ int rank_g(const GemmArgs& a, int g, int ad) {
   return r ? min(max(r[ad], 0), a.r_max) : a.r_max;
 }
 
-// Store features n..n+3 of token t of a [T][N] output (bounds-checked): the
-// residual, then one rounding to bf16.
-__device__ __forceinline__ void store4_out(uint16_t* y, const uint16_t* res, int64_t T, int64_t N,
-                                           int64_t t, int64_t n, f32x4 v) {
-  if (t >= T || n >= N) return;
-  float o[4] = {v[0], v[1], v[2], v[3]};
-  if (res) {
-    const u32x2 r = ld_global<u32x2>(res + t * N + n);
-    o[0] += __uint_as_float(r.x << 16);
-    o[1] += __uint_as_float(r.x & 0xffff0000u);
-    o[2] += __uint_as_float(r.y << 16);
-    o[3] += __uint_as_float(r.y & 0xffff0000u);
-  }
-  *reinterpret_cast<u32x2*>(y + t * N + n) = u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-}
-
 // Adapter of token t, or -1 (past the batch, no adapter, or out of range).
 __device__ __forceinline__ int token_adapter(const GemmArgs& a, int64_t t) {
   if (t >= a.T) return -1;
@@ -649,6 +633,8 @@ constexpr int kPfStages = 3;
 constexpr int kPfURow = 80;                       // bytes of a U_s tile row: 32 bf16 + pad
 constexpr int kPfUBytes = kPfM * kPfURow;         // 10 KB
 constexpr int kPfLdsBytes = kPfStages * kPfStageBytes + kPfUBytes;  // 154 KB
+constexpr int kPfOutRow = kPfN * 4 + 16;          // bytes of a token row of the output tile
+static_assert(kPfM * kPfOutRow <= kPfLdsBytes, "output tile in LDS");
 constexpr int kPfXDma = kPfM / 8 / kPfWaves;      // 1 KB loads of x per wave and step
 constexpr int kPfWDma = kPfN / 8 / kPfWaves;      // ... of W
 constexpr int kPfDma = kPfXDma + kPfWDma;
@@ -975,12 +961,52 @@ __global__ __launch_bounds__(kPfThreads, 1) void lora_prefill_kernel(GemmArgs a)
   }
   wait_vmcnt<0>();
 
+  // ---- output. The tile's fp32 sums go through LDS (the stages are free once
+  // every wave's loads have landed and its reads are done), so that each
+  // thread then finishes 8 consecutive features of one token: the residual
+  // and the output move as coalesced 16-byte pieces. Token rows are
+  // kPfOutRow bytes (1 KB + 16), so the 16 tokens of one MFMA tile written
+  // together fall in distinct banks.
+  wait_lgkm0_barrier();
 #pragma unroll
   for (int j = 0; j < kPfTT; ++j)
 #pragma unroll
     for (int i = 0; i < kPfFT; ++i)
-      store4_out(pick(a.gy, gq), pick(a.gres, gq), a.T, Ng, m0 + tw0 + 16 * j + col,
-                 fw0 - gbase + 16 * i + 4 * kgrp, acc[i][j]);
+      *reinterpret_cast<f32x4*>(pf_lds + (tw0 + 16 * j + col) * kPfOutRow +
+                                (16 * kPfFT * wn + 16 * i + 4 * kgrp) * 4) = acc[i][j];
+  wait_lgkm0_barrier();
+  const uint16_t* res = pick(a.gres, gq);
+  uint16_t* y = pick(a.gy, gq);
+  constexpr int kGroups = kPfN / 8;                       // 8-feature groups per token
+  constexpr int kItems = kPfM * kGroups / kPfThreads;     // per thread
+  u32x4 rv[kItems];
+#pragma unroll
+  for (int e = 0; e < kItems; ++e) {
+    const int item = tid + e * kPfThreads, tl = item / kGroups, f = 8 * (item % kGroups);
+    const int64_t t = m0 + tl, n = n0 - gbase + f;
+    rv[e] = (res && t < a.T && n < Ng) ? ld_global<u32x4>(res + t * Ng + n) : u32x4{0u, 0u, 0u, 0u};
+  }
+#pragma unroll
+  for (int e = 0; e < kItems; ++e) {
+    const int item = tid + e * kPfThreads, tl = item / kGroups, f = 8 * (item % kGroups);
+    const int64_t t = m0 + tl, n = n0 - gbase + f;
+    const uint8_t* src = pf_lds + tl * kPfOutRow + f * 4;
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(src);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(src + 16);
+    float o[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    if (res) {
+      const uint32_t r[4] = {rv[e].x, rv[e].y, rv[e].z, rv[e].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        o[2 * q] += __uint_as_float(r[q] << 16);
+        o[2 * q + 1] += __uint_as_float(r[q] & 0xffff0000u);
+      }
+    }
+    if (t < a.T && n < Ng)
+      *reinterpret_cast<u32x4*>(y + t * Ng + n) =
+          u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                pack_bf16x2(o[6], o[7])};
+  }
 }
 
 // ------------------------------------------------------------ long shrink
