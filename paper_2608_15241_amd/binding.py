@@ -2,8 +2,10 @@
 
 Every function here checks and marshals torch tensors to the C ABI declared in
 include/local.h and enqueues the library's HIP kernels on the current torch
-stream. No computation happens in Python and there is no fallback: if the
-built library is missing or fails to load, every call raises.
+stream; `KVManager` marshals numpy arrays to the host-side KV manager of
+include/local_kv.h. No computation happens in Python and there is no
+fallback: if the built library is missing or fails to load, every call
+raises.
 
 torch is imported before the library is loaded so that the library binds to
 the HIP runtime torch already loaded (both use the soname libamdhip64.so.7),
@@ -15,6 +17,7 @@ import ctypes
 import os
 from typing import Optional, Tuple
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -23,7 +26,14 @@ BLOCK_SIZE = 16
 
 EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
-           "local_block_version_check")
+           "local_block_version_check",
+           # host-side KV manager (local_kv.h)
+           "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
+           "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
+           "local_kvm_discard_staged", "local_kvm_versions", "local_kvm_alloc",
+           "local_kvm_release", "local_kvm_lookup", "local_kvm_insert",
+           "local_kvm_plan_stale_prefill", "local_kvm_path", "local_kvm_evict",
+           "local_kvm_scores", "local_kvm_stats")
 
 _STATUS = {0: "LOCAL_OK", 1: "LOCAL_ERR_NULL", 2: "LOCAL_ERR_SHAPE",
            3: "LOCAL_ERR_UNSUPPORTED", 4: "LOCAL_ERR_WORKSPACE", 5: "LOCAL_ERR_HIP"}
@@ -68,8 +78,48 @@ def load_library(path: str = LIB_PATH):
     lib.local_block_version_check.restype = ctypes.c_int
     lib.local_block_version_check.argtypes = [P, i32, i32, P, i32, P, i64, P, P, i64, P, P,
                                               P, SZ, P]
+    _declare_kvm(lib)
     _lib = lib
     return lib
+
+
+class KvmParams(ctypes.Structure):
+    """local_kvm_params_t (local_kv.h)."""
+    _fields_ = [(n, ctypes.c_double) for n in (
+        "lambda_p", "lambda_a", "beta", "chi", "eta", "zeta", "eps", "alpha_l", "l_max",
+        "c_tok", "c_ctx", "block_bytes")]
+
+
+def _declare_kvm(lib):
+    P, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    I32P, I64P, F64P = (ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64),
+                        ctypes.POINTER(ctypes.c_double))
+    sig = {
+        "local_kvm_default_params": (None, [ctypes.POINTER(KvmParams)]),
+        "local_kvm_create": (P, [i32, ctypes.POINTER(KvmParams)]),
+        "local_kvm_destroy": (None, [P]),
+        "local_kvm_tags": (I32P, [P]),
+        "local_kvm_set_committed": (ctypes.c_int, [P, i32, i32]),
+        "local_kvm_stage": (ctypes.c_int, [P, i32, i32]),
+        "local_kvm_publish": (ctypes.c_int, [P, i32, I32P]),
+        "local_kvm_discard_staged": (ctypes.c_int, [P, i32, I32P]),
+        "local_kvm_versions": (ctypes.c_int, [P, i32, I32P, I32P]),
+        "local_kvm_alloc": (ctypes.c_int, [P, i32, i32, I32P]),
+        "local_kvm_release": (ctypes.c_int, [P, I32P, i32]),
+        "local_kvm_lookup": (ctypes.c_int, [P, i32, i32, i32, I32P, i64, f64, f64, f64, I32P,
+                                            i32, I32P]),
+        "local_kvm_insert": (ctypes.c_int, [P, i32, i32, i32, I32P, i64, i32, I32P, i32,
+                                            I32P]),
+        "local_kvm_plan_stale_prefill": (ctypes.c_int, [P, i32, i32, I32P, I32P, I32P, I32P]),
+        "local_kvm_path": (ctypes.c_int, [P, i32, I32P, I32P, i64, I64P]),
+        "local_kvm_evict": (ctypes.c_int, [P, i32, I32P, i32, I32P]),
+        "local_kvm_scores": (ctypes.c_int, [P, i32, i32, i32, F64P, F64P, F64P, F64P]),
+        "local_kvm_stats": (ctypes.c_int, [P, I32P, I32P, I32P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
 
 
 def _check(status: int):
@@ -414,3 +464,130 @@ def local_block_version_check(*args, **kwargs
     Only the first min(n_stale, cap) rows of stale_pairs are written.
     """
     return prepare_block_version_check(*args, **kwargs)()
+
+
+# ------------------------------------------------------------ KV manager
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _p32(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+class KVManager:
+    """The host-side KV cache manager of local_kv.h (argument marshalling
+    only). Methods take the names of the C calls without the prefix."""
+
+    def __init__(self, num_blocks: int, params: Optional[dict] = None):
+        lib = load_library()
+        p = KvmParams()
+        lib.local_kvm_default_params(ctypes.byref(p))
+        for k, v in (params or {}).items():
+            setattr(p, k, float(v))
+        h = lib.local_kvm_create(int(num_blocks), ctypes.byref(p))
+        if not h:
+            raise LocalError(2, lib.local_last_error().decode())
+        self._lib, self._h, self.num_blocks = lib, ctypes.c_void_p(h), int(num_blocks)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.local_kvm_destroy(h)
+            self._h = None
+
+    def tags(self) -> np.ndarray:
+        """Copy of the version tag of every block (the `block_version` array)."""
+        ptr = self._lib.local_kvm_tags(self._h)
+        return np.ctypeslib.as_array(ptr, shape=(self.num_blocks,)).copy()
+
+    def set_committed(self, adapter: int, version: int):
+        _check(self._lib.local_kvm_set_committed(self._h, adapter, version))
+
+    def stage(self, adapter: int, version: int):
+        _check(self._lib.local_kvm_stage(self._h, adapter, version))
+
+    def publish(self, adapter: int) -> int:
+        old = ctypes.c_int32()
+        _check(self._lib.local_kvm_publish(self._h, adapter, ctypes.byref(old)))
+        return old.value
+
+    def discard_staged(self, adapter: int) -> int:
+        n = ctypes.c_int32()
+        _check(self._lib.local_kvm_discard_staged(self._h, adapter, ctypes.byref(n)))
+        return n.value
+
+    def versions(self, adapter: int) -> Tuple[int, int]:
+        c, st = ctypes.c_int32(), ctypes.c_int32()
+        _check(self._lib.local_kvm_versions(self._h, adapter, ctypes.byref(c), ctypes.byref(st)))
+        return c.value, st.value
+
+    def alloc(self, n: int, version: int) -> np.ndarray:
+        out = np.zeros(max(n, 0), dtype=np.int32)
+        _check(self._lib.local_kvm_alloc(self._h, n, version, _p32(out)))
+        return out
+
+    def release(self, blocks):
+        b = _i32(blocks)
+        _check(self._lib.local_kvm_release(self._h, _p32(b), b.size))
+
+    def lookup(self, ns: int, adapter: int, version: int, tokens, d_prefix: float = 0.0,
+               s_prefix: float = 0.0, d_adapter: float = 0.0,
+               max_blocks: Optional[int] = None) -> np.ndarray:
+        t = _i32(tokens)
+        mb = t.size // BLOCK_SIZE if max_blocks is None else int(max_blocks)
+        out = np.zeros(max(mb, 1), dtype=np.int32)
+        n = ctypes.c_int32()
+        _check(self._lib.local_kvm_lookup(self._h, ns, adapter, version, _p32(t), t.size,
+                                          d_prefix, s_prefix, d_adapter, _p32(out), mb,
+                                          ctypes.byref(n)))
+        return out[:n.value].copy()
+
+    def insert(self, ns: int, adapter: int, version: int, tokens, blocks,
+               first: int = 0) -> np.ndarray:
+        t, b = _i32(tokens), _i32(blocks)
+        rec = np.zeros(max(b.size, 1), dtype=np.int32)
+        _check(self._lib.local_kvm_insert(self._h, ns, adapter, version, _p32(t), t.size,
+                                          int(first), _p32(b), b.size, _p32(rec)))
+        return rec[:b.size].copy()
+
+    def plan_stale_prefill(self, adapter: int, max_prefixes: int = 8):
+        """[(node, covered_blocks, total_blocks)] ranked hottest first."""
+        m = max(int(max_prefixes), 1)
+        nodes, cov, tot = (np.zeros(m, dtype=np.int32) for _ in range(3))
+        n = ctypes.c_int32()
+        _check(self._lib.local_kvm_plan_stale_prefill(self._h, adapter, int(max_prefixes),
+                                                      _p32(nodes), _p32(cov), _p32(tot),
+                                                      ctypes.byref(n)))
+        return [(int(nodes[i]), int(cov[i]), int(tot[i])) for i in range(n.value)]
+
+    def path(self, node: int) -> Tuple[int, np.ndarray]:
+        """(namespace, tokens of the path from the root to `node`)."""
+        ns, n = ctypes.c_int32(), ctypes.c_int64()
+        _check(self._lib.local_kvm_path(self._h, node, ctypes.byref(ns), None, 0,
+                                        ctypes.byref(n)))
+        out = np.zeros(max(n.value, 1), dtype=np.int32)
+        _check(self._lib.local_kvm_path(self._h, node, ctypes.byref(ns), _p32(out), n.value,
+                                        ctypes.byref(n)))
+        return ns.value, out[:n.value].copy()
+
+    def evict(self, n_free: int) -> np.ndarray:
+        out = np.zeros(max(self.num_blocks, 1), dtype=np.int32)
+        n = ctypes.c_int32()
+        _check(self._lib.local_kvm_evict(self._h, n_free, _p32(out), self.num_blocks,
+                                         ctypes.byref(n)))
+        return out[:n.value].copy()
+
+    def scores(self, node: int, adapter: int, version: int) -> Tuple[float, float, float, float]:
+        """(H_P, H_A, H_KV, Pi_keep) at the current clock."""
+        v = [ctypes.c_double() for _ in range(4)]
+        _check(self._lib.local_kvm_scores(self._h, node, adapter, version,
+                                          *[ctypes.byref(x) for x in v]))
+        return tuple(x.value for x in v)
+
+    def stats(self) -> Tuple[int, int, int]:
+        """(free blocks, recorded blocks, trie nodes)."""
+        v = [ctypes.c_int32() for _ in range(3)]
+        _check(self._lib.local_kvm_stats(self._h, *[ctypes.byref(x) for x in v]))
+        return tuple(x.value for x in v)
