@@ -270,6 +270,10 @@ def main():
     if primary and not args.no_prefill:
         say("prefill projections")
         result["prefill"] = bench_prefill(torch, workloads, lk, dev)
+        say("prefill attention")
+        result["prefill_attn"] = bench_prefill_attn(torch, workloads, lk, dev)
+        say("stale-coverage prefill")
+        result["reprefill"] = bench_reprefill(torch, workloads, lk, dev)
 
     if primary and not args.no_cpu_baseline:
         say("cpu baseline")
@@ -366,6 +370,170 @@ def bench_prefill(torch, workloads, lk, dev, reps=20):
             "bound": "mfma", "flops_per_step": flops, "ms_per_step": round(ms, 5),
             "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
+def prefill_attn_flops(w, meta):
+    """2 * 2 * D flop per (query, key) pair attended: query i of request b at
+    position P_b + i sees keys 0 .. P_b + i, for every query head."""
+    pairs = 0
+    for b in range(meta.B):
+        n = int(meta.n_new[b])
+        P = int(meta.ctx_lens[b]) - n
+        pairs += n * P + n * (n + 1) // 2
+    return 4 * w.head_dim * w.hq * pairs
+
+
+def bench_prefill_attn(torch, workloads, lk, dev, reps=20):
+    """Matrix-core utilisation of the appending, version-masked paged prefill
+    attention of the prefill workload (4 chunks of 512 on prefixes
+    {0, 512, 1024, 2048}), timed as graph replays over two input sets."""
+    from paper_2608_15241_amd.step import meta_to_device
+    w = workloads.PREFILL_7B
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
+    D, T = w.head_dim, meta.T
+    calls, keep = [], []
+    for s in range(2):
+        pool = workloads.make_kv_pool(w, meta, dev, seed=600 + s)
+        q = workloads.randn_bf16((T, w.hq, D), 1.0, dev, seed=610 + s)
+        kn = workloads.randn_bf16((T, w.hkv, D), 1.0, dev, seed=620 + s)
+        vn = workloads.randn_bf16((T, w.hkv, D), 1.0, dev, seed=630 + s)
+        keep += [pool, q, kn, vn]
+        calls.append(lk.prepare_paged_attn_prefill(
+            q, md.q_indptr, pool[0, 0], pool[0, 1], md.block_table, md.ctx_lens,
+            md.block_version, md.req_version, 1 / math.sqrt(D), k_new=kn, v_new=vn, Hkv=w.hkv))
+    for c in calls:
+        c()
+    torch.cuda.synchronize()
+    graphs = []
+    for c in calls:
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            with torch.cuda.graph(g, stream=st):
+                c()
+        torch.cuda.current_stream().wait_stream(st)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for r in range(reps):
+        graphs[r % 2].replay()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flops = prefill_attn_flops(w, meta)
+    tflops = flops / (ms / 1e3) / 1e12
+    return {"workload": w.name, "kernel": "local_paged_attn_prefill (append + attention)",
+            "bound": "mfma", "flops_per_call": flops, "ms_per_call": round(ms, 5),
+            "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
+def bench_reprefill(torch, workloads, lk, dev, n_prefix=8, prefix_blocks=64, chunk_blocks=8):
+    """Stale-coverage prefill (§5.3) at the prefill workload's shapes: eight hot
+    prefixes of 1024 tokens, recorded under the committed version, re-prefilled
+    under the staged version in 128-token chunks (one prefill step per round,
+    every prefix advancing one chunk), the KV manager planning, matching,
+    allocating and recording on the host between rounds. Reports the warm-up's
+    throughput, the matrix-core utilisation of its projections, and the host
+    time of the manager."""
+    from paper_2608_15241_amd.step import Step, meta_to_device
+    w = workloads.PREFILL_7B
+    D, BS = w.head_dim, lk.BLOCK_SIZE
+    AD, C, S = 0, workloads.adapter_version(0), workloads.adapter_version(0) + 1
+    rng = np.random.default_rng(17)
+    num_blocks = 2 * n_prefix * prefix_blocks
+    lw = workloads.make_layer_weights(w, 0, dev, seed=500)
+    pool = workloads.randn_bf16((1, 2, num_blocks, w.hkv, BS * D), 1.0, dev, seed=501)
+    emb = workloads.randn_bf16((4096, w.hidden), 1.0, dev, seed=502)
+    paths = [rng.integers(0, 4096, size=BS * prefix_blocks).astype(np.int32)
+             for _ in range(n_prefix)]
+    m = lk.KVManager(num_blocks)
+    m.set_committed(AD, C)
+    for p in paths:  # committed coverage (its KV content does not matter here)
+        m.insert(0, AD, C, p, m.alloc(prefix_blocks, C))
+        m.lookup(0, AD, C, p)
+    m.stage(AD, S)
+
+    def round_inputs():
+        t0 = time.perf_counter()
+        plan = m.plan_stale_prefill(AD, n_prefix)
+        tables, ctx, n_new, toks, fresh = [], [], [], [], []
+        for node, cov, tot in plan:
+            pp = m.path(node)[1]
+            have = m.lookup(0, AD, S, pp)
+            nb = min(chunk_blocks, tot - len(have))
+            new = m.alloc(nb, S)
+            tables.append(np.concatenate([have, new]))
+            ctx.append(BS * (len(have) + nb))
+            n_new.append(BS * nb)
+            toks.append(pp[BS * len(have):BS * (len(have) + nb)])
+            fresh.append((pp, len(have), new))
+        host = time.perf_counter() - t0
+        if not plan:
+            return None, host
+        B = len(plan)
+        table = np.zeros((B, max(len(t) for t in tables)), dtype=np.int32)
+        for b, t in enumerate(tables):
+            table[b, :len(t)] = t
+        q_indptr = np.zeros(B + 1, dtype=np.int32)
+        q_indptr[1:] = np.cumsum(n_new)
+        T = int(q_indptr[-1])
+        meta = workloads.Meta(
+            ctx_lens=np.asarray(ctx, np.int32), n_new=np.asarray(n_new, np.int32),
+            q_indptr=q_indptr, request_adapter=np.full(B, AD, np.int32),
+            req_version=np.full(B, S, np.int32), block_table=table,
+            block_version=m.tags(), num_blocks=num_blocks, max_blocks=table.shape[1],
+            stale_entries=np.zeros((0, 2), np.int32), token_adapter=np.full(T, AD, np.int32),
+            token_scale=np.full(T, workloads.configs.LORA_SCALE, np.float32))
+        x = emb[torch.as_tensor(np.concatenate(toks).astype(np.int64), device=dev)].contiguous()
+        st = Step("prefill", x, [lw], meta_to_device(meta, dev), pool, w.hq, w.hkv, D,
+                  residual=False)
+        return (st, fresh, T, meta), host
+
+    rounds, tokens, host_s, gpu_ms, flops = 0, 0, 0.0, 0.0, 0
+    ev_a, ev_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    while True:
+        r, h = round_inputs()
+        host_s += h
+        if r is None:
+            break
+        st, fresh, T, meta = r
+        st()  # sets kernel attributes; then the round as one HIP graph, replayed
+        torch.cuda.synchronize()  # (it only rewrites the same slots)
+        g = st.capture()
+        g.replay()
+        torch.cuda.synchronize()
+        ev_a.record()
+        g.replay()
+        ev_b.record()
+        torch.cuda.synchronize()
+        gpu_ms += ev_a.elapsed_time(ev_b)
+        del g
+        t0 = time.perf_counter()
+        for pp, first, new in fresh:
+            m.insert(0, AD, S, pp, new, first=first)
+        host_s += time.perf_counter() - t0
+        rounds += 1
+        tokens += T
+        flops += prefill_gemm_flops(w, meta)
+    m.publish(AD)
+    tflops = flops / (gpu_ms / 1e3) / 1e12
+    return {"workload": "reprefill_7b_8x1024", "prefixes": n_prefix,
+            "prefix_tokens": BS * prefix_blocks, "chunk_tokens": BS * chunk_blocks,
+            "rounds": rounds, "tokens": tokens, "gpu_ms": round(gpu_ms, 4),
+            "tokens_per_s": round(tokens / (gpu_ms / 1e3), 1),
+            "projection_flops": flops, "step_tflops": round(tflops, 1),
+            "step_frac_of_mfma_peak": round(tflops / BF16_PEAK_TFLOPS, 4),
+            "host_manager_us_per_round": round(host_s / max(rounds, 1) * 1e6, 1),
+            "note": "each round is one whole prefill step (version check, q/k/v, appending "
+                    "causal attention, o) timed as a HIP graph replay; step_tflops counts the "
+                    "projections' flops only"}
 
 
 def cpu_baseline(torch, workloads, w, meta, set0, args):

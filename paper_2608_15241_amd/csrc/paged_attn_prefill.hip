@@ -4,26 +4,35 @@
 // prefill is the same computation under a staged version).
 //
 // Design (matrix-core bound):
-//  * An append kernel first writes the chunk's K/V into its slots; every
-//    attention workgroup that reads the chunk runs after it on the stream.
-//  * Attention workgroup = (query tile of 64*QT rows, query head h, request b):
-//    4 waves, each owning 16*QT query rows as matrix columns. The request's
-//    non-stale blocks up to the tile's causal limit are compacted with
-//    ballots, then staged KB blocks at a time into LDS in the pool's own
-//    layout (so every operand read is a contiguous 16- or 8-byte LDS slice).
+//  * Append: a workgroup per (request, block of its chunk, KV head) writes
+//    that block's new K slots as 16-byte pieces and its new V slots through
+//    an LDS transpose (V is dim-major in the pool), as whole 32-byte dim rows
+//    when the block is all new. Every attention workgroup runs after it.
+//  * Attention workgroup = (tile of 128 query rows, query head h, request b):
+//    4 waves of 32 rows (two 16-column MFMA tiles each). The request's
+//    non-stale blocks up to the tile's causal limit are listed in ascending
+//    order with ballots; then they stream, two blocks (32 keys) per step,
+//    through a ring of 4 LDS stages filled by direct global-to-LDS loads:
+//    each wave moves one 16*D*2-byte (block, head) tile of K or V per step,
+//    in the pool's own layout, so every operand read is a contiguous LDS
+//    slice, and the loads of step s + 3 go out as step s starts.
 //  * S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_bf16, the same
 //    transposed formulation as decode: the score accumulator is already the
 //    B operand of the value product, so no lane shuffle of P is needed.
-//    Causal and dead-slot masking, online softmax in the log2 domain.
+//    Causal masking per key, dead slots past the context end zeroed in V,
+//    online softmax in the log2 domain. Steps wholly past a wave's causal
+//    limit skip its arithmetic (the wave still takes part in the loads).
 #include "common.hpp"
 
 namespace localk {
 namespace {
 
-constexpr int kPfWaves = 4;
-constexpr int kPfThreads = kPfWaves * kWave;
-constexpr int kPfKB = 4;  // blocks staged per tile (64 keys)
-constexpr int kPfWindow = kPfThreads;  // block-table entries compacted per pass
+constexpr int kPaWaves = 4;
+constexpr int kPaThreads = kPaWaves * kWave;
+constexpr int kPaQT = 2;                        // 16-row query tiles per wave
+constexpr int kPaRows = kPaWaves * 16 * kPaQT;  // query rows per workgroup (128)
+constexpr int kPaStages = 4;                    // LDS ring depth
+constexpr int kPaWindow = 256;                  // block-table entries listed per pass
 constexpr float kNegBigPf = -1.0e30f;
 
 struct PrefillArgs {
@@ -48,62 +57,161 @@ __device__ __forceinline__ bool id_ok(int p, int64_t num_blocks) {
   return p >= 0 && p < num_blocks;
 }
 
-__device__ __forceinline__ int find_request(const int32_t* __restrict__ q_indptr, int B,
-                                            int64_t t) {
-  int lo = 0, hi = B - 1;  // last b with q_indptr[b] <= t
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (q_indptr[mid] <= t) lo = mid;
-    else hi = mid - 1;
+// The k-th unit of work (k >= 0), counting units from the last request
+// backwards and, within a request, from its last unit, where request b has
+// units(b) >= 0 of them. Returns the request (-1 when k is past the total)
+// and, in *u, the unit's index within its request. The host sizes grids by
+// an upper bound of the total, since the requests' sizes are device data; a
+// grid mapped this way has no idle workgroups among the working ones (they
+// all come at its end), and the dispatch order takes the last requests,
+// commonly those with the longest prefixes, first. The wave scans 64
+// requests at a time; every lane returns the same result.
+template <typename Units>
+__device__ int unit_from_end(int B, int k, Units units, int* u) {
+  const int lane = threadIdx.x % kWave;
+  for (int base = B - 1; base >= 0; base -= kWave) {
+    const int bb = base - lane;
+    const int n = bb >= 0 ? units(bb) : 0;
+    int incl = n;  // inclusive prefix over lanes (requests base, base-1, ...)
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    const int total = __shfl(incl, kWave - 1);
+    if (k < total) {
+      const uint64_t m = __ballot(incl > k);
+      const int l0 = __ffsll(static_cast<long long>(m)) - 1;
+      const int before = __shfl(incl - n, l0);
+      const int nb = __shfl(n, l0);
+      *u = nb - 1 - (k - before);
+      return base - l0;
+    }
+    k -= total;
   }
-  return lo;
+  return -1;
 }
 
-// One workgroup per chunk row: write its K and V for every KV head.
+// s_waitcnt encodings (gfx9 layout): wait until at most N vector memory
+// operations are outstanding / until all LDS operations are done, then the
+// workgroup barrier. The compiler does not track the LDS writes of direct
+// loads, so these waits are explicit.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkm0_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+// one 16-byte direct load: lane l of the wave writes at lds + 16 l
+__device__ __forceinline__ void lds_load16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+
+// Append. Workgroup = (one block that request b's chunk writes, KV head g),
+// mapped from a 1D grid (heads fastest); the block's slots [lo, hi) are new
+// (positions P_b .. L_b - 1). Thread t handles slot t / (D/8), dims
+// 8 (t % (D/8)) .. +8.
 template <int D>
 __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
-  const int64_t t = blockIdx.x;
-  int b = find_request(a.q_indptr, a.B, t);
-  while (b + 1 < a.B && a.q_indptr[b + 1] <= t) ++b;  // skip empty requests
-  const int n_b = a.q_indptr[b + 1] - a.q_indptr[b];
-  const int pos = a.ctx_lens[b] - n_b + static_cast<int>(t - a.q_indptr[b]);
-  // positions without a block, or blocks with an id outside the pool, are
-  // not written
-  if (pos < 0 || pos / kBlockSize >= a.max_blocks) return;
-  const int p = a.block_table[static_cast<int64_t>(b) * a.max_blocks + pos / kBlockSize];
-  if (!id_ok(p, a.num_blocks)) return;
-  const int slot = pos % kBlockSize;
-  const int n16 = a.Hkv * (D / 8);
-  for (int e = threadIdx.x; e < n16; e += blockDim.x) {
-    const int g = e / (D / 8), c = e % (D / 8);
-    const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
-    const u32x4 kv = ld_global<u32x4>(a.k_new + (t * a.Hkv + g) * D + 8 * c);
-    *reinterpret_cast<u32x4*>(a.k_cache + tile + c * (kBlockSize * 8) + slot * 8) = kv;
+  constexpr int C8 = D / 8;
+  __shared__ uint16_t vt[D][kBlockSize + 2];  // V of the block, dim-major (+2: banks)
+  const int g = blockIdx.x % a.Hkv;
+  int jb = 0;
+  // blocks request b's chunk writes: from its first new position's block to
+  // its last one's (none for an empty chunk or a chunk past the context)
+  auto chunk_blocks = [&](int bb) {
+    const int n = a.q_indptr[bb + 1] - a.q_indptr[bb];
+    const int L = a.ctx_lens[bb];
+    if (n <= 0 || L <= 0) return 0;
+    const int P = max(L - n, 0);
+    return (L - 1) / kBlockSize - P / kBlockSize + 1;
+  };
+  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hkv), chunk_blocks, &jb);
+  if (b < 0) return;
+  const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
+  const int n_b = r1 - r0;
+  const int L = a.ctx_lens[b], P = L - n_b;
+  const int j = (P >= 0 ? P : 0) / kBlockSize + jb;  // the block
+  const int lo = max(P, j * kBlockSize), hi = min(L, (j + 1) * kBlockSize);
+  if (lo >= hi || j >= a.max_blocks) return;
+  const int p = a.block_table[static_cast<int64_t>(b) * a.max_blocks + j];
+  if (!id_ok(p, a.num_blocks)) return;  // blocks outside the pool are not written
+  const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
+  for (int e = threadIdx.x; e < kBlockSize * C8; e += blockDim.x) {
+    const int slot = e / C8, c = e % C8;
+    const int pos = j * kBlockSize + slot;
+    u32x4 vv = {0u, 0u, 0u, 0u};
+    if (pos >= lo && pos < hi) {
+      const int64_t row = r0 + (pos - P);
+      const u32x4 kv = ld_global<u32x4>(a.k_new + (row * a.Hkv + g) * D + 8 * c);
+      vv = ld_global<u32x4>(a.v_new + (row * a.Hkv + g) * D + 8 * c);
+      *reinterpret_cast<u32x4*>(a.k_cache + tile + c * (kBlockSize * 8) + slot * 8) = kv;
+    }
+    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      vt[8 * c + 2 * q][slot] = static_cast<uint16_t>(w[q] & 0xffffu);
+      vt[8 * c + 2 * q + 1][slot] = static_cast<uint16_t>(w[q] >> 16);
+    }
   }
-  for (int e = threadIdx.x; e < a.Hkv * D; e += blockDim.x) {
-    const int g = e / D, d = e % D;
-    const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
-    a.v_cache[tile + d * kBlockSize + slot] = a.v_new[(t * a.Hkv + g) * D + d];
+  __syncthreads();
+  const bool whole = lo == j * kBlockSize && hi == (j + 1) * kBlockSize;
+  if (whole) {  // dim rows of 16 slots as two 16-byte pieces
+    for (int e = threadIdx.x; e < 2 * D; e += blockDim.x) {
+      const int d = e / 2, h = e % 2;
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        w[q] = static_cast<uint32_t>(vt[d][8 * h + 2 * q]) |
+               (static_cast<uint32_t>(vt[d][8 * h + 2 * q + 1]) << 16);
+      *reinterpret_cast<u32x4*>(a.v_cache + tile + d * kBlockSize + 8 * h) =
+          u32x4{w[0], w[1], w[2], w[3]};
+    }
+  } else {  // the chunk's first or last block: only its new slots
+    for (int e = threadIdx.x; e < kBlockSize * D; e += blockDim.x) {
+      const int d = e / kBlockSize, slot = e % kBlockSize;
+      const int pos = j * kBlockSize + slot;
+      if (pos >= lo && pos < hi) a.v_cache[tile + d * kBlockSize + slot] = vt[d][slot];
+    }
   }
 }
 
-template <int D, int QT>
-__global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a) {
-  constexpr int KC = D / 32, VT = D / 16;
-  constexpr int TILE = kBlockSize * D;          // elements per (block, head) tile
-  constexpr int ROWS_PER_WG = kPfWaves * 16 * QT;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kPfKB * TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kPfKB * TILE];
-  __shared__ int list[kPfWindow];
-  __shared__ int wave_cnt[kPfWaves];
+template <int D>
+__global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs a) {
+  constexpr int QT = kPaQT, KC = D / 32, VT = D / 16;
+  constexpr int TILE = kBlockSize * D;     // elements of a (block, head) tile
+  constexpr int TILE_B = 2 * TILE;         // its bytes
+  constexpr int DMA = TILE_B / 1024;       // 1 KB direct loads per tile
+  constexpr int STAGE_B = 4 * TILE_B;      // K and V tiles of two blocks
+  extern __shared__ __attribute__((aligned(16))) uint8_t ring[];  // [kPaStages][STAGE_B]
+  __shared__ int list[kPaWindow];    // logical blocks j, ascending
+  __shared__ int list_p[kPaWindow];  // their physical ids
+  __shared__ int wave_cnt[kPaWaves];
 
-  const int qtile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  // (query tile, head h, request b) from a 1D grid, heads fastest: the last
+  // requests' last tiles (a chunk's later rows see more keys, and requests
+  // are commonly listed by growing prefix) are dispatched first, so that the
+  // longest workgroups do not start behind short ones
+  const int h = blockIdx.x % a.Hq;
+  int qtile = 0;
+  auto row_tiles = [&](int bb) {
+    const int n = a.q_indptr[bb + 1] - a.q_indptr[bb];
+    return n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
+  };
+  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hq), row_tiles, &qtile);
+  if (b < 0) return;
   const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
   if (r0 < 0 || r1 > a.T || r1 < r0) return;  // not a row range of q
   const int n_b = r1 - r0;
-  const int row0 = qtile * ROWS_PER_WG;
+  const int row0 = qtile * kPaRows;
   if (row0 >= n_b) return;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
   const int L = a.ctx_lens[b];
   const int P = L - n_b;  // cached prefix
@@ -111,25 +219,32 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
 
-  // Query columns of this wave: rows row0 + wave*16*QT + 16*ct + col.
+  // Query columns of this wave: rows row0 + 32 wave + 16 ct + col.
   bf16x8 qv[QT][KC];
   int qpos[QT];
+  u32x4 qraw[QT][KC];
 #pragma unroll
   for (int ct = 0; ct < QT; ++ct) {
     const int row = row0 + wave * 16 * QT + 16 * ct + col;
     qpos[ct] = P + row;
+    const int rc = row < n_b ? row : 0;  // rows past the chunk load row 0, never stored
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+      qraw[ct][c] =
+          ld_global<u32x4>(a.q + (static_cast<int64_t>(r0 + rc) * a.Hq + h) * D + 32 * c + 8 * kgrp);
+  }
+  // the query is waited for here, before any direct load is issued (a wait
+  // for it after them would wait for them too)
+#pragma unroll
+  for (int ct = 0; ct < QT; ++ct)
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (row < n_b)
-        v = ld_global<u32x4>(a.q + (static_cast<int64_t>(r0 + row) * a.Hq + h) * D + 32 * c +
-                             8 * kgrp);
-      qv[ct][c] = as_bf16x8(v);
+      asm volatile("" : "+v"(qraw[ct][c]));
+      qv[ct][c] = as_bf16x8(qraw[ct][c]);
     }
-  }
   const int wave_last_row = min(row0 + (wave + 1) * 16 * QT, n_b) - 1;
   const int wave_limit = P + wave_last_row;  // largest key position this wave sees
-  const int wg_limit = P + min(row0 + ROWS_PER_WG, n_b) - 1;
+  const int wg_limit = P + min(row0 + kPaRows, n_b) - 1;
   const int nb_lim = wg_limit < 0 ? 0 : min(wg_limit / kBlockSize + 1, a.max_blocks);
 
   f32x4 acc[QT][VT];
@@ -142,12 +257,17 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
     for (int t = 0; t < VT; ++t) acc[ct][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int w0 = 0; w0 < nb_lim; w0 += kPfWindow) {
-    // ---- compact the non-stale blocks of this window (in ascending j)
-    const int j = w0 + threadIdx.x;
+  // wave w moves tile w of a step: block w / 2 of the step, K (w even) or V
+  const int my_blk = wave / 2, my_kind = wave % 2;
+  const uint16_t* pool = my_kind ? a.v_cache : a.k_cache;
+
+  for (int w0 = 0; w0 < nb_lim; w0 += kPaWindow) {
+    // ---- list the non-stale blocks of this window, in ascending j
+    const int j = w0 + tid;
     bool ok = false;
+    int p = 0;
     if (j < nb_lim) {
-      const int p = table[j];
+      p = table[j];
       ok = id_ok(p, a.num_blocks) && a.block_version[p] == rv;
     }
     const uint64_t mask = __ballot(ok);
@@ -155,108 +275,119 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
     if (lane == 0) wave_cnt[wave] = __popcll(mask);
     __syncthreads();
     int off = 0, cnt = 0;
-    for (int w = 0; w < kPfWaves; ++w) {
+    for (int w = 0; w < kPaWaves; ++w) {
       if (w < wave) off += wave_cnt[w];
       cnt += wave_cnt[w];
     }
-    if (ok) list[off + before] = j;
-    __syncthreads();
-
-    for (int t0 = 0; t0 < cnt; t0 += kPfKB) {
-      // ---- stage KB blocks (K and V tiles) into LDS
-      for (int e = threadIdx.x; e < kPfKB * TILE / 8; e += kPfThreads) {
-        const int kb = e / (TILE / 8), piece = e % (TILE / 8);
-        u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-        if (t0 + kb < cnt) {
-          const int jj = list[t0 + kb];
-          const int64_t tile = (static_cast<int64_t>(table[jj]) * a.Hkv + g) * TILE;
-          kv = ld_global<u32x4>(a.k_cache + tile + 8 * piece);
-          vv = ld_global<u32x4>(a.v_cache + tile + 8 * piece);
-          // V piece = 8 slots of one dim: clear slots past the context end
-          const int slot0 = (8 * piece) % kBlockSize;
-          const int live = L - jj * kBlockSize - slot0;  // live slots in this piece
-          if (live < 8) {
-            uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-            for (int e2 = 0; e2 < 8; ++e2)
-              if (e2 >= live) w[e2 / 2] &= (e2 & 1) ? 0x0000ffffu : 0xffff0000u;
-            vv = u32x4{w[0], w[1], w[2], w[3]};
-          }
-        }
-        *reinterpret_cast<u32x4*>(k_lds + kb * TILE + 8 * piece) = kv;
-        *reinterpret_cast<u32x4*>(v_lds + kb * TILE + 8 * piece) = vv;
-      }
-      __syncthreads();
-
-      const int first_pos = list[t0] * kBlockSize;
-      if (first_pos <= wave_limit) {
-#pragma unroll
-        for (int pr = 0; pr < kPfKB / 2; ++pr) {
-          const int kbA = 2 * pr, kbB = 2 * pr + 1;
-          const bool hasA = t0 + kbA < cnt, hasB = t0 + kbB < cnt;
-          if (!hasA) break;
-          const int jA = list[t0 + kbA];
-          const int jB = hasB ? list[t0 + kbB] : jA;
-          const uint16_t* kA = k_lds + kbA * TILE;
-          const uint16_t* kB = k_lds + kbB * TILE;
-          bf16x8 kfa[KC], kfb[KC];
-#pragma unroll
-          for (int c = 0; c < KC; ++c) {
-            kfa[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kA + c * 512 + lane * 8));
-            kfb[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kB + c * 512 + lane * 8));
-          }
-          bf16x8 vf[VT];
-#pragma unroll
-          for (int t = 0; t < VT; ++t) {
-            const u32x2 va = *reinterpret_cast<const u32x2*>(v_lds + kbA * TILE +
-                                                             (16 * t + col) * kBlockSize + 4 * kgrp);
-            const u32x2 vb = *reinterpret_cast<const u32x2*>(v_lds + kbB * TILE +
-                                                             (16 * t + col) * kBlockSize + 4 * kgrp);
-            vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
-          }
-#pragma unroll
-          for (int ct = 0; ct < QT; ++ct) {
-            f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int c = 0; c < KC; ++c) {
-              sA = mfma16x16x32(kfa[c], qv[ct][c], sA);
-              sB = mfma16x16x32(kfb[c], qv[ct][c], sB);
-            }
-            float s[8];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int posA = jA * kBlockSize + 4 * kgrp + i;
-              const int posB = jB * kBlockSize + 4 * kgrp + i;
-              s[i] = posA <= qpos[ct] ? sA[i] * a.scale_log2 : -INFINITY;
-              s[4 + i] = (hasB && posB <= qpos[ct]) ? sB[i] * a.scale_log2 : -INFINITY;
-            }
-            float mx = s[0];
-#pragma unroll
-            for (int i = 1; i < 8; ++i) mx = fmaxf(mx, s[i]);
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[ct], mx);
-            const float alpha = fast_exp2(m_run[ct] - m_new);
-            float psum = 0.f;
-            bf16x8 pb;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              const float p = fast_exp2(s[i] - m_new);
-              psum += p;
-              pb[i] = static_cast<__bf16>(p);
-            }
-            l_run[ct] = l_run[ct] * alpha + psum;
-            m_run[ct] = m_new;
-#pragma unroll
-            for (int t = 0; t < VT; ++t) {
-              acc[ct][t] *= alpha;
-              acc[ct][t] = mfma16x16x32(vf[t], pb, acc[ct][t]);
-            }
-          }
-        }
-      }
-      __syncthreads();
+    if (ok) {
+      list[off + before] = j;
+      list_p[off + before] = p;
     }
+    __syncthreads();
+    if (cnt == 0) continue;
+    const int steps = (cnt + 1) / 2;
+
+    // loads of step s into ring stage `stage`: this wave's tile. Physical
+    // ids come from LDS (a load of the block table here would make the wave
+    // wait for every load before it). A step's second block past the list
+    // end repeats its first (never used), and steps past the last repeat the
+    // last into the free stage, so every step issues the same loads and the
+    // wait counts hold.
+    auto issue = [&](int stage, int s) {
+      const int p = list_p[min(2 * s + my_blk, cnt - 1)];
+      const uint8_t* src = reinterpret_cast<const uint8_t*>(
+          pool + (static_cast<int64_t>(p) * a.Hkv + g) * TILE);
+      uint8_t* dst = ring + stage * STAGE_B + wave * TILE_B;
+#pragma unroll
+      for (int q = 0; q < DMA; ++q) lds_load16(src + 1024 * q + 16 * lane, dst + 1024 * q);
+    };
+#pragma unroll
+    for (int s = 0; s < kPaStages - 1; ++s) issue(s, min(s, steps - 1));
+
+    for (int s = 0; s < steps; ++s) {
+      // this wave's loads of step s are done (those of the two later steps
+      // may still fly); after the barrier everyone's are, and the stage of
+      // step s - 1 is free for step s + 3
+      wait_vmcnt<DMA * (kPaStages - 2)>();
+      wait_lgkm0_barrier();
+      issue((s + kPaStages - 1) % kPaStages, min(s + kPaStages - 1, steps - 1));
+      const int jA = list[2 * s];
+      const bool hasB = 2 * s + 1 < cnt;
+      const int jB = hasB ? list[2 * s + 1] : jA;
+      if (jA * kBlockSize > wave_limit) continue;  // wholly past this wave's rows
+      const uint8_t* st = ring + (s % kPaStages) * STAGE_B;
+      const uint16_t* kA = reinterpret_cast<const uint16_t*>(st);
+      const uint16_t* vA = reinterpret_cast<const uint16_t*>(st + TILE_B);
+      const uint16_t* kB = reinterpret_cast<const uint16_t*>(st + 2 * TILE_B);
+      const uint16_t* vB = reinterpret_cast<const uint16_t*>(st + 3 * TILE_B);
+      bf16x8 kfa[KC], kfb[KC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        kfa[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kA + c * 512 + lane * 8));
+        kfb[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kB + c * 512 + lane * 8));
+      }
+      // V fragments: slots 4 kgrp .. +4 of each block; slots at or past the
+      // context end are zeroed (they may hold anything)
+      const int liveA = L - jA * kBlockSize - 4 * kgrp;
+      const int liveB = hasB ? L - jB * kBlockSize - 4 * kgrp : 0;
+      bf16x8 vf[VT];
+#pragma unroll
+      for (int t = 0; t < VT; ++t) {
+        u32x2 va = *reinterpret_cast<const u32x2*>(vA + (16 * t + col) * kBlockSize + 4 * kgrp);
+        u32x2 vb = *reinterpret_cast<const u32x2*>(vB + (16 * t + col) * kBlockSize + 4 * kgrp);
+        if (liveA < 4) {
+          va.x = liveA <= 0 ? 0u : (liveA == 1 ? va.x & 0xffffu : va.x);
+          va.y = liveA <= 2 ? 0u : va.y & 0xffffu;
+        }
+        if (liveB < 4) {
+          vb.x = liveB <= 0 ? 0u : (liveB == 1 ? vb.x & 0xffffu : vb.x);
+          vb.y = liveB <= 2 ? 0u : vb.y & 0xffffu;
+        }
+        vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
+      }
+#pragma unroll
+      for (int ct = 0; ct < QT; ++ct) {
+        f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+          sA = mfma16x16x32(kfa[c], qv[ct][c], sA);
+          sB = mfma16x16x32(kfb[c], qv[ct][c], sB);
+        }
+        float sc[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int posA = jA * kBlockSize + 4 * kgrp + i;
+          const int posB = jB * kBlockSize + 4 * kgrp + i;
+          sc[i] = posA <= qpos[ct] ? sA[i] * a.scale_log2 : -INFINITY;
+          sc[4 + i] = (hasB && posB <= qpos[ct]) ? sB[i] * a.scale_log2 : -INFINITY;
+        }
+        float mx = sc[0];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[i]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run[ct], mx);
+        const float alpha = fast_exp2(m_run[ct] - m_new);
+        float psum = 0.f;
+        bf16x8 pb;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float pr = fast_exp2(sc[i] - m_new);
+          psum += pr;
+          pb[i] = static_cast<__bf16>(pr);
+        }
+        l_run[ct] = l_run[ct] * alpha + psum;
+        m_run[ct] = m_new;
+#pragma unroll
+        for (int t = 0; t < VT; ++t) {
+          acc[ct][t] *= alpha;
+          acc[ct][t] = mfma16x16x32(vf[t], pb, acc[ct][t]);
+        }
+      }
+    }
+    // every load has landed before the ring or the list is reused
+    wait_vmcnt<0>();
+    wait_lgkm0_barrier();
   }
 
   // ---- normalise and write this wave's rows
@@ -283,16 +414,24 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(PrefillArgs a)
 }
 
 template <int D>
-local_status_t launch_prefill(const PrefillArgs& a, int64_t T, int max_rows, hipStream_t s) {
-  constexpr int QT = 1;
+local_status_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   if (a.k_new) {
-    prefill_append_kernel<D><<<static_cast<unsigned>(T), 256, 0, s>>>(a);
+    // a chunk of n rows spans at most n / 16 + 2 blocks: T / 16 + 2 B in all
+    const int64_t units = a.T / kBlockSize + 2LL * a.B;
+    prefill_append_kernel<D><<<static_cast<unsigned>(units * a.Hkv), 256, 0, s>>>(a);
     local_status_t st = local_check_launch("paged_attn_prefill (append)");
     if (st != LOCAL_OK) return st;
   }
-  const int rows_per_wg = kPfWaves * 16 * QT;
-  dim3 grid((max_rows + rows_per_wg - 1) / rows_per_wg, a.Hq, a.B);
-  prefill_attn_kernel<D, QT><<<grid, kPfThreads, 0, s>>>(a);
+  constexpr int kLds = kPaStages * 4 * 2 * kBlockSize * D;
+  static bool done = false;
+  if (!done) {  // benign race: every caller sets the same value
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_attn_kernel<D>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+    done = true;
+  }
+  // a chunk of n rows has at most n / 128 + 1 tiles: T / 128 + B in all
+  const int64_t tiles = a.T / kPaRows + a.B;
+  prefill_attn_kernel<D><<<static_cast<unsigned>(tiles * a.Hq), kPaThreads, kLds, s>>>(a);
   return local_check_launch("paged_attn_prefill");
 }
 
@@ -352,8 +491,8 @@ extern "C" local_status_t local_paged_attn_prefill(
   a.group = Hq / Hkv;
   a.max_blocks = max_blocks;
   a.scale_log2 = sm_scale * kLog2e;
-  // A request's chunk is at most T rows and at most its table's width.
-  const int max_rows = static_cast<int>(T < 16LL * max_blocks ? T : 16LL * max_blocks);
+  if ((T / kBlockSize + 2LL * B) * Hq >= (1LL << 31))
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "paged_attn_prefill: T=%lld too large", (long long)T);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return D == 64 ? launch_prefill<64>(a, T, max_rows, s) : launch_prefill<128>(a, T, max_rows, s);
+  return D == 64 ? launch_prefill<64>(a, s) : launch_prefill<128>(a, s);
 }

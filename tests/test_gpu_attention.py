@@ -189,6 +189,35 @@ def test_prefill_matches_oracle(Hq, Hkv, D):
     assert_lse(lse.cpu().numpy(), rl, "lse")
 
 
+@pytest.mark.parametrize("B", [65, 130])
+def test_prefill_many_requests(B):
+    # more requests than a wavefront scans at once: the device-side mapping of
+    # the grid onto (request, tile) and (request, block) takes several passes;
+    # empty chunks, chunks starting and ending inside a block, long chunks
+    say("prefill many requests", B)
+    rng = np.random.default_rng(B)
+    Hq, Hkv, D = 8, 2, 64
+    prefix = rng.integers(0, 300, size=B)
+    chunk = rng.integers(0, 150, size=B)
+    chunk[::7] = 0
+    chunk[3] = 300
+    c = _prefill_case(rng, prefix, chunk, Hq, Hkv, D, 0.1)
+    kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    out, lse = lk.local_paged_attn_prefill(
+        dev_u16(c["q"]), dev(c["qi"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]),
+        dev(c["bv"]), dev(c["rv"]), 1.0 / math.sqrt(D), k_new=dev_u16(c["kn"]),
+        v_new=dev_u16(c["vn"]), Hkv=Hkv)
+    torch.cuda.synchronize()
+    kc, vc = c["kc"].copy(), c["vc"].copy()
+    oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
+    ro, rl = oracle.paged_attn(c["q"], c["qi"], Hq, Hkv, D, kc, vc, c["table"], c["ctx"],
+                               c["bv"], c["rv"], 1.0 / math.sqrt(D))
+    assert np.array_equal(host_u16(kc_d), kc), "appended K pool differs"
+    assert np.array_equal(host_u16(vc_d), vc), "appended V pool differs"
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
+
+
 def test_prefill_one_token_chunk_equals_decode():
     rng = np.random.default_rng(21)
     Hq, Hkv, D = 8, 2, 128
