@@ -244,6 +244,7 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     }
   const int wave_last_row = min(row0 + (wave + 1) * 16 * QT, n_b) - 1;
   const int wave_limit = P + wave_last_row;  // largest key position this wave sees
+  const int wave_first = P + row0 + wave * 16 * QT;  // position of its first row
   const int wg_limit = P + min(row0 + kPaRows, n_b) - 1;
   const int nb_lim = wg_limit < 0 ? 0 : min(wg_limit / kBlockSize + 1, a.max_blocks);
 
@@ -315,6 +316,9 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       const bool hasB = 2 * s + 1 < cnt;
       const int jB = hasB ? list[2 * s + 1] : jA;
       if (jA * kBlockSize > wave_limit) continue;  // wholly past this wave's rows
+      // every key of the step precedes every row of the wave (so it is also
+      // before the context end): no masking
+      const bool unmasked = hasB && jB * kBlockSize + kBlockSize - 1 <= wave_first;
       const uint8_t* st = ring + (s % kPaStages) * STAGE_B;
       const uint16_t* kA = reinterpret_cast<const uint16_t*>(st);
       const uint16_t* vA = reinterpret_cast<const uint16_t*>(st + TILE_B);
@@ -345,45 +349,78 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         }
         vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
       }
+      // S^T of both column tiles: 2 * QT independent chains of KC MFMAs,
+      // interleaved so that no MFMA waits on the one before it
+      f32x4 sA[QT], sB[QT];
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
-        f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
+        sA[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+        sB[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
-        for (int c = 0; c < KC; ++c) {
-          sA = mfma16x16x32(kfa[c], qv[ct][c], sA);
-          sB = mfma16x16x32(kfb[c], qv[ct][c], sB);
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int ct = 0; ct < QT; ++ct) {
+          sA[ct] = mfma16x16x32(kfa[c], qv[ct][c], sA[ct]);
+          sB[ct] = mfma16x16x32(kfb[c], qv[ct][c], sB[ct]);
         }
-        float sc[8];
+      // scaled (and, near the diagonal or the context end, masked) scores
+      float sc[QT][8], m_new[QT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int posA = jA * kBlockSize + 4 * kgrp + i;
-          const int posB = jB * kBlockSize + 4 * kgrp + i;
-          sc[i] = posA <= qpos[ct] ? sA[i] * a.scale_log2 : -INFINITY;
-          sc[4 + i] = (hasB && posB <= qpos[ct]) ? sB[i] * a.scale_log2 : -INFINITY;
+      for (int ct = 0; ct < QT; ++ct) {
+        if (unmasked) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            sc[ct][i] = sA[ct][i] * a.scale_log2;
+            sc[ct][4 + i] = sB[ct][i] * a.scale_log2;
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int posA = jA * kBlockSize + 4 * kgrp + i;
+            const int posB = jB * kBlockSize + 4 * kgrp + i;
+            sc[ct][i] = posA <= qpos[ct] ? sA[ct][i] * a.scale_log2 : -INFINITY;
+            sc[ct][4 + i] = (hasB && posB <= qpos[ct]) ? sB[ct][i] * a.scale_log2 : -INFINITY;
+          }
         }
-        float mx = sc[0];
+        float mx = sc[ct][0];
 #pragma unroll
-        for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[i]);
+        for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[ct][i]);
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[ct], mx);
-        const float alpha = fast_exp2(m_run[ct] - m_new);
-        float psum = 0.f;
-        bf16x8 pb;
+        m_new[ct] = fmaxf(m_run[ct], mx);
+      }
+      // the running sums are rescaled only when some column's maximum grew
+      // (elsewhere the factor is exactly 1)
+      bool grew = false;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float pr = fast_exp2(sc[i] - m_new);
-          psum += pr;
-          pb[i] = static_cast<__bf16>(pr);
-        }
-        l_run[ct] = l_run[ct] * alpha + psum;
-        m_run[ct] = m_new;
+      for (int ct = 0; ct < QT; ++ct) grew = grew || m_new[ct] > m_run[ct];
+      if (__ballot(grew) != 0ull) {
 #pragma unroll
-        for (int t = 0; t < VT; ++t) {
-          acc[ct][t] *= alpha;
-          acc[ct][t] = mfma16x16x32(vf[t], pb, acc[ct][t]);
+        for (int ct = 0; ct < QT; ++ct) {
+          const float alpha = fast_exp2(m_run[ct] - m_new[ct]);
+          l_run[ct] *= alpha;
+#pragma unroll
+          for (int t = 0; t < VT; ++t) acc[ct][t] *= alpha;
+          m_run[ct] = m_new[ct];
         }
       }
+      bf16x8 pb[QT];
+#pragma unroll
+      for (int ct = 0; ct < QT; ++ct) {
+        float psum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float pr = fast_exp2(sc[ct][i] - m_run[ct]);
+          psum += pr;
+          pb[ct][i] = static_cast<__bf16>(pr);
+        }
+        l_run[ct] += psum;
+      }
+#pragma unroll
+      for (int t = 0; t < VT; ++t)
+#pragma unroll
+        for (int ct = 0; ct < QT; ++ct) acc[ct][t] = mfma16x16x32(vf[t], pb[ct], acc[ct][t]);
     }
     // every load has landed before the ring or the list is reused
     wait_vmcnt<0>();
