@@ -67,6 +67,75 @@ __device__ __forceinline__ int owned_blocks(int L, int max_blocks) {
   return L <= 0 ? 0 : min((L + kBlockSize - 1) / kBlockSize, max_blocks);
 }
 
+// Position of the k-th (0-based) set bit of m (k < popcount(m)).
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int k) {
+  for (int i = 0; i < k; ++i) m &= m - 1ull;
+  return __ffsll(static_cast<long long>(m)) - 1;
+}
+
+// Requests a wavefront ranks at once: 64 per register, up to this many
+// registers (larger batches use the grid order below without ranking).
+constexpr int kRankChunks = 8;
+
+// The unit of work of dispatch slot k, longest first: every full partition,
+// row by row (partition z of each request that has it, ascending b), then
+// each request's partial partition, longest first (ties: smaller b); an
+// empty context is a partial partition of no block. Returns the request (-1
+// past the last unit) and, in *part, its partition index (a partial one is
+// numbered n_full, as in the merge). Every lane returns the same.
+__device__ int decode_unit(const DecodeArgs& a, int B, int k, int* part) {
+  const int lane = threadIdx.x % kWave;
+  const int nc = (B + kWave - 1) / kWave;
+  int nf[kRankChunks], rem[kRankChunks];
+  bool has_partial[kRankChunks];
+#pragma unroll
+  for (int c = 0; c < kRankChunks; ++c) {
+    const int b = c * kWave + lane;
+    const int nb = b < B ? owned_blocks(a.ctx_lens[b], a.max_blocks) : -1;
+    nf[c] = nb > 0 ? nb / kBlocksPerPart : 0;
+    rem[c] = nb > 0 ? nb % kBlocksPerPart : 0;
+    has_partial[c] = nb == 0 || rem[c] > 0;  // nb = -1: no request
+  }
+  for (int z = 0; z < a.n_parts; ++z) {
+    int cnt = 0;
+#pragma unroll
+    for (int c = 0; c < kRankChunks; ++c) {
+      if (c >= nc) break;
+      cnt += __popcll(__ballot(nf[c] > z));
+    }
+    if (cnt == 0) break;
+    if (k < cnt) {
+#pragma unroll
+      for (int c = 0; c < kRankChunks; ++c) {
+        if (c >= nc) break;
+        const uint64_t m = __ballot(nf[c] > z);
+        const int n = __popcll(m);
+        if (k < n) {
+          *part = z;
+          return c * kWave + nth_set_bit(m, k);
+        }
+        k -= n;
+      }
+    }
+    k -= cnt;
+  }
+  for (int v = kBlocksPerPart - 1; v >= 0; --v) {
+#pragma unroll
+    for (int c = 0; c < kRankChunks; ++c) {
+      if (c >= nc) break;
+      const uint64_t m = __ballot(has_partial[c] && rem[c] == v);
+      const int n = __popcll(m);
+      if (k < n) {
+        const int l = nth_set_bit(m, k);
+        *part = __shfl(nf[c], l);
+        return c * kWave + l;
+      }
+      k -= n;
+    }
+  }
+  return -1;
+}
+
 // The 4 V values a lane holds for one block (slots slot0..slot0+3), with
 // slots past s_live set to 0 (their cache contents are undefined and must not
 // reach the product) and slot s_new replaced by vnew. For a block that is
@@ -106,30 +175,42 @@ struct BlockRegs {
   u32x2 v[D / 16];
 };
 
-template <int D, int DEPTH>
-__global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a) {
+template <int D, int DEPTH, bool RANKED>
+__global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B) {
   constexpr int KC = D / 32;  // 32-dim chunks of the QK product
   constexpr int VT = D / 16;  // 16-dim tiles of the PV product
 
-  const int g = blockIdx.x, b = blockIdx.y;
   const int lane = threadIdx.x;
   const int col = lane % 16, kgrp = lane / 16;
+  // Partition p covers blocks [nb - 32(p+1), nb - 32p) of b: the full ones
+  // counted from the end of the context, then at most one partial one at the
+  // start. An empty context runs partition 0 with no block (zero output,
+  // lse = -inf). The grid is 1D, KV heads fastest, sized for n_parts + 1
+  // partitions of every request; the slots map to units longest first (full
+  // partitions, then the partial ones by decreasing length), so the last
+  // waves to start are the shortest and the idle slots come last. Batches
+  // wider than the ranking takes dispatch each partition row in request
+  // order instead, the partial partitions last.
+  const int g = blockIdx.x % a.Hkv;
+  const int slot = blockIdx.x / a.Hkv;
+  int b, part;
+  if (RANKED) {
+    b = decode_unit(a, B, slot, &part);
+    if (b < 0) return;
+  } else {
+    b = slot % B;
+    part = slot / B;
+  }
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  // Partition p covers blocks [nb - 32(p+1), nb - 32p) of b: the full ones
-  // first, counted from the end of the context, then at most one partial one
-  // at the start. blockIdx.z < n_parts takes full partition z, blockIdx.z =
-  // n_parts the partial one, so every full partition is dispatched before any
-  // partial one and the last waves to start are short. An empty context runs
-  // partition 0 with no block (zero output, lse = -inf).
   const int n_full = nb / kBlocksPerPart, rem = nb % kBlocksPerPart;
-  int part;
-  if (blockIdx.z < static_cast<unsigned>(a.n_parts)) {
-    part = blockIdx.z;
-    if (part >= n_full && !(nb == 0 && part == 0)) return;
-  } else {
-    if (rem == 0) return;
-    part = n_full;
+  if (!RANKED) {
+    if (part < a.n_parts) {
+      if (part >= n_full && !(nb == 0 && part == 0)) return;
+    } else {
+      if (rem == 0) return;
+      part = n_full;
+    }
   }
   const int j_end_part = nb - part * kBlocksPerPart;
   const int j0 = max(0, j_end_part - kBlocksPerPart);
@@ -354,8 +435,16 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
 
 template <int D>
 local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
-  dim3 grid(a.Hkv, B, a.n_parts + 1);  // full partitions, then the partial ones
-  decode_attn_kernel<D, LOCAL_DECODE_DEPTH><<<grid, kWave, 0, s>>>(a);
+  const int64_t wgs = static_cast<int64_t>(a.Hkv) * B * (a.n_parts + 1);
+  if (wgs >= (1LL << 31))
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "paged_attn_decode: grid of %lld workgroups",
+                      (long long)wgs);
+  if (B <= kRankChunks * kWave)
+    decode_attn_kernel<D, LOCAL_DECODE_DEPTH, true><<<static_cast<unsigned>(wgs), kWave, 0, s>>>(
+        a, B);
+  else
+    decode_attn_kernel<D, LOCAL_DECODE_DEPTH, false><<<static_cast<unsigned>(wgs), kWave, 0, s>>>(
+        a, B);
   if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
   return local_check_launch("paged_attn_decode");
 }
