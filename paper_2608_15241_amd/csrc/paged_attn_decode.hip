@@ -96,6 +96,13 @@ __device__ int decode_unit(const DecodeArgs& a, int B, int k, int* part) {
     rem[c] = nb > 0 ? nb % kBlocksPerPart : 0;
     has_partial[c] = nb == 0 || rem[c] > 0;  // nb = -1: no request
   }
+  // slots past the last unit leave before any ranking
+  int units = 0;
+#pragma unroll
+  for (int c = 0; c < kRankChunks; ++c) units += nf[c] + (has_partial[c] ? 1 : 0);
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) units += __shfl_xor(units, off);
+  if (k >= units) return -1;
   for (int z = 0; z < a.n_parts; ++z) {
     int cnt = 0;
 #pragma unroll
