@@ -160,7 +160,9 @@ local_status_t local_lora_linear(
  *  All projections share x, T, K, adapter_idx, scale, n_adapters and r_max;
  *  sizes as for local_lora_linear, for every N[g]. At decode sizes (T <= 256)
  *  the projections run as one virtual weight of sum N[g] rows, so one pass
- *  of launches serves all of them; above, they run one after another.
+ *  of launches serves all of them. Above, one shrink pass reads x once for
+ *  every projection and one product covers the tiles of all of them when
+ *  every N[g] is a multiple of 256; otherwise they run one after another.
  *  Errors as for local_lora_linear; LOCAL_ERR_UNSUPPORTED for G outside 1..4,
  *  LOCAL_ERR_NULL for a NULL array.
  */
@@ -172,6 +174,74 @@ local_status_t local_lora_linear_grouped(
     const int32_t* const* ranks,
     const int32_t* adapter_idx, const float* scale,
     uint16_t* const* y,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
+ * local_lora_grad — adapter gradients of the mixed-adapter projection, for
+ * the training chunks that update adapters while the frozen base serves
+ * (§2.2: adapters trained on a frozen base model; §4: background training
+ * in bounded chunks). With the forward of local_lora_linear, upstream
+ * gradient dy, a = adapter_idx[t], r = rank(a), j < r:
+ *
+ *   u[t,j] = sum_k x[t,k] A[a,j,k]          g[t,j] = scale[t] sum_n dy[t,n] B[a,n,j]
+ *   dB[a,n,j] = sum_{t : adapter t = a} scale[t] dy[t,n] u[t,j]
+ *   dA[a,j,k] = sum_{t : adapter t = a} g[t,j] x[t,k]
+ *
+ *  and dB[a,n,j] = dA[a,j,k] = 0 for j >= r and for adapters without tokens.
+ *  The base weight is frozen: it has no gradient and is not an argument.
+ *
+ *   x            [T][K]               bf16, the forward's activations
+ *   dy           [T][N]               bf16, upstream gradient of y
+ *   A, B, ranks, adapter_idx, scale   as for local_lora_linear (n_adapters >= 1;
+ *                                     tokens with an index outside
+ *                                     [0, n_adapters) contribute nothing)
+ *   dA           [n_adapters][r_max][K]  float32 output
+ *   dB           [n_adapters][N][r_max]  float32 output
+ *
+ *  Sizes: T >= 0 (T = 0 writes zero gradients), K and N positive multiples
+ *  of 64, 1 <= n_adapters <= 256, r_max a multiple of 8 in [8, 128].
+ *  u and g are float32 (not rounded); every sum is float32, over the tokens
+ *  of one adapter in token order within chunks of 64, chunks added in
+ *  order: the result does not depend on the launch. Outputs must not alias
+ *  the inputs. Errors as for local_lora_linear.
+ */
+local_status_t local_lora_grad(
+    const uint16_t* x, int64_t T, int64_t K,
+    const uint16_t* dy, int64_t N,
+    const uint16_t* A, const uint16_t* B,
+    int32_t n_adapters, int32_t r_max,
+    const int32_t* ranks,
+    const int32_t* adapter_idx, const float* scale,
+    float* dA, float* dB,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
+ * local_lora_grad_input — input gradient of the mixed-adapter projection
+ * (the same passage as local_lora_grad):
+ *
+ *   dx[t,k] = sum_n dy[t,n] W[n,k] + sum_{j < r} g[t,j] A[a,j,k]
+ *
+ *  with g as above; tokens without an adapter get the base term only.
+ *   dy           [T][N]   bf16
+ *   Wt           [K][N]   bf16, the frozen base weight TRANSPOSED (W^T; a
+ *                         frozen weight is transposed once, at load)
+ *   A, B, ranks, adapter_idx, scale   as for local_lora_grad
+ *   dx           [T][K]   bf16 output; must not alias the inputs
+ *
+ *  This is local_lora_linear applied to dy with weight Wt and the adapters
+ *  transposed (B^T as the down-projection, A^T as the up-projection, built
+ *  in the workspace), so its numerics are those of local_lora_linear: float32
+ *  accumulation, g rounded to bf16 before the product with A, dx rounded
+ *  once. Sizes and errors as for local_lora_grad (T = 0 launches nothing).
+ */
+local_status_t local_lora_grad_input(
+    const uint16_t* dy, int64_t T, int64_t N,
+    const uint16_t* Wt, int64_t K,
+    const uint16_t* A, const uint16_t* B,
+    int32_t n_adapters, int32_t r_max,
+    const int32_t* ranks,
+    const int32_t* adapter_idx, const float* scale,
+    uint16_t* dx,
     void* ws, size_t* ws_bytes, void* stream);
 
 /*

@@ -26,7 +26,7 @@ BLOCK_SIZE = 16
 
 EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
-           "local_block_version_check",
+           "local_block_version_check", "local_lora_grad", "local_lora_grad_input",
            # host-side KV manager (local_kv.h)
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
@@ -78,6 +78,12 @@ def load_library(path: str = LIB_PATH):
     lib.local_block_version_check.restype = ctypes.c_int
     lib.local_block_version_check.argtypes = [P, i32, i32, P, i32, P, i64, P, P, i64, P, P,
                                               P, SZ, P]
+    lib.local_lora_grad.restype = ctypes.c_int
+    lib.local_lora_grad.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P, P, SZ,
+                                    P]
+    lib.local_lora_grad_input.restype = ctypes.c_int
+    lib.local_lora_grad_input.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
+                                          SZ, P]
     _declare_kvm(lib)
     _lib = lib
     return lib
@@ -244,6 +250,86 @@ def prepare_lora_linear(x, W, A=None, B=None, ranks=None, adapter_idx=None, scal
 def local_lora_linear(*args, **kwargs):
     """y = residual + x W^T + scale_t (x A_a^T) B_a^T per token (bf16 in and out)."""
     return prepare_lora_linear(*args, **kwargs)()
+
+
+def _adapter_checks(A, B, ranks, adapter_idx, scale, T, K, N):
+    _req(A, "A", torch.bfloat16, 3)
+    _req(B, "B", torch.bfloat16, 3)
+    n_ad, r_max = A.shape[0], A.shape[1]
+    if A.shape[2] != K or tuple(B.shape) != (n_ad, N, r_max):
+        raise ValueError("A must be [n_ad, r_max, K=%d] and B [n_ad, N=%d, r_max]" % (K, N))
+    _req(adapter_idx, "adapter_idx", torch.int32, 1)
+    _req(scale, "scale", torch.float32, 1)
+    if adapter_idx.shape[0] != T or scale.shape[0] != T:
+        raise ValueError("adapter_idx and scale must have T=%d entries" % T)
+    if ranks is not None:
+        _req(ranks, "ranks", torch.int32, 1)
+        if ranks.shape[0] != n_ad:
+            raise ValueError("ranks must have n_adapters entries")
+    return n_ad, r_max
+
+
+def prepare_lora_grad(x, dy, A, B, ranks, adapter_idx, scale, dA=None, dB=None,
+                      workspace: Optional[Workspace] = None) -> Call:
+    """Prepared adapter gradients of the mixed-adapter projection: returns
+    (dA [n_ad, r_max, K], dB [n_ad, N, r_max]) in float32."""
+    lib = load_library()
+    _req(x, "x", torch.bfloat16, 2)
+    _req(dy, "dy", torch.bfloat16, 2)
+    T, K = x.shape
+    N = dy.shape[1]
+    if dy.shape[0] != T:
+        raise ValueError("dy must be [T=%d, N]" % T)
+    n_ad, r_max = _adapter_checks(A, B, ranks, adapter_idx, scale, T, K, N)
+    if dA is None:
+        dA = torch.empty((n_ad, r_max, K), dtype=torch.float32, device=x.device)
+    if dB is None:
+        dB = torch.empty((n_ad, N, r_max), dtype=torch.float32, device=x.device)
+    _req(dA, "dA", torch.float32, 3)
+    _req(dB, "dB", torch.float32, 3)
+    if tuple(dA.shape) != (n_ad, r_max, K) or tuple(dB.shape) != (n_ad, N, r_max):
+        raise ValueError("dA must be [n_ad, r_max, K] and dB [n_ad, N, r_max]")
+    args = [_ptr(x), T, K, _ptr(dy), N, _ptr(A), _ptr(B), n_ad, r_max, _ptr(ranks),
+            _ptr(adapter_idx), _ptr(scale), _ptr(dA), _ptr(dB)]
+    c = Call(lib.local_lora_grad, args, workspace, x.device,
+             keep=(x, dy, A, B, ranks, adapter_idx, scale, dA, dB))
+    c.outputs = (dA, dB)
+    return c
+
+
+def local_lora_grad(*args, **kwargs):
+    """(dA, dB) of the mixed-adapter projection (see prepare_lora_grad)."""
+    return prepare_lora_grad(*args, **kwargs)()
+
+
+def prepare_lora_grad_input(dy, Wt, A, B, ranks, adapter_idx, scale, out=None,
+                            workspace: Optional[Workspace] = None) -> Call:
+    """Prepared dx = dy W + scale_t (dy B_a) A_a (bf16), with the frozen base
+    weight given transposed, Wt = W^T [K, N]."""
+    lib = load_library()
+    _req(dy, "dy", torch.bfloat16, 2)
+    _req(Wt, "Wt", torch.bfloat16, 2)
+    T, N = dy.shape
+    K = Wt.shape[0]
+    if Wt.shape[1] != N:
+        raise ValueError("Wt must be [K, N=%d], got %s" % (N, tuple(Wt.shape)))
+    n_ad, r_max = _adapter_checks(A, B, ranks, adapter_idx, scale, T, K, N)
+    if out is None:
+        out = torch.empty((T, K), dtype=torch.bfloat16, device=dy.device)
+    _req(out, "out", torch.bfloat16, 2)
+    if tuple(out.shape) != (T, K):
+        raise ValueError("out must be [T, K]")
+    args = [_ptr(dy), T, N, _ptr(Wt), K, _ptr(A), _ptr(B), n_ad, r_max, _ptr(ranks),
+            _ptr(adapter_idx), _ptr(scale), _ptr(out)]
+    c = Call(lib.local_lora_grad_input, args, workspace, dy.device,
+             keep=(dy, Wt, A, B, ranks, adapter_idx, scale, out))
+    c.outputs = out
+    return c
+
+
+def local_lora_grad_input(*args, **kwargs):
+    """dx of the mixed-adapter projection (see prepare_lora_grad_input)."""
+    return prepare_lora_grad_input(*args, **kwargs)()
 
 
 def _ptr_array(ts):

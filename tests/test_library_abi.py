@@ -162,3 +162,46 @@ def test_lora_linear_grouped_workspace_and_errors(lib):
     assert _size(f, FAKE, 32, 4096, 3, ptrs(3), bad, None, None, 0, 0, None, None, None,
                  ptrs(3))[0] == ERR_UNSUPPORTED
     assert b"grouped" in lib.local_last_error()
+
+
+def test_lora_grad_workspace_and_errors(lib):
+    f = lib.local_lora_grad
+    # T=300, K=512, N=640, 4 adapters of rank 16. Parts, each 256-byte aligned:
+    # the bucketed token order (T int32), the adapter offsets (n+1 int32), B
+    # transposed (n x r_max x N bf16), the shrink's partial sums (the larger of
+    # x against A, 8 K slices, and dy against B^T, 10 slices: 10 x T x r_max
+    # fp32, plus 32 bytes of adapter bitmap per 64-token tile), the two
+    # coefficient arrays (T x r_max fp32 each), then the partial products of
+    # at most T/64 + n 64-token units (units x max(K, N) x r_max fp32).
+    a = lambda v: (v + 255) // 256 * 256
+    st, n = _size(f, FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE)
+    assert st == OK
+    assert n == (a(300 * 4) + a(5 * 4) + a(4 * 16 * 640 * 2) + a(10 * 300 * 16 * 4) + a(5 * 32)
+                 + 2 * a(300 * 16 * 4) + a((300 // 64 + 4) * 640 * 16 * 4))
+    st, n0 = _size(f, FAKE, 0, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE)
+    assert st == OK and n0 > 0                     # T = 0 still runs the bucket and reduce passes
+    assert _size(f, FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 12, None, FAKE, FAKE, FAKE,
+                 FAKE)[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 300, 100, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE,
+                 FAKE)[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 0, 16, None, FAKE, FAKE, FAKE,
+                 FAKE)[0] == ERR_SHAPE
+    assert b"lora_grad" in lib.local_last_error()
+    big = ctypes.c_size_t(1 << 40)
+    assert f(None, 300, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE, FAKE,
+             ctypes.byref(big), None) == ERR_NULL
+    assert f(FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, None, FAKE, FAKE,
+             ctypes.byref(big), None) == ERR_NULL
+    small = ctypes.c_size_t(n - 1)
+    assert f(FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE, FAKE,
+             ctypes.byref(small), None) == ERR_WORKSPACE
+    g = lib.local_lora_grad_input
+    # the transposed adapters, then the forward projection's workspace for
+    # x = dy [T, N] against the transposed weight [K, N]
+    st, m = _size(g, FAKE, 300, 640, FAKE, 512, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE)
+    st2, fw = _size(lib.local_lora_linear, FAKE, 300, 640, FAKE, 512, FAKE, FAKE, 4, 16, None,
+                    FAKE, FAKE, None, FAKE)
+    assert st == OK and st2 == OK
+    assert m == a(4 * 16 * 640 * 2) + a(4 * 512 * 16 * 2) + fw
+    assert g(FAKE, 300, 640, FAKE, 512, FAKE, FAKE, 4, 16, None, FAKE, FAKE, None, FAKE,
+             ctypes.byref(big), None) == ERR_NULL
