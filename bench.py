@@ -274,6 +274,8 @@ def main():
         result["prefill_attn"] = bench_prefill_attn(torch, workloads, lk, dev)
         say("stale-coverage prefill")
         result["reprefill"] = bench_reprefill(torch, workloads, lk, dev)
+        say("lora backward")
+        result["lora_grad"] = bench_lora_grad(torch, workloads, lk, dev)
 
     if primary and not args.no_cpu_baseline:
         say("cpu baseline")
@@ -534,6 +536,103 @@ def bench_reprefill(torch, workloads, lk, dev, n_prefix=8, prefix_blocks=64, chu
             "note": "each round is one whole prefill step (version check, q/k/v, appending "
                     "causal attention, o) timed as a HIP graph replay; step_tflops counts the "
                     "projections' flops only"}
+
+
+def lora_grad_bytes(w, T):
+    """Algorithmic HBM bytes of the adapter gradients of the four projections:
+    x and dy read once (bf16), the token routing read once (int32 index and
+    fp32 scale per token and projection), every adapter's A and B read once
+    (bf16) and dA, dB written once (fp32)."""
+    total = 0
+    for proj in ("q", "k", "v", "o"):
+        N, K = w.proj_shape(proj)
+        total += 2 * T * (K + N) + 8 * T + w.n_adapters * w.r_max * (K + N) * (2 + 4)
+    return total
+
+
+def lora_grad_input_flops(w, T):
+    """2 T N K per projection for dy W, plus 2 T r (N + K) for the adapter term."""
+    total = 0
+    for proj in ("q", "k", "v", "o"):
+        N, K = w.proj_shape(proj)
+        total += 2 * T * N * K + 2 * T * w.r_max * (N + K)
+    return total
+
+
+def bench_lora_grad(torch, workloads, lk, dev, reps=20):
+    """The LoRA backward of one training chunk at the prefill workload's shapes
+    (2048 tokens over 4 rank-16 adapters, q/k/v/o of a 4096-wide layer): the
+    adapter gradients (HBM-bound) and the input gradient (matrix-core bound)
+    of the four projections, each timed as graph replays over two input sets."""
+    from paper_2608_15241_amd.step import meta_to_device
+    w = workloads.PREFILL_7B
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
+    T = meta.T
+    grads, inputs, keep = [], [], []
+    for s in range(2):
+        lw = workloads.make_layer_weights(w, 0, dev, seed=700 + s)
+        ws = lk.Workspace(dev)
+        g_calls, i_calls = [], []
+        for proj in ("q", "k", "v", "o"):
+            N, K = w.proj_shape(proj)
+            x = workloads.randn_bf16((T, K), 1.0, dev, seed=710 + 10 * s + len(g_calls))
+            dy = workloads.randn_bf16((T, N), 1.0, dev, seed=750 + 10 * s + len(g_calls))
+            Wt = lw["W_" + proj].t().contiguous()
+            keep += [x, dy, Wt]
+            args = (lw["A_" + proj], lw["B_" + proj], lw["ranks_" + proj], md.token_adapter,
+                    md.token_scale)
+            g_calls.append(lk.prepare_lora_grad(x, dy, *args, workspace=ws))
+            i_calls.append(lk.prepare_lora_grad_input(dy, Wt, *args, workspace=ws))
+        keep.append(lw)
+        grads.append(g_calls)
+        inputs.append(i_calls)
+
+    def graphs_of(sets):
+        out = []
+        for calls in sets:
+            for c in calls:
+                c()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            st = torch.cuda.Stream()
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                with torch.cuda.graph(g, stream=st):
+                    for c in calls:
+                        c()
+            torch.cuda.current_stream().wait_stream(st)
+            out.append(g)
+        return out
+
+    def time_graphs(gs):
+        for g in gs:
+            g.replay()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            gs[r % 2].replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    ms_g = time_graphs(graphs_of(grads))
+    ms_i = time_graphs(graphs_of(inputs))
+    gb = lora_grad_bytes(w, T)
+    fl = lora_grad_input_flops(w, T)
+    gbps = gb / (ms_g / 1e3) / 1e9
+    tflops = fl / (ms_i / 1e3) / 1e12
+    return {"workload": "lora_backward_7b_t%d_4x_r16" % T,
+            "adapter_grads": {"kernel": "local_lora_grad x 4 (q,k,v,o)", "bound": "hbm",
+                              "bytes_per_pass": gb, "ms_per_pass": round(ms_g, 5),
+                              "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+                              "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4)},
+            "input_grad": {"kernel": "local_lora_grad_input x 4 (q,k,v,o)", "bound": "mfma",
+                           "flops_per_pass": fl, "ms_per_pass": round(ms_i, 5),
+                           "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}}
 
 
 def cpu_baseline(torch, workloads, w, meta, set0, args):

@@ -6,23 +6,26 @@
 //   dB_a = sum_{t of a} s_t dy_t^T u_t,  dA_a = sum_{t of a} g_t^T x_t,
 //   dx_t = dy_t W + g_t A_a.
 //
-// Design (HBM-bound for the adapter gradients: 2 T r (K + N) flop against
-// T (K + N) bf16 read):
-//  * The tokens are bucketed by adapter (a stable counting sort in one
-//    workgroup), as in SGMV.
-//  * u and g come from the long-chunk shrink of the forward path: x against
-//    A, and dy against B transposed per adapter (a small transpose), then a
-//    pass that sums its K slices in order and scales by s_t (tokens without
-//    an adapter, and columns at or past the rank, get 0).
-//  * dB and dA are segmented outer products: a workgroup per (64 tokens of
-//    one adapter, 256 threads x PT columns of dy or x); each thread keeps
-//    PT x r_max float32 sums over its tokens, with the tokens' coefficients
-//    broadcast from LDS and each token's row read once, coalesced. Partial
-//    sums per 64-token unit are added in unit order by a reduce pass:
-//    deterministic, no atomics.
-//  * dx runs the forward fused projection on the transposed weights: with
-//    x := dy, W := W^T, A := B^T and B := A^T, its shrink is dy B and its
-//    delta s (dy B) A, so dx needs no kernel of its own.
+// Design (HBM-bound for the adapter gradients: 4 T r (K + N) flop, shrinks
+// included, against T (K + N) bf16 read), four launches:
+//  * set-up: the tokens bucketed by adapter (a stable counting sort in one
+//    workgroup, as in SGMV) while the other workgroups transpose B per
+//    adapter to [r_max][N];
+//  * u = x A^T and dy B from the long-chunk shrink of the forward path, as
+//    float32 partial sums over K slices (two launches);
+//  * dB and dA as segmented outer products, both in one launch: a workgroup
+//    per (64 tokens of one adapter, 256 threads x PT columns of dy or x)
+//    forms the tokens' coefficients in LDS (slices summed in order, times
+//    s_t, 0 past the rank), then each thread keeps PT x r_max float32 sums
+//    over the tokens, each token's row read once, coalesced;
+//  * the partial sums of the 64-token units added in unit order by a reduce
+//    pass: deterministic, no atomics.
+//  dx runs the forward fused projection on the transposed weights: with
+//  x := dy, W := W^T, A := B^T and B := A^T, its shrink is dy B and its
+//  delta s (dy B) A, so dx needs no kernel of its own.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.hpp"
 #include "lora_internal.hpp"
 
@@ -33,47 +36,99 @@ constexpr int kGrUnit = 64;      // tokens per unit of the segmented products
 constexpr int kGrThreads = 256;
 constexpr int kGrMaxAdapters = 256;
 
+constexpr int kGrCachedTokens = 8192;  // adapter indices the bucket pass keeps in LDS
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
 size_t al256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = threadIdx.x % kWave;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int u = __shfl_up(v, off);
+    if (lane >= off) v += u;
+  }
+  return v;
+}
 
 // ---- tokens bucketed by adapter, stable: perm[seg[a] .. seg[a+1]) holds the
 // tokens of adapter a in ascending order; tokens without one are left out.
-// One workgroup; the tokens go in passes of 1024, 64 per wave, in order.
-__global__ __launch_bounds__(1024) void grad_bucket_kernel(const int32_t* __restrict__ idx,
-                                                           int64_t T, int n_ad,
-                                                           int32_t* __restrict__ perm,
-                                                           int32_t* __restrict__ seg) {
+// useg[a] = sum over b < a of ceil(T_b / 64): the first 64-token unit of a;
+// utab[k] = (adapter, first position in perm, token count) of unit k.
+// One workgroup: the indices are counted (8 loads in flight per thread, one
+// LDS atomic per wave and adapter, the first 8192 indices kept in LDS), then
+// the tokens are placed in passes of 256, 64 per wave, in order.
+__device__ void bucket_tokens(const int32_t* __restrict__ idx, int64_t T, int n_ad,
+                              int32_t* __restrict__ perm, int32_t* __restrict__ seg,
+                              int32_t* __restrict__ useg, i32x4* __restrict__ utab) {
+  constexpr int kWaves = kGrThreads / kWave;
+  constexpr int kBatch = 8;  // index loads in flight per thread
   __shared__ int base[kGrMaxAdapters];
-  __shared__ int wcnt[16][kGrMaxAdapters];  // tokens per adapter in each wave of a pass
+  __shared__ int wcnt[kWaves][kGrMaxAdapters];  // tokens per adapter in each wave of a pass
+  __shared__ int16_t cache[kGrCachedTokens];     // adapter of token t (-1: none), t < cached
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  for (int a = tid; a < n_ad; a += 1024) base[a] = 0;
+  const int64_t cached = T < kGrCachedTokens ? T : kGrCachedTokens;
+  auto adapter_of = [&](int32_t v) { return (v >= 0 && v < n_ad) ? v : -1; };
+  for (int a = tid; a < n_ad; a += kGrThreads) base[a] = 0;
   __syncthreads();
-  for (int64_t t = tid; t < T; t += 1024) {
-    const int a = idx[t];
-    if (a >= 0 && a < n_ad) atomicAdd(&base[a], 1);
-  }
-  __syncthreads();
-  if (tid == 0) {  // exclusive prefix (n_ad <= 256)
-    int run = 0;
-    for (int a = 0; a < n_ad; ++a) {
-      const int c = base[a];
-      seg[a] = run;
-      base[a] = run;
-      run += c;
+  for (int64_t t0 = 0; t0 < T; t0 += kBatch * kGrThreads) {
+    int my[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int64_t t = t0 + b * kGrThreads + tid;
+      my[b] = t < T ? adapter_of(idx[t]) : -1;
     }
-    seg[n_ad] = run;
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int64_t t = t0 + b * kGrThreads + tid;
+      if (t < cached) cache[t] = static_cast<int16_t>(my[b]);
+      // one LDS atomic per (wave, adapter): equal adapters grouped by ballot
+      uint64_t pending = __ballot(my[b] >= 0);
+      while (pending) {
+        const int ad = __builtin_amdgcn_readlane(my[b], __ffsll(static_cast<long long>(pending)) - 1);
+        const uint64_t m = __ballot(my[b] == ad);
+        if (lane == 0) atomicAdd(&base[ad], __popcll(m));
+        pending &= ~m;
+      }
+    }
   }
   __syncthreads();
-  for (int64_t t0 = 0; t0 < T; t0 += 1024) {
+  if (wave == 0) {  // exclusive prefixes of the counts and of the unit counts
+    int run = 0, urun = 0;
+    for (int a0 = 0; a0 < n_ad; a0 += kWave) {
+      const int a = a0 + lane;
+      const int c = a < n_ad ? base[a] : 0;
+      const int u = (c + kGrUnit - 1) / kGrUnit;
+      const int ic = wave_incl_scan(c), iu = wave_incl_scan(u);
+      if (a < n_ad) {
+        const int s0 = run + ic - c, u0 = urun + iu - u;
+        seg[a] = s0;
+        base[a] = s0;
+        useg[a] = u0;
+        for (int k = 0; k < u; ++k)
+          utab[u0 + k] = i32x4{a, s0 + kGrUnit * k, min(kGrUnit, c - kGrUnit * k), 0};
+      }
+      run += __shfl(ic, kWave - 1);
+      urun += __shfl(iu, kWave - 1);
+    }
+    if (lane == 0) {
+      seg[n_ad] = run;
+      useg[n_ad] = urun;
+    }
+  }
+  __syncthreads();
+  for (int64_t t0 = 0; t0 < T; t0 += kGrThreads) {
     const int64_t t = t0 + tid;
-    const int a = t < T ? idx[t] : -1;
-    const int my = (a >= 0 && a < n_ad) ? a : -1;
+    const int my = t < cached ? cache[t] : (t < T ? adapter_of(idx[t]) : -1);
     for (int e = lane; e < n_ad; e += kWave) wcnt[wave][e] = 0;
     // rank among the wave's earlier lanes of the same adapter, and the
     // wave's count of each adapter present in it
     int rank = 0;
     uint64_t pending = __ballot(my >= 0);
     while (pending) {
-      const int ad = __shfl(my, __ffsll(static_cast<long long>(pending)) - 1);
+      const int ad = __builtin_amdgcn_readlane(my, __ffsll(static_cast<long long>(pending)) - 1);
       const uint64_t m = __ballot(my == ad);
       if (my == ad) rank = __popcll(m & ((1ull << lane) - 1ull));
       if (lane == 0) wcnt[wave][ad] = __popcll(m);
@@ -86,202 +141,392 @@ __global__ __launch_bounds__(1024) void grad_bucket_kernel(const int32_t* __rest
       perm[base[my] + before + rank] = static_cast<int32_t>(t);
     }
     __syncthreads();
-    for (int a2 = tid; a2 < n_ad; a2 += 1024) {
+    for (int a2 = tid; a2 < n_ad; a2 += kGrThreads) {
       int c = 0;
-      for (int w = 0; w < 16; ++w) c += wcnt[w][a2];
+      for (int w = 0; w < kWaves; ++w) c += wcnt[w][a2];
       base[a2] += c;
     }
     __syncthreads();
   }
 }
 
-// ---- dst[i][c][r] = src[i][r][c] for n matrices of R x C bf16 (R and C
-// multiples of 8), through 64 x 64 LDS tiles: rows read and written whole.
-__global__ __launch_bounds__(kGrThreads) void grad_transpose_kernel(
-    const uint16_t* __restrict__ src, int64_t R, int64_t C, uint16_t* __restrict__ dst) {
-  __shared__ uint16_t tile[64][64 + 2];
-  const int64_t i = blockIdx.z;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64, c0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const uint16_t* s = src + i * R * C;
-  uint16_t* d = dst + i * R * C;
-  for (int e = threadIdx.x; e < 64 * 64; e += kGrThreads) {
-    const int rr = e / 64, cc = e % 64;
-    if (r0 + rr < R && c0 + cc < C) tile[rr][cc] = s[(r0 + rr) * C + c0 + cc];
+// ---- per-matrix transposes dst[i][c][r] = src[i][r][c] of n matrices of
+// R x C bf16 (R and C multiples of 8). A tile of TR x TC (at most 2048
+// elements) goes through LDS: 16-byte loads along the source rows, 16-byte
+// stores along the destination rows.
+struct TransposeJob {
+  const uint16_t* src;
+  uint16_t* dst;
+  int64_t R, C;
+  int TR, TC, tiles_c, tiles;
+};
+
+TransposeJob transpose_job(const uint16_t* src, uint16_t* dst, int64_t n, int64_t R,
+                           int64_t C) {
+  TransposeJob j{src, dst, R, C, 0, 0, 0, 0};
+  if (R < C) {
+    j.TR = static_cast<int>(std::min<int64_t>(R, 64));
+    j.TC = 2048 / j.TR / 8 * 8;
+  } else {
+    j.TC = static_cast<int>(std::min<int64_t>(C, 64));
+    j.TR = 2048 / j.TC / 8 * 8;
+  }
+  j.tiles_c = static_cast<int>((C + j.TC - 1) / j.TC);
+  j.tiles = j.tiles_c * static_cast<int>((R + j.TR - 1) / j.TR) * static_cast<int>(n);
+  return j;
+}
+
+// Tile k of job j (tiles of matrix 0 first, then of matrix 1, ...).
+__device__ void transpose_tile(const TransposeJob& j, int k) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[4096];  // TR x (TC + 8)
+  const int TR = j.TR, TC = j.TC, ld = TC + 8;
+  const int per_mat = j.tiles_c * static_cast<int>((j.R + TR - 1) / TR);
+  const int64_t i = k / per_mat;
+  const int kk = k % per_mat;
+  const int64_t r0 = static_cast<int64_t>(kk / j.tiles_c) * TR;
+  const int64_t c0 = static_cast<int64_t>(kk % j.tiles_c) * TC;
+  const uint16_t* s = j.src + i * j.R * j.C;
+  uint16_t* d = j.dst + i * j.R * j.C;
+  const int e8 = threadIdx.x * 8;
+  if (e8 < TR * TC) {
+    const int rr = e8 / TC, cc = e8 % TC;
+    if (r0 + rr < j.R && c0 + cc < j.C)
+      *reinterpret_cast<u32x4*>(tile + rr * ld + cc) =
+          ld_global<u32x4>(s + (r0 + rr) * j.C + c0 + cc);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += kGrThreads) {
-    const int cc = e / 64, rr = e % 64;
-    if (r0 + rr < R && c0 + cc < C) d[(c0 + cc) * R + r0 + rr] = tile[rr][cc];
-  }
-}
-
-// ---- coefficients c[t][j] = s_t * (sum of the shrink's K slices, in order)
-// for j below the rank of t's adapter; 0 elsewhere and for tokens without one.
-__global__ __launch_bounds__(kGrThreads) void grad_coef_kernel(
-    const float* __restrict__ P, int ks, int64_t T, int r_max, const int32_t* __restrict__ idx,
-    const float* __restrict__ scale, const int32_t* __restrict__ ranks, int n_ad,
-    float* __restrict__ c) {
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * kGrThreads + threadIdx.x;
-  if (e >= T * r_max) return;
-  const int64_t t = e / r_max;
-  const int j = static_cast<int>(e % r_max);
-  const int a = idx[t];
-  float v = 0.f;
-  if (a >= 0 && a < n_ad) {
-    const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
-    if (j < rk) {
-      float sum = 0.f;
-      for (int z = 0; z < ks; ++z) sum += P[(static_cast<int64_t>(z) * T + t) * r_max + j];
-      v = scale[t] * sum;
-    }
-  }
-  c[e] = v;
-}
-
-// Adapter and 64-token unit of unit slot k (adapters ascending, units in
-// token order), or -1 past the last unit; every lane returns the same.
-__device__ int grad_unit(const int32_t* __restrict__ seg, int n_ad, int k, int* unit) {
-  const int lane = threadIdx.x % kWave;
-  for (int a0 = 0; a0 < n_ad; a0 += kWave) {
-    const int a = a0 + lane;
-    const int n = a < n_ad ? (seg[a + 1] - seg[a] + kGrUnit - 1) / kGrUnit : 0;
-    int incl = n;
+  if (e8 < TR * TC) {
+    const int cc = e8 / TR, rr = e8 % TR;
+    if (c0 + cc < j.C && r0 + rr < j.R) {
+      uint32_t w[4];
 #pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int v = __shfl_up(incl, off);
-      if (lane >= off) incl += v;
+      for (int q = 0; q < 4; ++q)
+        w[q] = static_cast<uint32_t>(tile[(rr + 2 * q) * ld + cc]) |
+               (static_cast<uint32_t>(tile[(rr + 2 * q + 1) * ld + cc]) << 16);
+      *reinterpret_cast<u32x4*>(d + (c0 + cc) * j.R + r0 + rr) = u32x4{w[0], w[1], w[2], w[3]};
     }
-    const int total = __shfl(incl, kWave - 1);
-    if (k < total) {
-      const uint64_t m = __ballot(incl > k);
-      const int l0 = __ffsll(static_cast<long long>(m)) - 1;
-      *unit = k - __shfl(incl - n, l0);
-      return a0 + l0;
-    }
-    k -= total;
   }
-  return -1;
 }
 
-// ---- segmented outer products. Workgroup = (unit slot, column tile of
-// 256 PT columns): partial sums over the unit's tokens of c_t[j] V_t[p] for
-// its PT columns per thread. Written per unit slot, [P][r_max] (dB) or
-// [r_max][P] (TRANS, dA).
-template <int PT, int RJ, bool TRANS>
-__global__ __launch_bounds__(kGrThreads) void grad_outer_kernel(
-    const uint16_t* __restrict__ V, int64_t P, const float* __restrict__ C, int r_max,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ seg, int n_ad,
-    float* __restrict__ part) {
-  __shared__ float cl[kGrUnit][RJ];
-  __shared__ int tok[kGrUnit];
-  const int64_t ptiles = (P + kGrThreads * PT - 1) / (kGrThreads * PT);
-  const int slot = static_cast<int>(blockIdx.x / ptiles);
-  const int64_t pt = blockIdx.x % ptiles;
-  int unit = 0;
-  const int a = grad_unit(seg, n_ad, slot, &unit);
-  if (a < 0) return;
-  const int first = seg[a] + unit * kGrUnit;
-  const int nt = min(kGrUnit, seg[a + 1] - first);
-  const int tid = threadIdx.x;
-  if (tid < nt) tok[tid] = perm[first + tid];
-  __syncthreads();
-  for (int e = tid; e < kGrUnit * RJ; e += kGrThreads) {
-    const int i = e / RJ, j = e % RJ;
-    cl[i][j] = (i < nt && j < r_max) ? C[static_cast<int64_t>(tok[i]) * r_max + j] : 0.f;
+// One launch for the set-up work: workgroup 0 buckets the tokens (when
+// idx is given), the others transpose tiles of job 0, then of job 1.
+struct PrepArgs {
+  TransposeJob job[2];
+  int n_jobs;
+  const int32_t* idx;
+  int64_t T;
+  int n_ad;
+  int32_t *perm, *seg, *useg;
+  i32x4* utab;
+};
+
+__global__ __launch_bounds__(kGrThreads) void grad_prep_kernel(PrepArgs a) {
+  int k = blockIdx.x;
+  if (a.idx) {
+    if (k == 0) {
+      bucket_tokens(a.idx, a.T, a.n_ad, a.perm, a.seg, a.useg, a.utab);
+      return;
+    }
+    --k;
   }
+  if (k < a.job[0].tiles) {
+    transpose_tile(a.job[0], k);
+    return;
+  }
+  k -= a.job[0].tiles;
+  if (a.n_jobs > 1 && k < a.job[1].tiles) transpose_tile(a.job[1], k);
+}
+
+local_status_t run_prep(hipStream_t s, PrepArgs a) {
+  const int tiles = a.job[0].tiles + (a.n_jobs > 1 ? a.job[1].tiles : 0);
+  grad_prep_kernel<<<static_cast<unsigned>(tiles + (a.idx ? 1 : 0)), kGrThreads, 0, s>>>(a);
+  return local_check_launch("lora_grad (prep)");
+}
+
+// Coefficients of a unit's tokens into LDS: cl[i][j] = s_i * (sum over the
+// shrink's K slices, in slice order) for j below the rank, 0 elsewhere and
+// for i >= nt. Each thread forms 4 consecutive j of one token at a time with
+// 16-byte loads, 8 slices in flight (the sum stays in slice order).
+template <int RJ>
+__device__ __forceinline__ void stage_coefficients(float (*cl)[RJ], const int* tok,
+                                                   const float* tsc, const float* S, int ks,
+                                                   int64_t T, int r_max, int nt, int rk) {
+  for (int e = threadIdx.x; e < kGrUnit * RJ / 4; e += kGrThreads) {
+    const int i = e / (RJ / 4), j = 4 * (e % (RJ / 4));
+    f32x4 sum{0.f, 0.f, 0.f, 0.f};
+    if (i < nt && j < rk) {
+      const float* src = S + static_cast<int64_t>(tok[i]) * r_max + j;
+      for (int z0 = 0; z0 < ks; z0 += 8) {
+        f32x4 v[8];
+#pragma unroll
+        for (int z = 0; z < 8; ++z)
+          v[z] = z0 + z < ks
+                     ? *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(z0 + z) * T * r_max)
+                     : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int z = 0; z < 8; ++z) sum += v[z];
+      }
+      sum *= tsc[i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (j + q >= rk) sum[q] = 0.f;
+    }
+    *reinterpret_cast<f32x4*>(&cl[i][j]) = sum;
+  }
+}
+
+// ---- segmented outer products, both gradients in one launch. blockIdx.y =
+// job: 0 = dB (V = dy, P = N, coefficients s u, partials [P][r_max]),
+// 1 = dA (V = x, P = K, coefficients g = s dy B, partials [r_max][P]).
+// Workgroup = (unit, column tile of 256 PT columns). The unit's 64 token
+// rows are loaded at once, ahead of everything else, so that a workgroup
+// waits for memory about three times (unit table, token ids, rows and
+// coefficients together). The coefficients are formed in LDS from the
+// shrink's K-slice partial sums (u = x A^T, or dy B): summed over the slices
+// in order, times s_t, 0 at or past the adapter's rank. Each thread then
+// keeps PT x RJ float32 sums of c_t[j] V_t[p] over the unit's tokens.
+struct OuterArgs {
+  const uint16_t* V[2];
+  const float* S[2];  // shrink partial sums [ks][T][r_max]
+  int ks[2];
+  float* part[2];
+  int64_t P[2];
+};
+
+template <int PT, int RJ>
+__global__ __launch_bounds__(kGrThreads) void grad_outer_kernel(
+    OuterArgs args, int64_t T, int64_t ptiles, int r_max, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ useg, const i32x4* __restrict__ utab, int n_ad,
+    const int32_t* __restrict__ ranks, const float* __restrict__ scale) {
+  using RowT = typename std::conditional<PT == 2, uint32_t, uint16_t>::type;
+  __shared__ __attribute__((aligned(16))) float cl[kGrUnit][RJ];
+  __shared__ int tok[kGrUnit];
+  __shared__ float tsc[kGrUnit];
+  const int job = blockIdx.y;
+  const int64_t P = job ? args.P[1] : args.P[0];
+  const int slot = static_cast<int>(blockIdx.x / ptiles);
+  const int64_t p0 = ((blockIdx.x % ptiles) * kGrThreads + threadIdx.x) * PT;
+  if ((blockIdx.x % ptiles) * kGrThreads * PT >= P) return;  // the whole tile is past P
+  if (slot >= useg[n_ad]) return;                             // past the last unit
+  const i32x4 ut = utab[slot];
+  const int a = ut.x, first = ut.y, nt = ut.z;
+  const uint16_t* V = job ? args.V[1] : args.V[0];
+  const float* S = job ? args.S[1] : args.S[0];
+  const int ks = job ? args.ks[1] : args.ks[0];
+  const int tid = threadIdx.x;
+  if (tid < nt) {
+    const int t = perm[first + tid];
+    tok[tid] = t;
+    tsc[tid] = scale[t];
+  }
+  const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
   __syncthreads();
-  const int64_t p0 = (pt * kGrThreads + tid) * PT;
+  // every row of the unit in flight at once (rows past nt read as zero)
+  const bool live = p0 < P;
+  RowT raw[kGrUnit];
+#pragma unroll
+  for (int i = 0; i < kGrUnit; ++i)
+    raw[i] = (live && i < nt)
+                 ? ld_global<RowT>(V + static_cast<int64_t>(tok[i]) * P + p0)
+                 : RowT(0);
+  stage_coefficients<RJ>(cl, tok, tsc, S, ks, T, r_max, nt, rk);
+  __syncthreads();
   float acc[PT][RJ];
 #pragma unroll
   for (int q = 0; q < PT; ++q)
 #pragma unroll
     for (int j = 0; j < RJ; ++j) acc[q][j] = 0.f;
-  if (p0 < P) {
-    for (int i = 0; i < nt; ++i) {
-      const uint16_t* row = V + static_cast<int64_t>(tok[i]) * P + p0;
-      float v[PT];
-      if constexpr (PT == 4) {
-        const u32x2 w = ld_global<u32x2>(row);
-        v[0] = __uint_as_float(w.x << 16);
-        v[1] = __uint_as_float(w.x & 0xffff0000u);
-        v[2] = __uint_as_float(w.y << 16);
-        v[3] = __uint_as_float(w.y & 0xffff0000u);
-      } else if constexpr (PT == 2) {
-        const uint32_t w = ld_global<uint32_t>(row);
-        v[0] = __uint_as_float(w << 16);
-        v[1] = __uint_as_float(w & 0xffff0000u);
-      } else {
-        v[0] = __uint_as_float(static_cast<uint32_t>(row[0]) << 16);
-      }
 #pragma unroll
-      for (int j = 0; j < RJ; ++j) {
-        const float cj = cl[i][j];
+  for (int i = 0; i < kGrUnit; ++i) {
+    float v[PT];
+    if constexpr (PT == 2) {
+      v[0] = __uint_as_float(static_cast<uint32_t>(raw[i]) << 16);
+      v[1] = __uint_as_float(static_cast<uint32_t>(raw[i]) & 0xffff0000u);
+    } else {
+      v[0] = __uint_as_float(static_cast<uint32_t>(raw[i]) << 16);
+    }
 #pragma unroll
-        for (int q = 0; q < PT; ++q) acc[q][j] += cj * v[q];
+    for (int j4 = 0; j4 < RJ; j4 += 4) {
+      const f32x4 cj = *reinterpret_cast<const f32x4*>(&cl[i][j4]);
+#pragma unroll
+      for (int q = 0; q < PT; ++q) {
+        acc[q][j4] += cj[0] * v[q];
+        acc[q][j4 + 1] += cj[1] * v[q];
+        acc[q][j4 + 2] += cj[2] * v[q];
+        acc[q][j4 + 3] += cj[3] * v[q];
       }
     }
   }
-  if (p0 >= P) return;
-  float* out = part + static_cast<int64_t>(slot) * P * r_max;
+  if (!live) return;
+  float* out = (job ? args.part[1] : args.part[0]) + static_cast<int64_t>(slot) * P * r_max;
+  if (job) {
 #pragma unroll
-  for (int q = 0; q < PT; ++q)
+    for (int q = 0; q < PT; ++q)
 #pragma unroll
-    for (int j = 0; j < RJ; ++j)
-      if (j < r_max) {
-        if (TRANS)
-          out[static_cast<int64_t>(j) * P + p0 + q] = acc[q][j];
-        else
-          out[(p0 + q) * r_max + j] = acc[q][j];
-      }
-}
-
-// ---- out[a][e] = sum of the partial sums of a's units, in unit order, for
-// e < E = P * r_max; 0 for an adapter without tokens and at or past its rank.
-__global__ __launch_bounds__(kGrThreads) void grad_reduce_kernel(
-    const float* __restrict__ part, int64_t E, int64_t P, int r_max, bool trans,
-    const int32_t* __restrict__ seg, int n_ad, const int32_t* __restrict__ ranks,
-    float* __restrict__ out) {
-  __shared__ int first_unit;
-  const int a = blockIdx.y;
-  if (threadIdx.x == 0) {
-    int u = 0;
-    for (int b = 0; b < a; ++b) u += (seg[b + 1] - seg[b] + kGrUnit - 1) / kGrUnit;
-    first_unit = u;
+      for (int j = 0; j < RJ; ++j)
+        if (j < r_max) out[static_cast<int64_t>(j) * P + p0 + q] = acc[q][j];
+  } else {
+#pragma unroll
+    for (int q = 0; q < PT; ++q)
+#pragma unroll
+      for (int j = 0; j < RJ; j += 4)
+        if (j < r_max)
+          *reinterpret_cast<f32x4*>(out + (p0 + q) * r_max + j) =
+              f32x4{acc[q][j], acc[q][j + 1], acc[q][j + 2], acc[q][j + 3]};
   }
-  __syncthreads();
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * kGrThreads + threadIdx.x;
-  if (e >= E) return;
-  const int nu = (seg[a + 1] - seg[a] + kGrUnit - 1) / kGrUnit;
-  const int j = trans ? static_cast<int>(e / P) : static_cast<int>(e % r_max);
-  const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
-  float sum = 0.f;
-  if (j < rk)
-    for (int u = 0; u < nu; ++u) sum += part[static_cast<int64_t>(first_unit + u) * E + e];
-  out[static_cast<int64_t>(a) * E + e] = sum;
 }
 
-template <bool TRANS>
-local_status_t launch_outer(const uint16_t* V, int64_t P, const float* C, int r_max,
-                            const int32_t* perm, const int32_t* seg, int n_ad, int64_t units,
-                            float* part, hipStream_t s) {
-  auto go = [&](auto kernel, int pt) {
-    const int64_t ptiles = (P + kGrThreads * pt - 1) / (kGrThreads * pt);
-    kernel<<<static_cast<unsigned>(units * ptiles), kGrThreads, 0, s>>>(V, P, C, r_max, perm,
-                                                                         seg, n_ad, part);
+// ---- the same products on the matrix cores (r_max <= 64), float32 MFMA
+// v_mfma_f32_16x16x4_f32: D[16 x 16] += A[16 x 4] B[4 x 16], lane l giving
+// A[l%16][l/16] and B[l/16][l%16] and holding D[4(l/16) + i][l%16]. With
+// the contraction over 4 tokens, A = the coefficients c[t][j] (j = row) and
+// B = the token rows V[t][col] (col = column): both are read along their
+// rows, so the token-major inputs need no transpose. A wave owns 128
+// columns: lane l loads 8 consecutive columns 8(l%16) .. +7 of token l/16
+// (16 bytes, 256 contiguous bytes per token), and MFMA e (e < 8) takes
+// element e, i.e. columns 8n + e for D column n. JT tiles of 16 cover
+// r_max. The unit's rows are all in flight before the first product.
+template <int JT>
+__global__ __launch_bounds__(kGrThreads) void grad_outer_mfma_kernel(
+    OuterArgs args, int64_t T, int64_t ptiles, int r_max, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ useg, const i32x4* __restrict__ utab, int n_ad,
+    const int32_t* __restrict__ ranks, const float* __restrict__ scale) {
+  constexpr int RJ = 16 * JT;
+  constexpr int kSteps = kGrUnit / 4;
+  __shared__ __attribute__((aligned(16))) float cl[kGrUnit][RJ];
+  __shared__ int tok[kGrUnit];
+  __shared__ float tsc[kGrUnit];
+  const int job = blockIdx.y;
+  const int64_t P = job ? args.P[1] : args.P[0];
+  const int slot = static_cast<int>(blockIdx.x / ptiles);
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int64_t wcol = ((blockIdx.x % ptiles) * (kGrThreads / kWave) + wave) * 128;
+  if ((blockIdx.x % ptiles) * 512 >= P) return;  // the whole tile is past P
+  if (slot >= useg[n_ad]) return;                // past the last unit
+  const i32x4 ut = utab[slot];
+  const int a = ut.x, first = ut.y, nt = ut.z;
+  const uint16_t* V = job ? args.V[1] : args.V[0];
+  const float* S = job ? args.S[1] : args.S[0];
+  const int ks = job ? args.ks[1] : args.ks[0];
+  if (tid < nt) {
+    const int t = perm[first + tid];
+    tok[tid] = t;
+    tsc[tid] = scale[t];
+  }
+  const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
+  __syncthreads();
+  const int n = lane % 16, k = lane / 16;
+  const int64_t col = wcol + 8 * n;  // this lane's 8 columns
+  const bool live = col < P;
+  u32x4 raw[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int i = 4 * st + k;
+    raw[st] = (live && i < nt) ? ld_global<u32x4>(V + static_cast<int64_t>(tok[i]) * P + col)
+                               : u32x4{0u, 0u, 0u, 0u};
+  }
+  stage_coefficients<RJ>(cl, tok, tsc, S, ks, T, r_max, nt, rk);
+  __syncthreads();
+  f32x4 acc[JT][8];
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[jt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    float v[8];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      v[2 * h] = __uint_as_float(raw[st][h] << 16);
+      v[2 * h + 1] = __uint_as_float(raw[st][h] & 0xffff0000u);
+    }
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const float c = cl[4 * st + k][16 * jt + n];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        acc[jt][e] = __builtin_amdgcn_mfma_f32_16x16x4f32(c, v[e], acc[jt][e], 0, 0, 0);
+    }
+  }
+  if (!live) return;
+  float* out = (job ? args.part[1] : args.part[0]) + static_cast<int64_t>(slot) * P * r_max;
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    const int j0 = 16 * jt + 4 * k;  // this lane's rows j0 .. j0 + 3
+    if (j0 >= r_max) continue;
+    if (job) {  // [r_max][P]: 8 consecutive columns per row
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float* o = out + static_cast<int64_t>(j0 + i) * P + col;
+        *reinterpret_cast<f32x4*>(o) =
+            f32x4{acc[jt][0][i], acc[jt][1][i], acc[jt][2][i], acc[jt][3][i]};
+        *reinterpret_cast<f32x4*>(o + 4) =
+            f32x4{acc[jt][4][i], acc[jt][5][i], acc[jt][6][i], acc[jt][7][i]};
+      }
+    } else {  // [P][r_max]: 4 consecutive rows per column
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<f32x4*>(out + (col + e) * r_max + j0) = acc[jt][e];
+    }
+  }
+}
+
+// ---- out[a][e .. e+4) = sum of the partial sums of a's units, in unit
+// order, for e < E = P * r_max; 0 for an adapter without tokens and at or
+// past its rank. blockIdx.z = job as for the outer products.
+struct ReduceArgs {
+  const float* part[2];
+  float* out[2];
+  int64_t P[2];
+};
+
+__global__ __launch_bounds__(kGrThreads) void grad_reduce_kernel(
+    ReduceArgs args, int r_max, const int32_t* __restrict__ useg,
+    const int32_t* __restrict__ ranks) {
+  const int job = blockIdx.z;
+  const int a = blockIdx.y;
+  const int64_t P = job ? args.P[1] : args.P[0];
+  const int64_t E = P * r_max;
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * kGrThreads + threadIdx.x) * 4;
+  if (e >= E) return;
+  const int u0 = useg[a], nu = useg[a + 1] - u0;
+  const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
+  const float* part = job ? args.part[1] : args.part[0];
+  f32x4 sum{0.f, 0.f, 0.f, 0.f};
+  int u = 0;
+  for (; u + 4 <= nu; u += 4) {  // four loads in flight, added in unit order
+    f32x4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(u0 + u + q) * E + e);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sum += v[q];
+  }
+  for (; u < nu; ++u)
+    sum += *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(u0 + u) * E + e);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = job ? static_cast<int>((e + q) / P) : static_cast<int>((e + q) % r_max);
+    if (j >= rk) sum[q] = 0.f;
+  }
+  *reinterpret_cast<f32x4*>((job ? args.out[1] : args.out[0]) + static_cast<int64_t>(a) * E + e) =
+      sum;
+}
+
+local_status_t launch_outer(const OuterArgs& o, int64_t T, int r_max, const int32_t* perm,
+                            const int32_t* useg, const i32x4* utab, int n_ad, int64_t units,
+                            const int32_t* ranks, const float* scale, hipStream_t s) {
+  const int64_t pmax = std::max(o.P[0], o.P[1]);
+  auto go = [&](auto kernel, int64_t cols_per_wg) {
+    const int64_t ptiles = (pmax + cols_per_wg - 1) / cols_per_wg;
+    kernel<<<dim3(static_cast<unsigned>(units * ptiles), 2), kGrThreads, 0, s>>>(
+        o, T, ptiles, r_max, perm, useg, utab, n_ad, ranks, scale);
     return local_check_launch("lora_grad (outer)");
   };
-  if (r_max <= 16) return go(grad_outer_kernel<4, 16, TRANS>, 4);
-  if (r_max <= 32) return go(grad_outer_kernel<4, 32, TRANS>, 4);
-  if (r_max <= 64) return go(grad_outer_kernel<2, 64, TRANS>, 2);
-  return go(grad_outer_kernel<1, 128, TRANS>, 1);
-}
-
-local_status_t launch_transpose(const uint16_t* src, int64_t n, int64_t R, int64_t C,
-                                uint16_t* dst, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>((C + 63) / 64), static_cast<unsigned>((R + 63) / 64),
-                  static_cast<unsigned>(n));
-  grad_transpose_kernel<<<grid, kGrThreads, 0, s>>>(src, R, C, dst);
-  return local_check_launch("lora_grad (transpose)");
+  if (r_max <= 16) return go(grad_outer_mfma_kernel<1>, 512);
+  if (r_max <= 32) return go(grad_outer_mfma_kernel<2>, 512);
+  if (r_max <= 64) return go(grad_outer_mfma_kernel<4>, 512);
+  return go(grad_outer_kernel<1, 128>, kGrThreads);
 }
 
 local_status_t grad_checks(const char* who, int64_t T, int64_t K, int64_t N, int32_t n_ad,
@@ -311,19 +556,22 @@ extern "C" local_status_t local_lora_grad(
   local_status_t st = grad_checks("lora_grad", T, K, N, n_adapters, r_max);
   if (st != LOCAL_OK) return st;
   const int64_t Tw = T > 0 ? T : 1;
-  const int64_t units = Tw / kGrUnit + n_adapters;  // sum over adapters of ceil(T_a / 64)
+  const int64_t units = Tw / kGrUnit + n_adapters;  // >= sum over adapters of ceil(T_a / 64)
   int ks_x = 0, ks_dy = 0;
-  const size_t sh = std::max(token_shrink_bytes(Tw, K, r_max, &ks_x),
-                             token_shrink_bytes(Tw, N, r_max, &ks_dy));
+  const size_t sh_x = token_shrink_bytes(Tw, K, r_max, &ks_x);
+  const size_t sh_dy = token_shrink_bytes(Tw, N, r_max, &ks_dy);
+  // workspace: token order, adapter offsets, unit offsets, unit table, B^T, the two
+  // shrinks' partial sums, the two partial products
   const size_t o_perm = 0;
   const size_t o_seg = o_perm + al256(static_cast<size_t>(Tw) * 4);
-  const size_t o_bt = o_seg + al256(static_cast<size_t>(n_adapters + 1) * 4);
-  const size_t o_sh = o_bt + al256(static_cast<size_t>(n_adapters) * r_max * N * 2);
-  const size_t o_cu = o_sh + sh;
-  const size_t o_cg = o_cu + al256(static_cast<size_t>(Tw) * r_max * 4);
-  const size_t o_part = o_cg + al256(static_cast<size_t>(Tw) * r_max * 4);
-  const size_t need =
-      o_part + al256(static_cast<size_t>(units) * std::max(K, N) * r_max * 4);
+  const size_t o_useg = o_seg + al256(static_cast<size_t>(n_adapters + 1) * 4);
+  const size_t o_utab = o_useg + al256(static_cast<size_t>(n_adapters + 1) * 4);
+  const size_t o_bt = o_utab + al256(static_cast<size_t>(units) * 16);
+  const size_t o_shx = o_bt + al256(static_cast<size_t>(n_adapters) * r_max * N * 2);
+  const size_t o_shy = o_shx + sh_x;
+  const size_t o_pb = o_shy + sh_dy;
+  const size_t o_pa = o_pb + al256(static_cast<size_t>(units) * N * r_max * 4);
+  const size_t need = o_pa + al256(static_cast<size_t>(units) * K * r_max * 4);
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
@@ -331,57 +579,56 @@ extern "C" local_status_t local_lora_grad(
   if (*ws_bytes < need)
     return local_fail(LOCAL_ERR_WORKSPACE, "lora_grad: workspace %zu < %zu", *ws_bytes, need);
   if (!dA || !dB) return local_fail(LOCAL_ERR_NULL, "lora_grad: NULL output");
+  if (T > 0 && (!x || !dy || !A || !B || !adapter_idx || !scale))
+    return local_fail(LOCAL_ERR_NULL, "lora_grad: NULL pointer argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(ws);
   int32_t* perm = reinterpret_cast<int32_t*>(w + o_perm);
   int32_t* seg = reinterpret_cast<int32_t*>(w + o_seg);
+  int32_t* useg = reinterpret_cast<int32_t*>(w + o_useg);
+  i32x4* utab = reinterpret_cast<i32x4*>(w + o_utab);
   uint16_t* Bt = reinterpret_cast<uint16_t*>(w + o_bt);
-  float* cu = reinterpret_cast<float*>(w + o_cu);
-  float* cg = reinterpret_cast<float*>(w + o_cg);
-  float* part = reinterpret_cast<float*>(w + o_part);
-  const int64_t EdB = N * r_max, EdA = static_cast<int64_t>(r_max) * K;
-  if (T > 0 && (!x || !dy || !A || !B || !adapter_idx || !scale))
-    return local_fail(LOCAL_ERR_NULL, "lora_grad: NULL pointer argument");
-  // T = 0: the bucket pass leaves every adapter empty and the reduce pass
-  // writes zero gradients (no memset: the call stays capturable)
-  grad_bucket_kernel<<<1, 1024, 0, s>>>(adapter_idx, T, n_adapters, perm, seg);
-  if ((st = local_check_launch("lora_grad (bucket)")) != LOCAL_OK) return st;
+  float* pb = reinterpret_cast<float*>(w + o_pb);
+  float* pa = reinterpret_cast<float*>(w + o_pa);
+  // tokens bucketed by adapter and B transposed per adapter to [r_max][N],
+  // in one launch. T = 0: every adapter is empty and the reduce pass writes
+  // zero gradients (no memset: the call stays capturable)
+  PrepArgs pr{};
+  pr.job[0] = transpose_job(B, Bt, n_adapters, N, r_max);
+  pr.n_jobs = T > 0 ? 1 : 0;
+  if (T == 0) pr.job[0].tiles = 0;
+  pr.idx = adapter_idx ? adapter_idx : reinterpret_cast<const int32_t*>(w);  // not read if T = 0
+  pr.T = T;
+  pr.n_ad = n_adapters;
+  pr.perm = perm;
+  pr.seg = seg;
+  pr.useg = useg;
+  pr.utab = utab;
+  if ((st = run_prep(s, pr)) != LOCAL_OK) return st;
   if (T > 0) {
-    // coefficients of dB: s u, u = x A^T
-    if ((st = token_shrink(x, T, K, A, n_adapters, r_max, adapter_idx, w + o_sh, s)) != LOCAL_OK)
+    // u = x A^T and dy B as the shrink's K-slice partial sums
+    if ((st = token_shrink(x, T, K, A, n_adapters, r_max, adapter_idx, w + o_shx, s)) != LOCAL_OK)
       return st;
-    const unsigned cgrid = static_cast<unsigned>((T * r_max + kGrThreads - 1) / kGrThreads);
-    grad_coef_kernel<<<cgrid, kGrThreads, 0, s>>>(reinterpret_cast<const float*>(w + o_sh), ks_x,
-                                                  T, r_max, adapter_idx, scale, ranks,
-                                                  n_adapters, cu);
-    if ((st = local_check_launch("lora_grad (coef)")) != LOCAL_OK) return st;
-    // coefficients of dA: g = s dy B, with B transposed per adapter to [r_max][N]
-    if ((st = launch_transpose(B, n_adapters, N, r_max, Bt, s)) != LOCAL_OK) return st;
-    if ((st = token_shrink(dy, T, N, Bt, n_adapters, r_max, adapter_idx, w + o_sh, s)) !=
+    if ((st = token_shrink(dy, T, N, Bt, n_adapters, r_max, adapter_idx, w + o_shy, s)) !=
         LOCAL_OK)
       return st;
-    grad_coef_kernel<<<cgrid, kGrThreads, 0, s>>>(reinterpret_cast<const float*>(w + o_sh),
-                                                  ks_dy, T, r_max, adapter_idx, scale, ranks,
-                                                  n_adapters, cg);
-    if ((st = local_check_launch("lora_grad (coef)")) != LOCAL_OK) return st;
+    // dB partials from (dy, s u), dA partials from (x, s dy B)
+    const OuterArgs oa{{dy, x},
+                       {reinterpret_cast<const float*>(w + o_shx),
+                        reinterpret_cast<const float*>(w + o_shy)},
+                       {ks_x, ks_dy},
+                       {pb, pa},
+                       {N, K}};
+    if ((st = launch_outer(oa, T, r_max, perm, useg, utab, n_adapters, units, ranks, scale, s)) !=
+        LOCAL_OK)
+      return st;
   }
-  // dB [n_ad][N][r_max]
-  if (T > 0 &&
-      (st = launch_outer<false>(dy, N, cu, r_max, perm, seg, n_adapters, units, part, s)) !=
-          LOCAL_OK)
-    return st;
-  grad_reduce_kernel<<<dim3(static_cast<unsigned>((EdB + kGrThreads - 1) / kGrThreads),
-                            static_cast<unsigned>(n_adapters)),
-                       kGrThreads, 0, s>>>(part, EdB, N, r_max, false, seg, n_adapters, ranks, dB);
-  if ((st = local_check_launch("lora_grad (reduce)")) != LOCAL_OK) return st;
-  // dA [n_ad][r_max][K]
-  if (T > 0 &&
-      (st = launch_outer<true>(x, K, cg, r_max, perm, seg, n_adapters, units, part, s)) !=
-          LOCAL_OK)
-    return st;
-  grad_reduce_kernel<<<dim3(static_cast<unsigned>((EdA + kGrThreads - 1) / kGrThreads),
-                            static_cast<unsigned>(n_adapters)),
-                       kGrThreads, 0, s>>>(part, EdA, K, r_max, true, seg, n_adapters, ranks, dA);
+  // dB [n_ad][N][r_max], dA [n_ad][r_max][K]
+  const ReduceArgs ra{{pb, pa}, {dB, dA}, {N, K}};
+  const int64_t emax = std::max(N, K) * r_max;
+  grad_reduce_kernel<<<dim3(static_cast<unsigned>((emax / 4 + kGrThreads - 1) / kGrThreads),
+                            static_cast<unsigned>(n_adapters), 2),
+                       kGrThreads, 0, s>>>(ra, r_max, useg, ranks);
   return local_check_launch("lora_grad (reduce)");
 }
 
@@ -418,8 +665,11 @@ extern "C" local_status_t local_lora_grad_input(
   char* w = static_cast<char*>(ws);
   uint16_t* Bt = reinterpret_cast<uint16_t*>(w + o_bt);
   uint16_t* At = reinterpret_cast<uint16_t*>(w + o_at);
-  if ((st = launch_transpose(B, n_adapters, N, r_max, Bt, s)) != LOCAL_OK) return st;
-  if ((st = launch_transpose(A, n_adapters, r_max, K, At, s)) != LOCAL_OK) return st;
+  PrepArgs pr{};
+  pr.job[0] = transpose_job(B, Bt, n_adapters, N, r_max);
+  pr.job[1] = transpose_job(A, At, n_adapters, r_max, K);
+  pr.n_jobs = 2;
+  if ((st = run_prep(s, pr)) != LOCAL_OK) return st;
   size_t rest = *ws_bytes - o_fw;
   return local_lora_linear(dy, T, N, Wt, K, Bt, At, n_adapters, r_max, ranks, adapter_idx,
                            scale, nullptr, dx, w + o_fw, &rest, stream);

@@ -167,17 +167,20 @@ def test_lora_linear_grouped_workspace_and_errors(lib):
 def test_lora_grad_workspace_and_errors(lib):
     f = lib.local_lora_grad
     # T=300, K=512, N=640, 4 adapters of rank 16. Parts, each 256-byte aligned:
-    # the bucketed token order (T int32), the adapter offsets (n+1 int32), B
-    # transposed (n x r_max x N bf16), the shrink's partial sums (the larger of
-    # x against A, 8 K slices, and dy against B^T, 10 slices: 10 x T x r_max
-    # fp32, plus 32 bytes of adapter bitmap per 64-token tile), the two
-    # coefficient arrays (T x r_max fp32 each), then the partial products of
-    # at most T/64 + n 64-token units (units x max(K, N) x r_max fp32).
+    # the bucketed token order (T int32), the adapter offsets and the unit
+    # offsets (n+1 int32 each), the unit table (16 bytes for each of at most
+    # T/64 + n 64-token units), B transposed (n x r_max x N bf16), the
+    # shrinks' partial sums of x against A (8 K slices x T x r_max fp32) and of
+    # dy against B^T (10 slices), each followed by 32 bytes of adapter bitmap
+    # per 64-token tile, then the units' partial products (units x N x r_max
+    # and units x K x r_max fp32).
     a = lambda v: (v + 255) // 256 * 256
     st, n = _size(f, FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE)
     assert st == OK
-    assert n == (a(300 * 4) + a(5 * 4) + a(4 * 16 * 640 * 2) + a(10 * 300 * 16 * 4) + a(5 * 32)
-                 + 2 * a(300 * 16 * 4) + a((300 // 64 + 4) * 640 * 16 * 4))
+    units = 300 // 64 + 4
+    assert n == (a(300 * 4) + 2 * a(5 * 4) + a(units * 16) + a(4 * 16 * 640 * 2)
+                 + a(8 * 300 * 16 * 4) + a(5 * 32) + a(10 * 300 * 16 * 4) + a(5 * 32)
+                 + a(units * 640 * 16 * 4) + a(units * 512 * 16 * 4))
     st, n0 = _size(f, FAKE, 0, 512, FAKE, 640, FAKE, FAKE, 4, 16, None, FAKE, FAKE, FAKE, FAKE)
     assert st == OK and n0 > 0                     # T = 0 still runs the bucket and reduce passes
     assert _size(f, FAKE, 300, 512, FAKE, 640, FAKE, FAKE, 4, 12, None, FAKE, FAKE, FAKE,
