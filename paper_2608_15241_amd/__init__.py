@@ -4,7 +4,8 @@ The computation lives in liblocal.so (HIP kernels for gfx950 behind the C ABI
 of include/local.h). This package holds its sources, its build and a thin
 ctypes binding with the same names as the C entry points.
 """
-from .binding import (BLOCK_SIZE, EXPORTS, LIB_PATH, Call, KVManager, LocalError, Workspace,
+from .binding import (BLOCK_SIZE, EXPORTS, LIB_PATH, Call, KVManager, LocalError, Scheduler,
+                      Workspace,
                       load_library, local_block_version_check, local_lora_grad,
                       local_lora_grad_input, local_lora_linear,
                       local_lora_linear_grouped, local_paged_attn_decode,

@@ -33,7 +33,12 @@ EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_kvm_discard_staged", "local_kvm_versions", "local_kvm_alloc",
            "local_kvm_release", "local_kvm_lookup", "local_kvm_insert",
            "local_kvm_plan_stale_prefill", "local_kvm_path", "local_kvm_evict",
-           "local_kvm_scores", "local_kvm_stats")
+           "local_kvm_scores", "local_kvm_stats",
+           # host-side cooperative scheduler (local_sched.h)
+           "local_sched_default_params", "local_sched_create", "local_sched_destroy",
+           "local_sched_submit", "local_sched_cancel", "local_sched_next",
+           "local_sched_should_yield", "local_sched_complete", "local_sched_yield",
+           "local_sched_estimates", "local_sched_prefill_estimate", "local_sched_stats")
 
 _STATUS = {0: "LOCAL_OK", 1: "LOCAL_ERR_NULL", 2: "LOCAL_ERR_SHAPE",
            3: "LOCAL_ERR_UNSUPPORTED", 4: "LOCAL_ERR_WORKSPACE", 5: "LOCAL_ERR_HIP"}
@@ -85,6 +90,7 @@ def load_library(path: str = LIB_PATH):
     lib.local_lora_grad_input.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
                                           SZ, P]
     _declare_kvm(lib)
+    _declare_sched(lib)
     _lib = lib
     return lib
 
@@ -121,6 +127,47 @@ def _declare_kvm(lib):
         "local_kvm_evict": (ctypes.c_int, [P, i32, I32P, i32, I32P]),
         "local_kvm_scores": (ctypes.c_int, [P, i32, i32, i32, F64P, F64P, F64P, F64P]),
         "local_kvm_stats": (ctypes.c_int, [P, I32P, I32P, I32P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+
+
+class SchedParams(ctypes.Structure):
+    """local_sched_params_t (local_sched.h)."""
+    _fields_ = [(n, ctypes.c_double) for n in (
+        "alpha_judge", "alpha_train", "alpha_prefill", "reserve", "window", "delta")]
+
+
+class SchedTask(ctypes.Structure):
+    """local_sched_task_t (local_sched.h)."""
+    _fields_ = [("cls", ctypes.c_int32), ("priority", ctypes.c_int32),
+                ("adapter", ctypes.c_int32), ("version", ctypes.c_int32),
+                ("duration", ctypes.c_double), ("mem", ctypes.c_double),
+                ("max_nonyield", ctypes.c_double), ("utility", ctypes.c_double),
+                ("deadline", ctypes.c_double), ("tokens", ctypes.c_int32),
+                ("prefix_len", ctypes.c_int32)]
+
+
+def _declare_sched(lib):
+    P, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    I32P, I64P, F64P = (ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64),
+                        ctypes.POINTER(ctypes.c_double))
+    sig = {
+        "local_sched_default_params": (None, [ctypes.POINTER(SchedParams)]),
+        "local_sched_create": (ctypes.c_int, [ctypes.POINTER(SchedParams),
+                                              ctypes.POINTER(ctypes.c_void_p)]),
+        "local_sched_destroy": (None, [P]),
+        "local_sched_submit": (ctypes.c_int, [P, ctypes.POINTER(SchedTask), I64P]),
+        "local_sched_cancel": (ctypes.c_int, [P, i64]),
+        "local_sched_next": (ctypes.c_int, [P, f64, f64, i32, I32P, I64P, F64P, F64P]),
+        "local_sched_should_yield": (i32, [P]),
+        "local_sched_complete": (ctypes.c_int, [P, i64, f64]),
+        "local_sched_yield": (ctypes.c_int, [P, i64, i32]),
+        "local_sched_estimates": (ctypes.c_int, [P, i32, F64P, F64P, F64P]),
+        "local_sched_prefill_estimate": (ctypes.c_int, [P, i32, i32, F64P]),
+        "local_sched_stats": (ctypes.c_int, [P, I32P, I32P, I64P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -677,3 +724,78 @@ class KVManager:
         v = [ctypes.c_int32() for _ in range(3)]
         _check(self._lib.local_kvm_stats(self._h, *[ctypes.byref(x) for x in v]))
         return tuple(x.value for x in v)
+
+
+class Scheduler:
+    """The host-side cooperative scheduler of local_sched.h (argument
+    marshalling only). Methods take the names of the C calls without the
+    prefix; a task is given as keyword arguments of local_sched_task_t."""
+
+    FOREGROUND, JUDGE, TRAIN, PREFILL = 0, 1, 2, 3
+    RUN, BUSY, IDLE, OFFLOAD = 0, 1, 2, 3
+
+    def __init__(self, params: Optional[dict] = None):
+        lib = load_library()
+        p = SchedParams()
+        lib.local_sched_default_params(ctypes.byref(p))
+        for k, v in (params or {}).items():
+            setattr(p, k, float(v))
+        h = ctypes.c_void_p()
+        _check(lib.local_sched_create(ctypes.byref(p), ctypes.byref(h)))
+        self._lib, self._h = lib, h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.local_sched_destroy(h)
+            self._h = None
+
+    def submit(self, cls, priority=0, adapter=0, version=0, duration=-1.0, mem=0.0,
+               max_nonyield=0.0, utility=0.0, deadline=-1.0, tokens=0, prefix_len=0) -> int:
+        t = SchedTask(int(cls), int(priority), int(adapter), int(version), float(duration),
+                      float(mem), float(max_nonyield), float(utility), float(deadline),
+                      int(tokens), int(prefix_len))
+        i = ctypes.c_int64(-1)
+        _check(self._lib.local_sched_submit(self._h, ctypes.byref(t), ctypes.byref(i)))
+        return i.value
+
+    def cancel(self, task_id: int):
+        _check(self._lib.local_sched_cancel(self._h, int(task_id)))
+
+    def next(self, now: float, mem_free: float, turn_window: bool = False):
+        """(decision, task id or -1, duration estimate or -1, deficit bytes)."""
+        d, t = ctypes.c_int32(), ctypes.c_int64()
+        e, df = ctypes.c_double(), ctypes.c_double()
+        _check(self._lib.local_sched_next(self._h, float(now), float(mem_free),
+                                          1 if turn_window else 0, ctypes.byref(d),
+                                          ctypes.byref(t), ctypes.byref(e), ctypes.byref(df)))
+        return d.value, t.value, e.value, df.value
+
+    def should_yield(self) -> bool:
+        return bool(self._lib.local_sched_should_yield(self._h))
+
+    def complete(self, task_id: int, seconds: float):
+        _check(self._lib.local_sched_complete(self._h, int(task_id), float(seconds)))
+
+    def yield_(self, task_id: int, requeue: bool = True):
+        _check(self._lib.local_sched_yield(self._h, int(task_id), 1 if requeue else 0))
+
+    def estimates(self, prefix_len: int = 0):
+        """(judge EMA, training EMA, prefill rate of bucket b(prefix_len)); -1 if unset."""
+        j, t, r = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        _check(self._lib.local_sched_estimates(self._h, int(prefix_len), ctypes.byref(j),
+                                               ctypes.byref(t), ctypes.byref(r)))
+        return j.value, t.value, r.value
+
+    def prefill_estimate(self, tokens: int, prefix_len: int) -> float:
+        v = ctypes.c_double()
+        _check(self._lib.local_sched_prefill_estimate(self._h, int(tokens), int(prefix_len),
+                                                      ctypes.byref(v)))
+        return v.value
+
+    def stats(self):
+        """(queued foreground, queued background, running task id or -1)."""
+        f, b, r = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        _check(self._lib.local_sched_stats(self._h, ctypes.byref(f), ctypes.byref(b),
+                                           ctypes.byref(r)))
+        return f.value, b.value, r.value
