@@ -422,15 +422,34 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   const int nb = owned_blocks(L, a.max_blocks);
   const int np = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
   if (np == 1) return;  // written by the main kernel
-  float M = kNegBig;
+  // one pass over the partitions, 8 at a time with all their loads in flight;
+  // the running sums are rescaled when a batch raises the maximum
+  constexpr int kMergeBatch = 8;
   const float* ml = a.part_ml + static_cast<int64_t>(bh) * a.n_parts * 2;
-  for (int p = 0; p < np; ++p) M = fmaxf(M, ml[2 * p]);
-  float den = 0.f, num = 0.f;
   const float* po = a.part_o + static_cast<int64_t>(bh) * a.n_parts * D;
-  for (int p = 0; p < np; ++p) {
-    const float f = fast_exp2(ml[2 * p] - M);
-    den += ml[2 * p + 1] * f;
-    num += po[static_cast<int64_t>(p) * D + d] * f;
+  float M = kNegBig, den = 0.f, num = 0.f;
+  for (int p0 = 0; p0 < np; p0 += kMergeBatch) {
+    float2 mlv[kMergeBatch];
+    float ov[kMergeBatch];
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const bool in = p0 + q < np;
+      mlv[q] = in ? *reinterpret_cast<const float2*>(ml + 2 * (p0 + q)) : float2{kNegBig, 0.f};
+      ov[q] = in ? po[static_cast<int64_t>(p0 + q) * D + d] : 0.f;
+    }
+    float Mb = M;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) Mb = fmaxf(Mb, mlv[q].x);
+    const float c = fast_exp2(M - Mb);
+    den *= c;
+    num *= c;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const float f = fast_exp2(mlv[q].x - Mb);
+      den += mlv[q].y * f;
+      num += ov[q] * f;
+    }
+    M = Mb;
   }
   a.out[static_cast<int64_t>(bh) * D + d] = f32_to_bf16(den > 0.f ? num / den : 0.f);
   if (d == 0 && a.lse) a.lse[bh] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
