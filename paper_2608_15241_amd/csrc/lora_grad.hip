@@ -36,8 +36,6 @@ constexpr int kGrUnit = 64;      // tokens per unit of the segmented products
 constexpr int kGrThreads = 256;
 constexpr int kGrMaxAdapters = 256;
 
-constexpr int kGrCachedTokens = 8192;  // adapter indices the bucket pass keeps in LDS
-
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 size_t al256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -57,56 +55,58 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 // tokens of adapter a in ascending order; tokens without one are left out.
 // useg[a] = sum over b < a of ceil(T_b / 64): the first 64-token unit of a;
 // utab[k] = (adapter, first position in perm, token count) of unit k.
-// One workgroup: the indices are counted (8 loads in flight per thread, one
-// LDS atomic per wave and adapter, the first 8192 indices kept in LDS), then
-// the tokens are placed in passes of 256, 64 per wave, in order.
+// One workgroup of kPrepThreads: wave w owns a contiguous chunk of the
+// tokens. It counts its chunk per adapter (ballots over equal adapters),
+// then one prefix over (adapter, wave) gives every wave its own running
+// offsets, and each wave places its chunk in order with no further barrier.
+constexpr int kPrepThreads = 1024;
+constexpr int kPrepWaves = kPrepThreads / kWave;
+
 __device__ void bucket_tokens(const int32_t* __restrict__ idx, int64_t T, int n_ad,
                               int32_t* __restrict__ perm, int32_t* __restrict__ seg,
                               int32_t* __restrict__ useg, i32x4* __restrict__ utab) {
-  constexpr int kWaves = kGrThreads / kWave;
-  constexpr int kBatch = 8;  // index loads in flight per thread
-  __shared__ int base[kGrMaxAdapters];
-  __shared__ int wcnt[kWaves][kGrMaxAdapters];  // tokens per adapter in each wave of a pass
-  __shared__ int16_t cache[kGrCachedTokens];     // adapter of token t (-1: none), t < cached
+  __shared__ int cnt[kPrepWaves][kGrMaxAdapters];  // per wave: count, then running offset
+  __shared__ int tot[kGrMaxAdapters];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int64_t cached = T < kGrCachedTokens ? T : kGrCachedTokens;
-  auto adapter_of = [&](int32_t v) { return (v >= 0 && v < n_ad) ? v : -1; };
-  for (int a = tid; a < n_ad; a += kGrThreads) base[a] = 0;
-  __syncthreads();
-  for (int64_t t0 = 0; t0 < T; t0 += kBatch * kGrThreads) {
-    int my[kBatch];
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int64_t t = t0 + b * kGrThreads + tid;
-      my[b] = t < T ? adapter_of(idx[t]) : -1;
-    }
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int64_t t = t0 + b * kGrThreads + tid;
-      if (t < cached) cache[t] = static_cast<int16_t>(my[b]);
-      // one LDS atomic per (wave, adapter): equal adapters grouped by ballot
-      uint64_t pending = __ballot(my[b] >= 0);
-      while (pending) {
-        const int ad = __builtin_amdgcn_readlane(my[b], __ffsll(static_cast<long long>(pending)) - 1);
-        const uint64_t m = __ballot(my[b] == ad);
-        if (lane == 0) atomicAdd(&base[ad], __popcll(m));
-        pending &= ~m;
-      }
+  const int64_t chunk = (T + kPrepWaves * kWave - 1) / (kPrepWaves * kWave) * kWave;
+  const int64_t c0 = wave * chunk, c1 = min(T, c0 + chunk);
+  auto adapter_at = [&](int64_t t) {
+    const int32_t v = t < c1 ? idx[t] : -1;
+    return (v >= 0 && v < n_ad) ? v : -1;
+  };
+  for (int a = lane; a < n_ad; a += kWave) cnt[wave][a] = 0;
+  // 1. counts of the wave's chunk (lane 0 writes the wave's own row)
+  for (int64_t t0 = c0; t0 < c1; t0 += kWave) {
+    const int my = adapter_at(t0 + lane);
+    uint64_t pending = __ballot(my >= 0);
+    while (pending) {
+      const int ad = __builtin_amdgcn_readlane(my, __ffsll(static_cast<long long>(pending)) - 1);
+      const uint64_t m = __ballot(my == ad);
+      if (lane == 0) cnt[wave][ad] += __popcll(m);
+      pending &= ~m;
     }
   }
   __syncthreads();
-  if (wave == 0) {  // exclusive prefixes of the counts and of the unit counts
+  // 2. per adapter totals; prefixes over adapters (wave 0); each wave's
+  //    first position per adapter
+  for (int a = tid; a < n_ad; a += kPrepThreads) {
+    int c = 0;
+    for (int w = 0; w < kPrepWaves; ++w) c += cnt[w][a];
+    tot[a] = c;
+  }
+  __syncthreads();
+  if (wave == 0) {
     int run = 0, urun = 0;
     for (int a0 = 0; a0 < n_ad; a0 += kWave) {
       const int a = a0 + lane;
-      const int c = a < n_ad ? base[a] : 0;
+      const int c = a < n_ad ? tot[a] : 0;
       const int u = (c + kGrUnit - 1) / kGrUnit;
       const int ic = wave_incl_scan(c), iu = wave_incl_scan(u);
       if (a < n_ad) {
         const int s0 = run + ic - c, u0 = urun + iu - u;
         seg[a] = s0;
-        base[a] = s0;
         useg[a] = u0;
+        tot[a] = s0;
         for (int k = 0; k < u; ++k)
           utab[u0 + k] = i32x4{a, s0 + kGrUnit * k, min(kGrUnit, c - kGrUnit * k), 0};
       }
@@ -119,34 +119,27 @@ __device__ void bucket_tokens(const int32_t* __restrict__ idx, int64_t T, int n_
     }
   }
   __syncthreads();
-  for (int64_t t0 = 0; t0 < T; t0 += kGrThreads) {
-    const int64_t t = t0 + tid;
-    const int my = t < cached ? cache[t] : (t < T ? adapter_of(idx[t]) : -1);
-    for (int e = lane; e < n_ad; e += kWave) wcnt[wave][e] = 0;
-    // rank among the wave's earlier lanes of the same adapter, and the
-    // wave's count of each adapter present in it
-    int rank = 0;
+  for (int a = tid; a < n_ad; a += kPrepThreads) {
+    int off = tot[a];
+    for (int w = 0; w < kPrepWaves; ++w) {
+      const int c = cnt[w][a];
+      cnt[w][a] = off;
+      off += c;
+    }
+  }
+  __syncthreads();
+  // 3. the wave places its chunk in order
+  for (int64_t t0 = c0; t0 < c1; t0 += kWave) {
+    const int my = adapter_at(t0 + lane);
     uint64_t pending = __ballot(my >= 0);
     while (pending) {
       const int ad = __builtin_amdgcn_readlane(my, __ffsll(static_cast<long long>(pending)) - 1);
       const uint64_t m = __ballot(my == ad);
-      if (my == ad) rank = __popcll(m & ((1ull << lane) - 1ull));
-      if (lane == 0) wcnt[wave][ad] = __popcll(m);
+      const int base = cnt[wave][ad];
+      if (my == ad) perm[base + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int32_t>(t0 + lane);
+      if (lane == 0) cnt[wave][ad] = base + __popcll(m);
       pending &= ~m;
     }
-    __syncthreads();
-    if (my >= 0) {
-      int before = 0;
-      for (int w = 0; w < wave; ++w) before += wcnt[w][my];
-      perm[base[my] + before + rank] = static_cast<int32_t>(t);
-    }
-    __syncthreads();
-    for (int a2 = tid; a2 < n_ad; a2 += kGrThreads) {
-      int c = 0;
-      for (int w = 0; w < kWaves; ++w) c += wcnt[w][a2];
-      base[a2] += c;
-    }
-    __syncthreads();
   }
 }
 
@@ -176,40 +169,45 @@ TransposeJob transpose_job(const uint16_t* src, uint16_t* dst, int64_t n, int64_
   return j;
 }
 
-// Tile k of job j (tiles of matrix 0 first, then of matrix 1, ...).
-__device__ void transpose_tile(const TransposeJob& j, int k) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[4096];  // TR x (TC + 8)
+// Tile k of job j (tiles of matrix 0 first, then of matrix 1, ...), by the
+// 256 threads of quarter q of the workgroup; every thread of the workgroup
+// calls it (the barrier is shared), a quarter without a tile with live false.
+__device__ void transpose_tile(const TransposeJob& j, int k, bool live) {
+  __shared__ __attribute__((aligned(16))) uint16_t tiles[kPrepThreads / kGrThreads][4096];
+  const int q = threadIdx.x / kGrThreads;
+  uint16_t* tile = tiles[q];  // TR x (TC + 8)
   const int TR = j.TR, TC = j.TC, ld = TC + 8;
   const int per_mat = j.tiles_c * static_cast<int>((j.R + TR - 1) / TR);
-  const int64_t i = k / per_mat;
-  const int kk = k % per_mat;
+  const int64_t i = live ? k / per_mat : 0;
+  const int kk = live ? k % per_mat : 0;
   const int64_t r0 = static_cast<int64_t>(kk / j.tiles_c) * TR;
   const int64_t c0 = static_cast<int64_t>(kk % j.tiles_c) * TC;
   const uint16_t* s = j.src + i * j.R * j.C;
   uint16_t* d = j.dst + i * j.R * j.C;
-  const int e8 = threadIdx.x * 8;
-  if (e8 < TR * TC) {
+  const int e8 = (threadIdx.x % kGrThreads) * 8;
+  if (live && e8 < TR * TC) {
     const int rr = e8 / TC, cc = e8 % TC;
     if (r0 + rr < j.R && c0 + cc < j.C)
       *reinterpret_cast<u32x4*>(tile + rr * ld + cc) =
           ld_global<u32x4>(s + (r0 + rr) * j.C + c0 + cc);
   }
   __syncthreads();
-  if (e8 < TR * TC) {
+  if (live && e8 < TR * TC) {
     const int cc = e8 / TR, rr = e8 % TR;
     if (c0 + cc < j.C && r0 + rr < j.R) {
       uint32_t w[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        w[q] = static_cast<uint32_t>(tile[(rr + 2 * q) * ld + cc]) |
-               (static_cast<uint32_t>(tile[(rr + 2 * q + 1) * ld + cc]) << 16);
+      for (int h = 0; h < 4; ++h)
+        w[h] = static_cast<uint32_t>(tile[(rr + 2 * h) * ld + cc]) |
+               (static_cast<uint32_t>(tile[(rr + 2 * h + 1) * ld + cc]) << 16);
       *reinterpret_cast<u32x4*>(d + (c0 + cc) * j.R + r0 + rr) = u32x4{w[0], w[1], w[2], w[3]};
     }
   }
 }
 
-// One launch for the set-up work: workgroup 0 buckets the tokens (when
-// idx is given), the others transpose tiles of job 0, then of job 1.
+// One launch for the set-up work, workgroups of kPrepThreads: workgroup 0
+// buckets the tokens (when idx is given); each other workgroup transposes
+// four tiles (one per quarter), those of job 0, then of job 1.
 struct PrepArgs {
   TransposeJob job[2];
   int n_jobs;
@@ -220,26 +218,32 @@ struct PrepArgs {
   i32x4* utab;
 };
 
-__global__ __launch_bounds__(kGrThreads) void grad_prep_kernel(PrepArgs a) {
-  int k = blockIdx.x;
+__global__ __launch_bounds__(kPrepThreads) void grad_prep_kernel(PrepArgs a) {
+  int wg = blockIdx.x;
   if (a.idx) {
-    if (k == 0) {
+    if (wg == 0) {
       bucket_tokens(a.idx, a.T, a.n_ad, a.perm, a.seg, a.useg, a.utab);
       return;
     }
-    --k;
+    --wg;
   }
-  if (k < a.job[0].tiles) {
-    transpose_tile(a.job[0], k);
-    return;
-  }
-  k -= a.job[0].tiles;
-  if (a.n_jobs > 1 && k < a.job[1].tiles) transpose_tile(a.job[1], k);
+  const int k = wg * (kPrepThreads / kGrThreads) + threadIdx.x / kGrThreads;  // tile
+  const int t0 = a.job[0].tiles, t1 = a.n_jobs > 1 ? a.job[1].tiles : 0;
+  // the workgroup's four tiles all lie in job 0, or all past it (job 0's
+  // tile count is rounded up to whole workgroups)
+  const int t0r = (t0 + 3) / 4 * 4;
+  if (wg * 4 < t0r)
+    transpose_tile(a.job[0], k, k < t0);
+  else
+    transpose_tile(a.job[1], k - t0r, k - t0r < t1);
 }
 
 local_status_t run_prep(hipStream_t s, PrepArgs a) {
-  const int tiles = a.job[0].tiles + (a.n_jobs > 1 ? a.job[1].tiles : 0);
-  grad_prep_kernel<<<static_cast<unsigned>(tiles + (a.idx ? 1 : 0)), kGrThreads, 0, s>>>(a);
+  const int per = kPrepThreads / kGrThreads;
+  const int wgs = (a.job[0].tiles + per - 1) / per +
+                  (a.n_jobs > 1 ? (a.job[1].tiles + per - 1) / per : 0);
+  if (wgs + (a.idx ? 1 : 0) == 0) return LOCAL_OK;
+  grad_prep_kernel<<<static_cast<unsigned>(wgs + (a.idx ? 1 : 0)), kPrepThreads, 0, s>>>(a);
   return local_check_launch("lora_grad (prep)");
 }
 
