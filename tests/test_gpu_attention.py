@@ -231,3 +231,26 @@ def test_prefill_one_token_chunk_equals_decode():
     torch.cuda.synchronize()
     assert_rel(f64(out_p), f64(out_d), "prefill vs decode", tol=1e-2)
     assert_lse(lse_p.cpu().numpy(), lse_d.cpu().numpy(), "lse", tol=1e-3)
+
+
+@pytest.mark.parametrize("sm_scale", [-0.09, 0.0, 0.3])
+def test_prefill_any_sign_of_the_scale(sm_scale):
+    # any sign of the softmax scale: a negative one reverses the ranking of the
+    # keys, a zero one gives the mean of the visible values (masked positions
+    # and stale blocks stay out)
+    say("prefill scale", sm_scale)
+    rng = np.random.default_rng(int(1000 * abs(sm_scale)) + (7 if sm_scale < 0 else 5))
+    Hq, Hkv, D = 8, 2, 128
+    c = _prefill_case(rng, [0, 40, 300], [37, 130, 64], Hq, Hkv, D, 0.2)
+    kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    out, lse = lk.local_paged_attn_prefill(
+        dev_u16(c["q"]), dev(c["qi"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]),
+        dev(c["bv"]), dev(c["rv"]), sm_scale, k_new=dev_u16(c["kn"]),
+        v_new=dev_u16(c["vn"]), Hkv=Hkv)
+    torch.cuda.synchronize()
+    kc, vc = c["kc"].copy(), c["vc"].copy()
+    oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
+    ro, rl = oracle.paged_attn(c["q"], c["qi"], Hq, Hkv, D, kc, vc, c["table"], c["ctx"],
+                               c["bv"], c["rv"], sm_scale)
+    assert_rel(f64(out), ro, "out")
+    assert_lse(lse.cpu().numpy(), rl, "lse")
