@@ -106,6 +106,23 @@ __device__ __forceinline__ u32x2 buf_load8_stream(__amdgpu_buffer_rsrc_t r, uint
   return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(byte_off), 0, kCacheStream);
 }
 
+// ---------------------------------------------------------------- lanes
+// Maximum of v over lanes l and l ^ 16 (l ^ 32), by the gfx950 lane swaps of
+// the vector unit (no LDS round trip): swapping a register with itself
+// leaves each lane its own value in one result and its partner's in the
+// other, so their maximum is the pair's.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // ---------------------------------------------------------------- math
 __device__ __forceinline__ float fast_exp2(float x) {
   return __builtin_amdgcn_exp2f(x);

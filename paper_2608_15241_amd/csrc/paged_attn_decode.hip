@@ -291,7 +291,7 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
     const bool live = i >= 0;
     // the block id is the same in every lane: keep it (and the descriptors)
     // in scalar registers
-    const int p = live ? __builtin_amdgcn_readfirstlane(__shfl(my_phys, i)) : 0;
+    const int p = live ? __builtin_amdgcn_readlane(my_phys, i) : 0;
     const int64_t tile = (static_cast<int64_t>(p) * a.Hkv + g) * (kBlockSize * D);
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(a.k_cache + tile, live ? kTileBytes : 0u);
     const __amdgpu_buffer_rsrc_t rv2 = make_rsrc(a.v_cache + tile, live ? kTileBytes : 0u);
@@ -318,8 +318,7 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
     for (int e = 0; e < 4; ++e)
       s[e] = j * kBlockSize + 4 * kgrp + e < L ? sc[e] * a.scale_log2 : -INFINITY;
     float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_xor32(max_xor16(mx));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
     bf16x4 pb;

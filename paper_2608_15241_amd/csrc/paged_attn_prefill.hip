@@ -386,8 +386,7 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         float mx = sc[ct][0];
 #pragma unroll
         for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[ct][i]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx = max_xor32(max_xor16(mx));
         m_new[ct] = fmaxf(m_run[ct], mx);
       }
       // the running sums are rescaled only when some column's maximum grew
