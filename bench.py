@@ -539,14 +539,17 @@ def bench_reprefill(torch, workloads, lk, dev, n_prefix=8, prefix_blocks=64, chu
 
 
 def lora_grad_bytes(w, T):
-    """Algorithmic HBM bytes of the adapter gradients of the four projections:
-    x and dy read once (bf16), the token routing read once (int32 index and
-    fp32 scale per token and projection), every adapter's A and B read once
-    (bf16) and dA, dB written once (fp32)."""
+    """Algorithmic HBM bytes of the adapter gradients of a layer's projections:
+    the q/k/v input read once for the three (they share it) and the o input
+    once, every dy once (bf16), the token routing once per call (int32 index
+    and fp32 scale per token), every adapter's A and B read once (bf16) and
+    dA, dB written once (fp32)."""
     total = 0
     for proj in ("q", "k", "v", "o"):
         N, K = w.proj_shape(proj)
-        total += 2 * T * (K + N) + 8 * T + w.n_adapters * w.r_max * (K + N) * (2 + 4)
+        total += 2 * T * N + w.n_adapters * w.r_max * (K + N) * (2 + 4)
+    total += 2 * T * w.proj_shape("q")[1] + 2 * T * w.proj_shape("o")[1]  # the two inputs
+    total += 2 * 8 * T  # routing, once per call
     return total
 
 
@@ -562,8 +565,9 @@ def lora_grad_input_flops(w, T):
 def bench_lora_grad(torch, workloads, lk, dev, reps=20):
     """The LoRA backward of one training chunk at the prefill workload's shapes
     (2048 tokens over 4 rank-16 adapters, q/k/v/o of a 4096-wide layer): the
-    adapter gradients (HBM-bound) and the input gradient (matrix-core bound)
-    of the four projections, each timed as graph replays over two input sets."""
+    adapter gradients (HBM-bound; q, k and v share their input and run as one
+    grouped call) and the input gradient (matrix-core bound) of the four
+    projections, each timed as graph replays over two input sets."""
     from paper_2608_15241_amd.step import meta_to_device
     w = workloads.PREFILL_7B
     meta = workloads.make_meta(w, seed=0)
@@ -574,17 +578,26 @@ def bench_lora_grad(torch, workloads, lk, dev, reps=20):
         lw = workloads.make_layer_weights(w, 0, dev, seed=700 + s)
         ws = lk.Workspace(dev)
         g_calls, i_calls = [], []
-        for proj in ("q", "k", "v", "o"):
+        route = (md.token_adapter, md.token_scale)
+        # q, k, v share their input: one grouped call; o has its own
+        x_in = workloads.randn_bf16((T, w.proj_shape("q")[1]), 1.0, dev, seed=710 + 10 * s)
+        x_o = workloads.randn_bf16((T, w.proj_shape("o")[1]), 1.0, dev, seed=711 + 10 * s)
+        dys = {}
+        for i, proj in enumerate(("q", "k", "v", "o")):
             N, K = w.proj_shape(proj)
-            x = workloads.randn_bf16((T, K), 1.0, dev, seed=710 + 10 * s + len(g_calls))
-            dy = workloads.randn_bf16((T, N), 1.0, dev, seed=750 + 10 * s + len(g_calls))
+            dys[proj] = workloads.randn_bf16((T, N), 1.0, dev, seed=750 + 10 * s + i)
             Wt = lw["W_" + proj].t().contiguous()
-            keep += [x, dy, Wt]
-            args = (lw["A_" + proj], lw["B_" + proj], lw["ranks_" + proj], md.token_adapter,
-                    md.token_scale)
-            g_calls.append(lk.prepare_lora_grad(x, dy, *args, workspace=ws))
-            i_calls.append(lk.prepare_lora_grad_input(dy, Wt, *args, workspace=ws))
-        keep.append(lw)
+            keep += [dys[proj], Wt]
+            i_calls.append(lk.prepare_lora_grad_input(
+                dys[proj], Wt, lw["A_" + proj], lw["B_" + proj], lw["ranks_" + proj], *route,
+                workspace=ws))
+        qkv = ("q", "k", "v")
+        g_calls.append(lk.prepare_lora_grad_grouped(
+            x_in, [dys[n] for n in qkv], [lw["A_" + n] for n in qkv], [lw["B_" + n] for n in qkv],
+            [lw["ranks_" + n] for n in qkv], *route, workspace=ws))
+        g_calls.append(lk.prepare_lora_grad(x_o, dys["o"], lw["A_o"], lw["B_o"], lw["ranks_o"],
+                                            *route, workspace=ws))
+        keep += [lw, x_in, x_o]
         grads.append(g_calls)
         inputs.append(i_calls)
 
@@ -625,7 +638,8 @@ def bench_lora_grad(torch, workloads, lk, dev, reps=20):
     gbps = gb / (ms_g / 1e3) / 1e9
     tflops = fl / (ms_i / 1e3) / 1e12
     return {"workload": "lora_backward_7b_t%d_4x_r16" % T,
-            "adapter_grads": {"kernel": "local_lora_grad x 4 (q,k,v,o)", "bound": "hbm",
+            "adapter_grads": {"kernel": "local_lora_grad_grouped (q,k,v) + local_lora_grad (o)",
+                              "bound": "hbm",
                               "bytes_per_pass": gb, "ms_per_pass": round(ms_g, 5),
                               "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
                               "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4)},

@@ -216,6 +216,33 @@ local_status_t local_lora_grad(
     void* ws, size_t* ws_bytes, void* stream);
 
 /*
+ * local_lora_grad_grouped — adapter gradients of G (1..4) projections of the
+ * same activations, e.g. the q, k and v projections of a layer (the same
+ * passage as local_lora_grad): for every g, dA[g] and dB[g] equal what
+ * local_lora_grad computes from (x, dy[g], N[g], A[g], B[g], ranks[g]), up
+ * to float32 summation order. One call sorts the tokens once, reads x once
+ * for every u_g = x A_g^T, and runs every projection's outer products and
+ * reductions in one launch each.
+ *
+ *   dy, N, A, B, ranks, dA, dB   HOST arrays of G entries: device pointers (or,
+ *                          for N, the sizes) of each projection, with the
+ *                          layouts of local_lora_grad; ranks or an entry of
+ *                          it may be NULL (every rank = r_max). The arrays are
+ *                          read during the call only.
+ *  Sizes and errors as for local_lora_grad, for every N[g];
+ *  LOCAL_ERR_UNSUPPORTED for G outside 1..4, LOCAL_ERR_NULL for a NULL array.
+ */
+local_status_t local_lora_grad_grouped(
+    const uint16_t* x, int64_t T, int64_t K, int32_t G,
+    const uint16_t* const* dy, const int64_t* N,
+    const uint16_t* const* A, const uint16_t* const* B,
+    int32_t n_adapters, int32_t r_max,
+    const int32_t* const* ranks,
+    const int32_t* adapter_idx, const float* scale,
+    float* const* dA, float* const* dB,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
  * local_lora_grad_input — input gradient of the mixed-adapter projection
  * (the same passage as local_lora_grad):
  *

@@ -27,6 +27,7 @@ BLOCK_SIZE = 16
 EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
            "local_block_version_check", "local_lora_grad", "local_lora_grad_input",
+           "local_lora_grad_grouped",
            # host-side KV manager (local_kv.h)
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
@@ -86,6 +87,9 @@ def load_library(path: str = LIB_PATH):
     lib.local_lora_grad.restype = ctypes.c_int
     lib.local_lora_grad.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P, P, SZ,
                                     P]
+    lib.local_lora_grad_grouped.restype = ctypes.c_int
+    lib.local_lora_grad_grouped.argtypes = [P, i64, i64, i32, P, P, P, P, i32, i32, P, P, P,
+                                            P, P, P, SZ, P]
     lib.local_lora_grad_input.restype = ctypes.c_int
     lib.local_lora_grad_input.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
                                           SZ, P]
@@ -347,6 +351,57 @@ def prepare_lora_grad(x, dy, A, B, ranks, adapter_idx, scale, dA=None, dB=None,
 def local_lora_grad(*args, **kwargs):
     """(dA, dB) of the mixed-adapter projection (see prepare_lora_grad)."""
     return prepare_lora_grad(*args, **kwargs)()
+
+
+def prepare_lora_grad_grouped(x, dys, As, Bs, ranks, adapter_idx, scale, dAs=None, dBs=None,
+                              workspace: Optional[Workspace] = None) -> Call:
+    """Prepared adapter gradients of up to 4 projections of one x: returns
+    ([dA_g [n_ad, r_max, K]], [dB_g [n_ad, N_g, r_max]]) in float32."""
+    lib = load_library()
+    _req(x, "x", torch.bfloat16, 2)
+    T, K = x.shape
+    G = len(dys)
+    if not 1 <= G <= 4 or len(As) != G or len(Bs) != G:
+        raise ValueError("dys, As and Bs must have the same length, 1..4")
+    ranks = list(ranks) if ranks is not None else [None] * G
+    Ns = []
+    for g in range(G):
+        _req(dys[g], "dy", torch.bfloat16, 2)
+        if dys[g].shape[0] != T:
+            raise ValueError("dy must be [T=%d, N]" % T)
+        Ns.append(dys[g].shape[1])
+        n_ad, r_max = _adapter_checks(As[g], Bs[g], ranks[g], adapter_idx, scale, T, K, Ns[g])
+        if g and (n_ad, r_max) != (As[0].shape[0], As[0].shape[1]):
+            raise ValueError("every projection needs the same n_adapters and r_max")
+    n_ad, r_max = As[0].shape[0], As[0].shape[1]
+    dAs = dAs or [torch.empty((n_ad, r_max, K), dtype=torch.float32, device=x.device)
+                  for _ in range(G)]
+    dBs = dBs or [torch.empty((n_ad, Ns[g], r_max), dtype=torch.float32, device=x.device)
+                  for g in range(G)]
+    for g in range(G):
+        _req(dAs[g], "dA", torch.float32, 3)
+        _req(dBs[g], "dB", torch.float32, 3)
+        if tuple(dAs[g].shape) != (n_ad, r_max, K) or tuple(dBs[g].shape) != (n_ad, Ns[g], r_max):
+            raise ValueError("dA must be [n_ad, r_max, K] and dB [n_ad, N, r_max]")
+    n_arr = (ctypes.c_int64 * G)(*Ns)
+    dy_arr, dy_p = _ptr_array(dys)
+    a_arr, a_p = _ptr_array(As)
+    b_arr, b_p = _ptr_array(Bs)
+    r_arr, r_p = _ptr_array(ranks)
+    da_arr, da_p = _ptr_array(dAs)
+    db_arr, db_p = _ptr_array(dBs)
+    args = [_ptr(x), T, K, G, dy_p, ctypes.cast(n_arr, ctypes.c_void_p), a_p, b_p, n_ad, r_max,
+            r_p, _ptr(adapter_idx), _ptr(scale), da_p, db_p]
+    keep = (x, adapter_idx, scale, n_arr, dy_arr, a_arr, b_arr, r_arr, da_arr, db_arr) + \
+        tuple(dys) + tuple(As) + tuple(Bs) + tuple(ranks) + tuple(dAs) + tuple(dBs)
+    c = Call(lib.local_lora_grad_grouped, args, workspace, x.device, keep=keep)
+    c.outputs = (dAs, dBs)
+    return c
+
+
+def local_lora_grad_grouped(*args, **kwargs):
+    """Adapter gradients of up to 4 projections of one x (see prepare_lora_grad_grouped)."""
+    return prepare_lora_grad_grouped(*args, **kwargs)()
 
 
 def prepare_lora_grad_input(dy, Wt, A, B, ranks, adapter_idx, scale, out=None,

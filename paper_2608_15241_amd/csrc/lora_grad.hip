@@ -35,6 +35,8 @@ namespace {
 constexpr int kGrUnit = 64;      // tokens per unit of the segmented products
 constexpr int kGrThreads = 256;
 constexpr int kGrMaxAdapters = 256;
+constexpr int kGrGroup = 4;            // projections of one x in a call
+constexpr int kGrJobs = 2 * kGrGroup;  // (dB, dA) per projection
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
@@ -207,9 +209,9 @@ __device__ void transpose_tile(const TransposeJob& j, int k, bool live) {
 
 // One launch for the set-up work, workgroups of kPrepThreads: workgroup 0
 // buckets the tokens (when idx is given); each other workgroup transposes
-// four tiles (one per quarter), those of job 0, then of job 1.
+// four tiles (one per quarter) of one job, the jobs one after another.
 struct PrepArgs {
-  TransposeJob job[2];
+  TransposeJob job[kGrGroup];
   int n_jobs;
   const int32_t* idx;
   int64_t T;
@@ -219,6 +221,7 @@ struct PrepArgs {
 };
 
 __global__ __launch_bounds__(kPrepThreads) void grad_prep_kernel(PrepArgs a) {
+  constexpr int per = kPrepThreads / kGrThreads;
   int wg = blockIdx.x;
   if (a.idx) {
     if (wg == 0) {
@@ -227,23 +230,22 @@ __global__ __launch_bounds__(kPrepThreads) void grad_prep_kernel(PrepArgs a) {
     }
     --wg;
   }
-  const int k = wg * (kPrepThreads / kGrThreads) + threadIdx.x / kGrThreads;  // tile
-  const int t0 = a.job[0].tiles, t1 = a.n_jobs > 1 ? a.job[1].tiles : 0;
-  // the workgroup's four tiles all lie in job 0, or all past it (job 0's
-  // tile count is rounded up to whole workgroups)
-  const int t0r = (t0 + 3) / 4 * 4;
-  if (wg * 4 < t0r)
-    transpose_tile(a.job[0], k, k < t0);
-  else
-    transpose_tile(a.job[1], k - t0r, k - t0r < t1);
+  // the job of this workgroup (each job's tiles fill whole workgroups)
+  int q = 0;
+  while (q + 1 < a.n_jobs && wg >= (a.job[q].tiles + per - 1) / per) {
+    wg -= (a.job[q].tiles + per - 1) / per;
+    ++q;
+  }
+  const int k = wg * per + static_cast<int>(threadIdx.x) / kGrThreads;
+  transpose_tile(a.job[q], k, k < a.job[q].tiles);
 }
 
-local_status_t run_prep(hipStream_t s, PrepArgs a) {
-  const int per = kPrepThreads / kGrThreads;
-  const int wgs = (a.job[0].tiles + per - 1) / per +
-                  (a.n_jobs > 1 ? (a.job[1].tiles + per - 1) / per : 0);
-  if (wgs + (a.idx ? 1 : 0) == 0) return LOCAL_OK;
-  grad_prep_kernel<<<static_cast<unsigned>(wgs + (a.idx ? 1 : 0)), kPrepThreads, 0, s>>>(a);
+local_status_t run_prep(hipStream_t s, const PrepArgs& a) {
+  constexpr int per = kPrepThreads / kGrThreads;
+  int wgs = a.idx ? 1 : 0;
+  for (int q = 0; q < a.n_jobs; ++q) wgs += (a.job[q].tiles + per - 1) / per;
+  if (wgs == 0) return LOCAL_OK;
+  grad_prep_kernel<<<static_cast<unsigned>(wgs), kPrepThreads, 0, s>>>(a);
   return local_check_launch("lora_grad (prep)");
 }
 
@@ -279,9 +281,10 @@ __device__ __forceinline__ void stage_coefficients(float (*cl)[RJ], const int* t
   }
 }
 
-// ---- segmented outer products, both gradients in one launch. blockIdx.y =
-// job: 0 = dB (V = dy, P = N, coefficients s u, partials [P][r_max]),
-// 1 = dA (V = x, P = K, coefficients g = s dy B, partials [r_max][P]).
+// ---- segmented outer products, every gradient of the call in one launch.
+// blockIdx.y = job: 2g = dB of projection g (V = dy_g, P = N_g, coefficients
+// s u_g, partials [P][r_max]), 2g + 1 = dA of projection g (V = x, P = K,
+// coefficients g_g = s dy_g B_g, partials [r_max][P]).
 // Workgroup = (unit, column tile of 256 PT columns). The unit's 64 token
 // rows are loaded at once, ahead of everything else, so that a workgroup
 // waits for memory about three times (unit table, token ids, rows and
@@ -290,39 +293,41 @@ __device__ __forceinline__ void stage_coefficients(float (*cl)[RJ], const int* t
 // in order, times s_t, 0 at or past the adapter's rank. Each thread then
 // keeps PT x RJ float32 sums of c_t[j] V_t[p] over the unit's tokens.
 struct OuterArgs {
-  const uint16_t* V[2];
-  const float* S[2];  // shrink partial sums [ks][T][r_max]
-  int ks[2];
-  float* part[2];
-  int64_t P[2];
+  const uint16_t* V[kGrJobs];
+  const float* S[kGrJobs];  // shrink partial sums [ks][T][r_max]
+  int ks[kGrJobs];
+  float* part[kGrJobs];
+  int64_t P[kGrJobs];
+  const int32_t* ranks[kGrJobs];  // the projection's ranks, or NULL
 };
 
 template <int PT, int RJ>
 __global__ __launch_bounds__(kGrThreads) void grad_outer_kernel(
     OuterArgs args, int64_t T, int64_t ptiles, int r_max, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ useg, const i32x4* __restrict__ utab, int n_ad,
-    const int32_t* __restrict__ ranks, const float* __restrict__ scale) {
+    const float* __restrict__ scale) {
   using RowT = typename std::conditional<PT == 2, uint32_t, uint16_t>::type;
   __shared__ __attribute__((aligned(16))) float cl[kGrUnit][RJ];
   __shared__ int tok[kGrUnit];
   __shared__ float tsc[kGrUnit];
   const int job = blockIdx.y;
-  const int64_t P = job ? args.P[1] : args.P[0];
+  const int64_t P = args.P[job];
   const int slot = static_cast<int>(blockIdx.x / ptiles);
   const int64_t p0 = ((blockIdx.x % ptiles) * kGrThreads + threadIdx.x) * PT;
   if ((blockIdx.x % ptiles) * kGrThreads * PT >= P) return;  // the whole tile is past P
   if (slot >= useg[n_ad]) return;                             // past the last unit
   const i32x4 ut = utab[slot];
   const int a = ut.x, first = ut.y, nt = ut.z;
-  const uint16_t* V = job ? args.V[1] : args.V[0];
-  const float* S = job ? args.S[1] : args.S[0];
-  const int ks = job ? args.ks[1] : args.ks[0];
+  const uint16_t* V = args.V[job];
+  const float* S = args.S[job];
+  const int ks = args.ks[job];
   const int tid = threadIdx.x;
   if (tid < nt) {
     const int t = perm[first + tid];
     tok[tid] = t;
     tsc[tid] = scale[t];
   }
+  const int32_t* ranks = args.ranks[job];
   const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
   __syncthreads();
   // every row of the unit in flight at once (rows past nt read as zero)
@@ -362,8 +367,8 @@ __global__ __launch_bounds__(kGrThreads) void grad_outer_kernel(
     }
   }
   if (!live) return;
-  float* out = (job ? args.part[1] : args.part[0]) + static_cast<int64_t>(slot) * P * r_max;
-  if (job) {
+  float* out = args.part[job] + static_cast<int64_t>(slot) * P * r_max;
+  if (job & 1) {
 #pragma unroll
     for (int q = 0; q < PT; ++q)
 #pragma unroll
@@ -394,14 +399,14 @@ template <int JT>
 __global__ __launch_bounds__(kGrThreads) void grad_outer_mfma_kernel(
     OuterArgs args, int64_t T, int64_t ptiles, int r_max, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ useg, const i32x4* __restrict__ utab, int n_ad,
-    const int32_t* __restrict__ ranks, const float* __restrict__ scale) {
+    const float* __restrict__ scale) {
   constexpr int RJ = 16 * JT;
   constexpr int kSteps = kGrUnit / 4;
   __shared__ __attribute__((aligned(16))) float cl[kGrUnit][RJ];
   __shared__ int tok[kGrUnit];
   __shared__ float tsc[kGrUnit];
   const int job = blockIdx.y;
-  const int64_t P = job ? args.P[1] : args.P[0];
+  const int64_t P = args.P[job];
   const int slot = static_cast<int>(blockIdx.x / ptiles);
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
   const int64_t wcol = ((blockIdx.x % ptiles) * (kGrThreads / kWave) + wave) * 128;
@@ -409,14 +414,15 @@ __global__ __launch_bounds__(kGrThreads) void grad_outer_mfma_kernel(
   if (slot >= useg[n_ad]) return;                // past the last unit
   const i32x4 ut = utab[slot];
   const int a = ut.x, first = ut.y, nt = ut.z;
-  const uint16_t* V = job ? args.V[1] : args.V[0];
-  const float* S = job ? args.S[1] : args.S[0];
-  const int ks = job ? args.ks[1] : args.ks[0];
+  const uint16_t* V = args.V[job];
+  const float* S = args.S[job];
+  const int ks = args.ks[job];
   if (tid < nt) {
     const int t = perm[first + tid];
     tok[tid] = t;
     tsc[tid] = scale[t];
   }
+  const int32_t* ranks = args.ranks[job];
   const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
   __syncthreads();
   const int n = lane % 16, k = lane / 16;
@@ -453,12 +459,12 @@ __global__ __launch_bounds__(kGrThreads) void grad_outer_mfma_kernel(
     }
   }
   if (!live) return;
-  float* out = (job ? args.part[1] : args.part[0]) + static_cast<int64_t>(slot) * P * r_max;
+  float* out = args.part[job] + static_cast<int64_t>(slot) * P * r_max;
 #pragma unroll
   for (int jt = 0; jt < JT; ++jt) {
     const int j0 = 16 * jt + 4 * k;  // this lane's rows j0 .. j0 + 3
     if (j0 >= r_max) continue;
-    if (job) {  // [r_max][P]: 8 consecutive columns per row
+    if (job & 1) {  // [r_max][P]: 8 consecutive columns per row
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float* o = out + static_cast<int64_t>(j0 + i) * P + col;
@@ -479,23 +485,24 @@ __global__ __launch_bounds__(kGrThreads) void grad_outer_mfma_kernel(
 // order, for e < E = P * r_max; 0 for an adapter without tokens and at or
 // past its rank. blockIdx.z = job as for the outer products.
 struct ReduceArgs {
-  const float* part[2];
-  float* out[2];
-  int64_t P[2];
+  const float* part[kGrJobs];
+  float* out[kGrJobs];
+  int64_t P[kGrJobs];
+  const int32_t* ranks[kGrJobs];
 };
 
 __global__ __launch_bounds__(kGrThreads) void grad_reduce_kernel(
-    ReduceArgs args, int r_max, const int32_t* __restrict__ useg,
-    const int32_t* __restrict__ ranks) {
+    ReduceArgs args, int r_max, const int32_t* __restrict__ useg) {
   const int job = blockIdx.z;
   const int a = blockIdx.y;
-  const int64_t P = job ? args.P[1] : args.P[0];
+  const int64_t P = args.P[job];
   const int64_t E = P * r_max;
   const int64_t e = (static_cast<int64_t>(blockIdx.x) * kGrThreads + threadIdx.x) * 4;
   if (e >= E) return;
   const int u0 = useg[a], nu = useg[a + 1] - u0;
+  const int32_t* ranks = args.ranks[job];
   const int rk = ranks ? min(max(ranks[a], 0), r_max) : r_max;
-  const float* part = job ? args.part[1] : args.part[0];
+  const float* part = args.part[job];
   f32x4 sum{0.f, 0.f, 0.f, 0.f};
   int u = 0;
   for (; u + 4 <= nu; u += 4) {  // four loads in flight, added in unit order
@@ -510,21 +517,21 @@ __global__ __launch_bounds__(kGrThreads) void grad_reduce_kernel(
     sum += *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(u0 + u) * E + e);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int j = job ? static_cast<int>((e + q) / P) : static_cast<int>((e + q) % r_max);
+    const int j = (job & 1) ? static_cast<int>((e + q) / P) : static_cast<int>((e + q) % r_max);
     if (j >= rk) sum[q] = 0.f;
   }
-  *reinterpret_cast<f32x4*>((job ? args.out[1] : args.out[0]) + static_cast<int64_t>(a) * E + e) =
-      sum;
+  *reinterpret_cast<f32x4*>(args.out[job] + static_cast<int64_t>(a) * E + e) = sum;
 }
 
-local_status_t launch_outer(const OuterArgs& o, int64_t T, int r_max, const int32_t* perm,
-                            const int32_t* useg, const i32x4* utab, int n_ad, int64_t units,
-                            const int32_t* ranks, const float* scale, hipStream_t s) {
-  const int64_t pmax = std::max(o.P[0], o.P[1]);
+local_status_t launch_outer(const OuterArgs& o, int n_jobs, int64_t T, int r_max,
+                            const int32_t* perm, const int32_t* useg, const i32x4* utab,
+                            int n_ad, int64_t units, const float* scale, hipStream_t s) {
+  int64_t pmax = 0;
+  for (int q = 0; q < n_jobs; ++q) pmax = std::max(pmax, o.P[q]);
   auto go = [&](auto kernel, int64_t cols_per_wg) {
     const int64_t ptiles = (pmax + cols_per_wg - 1) / cols_per_wg;
-    kernel<<<dim3(static_cast<unsigned>(units * ptiles), 2), kGrThreads, 0, s>>>(
-        o, T, ptiles, r_max, perm, useg, utab, n_ad, ranks, scale);
+    kernel<<<dim3(static_cast<unsigned>(units * ptiles), static_cast<unsigned>(n_jobs)),
+             kGrThreads, 0, s>>>(o, T, ptiles, r_max, perm, useg, utab, n_ad, scale);
     return local_check_launch("lora_grad (outer)");
   };
   if (r_max <= 16) return go(grad_outer_mfma_kernel<1>, 512);
@@ -551,56 +558,76 @@ local_status_t grad_checks(const char* who, int64_t T, int64_t K, int64_t N, int
 
 using namespace localk;
 
-extern "C" local_status_t local_lora_grad(
-    const uint16_t* x, int64_t T, int64_t K, const uint16_t* dy, int64_t N, const uint16_t* A,
-    const uint16_t* B, int32_t n_adapters, int32_t r_max, const int32_t* ranks,
-    const int32_t* adapter_idx, const float* scale, float* dA, float* dB, void* ws,
-    size_t* ws_bytes, void* stream) {
-  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "lora_grad: ws_bytes is NULL");
-  local_status_t st = grad_checks("lora_grad", T, K, N, n_adapters, r_max);
-  if (st != LOCAL_OK) return st;
+namespace localk {
+namespace {
+
+// Adapter gradients of G projections that share x (and the routing).
+local_status_t grad_impl(const char* who, const uint16_t* x, int64_t T, int64_t K, int G,
+                         const uint16_t* const* dy, const int64_t* N, const uint16_t* const* A,
+                         const uint16_t* const* B, int32_t n_adapters, int32_t r_max,
+                         const int32_t* const* ranks, const int32_t* adapter_idx,
+                         const float* scale, float* const* dA, float* const* dB, void* ws,
+                         size_t* ws_bytes, hipStream_t s) {
+  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "%s: ws_bytes is NULL", who);
+  if (G < 1 || G > kGrGroup)
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "%s: G=%d (need 1..%d)", who, G, kGrGroup);
+  local_status_t st;
+  for (int g = 0; g < G; ++g)
+    if ((st = grad_checks(who, T, K, N[g], n_adapters, r_max)) != LOCAL_OK) return st;
   const int64_t Tw = T > 0 ? T : 1;
   const int64_t units = Tw / kGrUnit + n_adapters;  // >= sum over adapters of ceil(T_a / 64)
-  int ks_x = 0, ks_dy = 0;
-  const size_t sh_x = token_shrink_bytes(Tw, K, r_max, &ks_x);
-  const size_t sh_dy = token_shrink_bytes(Tw, N, r_max, &ks_dy);
-  // workspace: token order, adapter offsets, unit offsets, unit table, B^T, the two
-  // shrinks' partial sums, the two partial products
-  const size_t o_perm = 0;
-  const size_t o_seg = o_perm + al256(static_cast<size_t>(Tw) * 4);
-  const size_t o_useg = o_seg + al256(static_cast<size_t>(n_adapters + 1) * 4);
-  const size_t o_utab = o_useg + al256(static_cast<size_t>(n_adapters + 1) * 4);
-  const size_t o_bt = o_utab + al256(static_cast<size_t>(units) * 16);
-  const size_t o_shx = o_bt + al256(static_cast<size_t>(n_adapters) * r_max * N * 2);
-  const size_t o_shy = o_shx + sh_x;
-  const size_t o_pb = o_shy + sh_dy;
-  const size_t o_pa = o_pb + al256(static_cast<size_t>(units) * N * r_max * 4);
-  const size_t need = o_pa + al256(static_cast<size_t>(units) * K * r_max * 4);
+  int ks_x = 0, ks_dy[kGrGroup] = {};
+  const size_t sh_x = token_shrink_bytes(Tw, K, r_max, G, &ks_x);
+  // workspace: token order, adapter offsets, unit offsets, unit table, B_g^T,
+  // the shrinks' partial sums (x against every A_g, dy_g against B_g^T), the
+  // partial products of every job
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += al256(bytes);
+    return at;
+  };
+  const size_t o_perm = take(static_cast<size_t>(Tw) * 4);
+  const size_t o_seg = take(static_cast<size_t>(n_adapters + 1) * 4);
+  const size_t o_useg = take(static_cast<size_t>(n_adapters + 1) * 4);
+  const size_t o_utab = take(static_cast<size_t>(units) * 16);
+  size_t o_bt[kGrGroup], o_shy[kGrGroup], o_pb[kGrGroup], o_pa[kGrGroup];
+  for (int g = 0; g < G; ++g) o_bt[g] = take(static_cast<size_t>(n_adapters) * r_max * N[g] * 2);
+  const size_t o_shx = take(sh_x);
+  for (int g = 0; g < G; ++g) o_shy[g] = take(token_shrink_bytes(Tw, N[g], r_max, 1, &ks_dy[g]));
+  for (int g = 0; g < G; ++g) {
+    o_pb[g] = take(static_cast<size_t>(units) * N[g] * r_max * 4);
+    o_pa[g] = take(static_cast<size_t>(units) * K * r_max * 4);
+  }
   if (!ws) {
-    *ws_bytes = need;
+    *ws_bytes = o;
     return LOCAL_OK;
   }
-  if (*ws_bytes < need)
-    return local_fail(LOCAL_ERR_WORKSPACE, "lora_grad: workspace %zu < %zu", *ws_bytes, need);
-  if (!dA || !dB) return local_fail(LOCAL_ERR_NULL, "lora_grad: NULL output");
-  if (T > 0 && (!x || !dy || !A || !B || !adapter_idx || !scale))
-    return local_fail(LOCAL_ERR_NULL, "lora_grad: NULL pointer argument");
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (*ws_bytes < o)
+    return local_fail(LOCAL_ERR_WORKSPACE, "%s: workspace %zu < %zu", who, *ws_bytes, o);
+  for (int g = 0; g < G; ++g) {
+    if (!dA[g] || !dB[g]) return local_fail(LOCAL_ERR_NULL, "%s: NULL output", who);
+    if (T > 0 && (!dy[g] || !A[g] || !B[g]))
+      return local_fail(LOCAL_ERR_NULL, "%s: NULL pointer argument", who);
+  }
+  if (T > 0 && (!x || !adapter_idx || !scale))
+    return local_fail(LOCAL_ERR_NULL, "%s: NULL pointer argument", who);
   char* w = static_cast<char*>(ws);
   int32_t* perm = reinterpret_cast<int32_t*>(w + o_perm);
   int32_t* seg = reinterpret_cast<int32_t*>(w + o_seg);
   int32_t* useg = reinterpret_cast<int32_t*>(w + o_useg);
   i32x4* utab = reinterpret_cast<i32x4*>(w + o_utab);
-  uint16_t* Bt = reinterpret_cast<uint16_t*>(w + o_bt);
-  float* pb = reinterpret_cast<float*>(w + o_pb);
-  float* pa = reinterpret_cast<float*>(w + o_pa);
-  // tokens bucketed by adapter and B transposed per adapter to [r_max][N],
-  // in one launch. T = 0: every adapter is empty and the reduce pass writes
-  // zero gradients (no memset: the call stays capturable)
+  const uint16_t* Bt[kGrGroup];
+  // tokens bucketed by adapter and every B_g transposed per adapter to
+  // [r_max][N_g], in one launch. T = 0: every adapter is empty and the
+  // reduce pass writes zero gradients (no memset: the call stays capturable)
   PrepArgs pr{};
-  pr.job[0] = transpose_job(B, Bt, n_adapters, N, r_max);
-  pr.n_jobs = T > 0 ? 1 : 0;
-  if (T == 0) pr.job[0].tiles = 0;
+  pr.n_jobs = T > 0 ? G : 0;
+  for (int g = 0; g < G; ++g) {
+    uint16_t* bt = reinterpret_cast<uint16_t*>(w + o_bt[g]);
+    Bt[g] = bt;
+    if (T > 0) pr.job[g] = transpose_job(B[g], bt, n_adapters, N[g], r_max);
+  }
   pr.idx = adapter_idx ? adapter_idx : reinterpret_cast<const int32_t*>(w);  // not read if T = 0
   pr.T = T;
   pr.n_ad = n_adapters;
@@ -610,30 +637,82 @@ extern "C" local_status_t local_lora_grad(
   pr.utab = utab;
   if ((st = run_prep(s, pr)) != LOCAL_OK) return st;
   if (T > 0) {
-    // u = x A^T and dy B as the shrink's K-slice partial sums
-    if ((st = token_shrink(x, T, K, A, n_adapters, r_max, adapter_idx, w + o_shx, s)) != LOCAL_OK)
-      return st;
-    if ((st = token_shrink(dy, T, N, Bt, n_adapters, r_max, adapter_idx, w + o_shy, s)) !=
+    // u_g = x A_g^T for every g in one pass over x, then dy_g B_g for each g,
+    // as the shrink's K-slice partial sums
+    if ((st = token_shrink(x, T, K, G, A, n_adapters, r_max, adapter_idx, w + o_shx, s)) !=
         LOCAL_OK)
       return st;
-    // dB partials from (dy, s u), dA partials from (x, s dy B)
-    const OuterArgs oa{{dy, x},
-                       {reinterpret_cast<const float*>(w + o_shx),
-                        reinterpret_cast<const float*>(w + o_shy)},
-                       {ks_x, ks_dy},
-                       {pb, pa},
-                       {N, K}};
-    if ((st = launch_outer(oa, T, r_max, perm, useg, utab, n_adapters, units, ranks, scale, s)) !=
+    for (int g = 0; g < G; ++g)
+      if ((st = token_shrink(dy[g], T, N[g], 1, &Bt[g], n_adapters, r_max, adapter_idx,
+                             w + o_shy[g], s)) != LOCAL_OK)
+        return st;
+    // dB_g partials from (dy_g, s u_g), dA_g partials from (x, s dy_g B_g)
+    OuterArgs oa{};
+    for (int g = 0; g < G; ++g) {
+      const int32_t* rg = ranks ? ranks[g] : nullptr;
+      oa.V[2 * g] = dy[g];
+      oa.S[2 * g] = reinterpret_cast<const float*>(w + o_shx) +
+                    static_cast<int64_t>(g) * ks_x * T * r_max;
+      oa.ks[2 * g] = ks_x;
+      oa.part[2 * g] = reinterpret_cast<float*>(w + o_pb[g]);
+      oa.P[2 * g] = N[g];
+      oa.ranks[2 * g] = rg;
+      oa.V[2 * g + 1] = x;
+      oa.S[2 * g + 1] = reinterpret_cast<const float*>(w + o_shy[g]);
+      oa.ks[2 * g + 1] = ks_dy[g];
+      oa.part[2 * g + 1] = reinterpret_cast<float*>(w + o_pa[g]);
+      oa.P[2 * g + 1] = K;
+      oa.ranks[2 * g + 1] = rg;
+    }
+    if ((st = launch_outer(oa, 2 * G, T, r_max, perm, useg, utab, n_adapters, units, scale, s)) !=
         LOCAL_OK)
       return st;
   }
-  // dB [n_ad][N][r_max], dA [n_ad][r_max][K]
-  const ReduceArgs ra{{pb, pa}, {dB, dA}, {N, K}};
-  const int64_t emax = std::max(N, K) * r_max;
+  // dB_g [n_ad][N_g][r_max], dA_g [n_ad][r_max][K]
+  ReduceArgs ra{};
+  int64_t emax = 0;
+  for (int g = 0; g < G; ++g) {
+    const int32_t* rg = ranks ? ranks[g] : nullptr;
+    ra.part[2 * g] = reinterpret_cast<const float*>(w + o_pb[g]);
+    ra.out[2 * g] = dB[g];
+    ra.P[2 * g] = N[g];
+    ra.ranks[2 * g] = rg;
+    ra.part[2 * g + 1] = reinterpret_cast<const float*>(w + o_pa[g]);
+    ra.out[2 * g + 1] = dA[g];
+    ra.P[2 * g + 1] = K;
+    ra.ranks[2 * g + 1] = rg;
+    emax = std::max(emax, std::max(N[g], K) * r_max);
+  }
   grad_reduce_kernel<<<dim3(static_cast<unsigned>((emax / 4 + kGrThreads - 1) / kGrThreads),
-                            static_cast<unsigned>(n_adapters), 2),
-                       kGrThreads, 0, s>>>(ra, r_max, useg, ranks);
+                            static_cast<unsigned>(n_adapters), static_cast<unsigned>(2 * G)),
+                       kGrThreads, 0, s>>>(ra, r_max, useg);
   return local_check_launch("lora_grad (reduce)");
+}
+
+}  // namespace
+}  // namespace localk
+
+extern "C" local_status_t local_lora_grad(
+    const uint16_t* x, int64_t T, int64_t K, const uint16_t* dy, int64_t N, const uint16_t* A,
+    const uint16_t* B, int32_t n_adapters, int32_t r_max, const int32_t* ranks,
+    const int32_t* adapter_idx, const float* scale, float* dA, float* dB, void* ws,
+    size_t* ws_bytes, void* stream) {
+  return grad_impl("lora_grad", x, T, K, 1, &dy, &N, &A, &B, n_adapters, r_max, &ranks,
+                   adapter_idx, scale, &dA, &dB, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+extern "C" local_status_t local_lora_grad_grouped(
+    const uint16_t* x, int64_t T, int64_t K, int32_t G, const uint16_t* const* dy,
+    const int64_t* N, const uint16_t* const* A, const uint16_t* const* B, int32_t n_adapters,
+    int32_t r_max, const int32_t* const* ranks, const int32_t* adapter_idx, const float* scale,
+    float* const* dA, float* const* dB, void* ws, size_t* ws_bytes, void* stream) {
+  if (G < 1 || G > kGrGroup)
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "lora_grad_grouped: G=%d (need 1..%d)", G,
+                      kGrGroup);
+  if (!dy || !N || !A || !B || !dA || !dB)
+    return local_fail(LOCAL_ERR_NULL, "lora_grad_grouped: NULL argument array");
+  return grad_impl("lora_grad_grouped", x, T, K, G, dy, N, A, B, n_adapters, r_max, ranks,
+                   adapter_idx, scale, dA, dB, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
 extern "C" local_status_t local_lora_grad_input(

@@ -1525,16 +1525,17 @@ local_status_t check_args(const char* who, const uint16_t* x, int64_t T, int64_t
 }  // namespace
 
 // ---- the long-chunk shrink for other files (declared in lora_internal.hpp)
-size_t token_shrink_bytes(int64_t T, int64_t K, int r_max, int* slices) {
-  const ShrinkShape sh = shrink_shape(T, K, r_max, 1);
+size_t token_shrink_bytes(int64_t T, int64_t K, int r_max, int G, int* slices) {
+  const ShrinkShape sh = shrink_shape(T, K, r_max, G);
   if (slices) *slices = sh.ks;
-  return align256(static_cast<size_t>(sh.ks) * T * r_max * sizeof(float)) +
+  return align256(static_cast<size_t>(G) * sh.ks * T * r_max * sizeof(float)) +
          align256(static_cast<size_t>((T + 63) / 64) * 4 * sizeof(uint64_t));
 }
 
-local_status_t token_shrink(const uint16_t* x, int64_t T, int64_t K, const uint16_t* A,
-                            int n_ad, int r_max, const int32_t* idx, void* ws, hipStream_t s) {
-  const ShrinkShape sh = shrink_shape(T, K, r_max, 1);
+local_status_t token_shrink(const uint16_t* x, int64_t T, int64_t K, int G,
+                            const uint16_t* const* A, int n_ad, int r_max, const int32_t* idx,
+                            void* ws, hipStream_t s) {
+  const ShrinkShape sh = shrink_shape(T, K, r_max, G);
   GemmArgs g{};
   g.x = x;
   g.T = T;
@@ -1543,12 +1544,13 @@ local_status_t token_shrink(const uint16_t* x, int64_t T, int64_t K, const uint1
   g.n_ad = n_ad;
   g.r_max = r_max;
   g.R = n_ad * r_max;
-  g.G = 1;
-  g.ga[0] = A;
+  g.G = G;
+  for (int q = 0; q < G; ++q) g.ga[q] = A[q];
   g.pout = static_cast<float*>(ws);
   g.up_ks = sh.ks;
   g.tile_present = reinterpret_cast<uint64_t*>(
-      static_cast<char*>(ws) + align256(static_cast<size_t>(sh.ks) * T * r_max * sizeof(float)));
+      static_cast<char*>(ws) +
+      align256(static_cast<size_t>(G) * sh.ks * T * r_max * sizeof(float)));
   return launch_shrink_long(g, sh, s);
 }
 

@@ -153,3 +153,37 @@ def test_full_size_projection():
         assert_rel(f64(dB[a]), rB[a], "dB[%d]" % a)
     dx = _grad_input(dy, W, A, B, rk, idx, scale)
     assert_rel(f64(dx), rdx, "dx")
+
+
+@pytest.mark.parametrize("T,Ns,ranks", [
+    (300, (512, 128, 128), ([16, 3, 9, 0], [16, 16, 16, 16], None)),
+    (1000, (256, 256, 384, 128), ([16, 8, 1, 12], None, [4, 4, 16, 2], [16, 16, 16, 16])),
+    (0, (256, 128), (None, None)),
+], ids=["qkv", "four", "empty"])
+def test_grouped_matches_oracle(T, Ns, ranks):
+    # q/k/v-like projections of one x: each projection against the oracle
+    say("lora_grad grouped", T, Ns)
+    rng = np.random.default_rng(T + sum(Ns))
+    K, n_ad, r_max = 512, 4, 16
+    x = rand_bf16(rng, (T, K))
+    idx = rng.integers(0, n_ad, size=T).astype(np.int32)
+    idx[rng.random(T) < 0.15] = -1
+    scale = rng.uniform(0.5, 2.5, size=T).astype(np.float32)
+    dys, As, Bs, rks, Ws = [], [], [], [], []
+    for g, N in enumerate(Ns):
+        rk = ranks[g] if ranks[g] is not None else [r_max] * n_ad
+        _, dy, W, A, B, r, _, _ = _inputs(rng, T, K, N, n_ad, r_max, rk)
+        dys.append(dy), As.append(A), Bs.append(B), rks.append(r), Ws.append(W)
+    dev_r = [dev(rks[g]) if ranks[g] is not None else None for g in range(len(Ns))]
+    dAs, dBs = lk.local_lora_grad_grouped(dev_u16(x), [dev_u16(d) for d in dys],
+                                          [dev_u16(a) for a in As], [dev_u16(b) for b in Bs],
+                                          dev_r, dev(idx), dev(scale, torch.float32))
+    torch.cuda.synchronize()
+    for g in range(len(Ns)):
+        rA, rB, _ = lora_grad(x, dys[g], Ws[g], As[g], Bs[g], rks[g], idx, scale)
+        for a in range(n_ad):
+            if np.any(idx == a) and rks[g][a] > 0:
+                assert_rel(f64(dAs[g][a]), rA[a], "dA[%d][%d]" % (g, a))
+                assert_rel(f64(dBs[g][a]), rB[a], "dB[%d][%d]" % (g, a))
+            else:
+                assert not f64(dAs[g][a]).any() and not f64(dBs[g][a]).any(), (g, a)

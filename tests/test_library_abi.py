@@ -208,3 +208,24 @@ def test_lora_grad_workspace_and_errors(lib):
     assert m == a(4 * 16 * 640 * 2) + a(4 * 512 * 16 * 2) + fw
     assert g(FAKE, 300, 640, FAKE, 512, FAKE, FAKE, 4, 16, None, FAKE, FAKE, None, FAKE,
              ctypes.byref(big), None) == ERR_NULL
+
+
+def test_lora_grad_grouped_workspace_and_errors(lib):
+    f = lib.local_lora_grad_grouped
+    P = ctypes.c_void_p
+    ptrs = lambda n: (P * n)(*([FAKE] * n))
+    Ns = (ctypes.c_int64 * 3)(4096, 1024, 1024)
+    st, n = _size(f, FAKE, 2048, 4096, 3, ptrs(3), Ns, ptrs(3), ptrs(3), 4, 16, None, FAKE,
+                  FAKE, ptrs(3), ptrs(3))
+    assert st == OK
+    # at least the three projections' partial products (units x (N_g + K) x r_max fp32)
+    units = 2048 // 64 + 4
+    assert n > units * (4096 + 1024 + 1024 + 3 * 4096) * 16 * 4
+    assert _size(f, FAKE, 2048, 4096, 5, ptrs(5), Ns, ptrs(5), ptrs(5), 4, 16, None, FAKE,
+                 FAKE, ptrs(5), ptrs(5))[0] == ERR_UNSUPPORTED
+    assert _size(f, FAKE, 2048, 4096, 3, None, Ns, ptrs(3), ptrs(3), 4, 16, None, FAKE,
+                 FAKE, ptrs(3), ptrs(3))[0] == ERR_NULL
+    bad = (ctypes.c_int64 * 3)(4096, 100, 1024)
+    assert _size(f, FAKE, 2048, 4096, 3, ptrs(3), bad, ptrs(3), ptrs(3), 4, 16, None, FAKE,
+                 FAKE, ptrs(3), ptrs(3))[0] == ERR_UNSUPPORTED
+    assert b"lora_grad_grouped" in lib.local_last_error()
