@@ -11,7 +11,11 @@
  *   - attention over a paged KV cache whose blocks carry the adapter version
  *     that produced them, so that KV written under another version is rejected
  *     (§1 challenge (2) and §5.1: the adapter and its version are part of the
- *     validity key kappa; §3: a publish stales only KV owned by that adapter).
+ *     validity key kappa; §3: a publish stales only KV owned by that adapter);
+ *  and the backward of the projection for the training chunks that produce
+ *  new adapter versions (adapter gradients and the input gradient).
+ *  The host-side KV manager and cooperative scheduler have C ABIs of their
+ *  own (local_kv.h, local_sched.h) in the same library.
  *
  * Conventions shared by every entry point
  * ---------------------------------------

@@ -23,4 +23,4 @@ local_status_t local_check_launch(const char* what) {
 
 extern "C" const char* local_last_error(void) { return g_last_error; }
 
-extern "C" int32_t local_version(void) { return 100; }  // 0.1.0
+extern "C" int32_t local_version(void) { return 200; }  // 0.2.0
