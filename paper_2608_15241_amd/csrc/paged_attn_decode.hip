@@ -454,6 +454,12 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   if (d == 0 && a.lse) a.lse[bh] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
 }
 
+// Blocks in flight per wave: 4 with one query head per KV head, 3 with
+// grouped heads (measured: 4 is 1.7% faster on the MHA decode step and 1.2%
+// slower on the GQA one, whose waves do four heads' softmax per block).
+#ifndef LOCAL_DECODE_DEPTH_MHA
+#define LOCAL_DECODE_DEPTH_MHA 4
+#endif
 #ifndef LOCAL_DECODE_DEPTH
 #define LOCAL_DECODE_DEPTH 3
 #endif
@@ -464,12 +470,19 @@ local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
   if (wgs >= (1LL << 31))
     return local_fail(LOCAL_ERR_UNSUPPORTED, "paged_attn_decode: grid of %lld workgroups",
                       (long long)wgs);
-  if (B <= kRankChunks * kWave)
-    decode_attn_kernel<D, LOCAL_DECODE_DEPTH, true><<<static_cast<unsigned>(wgs), kWave, 0, s>>>(
-        a, B);
-  else
-    decode_attn_kernel<D, LOCAL_DECODE_DEPTH, false><<<static_cast<unsigned>(wgs), kWave, 0, s>>>(
-        a, B);
+  const unsigned grid = static_cast<unsigned>(wgs);
+  const bool ranked = B <= kRankChunks * kWave;
+  if (a.group == 1) {
+    if (ranked)
+      decode_attn_kernel<D, LOCAL_DECODE_DEPTH_MHA, true><<<grid, kWave, 0, s>>>(a, B);
+    else
+      decode_attn_kernel<D, LOCAL_DECODE_DEPTH_MHA, false><<<grid, kWave, 0, s>>>(a, B);
+  } else {
+    if (ranked)
+      decode_attn_kernel<D, LOCAL_DECODE_DEPTH, true><<<grid, kWave, 0, s>>>(a, B);
+    else
+      decode_attn_kernel<D, LOCAL_DECODE_DEPTH, false><<<grid, kWave, 0, s>>>(a, B);
+  }
   if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
   return local_check_launch("paged_attn_decode");
 }
