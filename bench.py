@@ -157,8 +157,8 @@ def prefill_gemm_flops(w, meta):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; --gpus %d is not supported "
-              "(multi-GPU sharding is described in DESIGN.md, not built)" % args.gpus,
+        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
+              "(sharding across GPUs is not implemented)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
     import torch

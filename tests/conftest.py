@@ -16,7 +16,7 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run in one process on the GPU machine. Without a GPU they are
+    # GPU tests run in one process on a machine with the GPU. Without one they are
     # skipped only when -m selects them anyway, so `-m "not gpu"` stays clean.
     try:
         import torch
