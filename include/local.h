@@ -325,7 +325,8 @@ local_status_t local_paged_attn_decode(
  * prefill runs this same computation under a staged version).
  *
  *  Request b owns query rows [q_indptr[b], q_indptr[b+1]) (n_b rows; a
- *  request whose range is not inside [0, T] is skipped) and has
+ *  request whose range is reversed or not inside [0, T] is skipped whole:
+ *  nothing of its chunk is appended and none of its rows is written) and has
  *  ctx_lens[b] = P_b + n_b tokens after the chunk, P_b its cached prefix.
  *  When k_new/v_new are given, row t of the chunk is first written at logical
  *  position P_b + (t - q_indptr[b]). Query row i of request b (position

@@ -514,13 +514,32 @@ def _pool_checks(k_cache, v_cache, Hkv, D):
     return k_cache.numel() // per_block
 
 
-def _meta_checks(block_table, ctx_lens, block_version, req_version, B):
+def _meta_checks(block_table, ctx_lens, block_version, req_version, B,
+                 num_blocks: Optional[int] = None):
     _req(block_table, "block_table", torch.int32, 2)
     _req(ctx_lens, "ctx_lens", torch.int32, 1)
     _req(block_version, "block_version", torch.int32, 1)
     _req(req_version, "req_version", torch.int32, 1)
     if block_table.shape[0] != B or ctx_lens.shape[0] != B or req_version.shape[0] != B:
         raise ValueError("block_table, ctx_lens and req_version must have B=%d rows" % B)
+    if num_blocks is not None and block_version.numel() < num_blocks:
+        raise ValueError("block_version must have a tag for each of the pool's %d blocks, "
+                         "got %d" % (num_blocks, block_version.numel()))
+
+
+def _attn_out_checks(out, lse, rows, Hq, D, device):
+    """out [rows, Hq, D] bf16 and lse [rows, Hq] float32 (allocated when None)."""
+    if out is None:
+        out = torch.empty((rows, Hq, D), dtype=torch.bfloat16, device=device)
+    if lse is None:
+        lse = torch.empty((rows, Hq), dtype=torch.float32, device=device)
+    _req(out, "out", torch.bfloat16, 3)
+    _req(lse, "lse", torch.float32, 2)
+    if tuple(out.shape) != (rows, Hq, D):
+        raise ValueError("out must be [%d, %d, %d], got %s" % (rows, Hq, D, tuple(out.shape)))
+    if tuple(lse.shape) != (rows, Hq):
+        raise ValueError("lse must be [%d, %d], got %s" % (rows, Hq, tuple(lse.shape)))
+    return out, lse
 
 
 def prepare_paged_attn_decode(q, k_cache, v_cache, block_table, ctx_lens, block_version,
@@ -536,18 +555,13 @@ def prepare_paged_attn_decode(q, k_cache, v_cache, block_table, ctx_lens, block_
             raise ValueError("Hkv is required when k_new is not given")
         Hkv = k_new.shape[1]
     num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
-    _meta_checks(block_table, ctx_lens, block_version, req_version, B)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B, num_blocks)
     if k_new is not None:
         _req(k_new, "k_new", torch.bfloat16, 3)
         _req(v_new, "v_new", torch.bfloat16, 3)
         if tuple(k_new.shape) != (B, Hkv, D) or tuple(v_new.shape) != (B, Hkv, D):
             raise ValueError("k_new/v_new must be [B, Hkv, D]")
-    if out is None:
-        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
-    if lse is None:
-        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
-    _req(out, "out", torch.bfloat16, 3)
-    _req(lse, "lse", torch.float32, 2)
+    out, lse = _attn_out_checks(out, lse, B, Hq, D, q.device)
     args = [_ptr(q), B, Hq, Hkv, D, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
             num_blocks, BLOCK_SIZE, _ptr(block_table), block_table.shape[1], _ptr(ctx_lens),
             _ptr(block_version), _ptr(req_version), float(sm_scale), _ptr(out), _ptr(lse)]
@@ -581,18 +595,13 @@ def prepare_paged_attn_prefill(q, q_indptr, k_cache, v_cache, block_table, ctx_l
             raise ValueError("Hkv is required when k_new is not given")
         Hkv = k_new.shape[1]
     num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
-    _meta_checks(block_table, ctx_lens, block_version, req_version, B)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B, num_blocks)
     if k_new is not None:
         _req(k_new, "k_new", torch.bfloat16, 3)
         _req(v_new, "v_new", torch.bfloat16, 3)
         if tuple(k_new.shape) != (T, Hkv, D) or tuple(v_new.shape) != (T, Hkv, D):
             raise ValueError("k_new/v_new must be [T, Hkv, D]")
-    if out is None:
-        out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=q.device)
-    if lse is None:
-        lse = torch.empty((T, Hq), dtype=torch.float32, device=q.device)
-    _req(out, "out", torch.bfloat16, 3)
-    _req(lse, "lse", torch.float32, 2)
+    out, lse = _attn_out_checks(out, lse, T, Hq, D, q.device)
     args = [_ptr(q), _ptr(q_indptr), B, T, Hq, Hkv, D, _ptr(k_new), _ptr(v_new),
             _ptr(k_cache), _ptr(v_cache), num_blocks, BLOCK_SIZE, _ptr(block_table),
             block_table.shape[1], _ptr(ctx_lens), _ptr(block_version), _ptr(req_version),

@@ -57,6 +57,13 @@ __device__ __forceinline__ bool id_ok(int p, int64_t num_blocks) {
   return p >= 0 && p < num_blocks;
 }
 
+// Request b's query rows [r0, r1) form a row range of q: inside [0, T] and
+// not reversed. A request whose range is not is skipped as a whole: it gets
+// no unit of either grid, appends nothing and writes no output row.
+__device__ __forceinline__ bool rows_ok(int r0, int r1, int64_t T) {
+  return r0 >= 0 && r1 >= r0 && r1 <= T;
+}
+
 // The k-th unit of work (k >= 0), counting units from the last request
 // backwards and, within a request, from its last unit, where request b has
 // units(b) >= 0 of them. Returns the request (-1 when k is past the total)
@@ -125,15 +132,17 @@ __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
   // blocks request b's chunk writes: from its first new position's block to
   // its last one's (none for an empty chunk or a chunk past the context)
   auto chunk_blocks = [&](int bb) {
-    const int n = a.q_indptr[bb + 1] - a.q_indptr[bb];
+    const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
+    const int n = r1 - r0;
     const int L = a.ctx_lens[bb];
-    if (n <= 0 || L <= 0) return 0;
+    if (!rows_ok(r0, r1, a.T) || n <= 0 || L <= 0) return 0;
     const int P = max(L - n, 0);
     return (L - 1) / kBlockSize - P / kBlockSize + 1;
   };
   const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hkv), chunk_blocks, &jb);
   if (b < 0) return;
   const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
+  if (!rows_ok(r0, r1, a.T)) return;  // never given a unit; checked before any row is read
   const int n_b = r1 - r0;
   const int L = a.ctx_lens[b], P = L - n_b;
   const int j = (P >= 0 ? P : 0) / kBlockSize + jb;  // the block
@@ -200,13 +209,14 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   const int h = blockIdx.x % a.Hq;
   int qtile = 0;
   auto row_tiles = [&](int bb) {
-    const int n = a.q_indptr[bb + 1] - a.q_indptr[bb];
-    return n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
+    const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
+    const int n = r1 - r0;
+    return rows_ok(r0, r1, a.T) && n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
   };
   const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hq), row_tiles, &qtile);
   if (b < 0) return;
   const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
-  if (r0 < 0 || r1 > a.T || r1 < r0) return;  // not a row range of q
+  if (!rows_ok(r0, r1, a.T)) return;  // never given a unit
   const int n_b = r1 - r0;
   const int row0 = qtile * kPaRows;
   if (row0 >= n_b) return;

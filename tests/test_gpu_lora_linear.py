@@ -246,3 +246,36 @@ def test_grouped_zero_up_projection_is_bitwise_base():
     y_base = _grouped_gpu(x, Ws, None, None, None, None, None)
     for a, b in zip(y_zero, y_base):
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("Ns", [(4096, 4096, 4096), (4096, 1024, 1024)],
+                         ids=["mha_qkv", "gqa_qkv"])
+def test_grouped_long_chunk_at_full_size(Ns):
+    # The grouped call as the prefill step issues it: q, k, v of one 2048 x
+    # 4096 activation over 4 rank-16 adapters (and unrouted tokens), one
+    # shrink pass and one product over every projection's tiles. Checked on
+    # sampled rows: each 128-token tile's first and last rows, the chunk
+    # boundaries, and random rows.
+    T, K, n_ad, r_max = 2048, 4096, 4, 16
+    say("lora_linear_grouped full size", Ns)
+    rng = np.random.default_rng(sum(Ns))
+    x = rand_bf16(rng, (T, K))
+    Ws = [rand_bf16(rng, (N, K), 0.02) for N in Ns]
+    As = [rand_bf16(rng, (n_ad, r_max, K), 1 / math.sqrt(r_max)) for _ in Ns]
+    Bs = [rand_bf16(rng, (n_ad, N, r_max), 0.01) for N in Ns]
+    Rs = [np.full(n_ad, r_max, np.int32) for _ in Ns]
+    idx = np.repeat(rng.integers(0, n_ad, size=T // 512), 512).astype(np.int32)
+    idx[rng.random(T) < 0.05] = -1
+    scale = rng.uniform(-2, 2, size=T).astype(np.float32)
+    ys = _grouped_gpu(x, Ws, As, Bs, Rs, idx, scale)
+    y0s = _grouped_gpu(x, Ws, None, None, None, None, None)
+    rows = np.unique(np.concatenate([np.arange(0, T, 128), np.arange(127, T, 128),
+                                     rng.choice(T, size=24, replace=False)]))
+    sel = idx[rows] >= 0
+    for g, (W, A, B, rk) in enumerate(zip(Ws, As, Bs, Rs)):
+        ref = oracle.lora_linear(x[rows], W, A, B, rk, idx[rows], scale[rows])
+        assert_rel(f64(ys[g])[rows], ref, "y[%d]" % g)
+        # the adapter delta alone, against the oracle's (y - base)
+        base = oracle.lora_linear(x[rows], W)
+        assert_rel(f64(ys[g])[rows][sel] - f64(y0s[g])[rows][sel], (ref - base)[sel],
+                   "delta[%d]" % g, tol=5e-2)

@@ -2,11 +2,13 @@
 
 Decode workloads run the whole step (version check, q/k/v projections,
 appending attention, output projection; in the 32-layer workload each layer's
-output is the next layer's input) and compare every stage with the oracle's own
-chain on the same generated inputs, for all requests or a seeded sample of
-them (requests are independent within a step, so a sample is exact). The
-chunked-prefill workload's projections and attention are each checked at full
-size on sampled output rows. Integer outputs are compared bit for bit.
+output is the next layer's input), for all requests or a seeded sample of them
+(requests are independent within a step, so a sample is exact). Each compared
+layer is checked stage by stage with the oracle fed the GPU's own bf16 input of
+that stage (teacher forcing), and the step's final output against the
+oracle's own chain through every layer. The chunked-prefill step runs whole
+at full size and is checked the same way on sampled rows. Integer outputs and
+appended pools are compared bit for bit.
 """
 import math
 
@@ -19,8 +21,8 @@ import oracle.chain as ochain
 import paper_2608_15241_amd as lk
 import workloads
 from paper_2608_15241_amd.step import Step, meta_to_device
-from tests.gpu_helpers import (assert_lse, assert_rel, dev, f64, gather_requests, host_u16,
-                               say)
+from tests.gpu_helpers import (assert_attn, assert_lse, assert_rel, dev, f64, gather_requests,
+                               host_u16, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -40,6 +42,31 @@ def _setup(w, seed=0):
     x = workloads.randn_bf16((meta.T, w.hidden), 1.0, "cuda", seed * 31 + 5)
     torch.cuda.synchronize()
     return meta, weights, pool, x
+
+
+def _stage_check(l, w, hw, buf, reqs, x_in, pool_l, table, bv, ctx, rv, tok_a, tok_s, qi,
+                 gpu_pool_after):
+    """Layer l checked stage by stage, each stage of the oracle fed the GPU's
+    own bf16 input of that stage (teacher forcing): q, k, v from the layer
+    input, the appended pool and attention from the GPU's q, k, v, and the
+    output projection from the GPU's attention output."""
+    D, T = w.head_dim, len(reqs)
+    for name in ("q", "k", "v"):
+        ref = ochain.project(x_in, hw, name, tok_a, tok_s)
+        assert_rel(f64(buf[name])[reqs], ref, "layer %d %s" % (l, name))
+    kh, vh = pool_l[0].copy(), pool_l[1].copy()
+    kq = host_u16(buf["k"])[reqs].reshape(T, w.hkv, D)
+    vq = host_u16(buf["v"])[reqs].reshape(T, w.hkv, D)
+    oracle.kv_append(kh, vh, w.hkv, D, table, qi, ctx, kq, vq)
+    assert np.array_equal(gpu_pool_after[0], kh), "layer %d appended K pool differs" % l
+    assert np.array_equal(gpu_pool_after[1], vh), "layer %d appended V pool differs" % l
+    qq = host_u16(buf["q"])[reqs].reshape(T, w.hq, D)
+    ro, rl = oracle.paged_attn(qq, qi, w.hq, w.hkv, D, kh, vh, table, ctx, bv, rv,
+                               1.0 / math.sqrt(D))
+    assert_attn(f64(buf["o"])[reqs], ro.reshape(T, w.hq * D), "layer %d o" % l, D)
+    assert_lse(buf["lse"].cpu().numpy()[reqs], rl, "layer %d lse" % l)
+    ref = ochain.project(host_u16(buf["o"])[reqs], hw, "o", tok_a, tok_s)
+    assert_rel(f64(buf["y"])[reqs], ref, "layer %d y" % l)
 
 
 def _decode_chain_check(w, reqs, seed=0, layers_to_compare=None):
@@ -66,25 +93,28 @@ def _decode_chain_check(w, reqs, seed=0, layers_to_compare=None):
     assert int(n.item()) == en
     assert np.array_equal(pairs[:en].cpu().numpy(), ep)
     assert np.array_equal(valid.cpu().numpy(), ev)
-    # oracle chain on the sample
-    say("oracle chain", w.name, "requests", len(reqs))
     ctx = meta.ctx_lens[reqs]
     rv = meta.req_version[reqs]
     tok_a = meta.token_adapter[reqs]
     tok_s = meta.token_scale[reqs]
     qi = np.arange(len(reqs) + 1, dtype=np.int32)
-    xo = x_host
     compare = set(range(w.n_layers)) if layers_to_compare is None else set(layers_to_compare)
+    # per layer, stage by stage, with the GPU's own inputs of each stage
+    for l in sorted(compare):
+        say("stage check", w.name, "layer", l)
+        after = gather_requests(pool[l, 0], pool[l, 1], w.hkv, D, meta.block_table,
+                                meta.ctx_lens, meta.block_version, reqs)[:2]
+        _stage_check(l, w, _host_weights(weights[l]), st.buffers[l], reqs,
+                     host_u16(st.buffers[l]["x"])[reqs], pools[l], table, bv, ctx, rv, tok_a,
+                     tok_s, qi, after)
+    # the oracle's own chain through every layer, against the step's output
+    say("oracle chain", w.name, "requests", len(reqs))
+    xo = x_host
     for l in range(w.n_layers):
         lw = _host_weights(weights[l])
         kh, vh = pools[l]
-        xo, stages = ochain.layer(xo, lw, kh, vh, w.hq, w.hkv, D, table, qi, ctx, bv, rv,
-                                  tok_a, tok_s, residual=False)
-        if l in compare:
-            buf = st.buffers[l]
-            for name in ("q", "k", "v", "o", "y"):
-                assert_rel(f64(buf[name])[reqs], stages[name], "layer %d %s" % (l, name))
-            assert_lse(buf["lse"].cpu().numpy()[reqs], stages["lse"], "layer %d lse" % l)
+        xo, _ = ochain.layer(xo, lw, kh, vh, w.hq, w.hkv, D, table, qi, ctx, bv, rv, tok_a,
+                             tok_s, residual=False)
     assert_rel(f64(st.out)[reqs], oracle.bf16_to_f64(xo), "final output")
     del st, pool, weights
     torch.cuda.empty_cache()
@@ -156,9 +186,60 @@ def test_prefill_7b_sampled():
                                w.hq, w.hkv, D, kh, vh, meta.block_table[b_of],
                                (pos + 1).astype(np.int32), meta.block_version,
                                meta.req_version[b_of], 1 / math.sqrt(D))
-    assert_rel(f64(out)[rows], ro, "prefill out")
+    assert_attn(f64(out)[rows], ro, "prefill out", D)
     assert_lse(lse.cpu().numpy()[rows], rl, "prefill lse")
     del pool
+    torch.cuda.empty_cache()
+
+
+def test_prefill_7b_step():
+    # The whole prefill step as the benchmark runs it (version check; q, k, v
+    # as one grouped call at T = 2048, K = 4096; appending causal attention;
+    # o), checked stage by stage on sampled rows with the oracle fed the
+    # GPU's own input of each stage, and the appended pool bit for bit.
+    w = workloads.PREFILL_7B
+    meta, weights, pool, x = _setup(w, 5)
+    D, T = w.head_dim, meta.T
+    rng = np.random.default_rng(8)
+    starts = meta.q_indptr[:-1]
+    rows = np.unique(np.concatenate([starts, meta.q_indptr[1:] - 1, starts + 127, starts + 128,
+                                     rng.choice(T, size=32, replace=False)]))
+    kh, vh = host_u16(pool[0, 0]).reshape(-1), host_u16(pool[0, 1]).reshape(-1)
+    say("GPU prefill step", w.name)
+    st = Step("prefill", x, weights, meta_to_device(meta, "cuda"), pool, w.hq, w.hkv, D,
+              residual=False)
+    st()
+    torch.cuda.synchronize()
+    pairs, n, valid = st.version_check.outputs
+    ep, en, ev = oracle.block_version_check(meta.block_table, meta.ctx_lens,
+                                            meta.block_version, meta.req_version)
+    assert int(n.item()) == en and np.array_equal(valid.cpu().numpy(), ev)
+    buf = st.buffers[0]
+    hw = _host_weights(weights[0])
+    tok_a, tok_s = meta.token_adapter[rows], meta.token_scale[rows]
+    xh = host_u16(x)[rows]
+    for name in ("q", "k", "v"):
+        say("prefill step stage", name)
+        ref = ochain.project(xh, hw, name, tok_a, tok_s)
+        assert_rel(f64(buf[name])[rows], ref, "step " + name)
+    say("prefill step append + attention")
+    oracle.kv_append(kh, vh, w.hkv, D, meta.block_table, meta.q_indptr, meta.ctx_lens,
+                     host_u16(buf["k"]).reshape(T, w.hkv, D),
+                     host_u16(buf["v"]).reshape(T, w.hkv, D))
+    assert np.array_equal(host_u16(pool[0, 0]).reshape(-1), kh), "appended K pool differs"
+    assert np.array_equal(host_u16(pool[0, 1]).reshape(-1), vh), "appended V pool differs"
+    b_of = np.searchsorted(meta.q_indptr, rows, side="right") - 1
+    pos = meta.ctx_lens[b_of] - meta.n_new[b_of] + (rows - meta.q_indptr[b_of])
+    qh = host_u16(buf["q"]).reshape(T, w.hq, D)[rows]
+    ro, rl = oracle.paged_attn(qh, np.arange(len(rows) + 1, dtype=np.int32), w.hq, w.hkv, D,
+                               kh, vh, meta.block_table[b_of], (pos + 1).astype(np.int32),
+                               meta.block_version, meta.req_version[b_of], 1 / math.sqrt(D))
+    assert_attn(f64(buf["o"])[rows], ro.reshape(len(rows), w.hq * D), "step o", D)
+    assert_lse(buf["lse"].cpu().numpy()[rows], rl, "step lse")
+    say("prefill step stage y")
+    ref = ochain.project(host_u16(buf["o"])[rows], hw, "o", tok_a, tok_s)
+    assert_rel(f64(buf["y"])[rows], ref, "step y")
+    del st, pool, weights
     torch.cuda.empty_cache()
 
 
