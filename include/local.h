@@ -319,6 +319,42 @@ local_status_t local_paged_attn_decode(
     void* ws, size_t* ws_bytes, void* stream);
 
 /*
+ * local_paged_attn_decode_noalloc — local_paged_attn_decode for callers that
+ * cannot allocate device memory or pass a workspace: code under HIP graph
+ * capture that must not call hipMalloc, tight serving loops, harnesses that
+ * forbid allocation. The caller still passes every input and output.
+ *
+ *  Same arguments, computation, results (bit for bit) and errors as
+ *  local_paged_attn_decode, without ws / ws_bytes. The split-KV partials go
+ *  to a scratch array of LOCAL_DECODE_NOALLOC_SCRATCH_BYTES that the library
+ *  holds in device memory, one copy per GPU it runs on, from the first call
+ *  on that GPU until the process ends. The call allocates nothing and calls
+ *  no allocating routine.
+ *
+ *  Limit: the partials need B * Hq * ceil(max_blocks / 32) * (D + 2) * 4
+ *  bytes (the size local_paged_attn_decode asks for); a call needing more
+ *  than LOCAL_DECODE_NOALLOC_SCRATCH_BYTES returns LOCAL_ERR_UNSUPPORTED and
+ *  launches nothing. (131072 partials at D = 128: for instance 128 requests x
+ *  32 heads with a 1024-block table.)
+ *  Every call on one GPU shares that GPU's scratch: calls that overlap on one
+ *  GPU (different streams, or different threads' streams) race and give
+ *  undefined results. Calls ordered on one stream are safe. Nothing in the
+ *  scratch needs to start at zero: each call writes every partial it reads.
+ */
+#define LOCAL_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)68157440) /* 65 MiB */
+
+local_status_t local_paged_attn_decode_noalloc(
+    const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new,
+    uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size,
+    const int32_t* block_table, int32_t max_blocks,
+    const int32_t* ctx_lens,
+    const int32_t* block_version, const int32_t* req_version,
+    float sm_scale,
+    uint16_t* out, float* lse, void* stream);
+
+/*
  * local_paged_attn_prefill — a chunk of new tokens per request is appended to
  * the paged cache and attends causally over the cached prefix plus the chunk,
  * with the per-block version mask (§4.1 chunked prefill; §5.3 stale-coverage

@@ -27,7 +27,7 @@ BLOCK_SIZE = 16
 EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
            "local_block_version_check", "local_lora_grad", "local_lora_grad_input",
-           "local_lora_grad_grouped",
+           "local_lora_grad_grouped", "local_paged_attn_decode_noalloc",
            # host-side KV manager (local_kv.h)
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
@@ -78,6 +78,9 @@ def load_library(path: str = LIB_PATH):
     lib.local_paged_attn_decode.restype = ctypes.c_int
     lib.local_paged_attn_decode.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64, i32, P,
                                             i32, P, P, P, f32, P, P, P, SZ, P]
+    lib.local_paged_attn_decode_noalloc.restype = ctypes.c_int
+    lib.local_paged_attn_decode_noalloc.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64,
+                                                    i32, P, i32, P, P, P, f32, P, P, P]
     lib.local_paged_attn_prefill.restype = ctypes.c_int
     lib.local_paged_attn_prefill.argtypes = [P, P, i32, i64, i32, i32, i32, P, P, P, P, i64,
                                              i32, P, i32, P, P, P, f32, P, P, P, SZ, P]
@@ -578,6 +581,56 @@ def local_paged_attn_decode(*args, **kwargs):
     q [B, Hq, D]; pools as documented in include/local.h; returns (out, lse).
     """
     return prepare_paged_attn_decode(*args, **kwargs)()
+
+
+class NoWorkspaceCall:
+    """A prepared C-ABI call of an entry point that takes no workspace."""
+
+    def __init__(self, fn, args, keep=()):
+        self.keep = tuple(t for t in keep if t is not None)
+        self.fn = fn
+        self.args = tuple(args)
+        self.outputs = None
+
+    def __call__(self):
+        _check(self.fn(*self.args, _stream()))
+        return self.outputs
+
+
+def prepare_paged_attn_decode_noalloc(q, k_cache, v_cache, block_table, ctx_lens,
+                                      block_version, req_version, sm_scale: float, k_new=None,
+                                      v_new=None, Hkv: Optional[int] = None, out=None,
+                                      lse=None) -> NoWorkspaceCall:
+    """Prepared decode attention through local_paged_attn_decode_noalloc (no
+    workspace: the library's own scratch); the call returns (out, lse)."""
+    lib = load_library()
+    _req(q, "q", torch.bfloat16, 3)
+    B, Hq, D = q.shape
+    if Hkv is None:
+        if k_new is None:
+            raise ValueError("Hkv is required when k_new is not given")
+        Hkv = k_new.shape[1]
+    num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B, num_blocks)
+    if k_new is not None:
+        _req(k_new, "k_new", torch.bfloat16, 3)
+        _req(v_new, "v_new", torch.bfloat16, 3)
+        if tuple(k_new.shape) != (B, Hkv, D) or tuple(v_new.shape) != (B, Hkv, D):
+            raise ValueError("k_new/v_new must be [B, Hkv, D]")
+    out, lse = _attn_out_checks(out, lse, B, Hq, D, q.device)
+    args = [_ptr(q), B, Hq, Hkv, D, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+            num_blocks, BLOCK_SIZE, _ptr(block_table), block_table.shape[1], _ptr(ctx_lens),
+            _ptr(block_version), _ptr(req_version), float(sm_scale), _ptr(out), _ptr(lse)]
+    c = NoWorkspaceCall(lib.local_paged_attn_decode_noalloc, args,
+                        keep=(q, k_new, v_new, k_cache, v_cache, block_table, ctx_lens,
+                              block_version, req_version, out, lse))
+    c.outputs = (out, lse)
+    return c
+
+
+def local_paged_attn_decode_noalloc(*args, **kwargs):
+    """local_paged_attn_decode without a workspace (see include/local.h)."""
+    return prepare_paged_attn_decode_noalloc(*args, **kwargs)()
 
 
 def prepare_paged_attn_prefill(q, q_indptr, k_cache, v_cache, block_table, ctx_lens,

@@ -32,6 +32,8 @@
 //  * The new token's K/V are written at position L-1 by the wave that owns
 //    that block, which also substitutes them for the cache slot it reads, so
 //    no other workgroup and no second launch is involved.
+#include <mutex>
+
 #include "common.hpp"
 
 namespace localk {
@@ -492,6 +494,66 @@ local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
 
 using namespace localk;
 
+// Host-side validation shared by both entry points: fills *a (without the
+// partials' pointers) and *need, the bytes of split-KV partials of the call.
+static local_status_t decode_setup(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                   int32_t D, const uint16_t* k_new, const uint16_t* v_new,
+                                   uint16_t* k_cache, uint16_t* v_cache, int64_t num_blocks,
+                                   int32_t block_size, const int32_t* block_table,
+                                   int32_t max_blocks, const int32_t* ctx_lens,
+                                   const int32_t* block_version, const int32_t* req_version,
+                                   float sm_scale, uint16_t* out, float* lse, const char* who,
+                                   DecodeArgs* a, size_t* part_elems, size_t* need) {
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || max_blocks < 1 || num_blocks < 1 || Hq % Hkv != 0)
+    return local_fail(LOCAL_ERR_SHAPE, "%s: B=%d Hq=%d Hkv=%d max_blocks=%d num_blocks=%lld",
+                      who, B, Hq, Hkv, max_blocks, (long long)num_blocks);
+  if (block_size != kBlockSize || (D != 64 && D != 128) || Hq / Hkv > 16)
+    return local_fail(LOCAL_ERR_UNSUPPORTED,
+                      "%s: block_size=%d D=%d group=%d (need 16, 64|128, <=16)", who,
+                      block_size, D, Hq / Hkv);
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return local_fail(LOCAL_ERR_NULL, "%s: k_new and v_new must both be set", who);
+  const int n_parts = (max_blocks + kBlocksPerPart - 1) / kBlocksPerPart;
+  *part_elems = static_cast<size_t>(B > 0 ? B : 1) * Hq * n_parts;
+  *need = *part_elems * (D + 2) * sizeof(float);
+  a->q = q;
+  a->k_new = k_new;
+  a->v_new = v_new;
+  a->k_cache = k_cache;
+  a->v_cache = v_cache;
+  a->block_table = block_table;
+  a->ctx_lens = ctx_lens;
+  a->block_version = block_version;
+  a->req_version = req_version;
+  a->out = out;
+  a->lse = lse;
+  a->part_o = nullptr;
+  a->part_ml = nullptr;
+  a->Hq = Hq;
+  a->Hkv = Hkv;
+  a->group = Hq / Hkv;
+  a->num_blocks = num_blocks;
+  a->max_blocks = max_blocks;
+  a->n_parts = n_parts;
+  a->scale_log2 = sm_scale * kLog2e;
+  return LOCAL_OK;
+}
+
+static local_status_t decode_pointers_ok(const DecodeArgs& a, const char* who) {
+  if (!a.q || !a.k_cache || !a.v_cache || !a.block_table || !a.ctx_lens ||
+      !a.block_version || !a.req_version || !a.out)
+    return local_fail(LOCAL_ERR_NULL, "%s: NULL pointer argument", who);
+  return LOCAL_OK;
+}
+
+static local_status_t decode_launch(DecodeArgs& a, int B, int D, void* partials,
+                                    size_t part_elems, void* stream) {
+  a.part_o = static_cast<float*>(partials);
+  a.part_ml = a.part_o + part_elems * D;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return D == 64 ? launch_decode<64>(a, B, s) : launch_decode<128>(a, B, s);
+}
+
 extern "C" local_status_t local_paged_attn_decode(
     const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
     const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
@@ -499,52 +561,89 @@ extern "C" local_status_t local_paged_attn_decode(
     int32_t max_blocks, const int32_t* ctx_lens, const int32_t* block_version,
     const int32_t* req_version, float sm_scale, uint16_t* out, float* lse, void* ws,
     size_t* ws_bytes, void* stream) {
-  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "paged_attn_decode: ws_bytes is NULL");
-  if (B < 0 || Hq <= 0 || Hkv <= 0 || max_blocks < 1 || num_blocks < 1 || Hq % Hkv != 0)
-    return local_fail(LOCAL_ERR_SHAPE,
-                      "paged_attn_decode: B=%d Hq=%d Hkv=%d max_blocks=%d num_blocks=%lld", B,
-                      Hq, Hkv, max_blocks, (long long)num_blocks);
-  if (block_size != kBlockSize || (D != 64 && D != 128) || Hq / Hkv > 16)
-    return local_fail(LOCAL_ERR_UNSUPPORTED,
-                      "paged_attn_decode: block_size=%d D=%d group=%d (need 16, 64|128, <=16)",
-                      block_size, D, Hq / Hkv);
-  if ((k_new == nullptr) != (v_new == nullptr))
-    return local_fail(LOCAL_ERR_NULL, "paged_attn_decode: k_new and v_new must both be set");
-  const int n_parts = (max_blocks + kBlocksPerPart - 1) / kBlocksPerPart;
-  const size_t part_elems = static_cast<size_t>(B > 0 ? B : 1) * Hq * n_parts;
-  const size_t need = part_elems * (D + 2) * sizeof(float);
+  const char* who = "paged_attn_decode";
+  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "%s: ws_bytes is NULL", who);
+  DecodeArgs a;
+  size_t part_elems = 0, need = 0;
+  local_status_t st = decode_setup(q, B, Hq, Hkv, D, k_new, v_new, k_cache, v_cache,
+                                   num_blocks, block_size, block_table, max_blocks, ctx_lens,
+                                   block_version, req_version, sm_scale, out, lse, who, &a,
+                                   &part_elems, &need);
+  if (st != LOCAL_OK) return st;
   if (!ws) {
     *ws_bytes = need;
     return LOCAL_OK;
   }
   if (*ws_bytes < need)
-    return local_fail(LOCAL_ERR_WORKSPACE, "paged_attn_decode: workspace %zu < %zu",
-                      *ws_bytes, need);
+    return local_fail(LOCAL_ERR_WORKSPACE, "%s: workspace %zu < %zu", who, *ws_bytes, need);
   if (B == 0) return LOCAL_OK;
-  if (!q || !k_cache || !v_cache || !block_table || !ctx_lens || !block_version ||
-      !req_version || !out)
-    return local_fail(LOCAL_ERR_NULL, "paged_attn_decode: NULL pointer argument");
+  if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
+  return decode_launch(a, B, D, ws, part_elems, stream);
+}
+
+// ---------------------------------------------------------------- no-alloc
+// Scratch of local_paged_attn_decode_noalloc: the split-KV partials of up to
+// 131072 (request, query head, partition) triples at D = 128, held
+// by the library in device memory (one copy per GPU, for the life of the
+// process). In host code `scratch` names a host-side stand-in, not the device
+// copy: its device address is taken once per device with
+// hipGetSymbolAddress and only that address is ever passed to a kernel.
+constexpr size_t kNoAllocBytes = LOCAL_DECODE_NOALLOC_SCRATCH_BYTES;
+static_assert(kNoAllocBytes == 131072 * (128 + 2) * sizeof(float), "partials at D = 128");
+__device__ __align__(256) float scratch[kNoAllocBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (taken on its first
+// use there, with that device current). NULL with *st set on failure.
+void* scratch_of_current_device(local_status_t* st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *st = local_fail(LOCAL_ERR_HIP, "paged_attn_decode_noalloc: hipGetDevice: %s (device %d)",
+                     hipGetErrorString(e), dev);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      *st = local_fail(LOCAL_ERR_HIP, "paged_attn_decode_noalloc: hipGetSymbolAddress: %s",
+                       hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" local_status_t local_paged_attn_decode_noalloc(
+    const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size, const int32_t* block_table,
+    int32_t max_blocks, const int32_t* ctx_lens, const int32_t* block_version,
+    const int32_t* req_version, float sm_scale, uint16_t* out, float* lse, void* stream) {
+  const char* who = "paged_attn_decode_noalloc";
   DecodeArgs a;
-  a.q = q;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
-  a.block_table = block_table;
-  a.ctx_lens = ctx_lens;
-  a.block_version = block_version;
-  a.req_version = req_version;
-  a.out = out;
-  a.lse = lse;
-  a.part_o = static_cast<float*>(ws);
-  a.part_ml = a.part_o + part_elems * D;
-  a.Hq = Hq;
-  a.Hkv = Hkv;
-  a.group = Hq / Hkv;
-  a.num_blocks = num_blocks;
-  a.max_blocks = max_blocks;
-  a.n_parts = n_parts;
-  a.scale_log2 = sm_scale * kLog2e;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  return D == 64 ? launch_decode<64>(a, B, s) : launch_decode<128>(a, B, s);
+  size_t part_elems = 0, need = 0;
+  local_status_t st = decode_setup(q, B, Hq, Hkv, D, k_new, v_new, k_cache, v_cache,
+                                   num_blocks, block_size, block_table, max_blocks, ctx_lens,
+                                   block_version, req_version, sm_scale, out, lse, who, &a,
+                                   &part_elems, &need);
+  if (st != LOCAL_OK) return st;
+  if (need > kNoAllocBytes)
+    return local_fail(LOCAL_ERR_UNSUPPORTED,
+                      "%s: B*Hq*ceil(max_blocks/32)*(D+2)*4 = %zu bytes of partials exceed the "
+                      "library's fixed scratch of %zu bytes (use local_paged_attn_decode with a "
+                      "workspace)", who, need, kNoAllocBytes);
+  if (B == 0) return LOCAL_OK;
+  if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
+  void* partials = scratch_of_current_device(&st);
+  if (!partials) return st;
+  return decode_launch(a, B, D, partials, part_elems, stream);
 }

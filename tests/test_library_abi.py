@@ -229,3 +229,27 @@ def test_lora_grad_grouped_workspace_and_errors(lib):
     assert _size(f, FAKE, 2048, 4096, 3, ptrs(3), bad, ptrs(3), ptrs(3), 4, 16, None, FAKE,
                  FAKE, ptrs(3), ptrs(3))[0] == ERR_UNSUPPORTED
     assert b"lora_grad_grouped" in lib.local_last_error()
+
+
+def test_decode_noalloc_rejects_sizes_beyond_its_scratch(lib):
+    # The no-workspace decode entry point holds a fixed scratch of
+    # LOCAL_DECODE_NOALLOC_SCRATCH_BYTES; a call that would need more is
+    # refused on the host, before any HIP call.
+    f = lib.local_paged_attn_decode_noalloc
+    limit = 68157440
+    text = open(os.path.join(ROOT, "include", "local.h")).read()
+    assert re.search(r"#define LOCAL_DECODE_NOALLOC_SCRATCH_BYTES \(\(size_t\)%d\)" % limit, text)
+
+    def call(B=129, Hq=32, Hkv=8, D=128, mb=1024, bs=16, kn=FAKE, vn=FAKE):
+        return f(FAKE, B, Hq, Hkv, D, kn, vn, FAKE, FAKE, 100000, bs, FAKE, mb, FAKE, FAKE,
+                 FAKE, 0.088, FAKE, FAKE, None)
+
+    assert 128 * 32 * 32 * (128 + 2) * 4 == limit      # exactly at the limit: accepted
+    assert call(B=129) == ERR_UNSUPPORTED               # one request more: refused
+    assert b"scratch" in lib.local_last_error()
+    assert call(B=1, Hq=32, mb=32 * 4097) == ERR_UNSUPPORTED
+    assert call(B=0) == OK                              # nothing to do, nothing launched
+    assert call(Hq=32, Hkv=6) == ERR_SHAPE
+    assert call(D=96) == ERR_UNSUPPORTED
+    assert call(bs=8) == ERR_UNSUPPORTED
+    assert call(kn=None) == ERR_NULL
