@@ -1,24 +1,34 @@
 #!/usr/bin/env python3
-"""Benchmark of the mixed-adapter LoRA decode step on one MI355X.
+"""Benchmark of the mixed-adapter LoRA step on one MI355X, every workload.
 
-One step = one pass of the whole path over one batch: the version check, the
-q/k/v LoRA projections, the appending, version-masked paged decode attention,
-and the output LoRA projection, for the 7B-class single-layer decode workload
-(hidden 4096, 32x128 MHA, batch 32, context U[256,4096], 8 rank-16 adapters on
-q/k/v/o). Inputs are seeded synthetic tensors already resident in HBM. Two
-independent input sets (weights, KV pools, activations) alternate between
-steps, so that the last-level cache cannot serve one step's weights to the
-next.
+A decode step is one pass of the whole path over one batch: the version
+check, the q/k/v LoRA projections (one grouped call), the appending,
+version-masked paged decode attention and the output LoRA projection, for
+every layer. A prefill step is the same with a chunk of tokens per request
+and causal prefill attention. Inputs are seeded synthetic tensors already
+resident in HBM; a step is one HIP-graph replay, timed with an event pair per
+step, and the median is reported.
 
-Prints ONE JSON line. `value` is decode tokens/s. `roofline` is for the
-dominant kernel (decode attention), timed with HIP events around its launches
-inside the timed region. `prefill` reports the matrix-core utilisation of the
-LoRA-fused projections of the chunked-prefill workload, timed the same way.
-`cpu_baseline` is the CPU oracle timed on this host on the same workload.
+Prints ONE JSON line:
+* the headline is the largest single-GPU workload, `churn_32l_b128` (32
+  layers, 32q/8kv x 128, batch 128, contexts U[1024,16384], 32 rank-16
+  adapters, 10% of block-table entries stale): `value` is its decode tokens/s,
+  `roofline` its dominant kernel (decode attention, HIP events around every
+  layer's launch), `hbm_step` the whole step's algorithmic bytes over the step
+  time, and `cpu_baseline` the oracle on a seeded sample of 8 of the 128
+  requests through all 32 layers (its rate, and the 128-request step time it
+  extrapolates to, labelled as such);
+* `workloads` holds the same record for the other four workloads:
+  `tiny_decode` (absolute time), `decode_7b_mha_b32` and `gqa_skew_b64`
+  (decode steps; two input sets alternate so that the last-level cache
+  cannot serve one step's weights to the next), and `prefill_7b_4x512` (the
+  whole prefill step, its LoRA-fused projections and its attention against
+  the matrix-core peak); each with the oracle timed on the whole step;
+* `reprefill` (stale-coverage prefill under a staged version) and
+  `lora_grad` (the LoRA backward of a training chunk).
 
-`--workload gqa_skew_b64 | churn_32l_b128 | tiny_decode` times the decode step
-of another workload the same way (without the prefill and CPU legs; the
-32-layer one with a single input set, since its KV pool is 146 GB).
+`--workload NAME` runs one workload alone (its record as the headline, no
+CPU leg, no other legs): for profiling runs.
 """
 from __future__ import annotations
 
@@ -33,6 +43,8 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix cores
+HEADLINE = "churn_32l_b128"
+CPU_SAMPLE_REQUESTS = 8         # oracle sample of the 32-layer workload
 
 
 def say(*a):
@@ -43,47 +55,50 @@ def say(*a):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--sets", type=int, default=2, help="input sets rotated across steps")
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--sets", type=int, default=2,
+                   help="input sets rotated across steps (single-layer workloads)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-prefill", action="store_true")
-    p.add_argument("--cpu-budget-s", type=float, default=15.0)
-    p.add_argument("--workload", default="decode_7b_mha_b32",
-                   choices=("tiny_decode", "decode_7b_mha_b32", "gqa_skew_b64",
-                            "churn_32l_b128"),
-                   help="decode workload of the step; prefill and cpu_baseline are reported "
-                        "with the default one only. The 32-layer workload uses one input set "
-                        "(its KV pool is 146 GB)")
+    p.add_argument("--cpu-budget-s", type=float, default=20.0,
+                   help="repeat a workload's oracle run (at most 3 times after a warm-up run) "
+                        "while the total stays within this budget")
+    p.add_argument("--workload", default="all",
+                   choices=("all", "tiny_decode", "decode_7b_mha_b32", "gqa_skew_b64",
+                            "churn_32l_b128", "prefill_7b_4x512"),
+                   help="one workload alone (no CPU leg, no other legs)")
     p.add_argument("--traffic-probe", action="store_true",
                    help="only run, eagerly, a 256 MiB device copy (the calibration of the "
-                        "HBM byte counters) and 5 decode attention launches of the workload; "
-                        "for rocprofv3 --pmc runs")
+                        "HBM byte counters) and 5 decode attention launches of the workload "
+                        "(layer 0); for rocprofv3 --pmc runs")
     return p.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                            "decode_attn_traffic_decode_7b_mha_b32.md")
+ROOT = os.path.dirname(os.path.abspath(__file__))
 DECODE_SOURCES = ("paper_2608_15241_amd/csrc/paged_attn_decode.hip",
                   "paper_2608_15241_amd/csrc/common.hpp")
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", "decode_attn_traffic_%s.md" % workload)
 
 
 def decode_source_hash():
     """sha256 over the sources of the decode attention kernels."""
     import hashlib
     h = hashlib.sha256()
-    root = os.path.dirname(os.path.abspath(__file__))
     for rel in DECODE_SOURCES:
-        with open(os.path.join(root, rel), "rb") as f:
+        with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per decode attention launch from the committed counter summary,
-    or None when it is missing or was taken on other kernel sources."""
+def measured_traffic(workload):
+    """HBM bytes per decode attention launch of `workload` from the committed
+    counter summary, or None when it is missing or was taken on other kernel
+    sources."""
     try:
-        text = open(TRAFFIC_FILE).read()
+        text = open(traffic_file(workload)).read()
     except OSError:
         return None
     vals = {}
@@ -102,7 +117,7 @@ def measured_traffic():
 def decode_bytes(w, meta):
     """Algorithmic HBM bytes of one layer's attention launch and of one decode
     step over all layers (each layer reads its own KV pool and weights)."""
-    D, hq, hkv, H = w.head_dim, w.hq, w.hkv, w.hidden
+    D, hq, hkv = w.head_dim, w.hq, w.hkv
     B = meta.B
     nb = (meta.ctx_lens.astype(np.int64) + 15) // 16
     # valid KV tokens: live tokens of non-stale blocks (version check rule)
@@ -142,6 +157,19 @@ def adapters_text(w):
     return "%d x %s on %s (%s)" % (w.n_adapters, r, "/".join(w.lora_targets), w.assignment)
 
 
+def workload_config(w, meta, n_sets, valid_tokens=None):
+    c = {"workload": w.name, "layers": w.n_layers, "hidden": w.hidden,
+         "heads": "%dq/%dkv x %d" % (w.hq, w.hkv, w.head_dim), "batch": meta.B,
+         "context": context_text(w), "sum_context": int(meta.ctx_lens.sum()),
+         "stale_frac": w.stale_frac, "adapters": adapters_text(w), "input_sets": n_sets}
+    if w.kind == "prefill":
+        c["chunk_tokens"] = w.chunk
+        c["tokens_per_step"] = meta.T
+    if valid_tokens is not None:
+        c["valid_kv_tokens"] = valid_tokens
+    return c
+
+
 def prefill_gemm_flops(w, meta):
     T = meta.T
     f = 0
@@ -154,28 +182,38 @@ def prefill_gemm_flops(w, meta):
     return f
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
-              "(sharding across GPUs is not implemented)" % args.gpus,
-              file=sys.stderr)
-        sys.exit(2)
-    import torch
-    import workloads
-    import paper_2608_15241_amd as lk
-    from paper_2608_15241_amd.step import Step, meta_to_device
+def cpu_cores():
+    """(threads the oracle runs on, CPUs in this process's affinity mask)."""
+    import oracle
+    return oracle.num_threads(), len(os.sched_getaffinity(0))
 
-    lk.load_library()
+
+def time_graph_steps(torch, graphs, steps, warmup):
+    """Replays graphs[i % n] `warmup` times, then times `steps` replays with
+    one event pair around each. Returns (median ms, mean ms over the
+    bracketed region)."""
+    for i in range(warmup):
+        graphs[i % len(graphs)].replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(steps):
+        graphs[i % len(graphs)].replay()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return float(np.median(per)), ev[0].elapsed_time(ev[-1]) / steps
+
+
+def bench_decode(torch, workloads, lk, w, args, with_cpu):
+    """Decode step of workload w: graph replays, attention launches, bytes, and
+    (with_cpu) the oracle on the same step. Frees its inputs before returning."""
+    from paper_2608_15241_amd.step import Step, meta_to_device
     dev = "cuda:0"
-    torch.cuda.set_device(0)
-    w = workloads.BY_NAME[args.workload]
-    primary = w.name == workloads.DECODE_7B.name
     meta = workloads.make_meta(w, seed=0)
     md = meta_to_device(meta, dev)
-    if args.traffic_probe:
-        traffic_probe(torch, workloads, w, meta, md, dev)
-        return
     n_sets = args.sets if w.n_layers == 1 else 1
     sets = []
     for s in range(n_sets):
@@ -187,39 +225,22 @@ def main():
         st = Step("decode", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
         sets.append((st, pool, weights, x))
     torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream()
-    # warmup (eager: sets kernel attributes on first launch), then one HIP
-    # graph per input set; a step is one graph replay
-    for i in range(max(args.warmup, len(sets))):
+    # eager steps first (they set kernel attributes), then one graph per set
+    for i in range(max(2, len(sets))):
         sets[i % len(sets)][0]()
     torch.cuda.synchronize()
     graphs = [st.capture() for st, *_ in sets]
-    for i in range(args.warmup):
-        graphs[i % len(graphs)].replay()
-    torch.cuda.synchronize()
-
-    say("timed steps")
+    say("timed steps", w.name)
     K = args.steps
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(K):
-        graphs[i % len(graphs)].replay()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_per_step = total_ms / K
+    ms_med, ms_mean = time_graph_steps(torch, graphs, K, args.warmup)
 
     # the dominant kernel (decode attention), timed with HIP events around
-    # each of its launches (every layer) in K eager steps on the same stream
-    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(K * w.n_layers)]
-    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K * w.n_layers)]
-    e_start = torch.cuda.Event(enable_timing=True)
-    e_end = torch.cuda.Event(enable_timing=True)
-    e_start.record(stream)
-    for i in range(K):
+    # each of its launches (every layer) in eager steps on the same stream
+    stream = torch.cuda.current_stream()
+    n_eager = max(2, min(K, 20))
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(n_eager * w.n_layers)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(n_eager * w.n_layers)]
+    for i in range(n_eager):
         st = sets[i % len(sets)][0]
         st.version_check()
         for l, lc in enumerate(st.layer_calls):
@@ -229,67 +250,270 @@ def main():
             lc["attn"]()
             ev_b[i * w.n_layers + l].record(stream)
             lc["o"]()
-    e_end.record(stream)
     torch.cuda.synchronize()
-    eager_ms = e_start.elapsed_time(e_end) / K
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]))
+    attn_ms = float(np.median([a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]))
 
     attn_bytes, step_bytes, valid_tokens = decode_bytes(w, meta)
-    tokens_per_s = meta.B / (ms_per_step / 1e3)
     attn_gbps = attn_bytes / (attn_ms / 1e3) / 1e9
-    step_gbps = step_bytes / (ms_per_step / 1e3) / 1e9
+    step_gbps = step_bytes / (ms_med / 1e3) / 1e9
+    rec = {
+        "tokens_per_s": round(meta.B / (ms_med / 1e3), 1),
+        "ms_per_step": round(ms_med, 5),
+        "ms_per_step_mean": round(ms_mean, 5),
+        "config": workload_config(w, meta, n_sets, valid_tokens),
+        "roofline": {"kernel": "local_paged_attn_decode", "bound": "hbm",
+                     "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": measured_traffic(w.name),
+                     "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5),
+                     "launches_timed": len(ev_a)},
+        "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
+                     "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
+    }
+    if w.name == "tiny_decode":
+        rec["note"] = ("launch-latency bound (the whole step's data fits in the last-level "
+                       "cache): the absolute step time is the figure; the fractions are not "
+                       "meaningful")
+    if with_cpu:
+        say("cpu baseline", w.name)
+        rec["cpu_baseline"] = cpu_decode(torch, workloads, w, meta, sets[0], args)
+    del graphs, sets, md
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
 
+
+def _h(torch, t):
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def _gather_blocks(torch, pool_l, hkv, D, meta, reqs):
+    """Host copies of the K and V blocks of `reqs` in one layer's pool, with
+    block ids renumbered in the order the requests own them. Returns
+    (k, v, table, block_version)."""
+    nb = [(int(meta.ctx_lens[b]) + 15) // 16 for b in reqs]
+    ids = np.concatenate([meta.block_table[b, :n] for b, n in zip(reqs, nb)]).astype(np.int64)
+    idx = torch.from_numpy(ids).to(pool_l.device)
+    per = hkv * 16 * D
+    k = _h(torch, pool_l[0].reshape(-1, per).index_select(0, idx)).reshape(-1)
+    v = _h(torch, pool_l[1].reshape(-1, per).index_select(0, idx)).reshape(-1)
+    table = np.zeros((len(reqs), max(nb)), np.int32)
+    off = 0
+    for i, n in enumerate(nb):
+        table[i, :n] = np.arange(off, off + n)
+        off += n
+    return k, v, table, meta.block_version[ids].astype(np.int32)
+
+
+def cpu_decode(torch, workloads, w, meta, set0, args):
+    """The oracle (float64 C, OpenMP) on the decode step of w on this host:
+    every request of a single-layer workload; for the 32-layer workload a
+    seeded sample of requests through every layer (the oracle's cost is linear
+    in the requests: each one reads every weight and its own KV), each layer's
+    blocks and weights copied to the host before its timed part."""
+    import oracle
+    import oracle.chain as ochain
+    st, pool, weights, x = set0
+    D = w.head_dim
+    if w.n_layers > 1:
+        rng = np.random.default_rng(2025)
+        reqs = np.sort(rng.choice(meta.B, size=CPU_SAMPLE_REQUESTS, replace=False))
+    else:
+        reqs = np.arange(meta.B)
+    ctx, rv = meta.ctx_lens[reqs], meta.req_version[reqs]
+    tok_a, tok_s = meta.token_adapter[reqs], meta.token_scale[reqs]
+    qi = np.arange(len(reqs) + 1, dtype=np.int32)
+
+    def run_once():
+        xo = _h(torch, x)[reqs]
+        t = 0.0
+        for l in range(w.n_layers):
+            lw = {k: (_h(torch, v) if v.dtype == torch.bfloat16 else v.cpu().numpy())
+                  for k, v in weights[l].items()}
+            kh, vh, table, bv = _gather_blocks(torch, pool[l], w.hkv, D, meta, reqs)
+            t0 = time.perf_counter()
+            if l == 0:
+                oracle.block_version_check(meta.block_table, meta.ctx_lens,
+                                           meta.block_version, meta.req_version)
+            xo, _ = ochain.layer(xo, lw, kh, vh, w.hq, w.hkv, D, table, qi, ctx, bv, rv,
+                                 tok_a, tok_s, residual=False)
+            t += time.perf_counter() - t0
+        return t
+
+    times = repeat_within_budget(run_once, args.cpu_budget_s)
+    t = float(np.median(times))
+    threads, affinity = cpu_cores()
+    rec = {"value": round(len(reqs) / t, 2), "unit": "tokens/s", "cores": threads,
+           "affinity_cpus": affinity, "kind": "oracle", "s_per_step": round(t, 4),
+           "runs": len(times)}
+    if w.n_layers > 1:
+        rec["sample"] = ("%d of %d requests (seeded) through all %d layers; timed part: the "
+                         "oracle's version check and layer steps, not the device-to-host "
+                         "copies of each layer's blocks and weights" %
+                         (len(reqs), meta.B, w.n_layers))
+        rec["extrapolated_s_per_step_%d_requests" % meta.B] = round(t * meta.B / len(reqs), 2)
+        rec["extrapolation"] = "linear in requests (labelled extrapolation, not measured)"
+    else:
+        rec["sample"] = "the whole decode step (%d requests, 1 layer)" % meta.B
+    return rec
+
+
+def repeat_within_budget(fn, budget_s):
+    """Runs fn once; if that run took under a quarter of the budget it was a
+    warm-up, and fn runs up to 3 more times while the total stays within the
+    budget. Returns the timed runs."""
+    t0 = time.time()
+    first = fn()
+    if first * 4 > budget_s:
+        return [first]
+    times = []
+    while len(times) < 3 and (time.time() - t0) + first <= budget_s:
+        times.append(fn())
+    return times or [first]
+
+
+def bench_prefill_step(torch, workloads, lk, args, with_cpu):
+    """The whole prefill step of prefill_7b_4x512 (version check, grouped
+    q/k/v, appending causal attention, o) as graph replays over two input
+    sets, plus its projections and its attention alone, and the oracle on the
+    same step."""
+    from paper_2608_15241_amd.step import Step, meta_to_device
+    w = workloads.PREFILL_7B
+    dev = "cuda:0"
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
+    sets = []
+    for s in range(2):
+        say("prefill input set", s)
+        weights = [workloads.make_layer_weights(w, 0, dev, seed=800 + s)]
+        pool = workloads.make_kv_pool(w, meta, dev, seed=800 + s)
+        x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=810 + s)
+        st = Step("prefill", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
+        sets.append((st, pool, weights, x))
+    for st, *_ in sets:
+        st()  # the step rewrites the same slots with the same values on every replay
+    torch.cuda.synchronize()
+    graphs = [st.capture() for st, *_ in sets]
+    ms_med, ms_mean = time_graph_steps(torch, graphs, args.steps, args.warmup)
+    gemm = prefill_gemm_flops(w, meta)
+    attn = prefill_attn_flops(w, meta)
+    tflops = (gemm + attn) / (ms_med / 1e3) / 1e12
+    rec = {"tokens_per_s": round(meta.T / (ms_med / 1e3), 1),
+           "ms_per_step": round(ms_med, 5), "ms_per_step_mean": round(ms_mean, 5),
+           "config": workload_config(w, meta, 2),
+           "mfma_step": {"flops_per_step": gemm + attn, "achieved": round(tflops, 1),
+                         "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}}
+    if with_cpu:
+        say("cpu baseline", w.name)
+        rec["cpu_baseline"] = cpu_prefill(torch, w, meta, sets[0], args)
+    del graphs, sets, md
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    say("prefill projections")
+    rec["projections"] = bench_prefill(torch, workloads, lk, dev)
+    say("prefill attention")
+    rec["attention"] = bench_prefill_attn(torch, workloads, lk, dev)
+    return rec
+
+
+def cpu_prefill(torch, w, meta, set0, args):
+    """The oracle on the whole prefill step (2048 tokens, 1 layer)."""
+    import oracle
+    import oracle.chain as ochain
+    st, pool, weights, x = set0
+    lw = {k: (_h(torch, v) if v.dtype == torch.bfloat16 else v.cpu().numpy())
+          for k, v in weights[0].items()}
+    kh, vh = _h(torch, pool[0, 0]).reshape(-1), _h(torch, pool[0, 1]).reshape(-1)
+    xh = _h(torch, x)
+
+    def run_once():
+        t0 = time.perf_counter()
+        oracle.block_version_check(meta.block_table, meta.ctx_lens, meta.block_version,
+                                   meta.req_version)
+        ochain.layer(xh, lw, kh, vh, w.hq, w.hkv, w.head_dim, meta.block_table,
+                     meta.q_indptr, meta.ctx_lens, meta.block_version, meta.req_version,
+                     meta.token_adapter, meta.token_scale, residual=False)
+        return time.perf_counter() - t0
+
+    times = repeat_within_budget(run_once, args.cpu_budget_s)
+    t = float(np.median(times))
+    threads, affinity = cpu_cores()
+    return {"value": round(meta.T / t, 2), "unit": "tokens/s", "cores": threads,
+            "affinity_cpus": affinity, "kind": "oracle", "s_per_step": round(t, 3),
+            "runs": len(times),
+            "sample": "the whole prefill step (%d tokens, 1 layer)" % meta.T}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
+              "(sharding across GPUs is not implemented)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads
+    import paper_2608_15241_amd as lk
+
+    lk.load_library()
+    torch.cuda.set_device(0)
+    if args.traffic_probe:
+        traffic_probe(torch, workloads, workloads.BY_NAME[
+            HEADLINE if args.workload == "all" else args.workload], "cuda:0")
+        return
+    alone = args.workload != "all"
+    head_name = HEADLINE if not alone else args.workload
+    with_cpu = not alone and not args.no_cpu_baseline
+
+    if head_name == "prefill_7b_4x512":
+        head = bench_prefill_step(torch, workloads, lk, args, False)
+        unit_tokens = "prefill tokens/s"
+    else:
+        head = bench_decode(torch, workloads, lk, workloads.BY_NAME[head_name], args,
+                            with_cpu)
+        unit_tokens = "tokens/s"
     result = {
         "metric": "decode tokens/s + achieved HBM GB/s (% peak); prefill LoRA-GEMM MFMA util",
-        "value": round(tokens_per_s, 1),
-        "unit": "tokens/s",
+        "value": head["tokens_per_s"],
+        "unit": unit_tokens,
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "layers": w.n_layers, "hidden": w.hidden,
-                   "heads": "%dq/%dkv x %d" % (w.hq, w.hkv, w.head_dim), "batch": meta.B,
-                   "context": context_text(w), "sum_context": int(meta.ctx_lens.sum()),
-                   "valid_kv_tokens": valid_tokens, "stale_frac": w.stale_frac,
-                   "adapters": adapters_text(w), "input_sets": n_sets},
-        "roofline": {"kernel": "local_paged_attn_decode", "bound": "hbm",
-                     "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": measured_traffic() if primary else None,
-                     "bytes_per_launch": attn_bytes, "ms_per_launch": round(attn_ms, 5)},
-        "hbm_step": {"bytes_per_step": step_bytes, "achieved": round(step_gbps, 1),
-                     "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4)},
-        "step_launch": {"mode": "hip_graph_replay", "eager_ms_per_step": round(eager_ms, 5)},
     }
+    for k, v in head.items():
+        if k not in ("tokens_per_s", "ms_per_step"):
+            result[k] = v
+    result["ms_per_step_note"] = "median of per-step event times over the timed graph replays"
 
-    if primary and not args.no_prefill:
-        say("prefill projections")
-        result["prefill"] = bench_prefill(torch, workloads, lk, dev)
-        say("prefill attention")
-        result["prefill_attn"] = bench_prefill_attn(torch, workloads, lk, dev)
+    if not alone:
+        subs = {}
+        for name in ("decode_7b_mha_b32", "gqa_skew_b64", "tiny_decode"):
+            subs[name] = bench_decode(torch, workloads, lk, workloads.BY_NAME[name], args,
+                                      with_cpu)
+        subs["prefill_7b_4x512"] = bench_prefill_step(torch, workloads, lk, args, with_cpu)
+        result["workloads"] = subs
         say("stale-coverage prefill")
-        result["reprefill"] = bench_reprefill(torch, workloads, lk, dev)
+        result["reprefill"] = bench_reprefill(torch, workloads, lk, "cuda:0")
         say("lora backward")
-        result["lora_grad"] = bench_lora_grad(torch, workloads, lk, dev)
-
-    if primary and not args.no_cpu_baseline:
-        say("cpu baseline")
-        result["cpu_baseline"] = cpu_baseline(torch, workloads, w, meta, sets[0], args)
-
-    del sets
+        result["lora_grad"] = bench_lora_grad(torch, workloads, lk, "cuda:0")
     print(json.dumps(result), flush=True)
 
 
-def traffic_probe(torch, workloads, w, meta, md, dev):
-    """A plain copy of known size, then decode attention launches, eagerly."""
-    from paper_2608_15241_amd.step import Step
+def traffic_probe(torch, workloads, w, dev):
+    """A plain copy of known size, then decode attention launches of layer 0
+    of workload w, eagerly."""
+    from paper_2608_15241_amd.step import Step, meta_to_device
+    meta = workloads.make_meta(w, seed=0)
+    md = meta_to_device(meta, dev)
     weights = [workloads.make_layer_weights(w, 0, dev, seed=100)]
-    pool = workloads.make_kv_pool(w, meta, dev, seed=100)
+    pool = workloads.make_kv_pool(w, meta, dev, seed=100, n_layers=1)
     x = workloads.randn_bf16((meta.T, w.hidden), 1.0, dev, seed=200)
     st = Step("decode", x, weights, md, pool, w.hq, w.hkv, w.head_dim, residual=False)
     st()
@@ -304,7 +528,8 @@ def traffic_probe(torch, workloads, w, meta, md, dev):
         st.layer_calls[0]["attn"]()
     torch.cuda.synchronize()
     attn_bytes, _, _ = decode_bytes(w, meta)
-    print(json.dumps({"traffic_probe": {"copy_read_bytes": n, "copy_write_bytes": n,
+    print(json.dumps({"traffic_probe": {"workload": w.name, "copy_read_bytes": n,
+                                        "copy_write_bytes": n,
                                         "copy_kernel": "torch.mul(src, 1.0, out=dst), bf16",
                                         "attn_launches": 5,
                                         "attn_algorithmic_bytes": attn_bytes,
@@ -647,43 +872,6 @@ def bench_lora_grad(torch, workloads, lk, dev, reps=20):
                            "flops_per_pass": fl, "ms_per_pass": round(ms_i, 5),
                            "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS,
                            "unit": "TFLOP/s", "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}}
-
-
-def cpu_baseline(torch, workloads, w, meta, set0, args):
-    """The oracle (float64 C, OpenMP) on the same decode step, on this host."""
-    import oracle
-    import oracle.chain as ochain
-    st, pool, weights, x = set0
-    D = w.head_dim
-
-    def h(t):
-        return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-
-    lw = {k: (h(v) if v.dtype == torch.bfloat16 else v.cpu().numpy())
-          for k, v in weights[0].items()}
-    kpool = h(pool[0, 0]).reshape(-1)
-    vpool = h(pool[0, 1]).reshape(-1)
-    xh = h(x)
-    qi = np.arange(meta.B + 1, dtype=np.int32)
-    times = []
-    t_budget = time.time() + args.cpu_budget_s
-    n_req = meta.B
-    while True:
-        kc, vc = kpool.copy(), vpool.copy()
-        t0 = time.perf_counter()
-        oracle.block_version_check(meta.block_table, meta.ctx_lens, meta.block_version,
-                                   meta.req_version)
-        ochain.layer(xh, lw, kc, vc, w.hq, w.hkv, D, meta.block_table, qi, meta.ctx_lens,
-                     meta.block_version, meta.req_version, meta.token_adapter,
-                     meta.token_scale, residual=False)
-        times.append(time.perf_counter() - t0)
-        if time.time() > t_budget or len(times) >= 5:
-            break
-    t = float(np.median(times))
-    return {"value": round(n_req / t, 2), "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "sample": "the whole decode step of the same workload "
-            "(%d requests, 1 layer), median of %d runs" % (n_req, len(times)),
-            "s_per_step": round(t, 3)}
 
 
 if __name__ == "__main__":
