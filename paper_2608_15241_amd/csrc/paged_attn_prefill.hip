@@ -33,7 +33,27 @@ constexpr int kPaQT = 2;                        // 16-row query tiles per wave
 constexpr int kPaRows = kPaWaves * 16 * kPaQT;  // query rows per workgroup (128)
 constexpr int kPaStages = 4;                    // LDS ring depth
 constexpr int kPaWindow = 256;                  // block-table entries listed per pass
-constexpr float kNegBigPf = -1.0e30f;
+constexpr float kNegBigPf = -1.0e30f;      // initial running maximum (finite)
+constexpr float kMaskedScore = -3.0e38f;   // score of a key a row may not see
+constexpr float kPaLazy = 8.0f;            // log2 of the largest weight before a rescale
+
+// max(a, b, c) in one instruction (fmaxf chains add NaN-quieting maxima)
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+// Tiles whose causal range spans more than kPaSplitBlocks blocks are split
+// into up to kPaMaxSplit key ranges of equal length, each its own workgroup;
+// a merge launch combines their partial results.
+#ifndef LOCAL_PA_SPLIT_BLOCKS
+#define LOCAL_PA_SPLIT_BLOCKS 48
+#endif
+#ifndef LOCAL_PA_MAX_SPLIT
+#define LOCAL_PA_MAX_SPLIT 4
+#endif
+constexpr int kPaSplitBlocks = LOCAL_PA_SPLIT_BLOCKS;
+constexpr int kPaMaxSplit = LOCAL_PA_MAX_SPLIT;
 
 struct PrefillArgs {
   const uint16_t* q;
@@ -48,9 +68,11 @@ struct PrefillArgs {
   const int32_t* req_version;
   uint16_t* out;
   float* lse;
+  float* part;  // workspace: partial results of split tiles
   int64_t T, num_blocks;
   int B, Hq, Hkv, group, max_blocks;
-  float scale_log2;
+  float scale_log2;  // |sm_scale| * log2(e)
+  uint32_t q_sign;   // 0x80008000 when sm_scale < 0 (q's sign bits flipped), else 0
 };
 
 __device__ __forceinline__ bool id_ok(int p, int64_t num_blocks) {
@@ -190,6 +212,30 @@ __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
   }
 }
 
+// Logical blocks that tile t of a request (prefix P, n_b rows) sees: up to
+// its last row's position, at most the table's width.
+__device__ __forceinline__ int tile_blocks(int P, int n_b, int t, int max_blocks) {
+  const int lim = P + min((t + 1) * kPaRows, n_b) - 1;
+  return lim < 0 ? 0 : min(lim / kBlockSize + 1, max_blocks);
+}
+
+// Key ranges a tile of nbl blocks is split into.
+__device__ __forceinline__ int tile_splits(int nbl) {
+  return nbl <= kPaSplitBlocks ? 1 : min(kPaMaxSplit, (nbl + kPaSplitBlocks - 1) / kPaSplitBlocks);
+}
+
+// Partial-result slot of (tile t of request b with rows from r0, head h,
+// split): r0/128 + b + t is unique over the requests' tiles and below
+// T/128 + B, the bound the host sizes the workspace by.
+__device__ __forceinline__ int64_t part_slot(int r0, int b, int t, int h, int Hq, int split) {
+  return (static_cast<int64_t>(r0 / kPaRows + b + t) * Hq + h) * kPaMaxSplit + split;
+}
+
+template <int D>
+constexpr int64_t part_slot_floats() {
+  return static_cast<int64_t>(kPaRows) * (D + 2);  // O [128][D], then (m, l) [128][2]
+}
+
 template <int D>
 __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs a) {
   constexpr int QT = kPaQT, KC = D / 32, VT = D / 16;
@@ -202,34 +248,53 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   __shared__ int list_p[kPaWindow];  // their physical ids
   __shared__ int wave_cnt[kPaWaves];
 
-  // (query tile, head h, request b) from a 1D grid, heads fastest: the last
-  // requests' last tiles (a chunk's later rows see more keys, and requests
-  // are commonly listed by growing prefix) are dispatched first, so that the
-  // longest workgroups do not start behind short ones
+  // (query tile, key range, head h, request b) from a 1D grid, heads
+  // fastest: the last requests' last tiles (a chunk's later rows see more
+  // keys, and requests are commonly listed by growing prefix) are dispatched
+  // first, so that the longest workgroups do not start behind short ones. A
+  // tile with a long causal range is split into key ranges (units of their
+  // own) so that no workgroup holds far more work than the mean.
   const int h = blockIdx.x % a.Hq;
-  int qtile = 0;
-  auto row_tiles = [&](int bb) {
+  int unit = 0;
+  auto units_of = [&](int bb) {
     const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
     const int n = r1 - r0;
-    return rows_ok(r0, r1, a.T) && n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
+    if (!rows_ok(r0, r1, a.T) || n <= 0) return 0;
+    const int P = a.ctx_lens[bb] - n;
+    int u = 0;
+    for (int t = 0; t * kPaRows < n; ++t) u += tile_splits(tile_blocks(P, n, t, a.max_blocks));
+    return u;
   };
-  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hq), row_tiles, &qtile);
+  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hq), units_of, &unit);
   if (b < 0) return;
   const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
   if (!rows_ok(r0, r1, a.T)) return;  // never given a unit
   const int n_b = r1 - r0;
+  const int L = a.ctx_lens[b];
+  const int P = L - n_b;  // cached prefix
+  int qtile = 0, split = 0, n_split = 1;
+  for (int t = 0, u = unit; t * kPaRows < n_b; ++t) {
+    const int ns = tile_splits(tile_blocks(P, n_b, t, a.max_blocks));
+    if (u < ns) {
+      qtile = t;
+      split = u;
+      n_split = ns;
+      break;
+    }
+    u -= ns;
+  }
   const int row0 = qtile * kPaRows;
   if (row0 >= n_b) return;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
-  const int L = a.ctx_lens[b];
-  const int P = L - n_b;  // cached prefix
   const int g = h / a.group;
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
 
-  // Query columns of this wave: rows row0 + 32 wave + 16 ct + col.
+  // Query columns of this wave: rows row0 + 32 wave + 16 ct + col. For a
+  // negative softmax scale the query's sign bits are flipped (exact), so
+  // the kernel only ever scales by |sm_scale|.
   bf16x8 qv[QT][KC];
   int qpos[QT];
   u32x4 qraw[QT][KC];
@@ -250,16 +315,19 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       asm volatile("" : "+v"(qraw[ct][c]));
-      qv[ct][c] = as_bf16x8(qraw[ct][c]);
+      qv[ct][c] = as_bf16x8(qraw[ct][c] ^ a.q_sign);
     }
+  const float scl = a.scale_log2;
   const int wave_last_row = min(row0 + (wave + 1) * 16 * QT, n_b) - 1;
   const int wave_limit = P + wave_last_row;  // largest key position this wave sees
   const int wave_first = P + row0 + wave * 16 * QT;  // position of its first row
-  const int wg_limit = P + min(row0 + kPaRows, n_b) - 1;
-  const int nb_lim = wg_limit < 0 ? 0 : min(wg_limit / kBlockSize + 1, a.max_blocks);
+  const int nb_tile = tile_blocks(P, n_b, qtile, a.max_blocks);
+  // this unit's key range: logical blocks [j_lo, j_hi) of the tile's range
+  const int j_lo = split * nb_tile / n_split, j_hi = (split + 1) * nb_tile / n_split;
 
   f32x4 acc[QT][VT];
-  float m_run[QT], l_run[QT];
+  float m_run[QT];             // running maximum in raw score units
+  float l_run[QT];             // this lane's part of the running sum of p
 #pragma unroll
   for (int ct = 0; ct < QT; ++ct) {
     m_run[ct] = kNegBigPf;
@@ -268,16 +336,48 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     for (int t = 0; t < VT; ++t) acc[ct][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // wave w moves tile w of a step: block w / 2 of the step, K (w even) or V
-  const int my_blk = wave / 2, my_kind = wave % 2;
-  const uint16_t* pool = my_kind ? a.v_cache : a.k_cache;
+  // A ring stage holds one step (two blocks A, B): K_A [KC][1 KB], K_B
+  // [KC][1 KB], then V as VT rows of 1 KB, row t = (A's dims 16t .. 16t+15,
+  // then B's), 512 bytes each. Within a 512-byte V row the 16-byte chunks are
+  // swizzled: chunk (dim d, slots 8 half .. +8) sits at chunk index
+  // 2 (d % 16) + (half ^ bit 3 of d), so that the 32 lanes of each half of a
+  // value-fragment read cover 256 contiguous bytes of banks, and a lane's
+  // fragments of A and B are one paired read 512 bytes apart. The stage is
+  // filled by NPIECE direct 1 KB loads, NPIECE / 4 per wave; lane l of a
+  // piece fetches the 16 bytes that land at byte 16 l of it.
+  constexpr int NPIECE = 2 * DMA + VT;
+  constexpr int PPW = NPIECE / kPaWaves;
+  static_assert(NPIECE % kPaWaves == 0 && STAGE_B == NPIECE * 1024, "stage layout");
+  int piece_blk[PPW];             // 0: block A, 1: block B
+  uint32_t piece_src[PPW];        // byte offset within that block's tile
+  const uint16_t* piece_pool[PPW];
+#pragma unroll
+  for (int i = 0; i < PPW; ++i) {
+    const int pc = wave * PPW + i;
+    if (pc < 2 * DMA) {  // K: 1 KB piece pc % DMA of block pc / DMA
+      piece_blk[i] = pc / DMA;
+      piece_src[i] = static_cast<uint32_t>(1024 * (pc % DMA) + 16 * lane);
+      piece_pool[i] = a.k_cache;
+    } else {             // V row t: lanes 0-31 from A, 32-63 from B
+      const int t = pc - 2 * DMA;
+      const int cidx = lane & 31;
+      const int dl = cidx >> 1;  // dim within the row (d = 16 t + dl)
+      const int half = (cidx & 1) ^ ((dl >> 3) & 1);
+      piece_blk[i] = lane >> 5;
+      piece_src[i] = static_cast<uint32_t>(32 * (16 * t + dl) + 16 * half);
+      piece_pool[i] = a.v_cache;
+    }
+  }
+  // this lane's value fragment in V row t of a stage (A's half; B's is 512
+  // bytes on): dim 16 t + col, slots 4 kgrp .. +4
+  const uint32_t v_off = 32 * col + 16 * ((kgrp >> 1) ^ ((col >> 3) & 1)) + 8 * (kgrp & 1);
 
-  for (int w0 = 0; w0 < nb_lim; w0 += kPaWindow) {
+  for (int w0 = j_lo; w0 < j_hi; w0 += kPaWindow) {
     // ---- list the non-stale blocks of this window, in ascending j
     const int j = w0 + tid;
     bool ok = false;
     int p = 0;
-    if (j < nb_lim) {
+    if (j < j_hi) {
       p = table[j];
       ok = id_ok(p, a.num_blocks) && a.block_version[p] == rv;
     }
@@ -298,19 +398,23 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     if (cnt == 0) continue;
     const int steps = (cnt + 1) / 2;
 
-    // loads of step s into ring stage `stage`: this wave's tile. Physical
+    // loads of step s into ring stage `stage`: this wave's pieces. Physical
     // ids come from LDS (a load of the block table here would make the wave
     // wait for every load before it). A step's second block past the list
     // end repeats its first (never used), and steps past the last repeat the
     // last into the free stage, so every step issues the same loads and the
     // wait counts hold.
     auto issue = [&](int stage, int s) {
-      const int p = list_p[min(2 * s + my_blk, cnt - 1)];
-      const uint8_t* src = reinterpret_cast<const uint8_t*>(
-          pool + (static_cast<int64_t>(p) * a.Hkv + g) * TILE);
-      uint8_t* dst = ring + stage * STAGE_B + wave * TILE_B;
+      const int pa = list_p[min(2 * s, cnt - 1)];
+      const int pb = list_p[min(2 * s + 1, cnt - 1)];
+      uint8_t* dst = ring + stage * STAGE_B + wave * PPW * 1024;
 #pragma unroll
-      for (int q = 0; q < DMA; ++q) lds_load16(src + 1024 * q + 16 * lane, dst + 1024 * q);
+      for (int i = 0; i < PPW; ++i) {
+        const int pp = piece_blk[i] ? pb : pa;
+        const uint8_t* src = reinterpret_cast<const uint8_t*>(
+            piece_pool[i] + (static_cast<int64_t>(pp) * a.Hkv + g) * TILE);
+        lds_load16(src + piece_src[i], dst + 1024 * i);
+      }
     };
 #pragma unroll
     for (int s = 0; s < kPaStages - 1; ++s) issue(s, min(s, steps - 1));
@@ -319,7 +423,7 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       // this wave's loads of step s are done (those of the two later steps
       // may still fly); after the barrier everyone's are, and the stage of
       // step s - 1 is free for step s + 3
-      wait_vmcnt<DMA * (kPaStages - 2)>();
+      wait_vmcnt<PPW * (kPaStages - 2)>();
       wait_lgkm0_barrier();
       issue((s + kPaStages - 1) % kPaStages, min(s + kPaStages - 1, steps - 1));
       const int jA = list[2 * s];
@@ -331,36 +435,40 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       const bool unmasked = hasB && jB * kBlockSize + kBlockSize - 1 <= wave_first;
       const uint8_t* st = ring + (s % kPaStages) * STAGE_B;
       const uint16_t* kA = reinterpret_cast<const uint16_t*>(st);
-      const uint16_t* vA = reinterpret_cast<const uint16_t*>(st + TILE_B);
-      const uint16_t* kB = reinterpret_cast<const uint16_t*>(st + 2 * TILE_B);
-      const uint16_t* vB = reinterpret_cast<const uint16_t*>(st + 3 * TILE_B);
+      const uint16_t* kB = reinterpret_cast<const uint16_t*>(st + TILE_B);
+      const uint8_t* vrow = st + 2 * TILE_B + v_off;
       bf16x8 kfa[KC], kfb[KC];
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
         kfa[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kA + c * 512 + lane * 8));
         kfb[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kB + c * 512 + lane * 8));
       }
-      // V fragments: slots 4 kgrp .. +4 of each block; slots at or past the
-      // context end are zeroed (they may hold anything)
-      const int liveA = L - jA * kBlockSize - 4 * kgrp;
-      const int liveB = hasB ? L - jB * kBlockSize - 4 * kgrp : 0;
+      // V fragments: slots 4 kgrp .. +4 of each block. Slots at or past the
+      // context end may hold anything and are zeroed; only a step that holds
+      // the context end (or has no second block) needs it, and that is the
+      // same for the whole wave.
       bf16x8 vf[VT];
 #pragma unroll
       for (int t = 0; t < VT; ++t) {
-        u32x2 va = *reinterpret_cast<const u32x2*>(vA + (16 * t + col) * kBlockSize + 4 * kgrp);
-        u32x2 vb = *reinterpret_cast<const u32x2*>(vB + (16 * t + col) * kBlockSize + 4 * kgrp);
-        if (liveA < 4) {
-          va.x = liveA <= 0 ? 0u : (liveA == 1 ? va.x & 0xffffu : va.x);
-          va.y = liveA <= 2 ? 0u : va.y & 0xffffu;
-        }
-        if (liveB < 4) {
-          vb.x = liveB <= 0 ? 0u : (liveB == 1 ? vb.x & 0xffffu : vb.x);
-          vb.y = liveB <= 2 ? 0u : vb.y & 0xffffu;
-        }
+        const u32x2 va = *reinterpret_cast<const u32x2*>(vrow + 1024 * t);
+        const u32x2 vb = *reinterpret_cast<const u32x2*>(vrow + 1024 * t + 512);
         vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
       }
+      const bool tail = !hasB || (jA + 1) * kBlockSize > L || (jB + 1) * kBlockSize > L;
+      if (tail) {
+        const int la = L - jA * kBlockSize - 4 * kgrp;
+        const int lb = hasB ? L - jB * kBlockSize - 4 * kgrp : 0;
+        const u32x4 mk = {la >= 2 ? ~0u : (la == 1 ? 0xffffu : 0u),
+                          la >= 4 ? ~0u : (la == 3 ? 0xffffu : 0u),
+                          lb >= 2 ? ~0u : (lb == 1 ? 0xffffu : 0u),
+                          lb >= 4 ? ~0u : (lb == 3 ? 0xffffu : 0u)};
+#pragma unroll
+        for (int t = 0; t < VT; ++t)
+          vf[t] = as_bf16x8(__builtin_bit_cast(u32x4, vf[t]) & mk);
+      }
       // S^T of both column tiles: 2 * QT independent chains of KC MFMAs,
-      // interleaved so that no MFMA waits on the one before it
+      // interleaved so that no MFMA waits on the one before it (raw scores:
+      // the scale is applied in the exponent)
       f32x4 sA[QT], sB[QT];
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
@@ -374,57 +482,65 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
           sA[ct] = mfma16x16x32(kfa[c], qv[ct][c], sA[ct]);
           sB[ct] = mfma16x16x32(kfb[c], qv[ct][c], sB[ct]);
         }
-      // scaled (and, near the diagonal or the context end, masked) scores
-      float sc[QT][8], m_new[QT];
+      // raw scores; near the diagonal or the context end a key a row may
+      // not see gets kMaskedScore, whose weight 2^(scale (s - m)) is 0 (the
+      // scale is never 0: a zero scale runs as a vanishing positive one)
+      float sc[QT][8];
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
-        if (unmasked) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            sc[ct][i] = sA[ct][i] * a.scale_log2;
-            sc[ct][4 + i] = sB[ct][i] * a.scale_log2;
-          }
-        } else {
+        for (int i = 0; i < 4; ++i) {
+          sc[ct][i] = sA[ct][i];
+          sc[ct][4 + i] = sB[ct][i];
+        }
+      }
+      if (!unmasked) {
+#pragma unroll
+        for (int ct = 0; ct < QT; ++ct)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int posA = jA * kBlockSize + 4 * kgrp + i;
             const int posB = jB * kBlockSize + 4 * kgrp + i;
-            sc[ct][i] = posA <= qpos[ct] ? sA[ct][i] * a.scale_log2 : -INFINITY;
-            sc[ct][4 + i] = (hasB && posB <= qpos[ct]) ? sB[ct][i] * a.scale_log2 : -INFINITY;
+            sc[ct][i] = posA <= qpos[ct] ? sc[ct][i] : kMaskedScore;
+            sc[ct][4 + i] = (hasB && posB <= qpos[ct]) ? sc[ct][4 + i] : kMaskedScore;
           }
-        }
-        float mx = sc[ct][0];
+      }
+      // Lazy rescale: the running maximum moves only when a column's maximum
+      // exceeds it by more than 2^kPaLazy in weight; weights up to that stay
+      // exact in float32 and bf16 alike, so the result is the same softmax.
+      bool grow = false;
+      float m_new[QT];
 #pragma unroll
-        for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[ct][i]);
+      for (int ct = 0; ct < QT; ++ct) {
+        float mx = max3f(max3f(sc[ct][0], sc[ct][1], sc[ct][2]),
+                         max3f(sc[ct][3], sc[ct][4], sc[ct][5]), fmaxf(sc[ct][6], sc[ct][7]));
         mx = max_xor32(max_xor16(mx));
         m_new[ct] = fmaxf(m_run[ct], mx);
+        grow = grow || (m_new[ct] - m_run[ct]) * scl > kPaLazy;
       }
-      // the running sums are rescaled only when some column's maximum grew
-      // (elsewhere the factor is exactly 1)
-      bool grew = false;
-#pragma unroll
-      for (int ct = 0; ct < QT; ++ct) grew = grew || m_new[ct] > m_run[ct];
-      if (__ballot(grew) != 0ull) {
+      if (__ballot(grow) != 0ull) {
 #pragma unroll
         for (int ct = 0; ct < QT; ++ct) {
-          const float alpha = fast_exp2(m_run[ct] - m_new[ct]);
+          const float alpha = fast_exp2((m_run[ct] - m_new[ct]) * scl);
           l_run[ct] *= alpha;
 #pragma unroll
           for (int t = 0; t < VT; ++t) acc[ct][t] *= alpha;
           m_run[ct] = m_new[ct];
         }
       }
+      // p = 2^(scale (s - m)), one fused multiply-add and one exponent each;
+      // the float32 sum as a pairwise tree
       bf16x8 pb[QT];
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
-        float psum = 0.f;
+        const float nms = -m_run[ct] * scl;
+        float pr[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const float pr = fast_exp2(sc[ct][i] - m_run[ct]);
-          psum += pr;
-          pb[ct][i] = static_cast<__bf16>(pr);
+          pr[i] = fast_exp2(__builtin_fmaf(sc[ct][i], scl, nms));
+          pb[ct][i] = static_cast<__bf16>(pr[i]);
         }
-        l_run[ct] += psum;
+        l_run[ct] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
       }
 #pragma unroll
       for (int t = 0; t < VT; ++t)
@@ -436,14 +552,16 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     wait_lgkm0_barrier();
   }
 
-  // ---- normalise and write this wave's rows
+  // ---- this wave's rows: normalised output, or the partial result of a split
 #pragma unroll
   for (int ct = 0; ct < QT; ++ct) {
     float l = l_run[ct];
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
-    const int row = row0 + wave * 16 * QT + 16 * ct + col;
-    if (row < n_b) {
+    const int rl = wave * 16 * QT + 16 * ct + col;  // row within the tile
+    const int row = row0 + rl;
+    if (row >= n_b) continue;
+    if (n_split == 1) {
       const int64_t orow = (static_cast<int64_t>(r0 + row) * a.Hq + h);
       const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
@@ -454,9 +572,89 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         *reinterpret_cast<u32x2*>(a.out + orow * D + d0) = u32x2{lo, hi};
       }
       if (kgrp == 0 && a.lse)
-        a.lse[orow] = l > 0.f ? (m_run[ct] + __log2f(l)) * kLn2 : -INFINITY;
+        a.lse[orow] = l > 0.f ? (m_run[ct] * scl + __log2f(l)) * kLn2 : -INFINITY;
+    } else {
+      float* slot = a.part + part_slot(r0, b, qtile, h, a.Hq, split) * part_slot_floats<D>();
+#pragma unroll
+      for (int t = 0; t < VT; ++t)
+        *reinterpret_cast<f32x4*>(slot + rl * D + 16 * t + 4 * kgrp) = acc[ct][t];
+      if (kgrp == 0)
+        *reinterpret_cast<float2*>(slot + kPaRows * D + 2 * rl) = float2{m_run[ct], l};
     }
   }
+}
+
+// Merge of the split tiles: workgroup = (tile, head, group of rows), the
+// tile and head mapped as in the attention grid without the splits; tiles
+// that were not split were written in place and leave at once. A thread owns
+// 8 dims of one row and issues every load of every key range before any
+// arithmetic.
+template <int D>
+__global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillArgs a) {
+  constexpr int TPR = D / 8;           // threads per row
+  constexpr int RPW = 256 / TPR;       // rows per workgroup
+  constexpr int RG = kPaRows / RPW;    // row groups per tile
+  const int rg = blockIdx.x % RG;
+  const int h = (blockIdx.x / RG) % a.Hq;
+  int qtile = 0;
+  auto row_tiles = [&](int bb) {
+    const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
+    const int n = r1 - r0;
+    return rows_ok(r0, r1, a.T) && n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
+  };
+  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / (RG * a.Hq)), row_tiles, &qtile);
+  if (b < 0) return;
+  const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
+  if (!rows_ok(r0, r1, a.T)) return;
+  const int n_b = r1 - r0;
+  const int P = a.ctx_lens[b] - n_b;
+  const int ns = tile_splits(tile_blocks(P, n_b, qtile, a.max_blocks));
+  if (ns == 1) return;
+  const int rl = rg * RPW + threadIdx.x / TPR;  // row within the tile
+  const int d0 = 8 * (threadIdx.x % TPR);
+  if (qtile * kPaRows + rl >= n_b) return;
+  const float* base = a.part + part_slot(r0, b, qtile, h, a.Hq, 0) * part_slot_floats<D>();
+  float2 ml[kPaMaxSplit];
+  f32x4 o0[kPaMaxSplit], o1[kPaMaxSplit];
+#pragma unroll
+  for (int i = 0; i < kPaMaxSplit; ++i) {
+    if (i < ns) {
+      const float* sl = base + i * part_slot_floats<D>();
+      ml[i] = *reinterpret_cast<const float2*>(sl + kPaRows * D + 2 * rl);
+      o0[i] = *reinterpret_cast<const f32x4*>(sl + rl * D + d0);
+      o1[i] = *reinterpret_cast<const f32x4*>(sl + rl * D + d0 + 4);
+    }
+  }
+  const float scl = a.scale_log2;
+  float M = kNegBigPf;
+#pragma unroll
+  for (int i = 0; i < kPaMaxSplit; ++i)
+    if (i < ns) M = fmaxf(M, ml[i].x);
+  float den = 0.f;
+  f32x4 n0 = {0.f, 0.f, 0.f, 0.f}, n1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < kPaMaxSplit; ++i) {
+    if (i < ns) {
+      const float f = fast_exp2((ml[i].x - M) * scl);
+      den += ml[i].y * f;
+      n0 += o0[i] * f;
+      n1 += o1[i] * f;
+    }
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const int64_t orow = static_cast<int64_t>(r0 + qtile * kPaRows + rl) * a.Hq + h;
+  *reinterpret_cast<u32x4*>(a.out + orow * D + d0) =
+      u32x4{pack_bf16x2(n0[0] * inv, n0[1] * inv), pack_bf16x2(n0[2] * inv, n0[3] * inv),
+            pack_bf16x2(n1[0] * inv, n1[1] * inv), pack_bf16x2(n1[2] * inv, n1[3] * inv)};
+  if (d0 == 0 && a.lse) a.lse[orow] = den > 0.f ? (M * scl + __log2f(den)) * kLn2 : -INFINITY;
+}
+
+// Workspace of the split tiles' partial results: one slot per (tile bound,
+// head, split).
+template <int D>
+size_t prefill_ws_bytes(int64_t T, int B, int Hq) {
+  const int64_t tiles = T / kPaRows + B;
+  return static_cast<size_t>(tiles) * Hq * kPaMaxSplit * part_slot_floats<D>() * sizeof(float);
 }
 
 template <int D>
@@ -475,10 +673,15 @@ local_status_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
                               hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
     done = true;
   }
-  // a chunk of n rows has at most n / 128 + 1 tiles: T / 128 + B in all
+  // a chunk of n rows has at most n / 128 + 1 tiles (T / 128 + B in all),
+  // each of at most kPaMaxSplit key ranges
   const int64_t tiles = a.T / kPaRows + a.B;
-  prefill_attn_kernel<D><<<static_cast<unsigned>(tiles * a.Hq), kPaThreads, kLds, s>>>(a);
-  return local_check_launch("paged_attn_prefill");
+  prefill_attn_kernel<D>
+      <<<static_cast<unsigned>(tiles * kPaMaxSplit * a.Hq), kPaThreads, kLds, s>>>(a);
+  local_status_t st = local_check_launch("paged_attn_prefill");
+  if (st != LOCAL_OK) return st;
+  prefill_merge_kernel<D><<<static_cast<unsigned>(tiles * a.Hq * (D / 16)), 256, 0, s>>>(a);
+  return local_check_launch("paged_attn_prefill (merge)");
 }
 
 }  // namespace
@@ -493,7 +696,6 @@ extern "C" local_status_t local_paged_attn_prefill(
     const int32_t* block_table, int32_t max_blocks, const int32_t* ctx_lens,
     const int32_t* block_version, const int32_t* req_version, float sm_scale,
     uint16_t* out, float* lse, void* ws, size_t* ws_bytes, void* stream) {
-  (void)ws;
   if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "paged_attn_prefill: ws_bytes is NULL");
   if (B < 0 || T < 0 || Hq <= 0 || Hkv <= 0 || max_blocks < 1 || num_blocks < 1 ||
       Hq % Hkv != 0)
@@ -505,10 +707,17 @@ extern "C" local_status_t local_paged_attn_prefill(
                       block_size, D);
   if ((k_new == nullptr) != (v_new == nullptr))
     return local_fail(LOCAL_ERR_NULL, "paged_attn_prefill: k_new and v_new must both be set");
+  if ((T / kPaRows + 2LL * B) * (kPaMaxSplit > 8 ? kPaMaxSplit : 8) * Hq >= (1LL << 31) ||
+      (T / kBlockSize + 2LL * B) * Hq >= (1LL << 31))
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "paged_attn_prefill: T=%lld too large", (long long)T);
+  const size_t need = D == 64 ? prefill_ws_bytes<64>(T, B, Hq) : prefill_ws_bytes<128>(T, B, Hq);
   if (!ws) {
-    *ws_bytes = 0;
+    *ws_bytes = need;
     return LOCAL_OK;
   }
+  if (*ws_bytes < need)
+    return local_fail(LOCAL_ERR_WORKSPACE, "paged_attn_prefill: workspace %zu < %zu", *ws_bytes,
+                      need);
   if (B == 0 || T == 0) return LOCAL_OK;
   if (!q || !q_indptr || !k_cache || !v_cache || !block_table || !ctx_lens ||
       !block_version || !req_version || !out)
@@ -536,9 +745,11 @@ extern "C" local_status_t local_paged_attn_prefill(
   a.Hkv = Hkv;
   a.group = Hq / Hkv;
   a.max_blocks = max_blocks;
-  a.scale_log2 = sm_scale * kLog2e;
-  if ((T / kBlockSize + 2LL * B) * Hq >= (1LL << 31))
-    return local_fail(LOCAL_ERR_UNSUPPORTED, "paged_attn_prefill: T=%lld too large", (long long)T);
+  a.part = static_cast<float*>(ws);
+  // |sm_scale|; a zero scale (every visible key weighs the same) runs as a
+  // vanishing positive one, under which masked keys still weigh exactly 0
+  a.scale_log2 = fmaxf(fabsf(sm_scale) * kLog2e, 1.0e-30f);
+  a.q_sign = sm_scale < 0.f ? 0x80008000u : 0u;
   hipStream_t s = static_cast<hipStream_t>(stream);
   return D == 64 ? launch_prefill<64>(a, s) : launch_prefill<128>(a, s);
 }

@@ -331,3 +331,34 @@ def test_binding_rejects_wrong_output_and_tag_shapes():
         lk.prepare_paged_attn_prefill(args[0], dev(qi), args[1], args[2], args[3], args[4],
                                       args[5], args[6], 0.125, Hkv=2, out=torch.empty(
                                           (3, 8, 64), dtype=torch.bfloat16, device="cuda"))
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_prefill_long_prefixes_split_key_ranges(D):
+    # Tiles whose causal range is long are split into 2 to 4 key ranges run
+    # by different workgroups and merged: long prefixes, chunks ending inside
+    # a tile, a request whose whole first key range is stale (a split with no
+    # valid key), a one-token chunk on a long prefix, and a negative scale
+    # for one of the two head dims.
+    say("prefill split key ranges", D)
+    rng = np.random.default_rng(900 + D)
+    Hq, Hkv = 8, 2
+    c = _prefill_case(rng, [3000, 1500, 800, 0, 5000, 2047], [130, 300, 17, 256, 1, 200],
+                      Hq, Hkv, D, 0.1)
+    # request 0: its first 70 blocks stale, so its tiles' first key range is empty
+    c["bv"][c["table"][0, :70]] = c["rv"][0] - 1
+    scale = -1.0 / math.sqrt(D) if D == 64 else 1.0 / math.sqrt(D)
+    kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    out, lse = lk.local_paged_attn_prefill(
+        dev_u16(c["q"]), dev(c["qi"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]),
+        dev(c["bv"]), dev(c["rv"]), scale, k_new=dev_u16(c["kn"]), v_new=dev_u16(c["vn"]),
+        Hkv=Hkv)
+    torch.cuda.synchronize()
+    kc, vc = c["kc"].copy(), c["vc"].copy()
+    oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
+    ro, rl = oracle.paged_attn(c["q"], c["qi"], Hq, Hkv, D, kc, vc, c["table"], c["ctx"],
+                               c["bv"], c["rv"], scale)
+    assert np.array_equal(host_u16(kc_d), kc), "appended K pool differs"
+    assert np.array_equal(host_u16(vc_d), vc), "appended V pool differs"
+    assert_attn(f64(out), ro, "out", D)
+    assert_lse(lse.cpu().numpy(), rl, "lse")

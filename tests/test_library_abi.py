@@ -109,7 +109,13 @@ def test_decode_workspace_and_errors(lib):
 def test_prefill_and_version_check_errors(lib):
     st, n = _size(lib.local_paged_attn_prefill, FAKE, FAKE, 4, 2048, 32, 32, 128, FAKE, FAKE,
                   FAKE, FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE)
-    assert st == OK and n == 0
+    # partial results of split tiles: (T/128 + B) tiles x 32 heads x 4 key ranges x
+    # 128 rows x (D + 2) floats
+    assert st == OK and n == (2048 // 128 + 4) * 32 * 4 * 128 * (128 + 2) * 4
+    ws = ctypes.c_size_t(n - 1)
+    assert lib.local_paged_attn_prefill(FAKE, FAKE, 4, 2048, 32, 32, 128, FAKE, FAKE, FAKE,
+                                        FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE,
+                                        FAKE, FAKE, ctypes.byref(ws), None) == ERR_WORKSPACE
     st, _ = _size(lib.local_paged_attn_prefill, FAKE, FAKE, 4, 2048, 32, 32, 80, FAKE, FAKE,
                   FAKE, FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE)
     assert st == ERR_UNSUPPORTED
