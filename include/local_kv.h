@@ -18,6 +18,10 @@
  *     manager plans which hot prefixes to re-prefill under it, the caller
  *     runs those chunks with the kernels under the staged version, and
  *     publication makes the staged version the committed one.
+ *   - §5.4 priority-based retention and offload: records held by an active
+ *     request (pinned, below) are never offload candidates; the others are
+ *     released coldest first (Pi_keep ascending, larger footprint first),
+ *     the shortest prefix of that order that reaches the target.
  *   - §4.3 failed work creates no reusable coverage: discarding a staged
  *     version drops every record made under it.
  *
@@ -29,7 +33,13 @@
  *              owns. Nothing here touches the GPU.
  *  Blocks      Physical block ids 0 .. num_blocks-1 of the KV pools passed to
  *              the kernels. A block is free, allocated (handed to the caller,
- *              not yet recorded) or recorded (owned by one record).
+ *              not yet recorded) or recorded (owned by one record). A
+ *              recorded block may also be pinned by the requests that hold
+ *              it (local_kvm_pin): pinned blocks are never evicted.
+ *  Versions    A version number belongs to the first adapter that uses it
+ *              (committed or staged); every other adapter is refused it, so
+ *              that a block's tag alone identifies both the adapter and the
+ *              version of the validity key.
  *  Tags        local_kvm_tags returns the version tag of every block, the
  *              `block_version` array the kernels read (the caller copies it
  *              to the device). An allocated or recorded block carries the
@@ -97,12 +107,13 @@ const int32_t* local_kvm_tags(const local_kvm_t* m);
 
 /* Registers adapter `adapter` (>= 0) with committed version `version`
  * (>= 1), or sets the committed version of a registered adapter that has no
- * staged version. */
+ * staged version. LOCAL_ERR_SHAPE when another adapter has used `version`. */
 local_status_t local_kvm_set_committed(local_kvm_t* m, int32_t adapter, int32_t version);
 
 /* Stages `version` (>= 1, different from the committed one and from every
- * version the adapter has had) for a registered adapter with no staged
- * version. Its adapter heat gets the staged-urgency signal (g_A = 1). */
+ * version the adapter has had, and never used by another adapter) for a
+ * registered adapter with no staged version. Its adapter heat gets the
+ * staged-urgency signal (g_A = 1). */
 local_status_t local_kvm_stage(local_kvm_t* m, int32_t adapter, int32_t version);
 
 /* Publication: the staged version becomes the committed one. *old_version
@@ -113,7 +124,8 @@ local_status_t local_kvm_publish(local_kvm_t* m, int32_t adapter, int32_t* old_v
 /* A staged version that will not be published (failed training, §4.3): every
  * record under it is dropped and its blocks freed; *n_freed (may be NULL)
  * receives their number. Blocks allocated under it and not yet recorded
- * stay with the caller, who releases them. */
+ * stay with the caller, who releases them. LOCAL_ERR_SHAPE (nothing dropped)
+ * while a record under it is pinned: the chunk holding it must end first. */
 local_status_t local_kvm_discard_staged(local_kvm_t* m, int32_t adapter, int32_t* n_freed);
 
 /* *committed and *staged (either may be NULL) of a registered adapter;
@@ -131,6 +143,17 @@ local_status_t local_kvm_alloc(local_kvm_t* m, int32_t n, int32_t version, int32
 /* Returns allocated, unrecorded blocks to the pool (tag 0): blocks of a
  * failed chunk, or blocks local_kvm_insert did not record. */
 local_status_t local_kvm_release(local_kvm_t* m, const int32_t* blocks, int32_t n);
+
+/* Pins the recorded blocks blocks[0..n) for an active request (§5.4: the
+ * active request's KV state is not an offload candidate), typically the
+ * blocks its local_kvm_lookup matched, for as long as it runs. Pins count:
+ * requests sharing a block pin it once each. LOCAL_ERR_SHAPE (nothing
+ * pinned) if any block is not recorded. */
+local_status_t local_kvm_pin(local_kvm_t* m, const int32_t* blocks, int32_t n);
+
+/* Drops one pin of each of blocks[0..n) (a block listed k times drops k).
+ * LOCAL_ERR_SHAPE (nothing changed) if a block has fewer pins than that. */
+local_status_t local_kvm_unpin(local_kvm_t* m, const int32_t* blocks, int32_t n);
 
 /* ---- the prefix table (§5.1) ---- */
 
@@ -184,15 +207,20 @@ local_status_t local_kvm_plan_stale_prefill(local_kvm_t* m, int32_t adapter,
 local_status_t local_kvm_path(const local_kvm_t* m, int32_t node, int32_t* ns, int32_t* tokens,
                               int64_t max_tokens, int64_t* n_tokens);
 
-/* ---- retention (§5.2) ---- */
+/* ---- retention and offload (§5.2, §5.4) ---- */
 
-/* Evicts records in ascending Pi_keep order until at least `n_free` blocks
- * are free or no record is left. Only a record with no record of the same
- * adapter state below it in the trie is a candidate (a record past a missing
- * one could never be matched); a parent becomes a candidate once its last
- * such child is evicted. Ties: smaller block id first. Evicted blocks are
- * freed (tag 0) and written to freed[0..*n_freed) up to max_freed entries
- * (freed may be NULL when max_freed is 0); *n_freed counts them all. */
+/* Releases records until at least `n_free` blocks are free or no eligible
+ * record is left (the target release R is n_free minus the free blocks). A
+ * record is eligible when it is not pinned and no record of the same adapter
+ * state lies below it in the trie (a record past a missing one could never
+ * be matched; a parent becomes eligible once its last such child goes).
+ * Eligible records go in the offload order of §5.4, Pi_keep ascending, then
+ * the larger footprint B first (every record owns one block, so B is equal),
+ * then the smaller block id: the shortest prefix of that order reaching R.
+ * Released blocks are freed (tag 0) and written to freed[0..*n_freed) up to
+ * max_freed entries (freed may be NULL when max_freed is 0); *n_freed counts
+ * them all. The KV of a released record is the caller's to move to host
+ * memory first, if it wants it back later. */
 local_status_t local_kvm_evict(local_kvm_t* m, int32_t n_free, int32_t* freed, int32_t max_freed,
                                int32_t* n_freed);
 

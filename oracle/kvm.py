@@ -14,6 +14,10 @@ scanning them: no trie, no heaps, no incremental bookkeeping.
         Pi_keep = H_KV * C_recompute / max(1, B); lower Pi_keep is evicted first.
   §5.3  a trained version is staged (foreground keeps binding the committed
         one), hot prefixes are re-prefilled under it, publication commits it.
+  §5.4  offload: the KV an active request holds is not eligible; eligible
+        records are ordered by (Pi_keep ascending, larger footprint B first)
+        and the shortest prefix of that order whose footprint reaches the
+        target is released.
   §4.3  a discarded staged version leaves no coverage.
 
 Readings where the paper is silent (they are the manager's documented
@@ -24,7 +28,13 @@ adapter-independent); the staged version of an adapter receives the urgency
 signal zeta at staging and at each request routed to that adapter; the
 recompute cost of one block at covered length L is 16 (c_tok + c_ctx L);
 ties in a ranking go to the smaller node or block id; node ids count trie
-nodes in creation order, a namespace's root first.
+nodes in creation order, a namespace's root first; a record becomes an
+offload candidate only once no record of the same adapter state lies below
+it (a record past a missing one could never be matched), so the order is
+re-evaluated after each release; an active request marks the blocks it holds
+by pinning them (a count per block); version numbers identify one adapter
+each (a version used by one adapter is refused for every other), so a block's
+tag alone tells the adapter and the version apart.
 """
 from __future__ import annotations
 
@@ -52,6 +62,8 @@ class KVMOracle:
         self.committed: Dict[int, int] = {}
         self.staged: Dict[int, int] = {}
         self.seen: Dict[int, set] = {}
+        self.version_owner: Dict[int, int] = {}  # version -> the adapter that has used it
+        self.pins: Dict[int, int] = {}           # block -> active requests holding it
         self.now = 0
 
     # ---- heat (§5.2) ----
@@ -94,13 +106,17 @@ class KVMOracle:
 
     # ---- adapters ----
     def set_committed(self, a, v):
+        assert a not in self.staged and self.version_owner.get(v, a) == a
         self.committed[a] = v
         self.seen.setdefault(a, set()).add(v)
+        self.version_owner[v] = a
 
     def stage(self, a, v):
         assert a in self.committed and a not in self.staged and v not in self.seen[a]
+        assert self.version_owner.get(v, a) == a
         self.staged[a] = v
         self.seen[a].add(v)
+        self.version_owner[v] = a
         self._bump(self.ha, (a, v), self.p["lambda_a"], self.p["zeta"])
 
     def publish(self, a):
@@ -109,8 +125,10 @@ class KVMOracle:
         return old
 
     def discard_staged(self, a):
-        v = self.staged.pop(a)
+        v = self.staged[a]
         gone = [k for k in self.records if k[2] == a and k[3] == v]
+        assert not any(self.pins.get(self.records[k], 0) for k in gone)
+        del self.staged[a]
         for k in gone:
             self._free(self.records.pop(k))
         return len(gone)
@@ -132,6 +150,21 @@ class KVMOracle:
         for b in blocks:
             assert self.state[b] == "allocated"
             self._free(b)
+
+    def pin(self, blocks):
+        assert all(self.state[b] == "recorded" for b in blocks)
+        for b in blocks:
+            self.pins[b] = self.pins.get(b, 0) + 1
+
+    def unpin(self, blocks):
+        need = {}
+        for b in blocks:
+            need[b] = need.get(b, 0) + 1
+        assert all(self.pins.get(b, 0) >= n for b, n in need.items())
+        for b in blocks:
+            self.pins[b] -= 1
+            if not self.pins[b]:
+                del self.pins[b]
 
     # ---- prefix table (§5.1) ----
     def lookup(self, ns, a, v, tokens, d_prefix=0.0, s_prefix=0.0, d_adapter=0.0,
@@ -207,19 +240,24 @@ class KVMOracle:
         ns, path = self.node_of[node]
         return ns, list(path)
 
-    # ---- retention (§5.2) ----
+    # ---- retention and offload (§5.2, §5.4) ----
     def evict(self, n_free):
+        """Release records until n_free blocks are free: among the eligible
+        ones (not pinned, nothing of the same adapter state below), the first
+        in the order (Pi_keep ascending, larger footprint B first, smaller
+        block id), one at a time."""
         freed = []
+        B = self.p["block_bytes"]  # every record owns one block
         while sum(st == "free" for st in self.state) < n_free:
             cands = []
             for (ns, path, a, v), b in self.records.items():
-                if self._has_child_record(ns, path, a, v):
+                if self.pins.get(b, 0) or self._has_child_record(ns, path, a, v):
                     continue
                 node = self.node_ids[(ns, path)]
-                cands.append((self.keep(node, a, v), b, (ns, path, a, v)))
+                cands.append(((self.keep(node, a, v), -B, b), b, (ns, path, a, v)))
             if not cands:
                 break
-            cands.sort(key=lambda c: (c[0], c[1]))
+            cands.sort(key=lambda c: c[0])
             _, b, key = cands[0]
             del self.records[key]
             self._free(b)

@@ -32,7 +32,8 @@ EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
            "local_kvm_discard_staged", "local_kvm_versions", "local_kvm_alloc",
-           "local_kvm_release", "local_kvm_lookup", "local_kvm_insert",
+           "local_kvm_release", "local_kvm_pin", "local_kvm_unpin", "local_kvm_lookup",
+           "local_kvm_insert",
            "local_kvm_plan_stale_prefill", "local_kvm_path", "local_kvm_evict",
            "local_kvm_scores", "local_kvm_stats",
            # host-side cooperative scheduler (local_sched.h)
@@ -125,6 +126,8 @@ def _declare_kvm(lib):
         "local_kvm_versions": (ctypes.c_int, [P, i32, I32P, I32P]),
         "local_kvm_alloc": (ctypes.c_int, [P, i32, i32, I32P]),
         "local_kvm_release": (ctypes.c_int, [P, I32P, i32]),
+        "local_kvm_pin": (ctypes.c_int, [P, I32P, i32]),
+        "local_kvm_unpin": (ctypes.c_int, [P, I32P, i32]),
         "local_kvm_lookup": (ctypes.c_int, [P, i32, i32, i32, I32P, i64, f64, f64, f64, I32P,
                                             i32, I32P]),
         "local_kvm_insert": (ctypes.c_int, [P, i32, i32, i32, I32P, i64, i32, I32P, i32,
@@ -781,6 +784,14 @@ class KVManager:
     def release(self, blocks):
         b = _i32(blocks)
         _check(self._lib.local_kvm_release(self._h, _p32(b), b.size))
+
+    def pin(self, blocks):
+        b = _i32(blocks)
+        _check(self._lib.local_kvm_pin(self._h, _p32(b), b.size))
+
+    def unpin(self, blocks):
+        b = _i32(blocks)
+        _check(self._lib.local_kvm_unpin(self._h, _p32(b), b.size))
 
     def lookup(self, ns: int, adapter: int, version: int, tokens, d_prefix: float = 0.0,
                s_prefix: float = 0.0, d_adapter: float = 0.0,

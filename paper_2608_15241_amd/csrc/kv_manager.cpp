@@ -1,7 +1,8 @@
 // Host-side KV cache manager (declared in local_kv.h): the radix-indexed
 // prefix table of validity keys (§5.1), hot-prefix statistics and the
-// retention priority (§5.2), and staged adapter versions with stale-coverage
-// prefill planning and publication (§5.3). Plain C++; nothing here touches
+// retention priority (§5.2), staged adapter versions with stale-coverage
+// prefill planning and publication (§5.3), and priority-based offload that
+// never touches the KV an active request holds (§5.4). Plain C++; nothing here touches
 // the GPU. It produces the block tables and the `block_version` tags that
 // the kernels consume.
 #include <algorithm>
@@ -82,6 +83,8 @@ struct local_kvm {
   std::vector<uint8_t> state;
   std::set<int32_t> free_ids;
   std::vector<int32_t> owner;  // node of a recorded block
+  std::vector<int32_t> pins;   // active requests holding a recorded block
+  std::unordered_map<int32_t, int32_t> version_owner;  // version -> its adapter
   std::vector<Node> nodes;
   std::unordered_map<int32_t, int32_t> roots;  // namespace -> root node
   std::unordered_map<int32_t, AdapterState> adapters;
@@ -209,6 +212,7 @@ local_kvm_t* local_kvm_create(int32_t num_blocks, const local_kvm_params_t* para
   m->tags.assign(num_blocks, 0);
   m->state.assign(num_blocks, kFree);
   m->owner.assign(num_blocks, -1);
+  m->pins.assign(num_blocks, 0);
   for (int32_t b = 0; b < num_blocks; ++b) m->free_ids.insert(m->free_ids.end(), b);
   return m;
 }
@@ -226,9 +230,14 @@ local_status_t local_kvm_set_committed(local_kvm_t* m, int32_t adapter, int32_t 
   if (s && s->staged)
     return local_fail(LOCAL_ERR_SHAPE, "kvm_set_committed: adapter %d has a staged version",
                       adapter);
+  auto vo = m->version_owner.find(version);
+  if (vo != m->version_owner.end() && vo->second != adapter)
+    return local_fail(LOCAL_ERR_SHAPE, "kvm_set_committed: version %d belongs to adapter %d",
+                      version, vo->second);
   AdapterState& st = m->adapters[adapter];
   st.committed = version;
   st.seen.insert(version);
+  m->version_owner[version] = adapter;
   return LOCAL_OK;
 }
 
@@ -242,8 +251,13 @@ local_status_t local_kvm_stage(local_kvm_t* m, int32_t adapter, int32_t version)
   if (version < 1 || s->seen.count(version))
     return local_fail(LOCAL_ERR_SHAPE, "kvm_stage: version %d not new for adapter %d", version,
                       adapter);
+  auto vo = m->version_owner.find(version);
+  if (vo != m->version_owner.end() && vo->second != adapter)
+    return local_fail(LOCAL_ERR_SHAPE, "kvm_stage: version %d belongs to adapter %d", version,
+                      vo->second);
   s->staged = version;
   s->seen.insert(version);
+  m->version_owner[version] = adapter;
   m->ha[akey(adapter, version)].update(m->prm.lambda_a, m->now, m->prm.zeta);
   return LOCAL_OK;
 }
@@ -266,6 +280,12 @@ local_status_t local_kvm_discard_staged(local_kvm_t* m, int32_t adapter, int32_t
     return local_fail(LOCAL_ERR_SHAPE, "kvm_discard_staged: adapter %d has no staged version",
                       adapter);
   const uint64_t k = akey(adapter, s->staged);
+  for (const auto& node : m->nodes) {
+    auto it = node.rec.find(k);
+    if (it != node.rec.end() && m->pins[it->second] > 0)
+      return local_fail(LOCAL_ERR_SHAPE, "kvm_discard_staged: block %d of adapter %d's staged "
+                        "version is pinned by an active request", it->second, adapter);
+  }
   int32_t n = 0;
   for (auto& node : m->nodes) {
     auto it = node.rec.find(k);
@@ -321,6 +341,33 @@ local_status_t local_kvm_release(local_kvm_t* m, const int32_t* blocks, int32_t 
                         b);
   }
   for (int32_t i = 0; i < n; ++i) m->free_block(blocks[i]);
+  return LOCAL_OK;
+}
+
+local_status_t local_kvm_pin(local_kvm_t* m, const int32_t* blocks, int32_t n) {
+  if (!m) return local_fail(LOCAL_ERR_NULL, "kvm_pin: NULL manager");
+  if (n < 0) return local_fail(LOCAL_ERR_SHAPE, "kvm_pin: n=%d", n);
+  if (n > 0 && !blocks) return local_fail(LOCAL_ERR_NULL, "kvm_pin: NULL blocks");
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t b = blocks[i];
+    if (b < 0 || b >= m->num_blocks || m->state[b] != kRecorded)
+      return local_fail(LOCAL_ERR_SHAPE, "kvm_pin: block %d is not a recorded block", b);
+  }
+  for (int32_t i = 0; i < n; ++i) ++m->pins[blocks[i]];
+  return LOCAL_OK;
+}
+
+local_status_t local_kvm_unpin(local_kvm_t* m, const int32_t* blocks, int32_t n) {
+  if (!m) return local_fail(LOCAL_ERR_NULL, "kvm_unpin: NULL manager");
+  if (n < 0) return local_fail(LOCAL_ERR_SHAPE, "kvm_unpin: n=%d", n);
+  if (n > 0 && !blocks) return local_fail(LOCAL_ERR_NULL, "kvm_unpin: NULL blocks");
+  std::unordered_map<int32_t, int32_t> need;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t b = blocks[i];
+    if (b < 0 || b >= m->num_blocks || ++need[b] > m->pins[b])
+      return local_fail(LOCAL_ERR_SHAPE, "kvm_unpin: block %d is not pinned that often", b);
+  }
+  for (int32_t i = 0; i < n; ++i) --m->pins[blocks[i]];
   return LOCAL_OK;
 }
 
@@ -486,18 +533,31 @@ local_status_t local_kvm_evict(local_kvm_t* m, int32_t n_free, int32_t* freed, i
   if (n_free < 0 || max_freed < 0)
     return local_fail(LOCAL_ERR_SHAPE, "kvm_evict: n_free=%d max_freed=%d", n_free, max_freed);
   if (max_freed > 0 && !freed) return local_fail(LOCAL_ERR_NULL, "kvm_evict: NULL freed");
+  // §5.4: eligible records (not held by an active request, nothing of the
+  // same adapter state below) in the order (Pi_keep ascending, larger
+  // footprint first, smaller block id), released one at a time until the
+  // target is reached: the shortest prefix of the order that reaches it. A
+  // parent becomes eligible when its last such child goes. Every record owns
+  // one block, so the footprints are equal and the second key never decides.
   struct Cand {
-    double keep;
+    double keep, bytes;
     int32_t block, node;
     uint64_t k;
   };
-  auto later = [](const Cand& x, const Cand& y) {  // min-heap on (keep, block)
-    return x.keep != y.keep ? x.keep > y.keep : x.block > y.block;
+  auto later = [](const Cand& x, const Cand& y) {  // min-heap on (keep, -bytes, block)
+    if (x.keep != y.keep) return x.keep > y.keep;
+    if (x.bytes != y.bytes) return x.bytes < y.bytes;
+    return x.block > y.block;
+  };
+  const double bytes = m->prm.block_bytes;
+  auto eligible = [&](int32_t node, uint64_t k, int32_t block) {
+    return m->pins[block] == 0 && !m->has_child_record(node, k);
   };
   std::priority_queue<Cand, std::vector<Cand>, decltype(later)> heap(later);
   for (int32_t id = 0; id < static_cast<int32_t>(m->nodes.size()); ++id)
     for (const auto& r : m->nodes[id].rec)
-      if (!m->has_child_record(id, r.first)) heap.push({m->keep(id, r.first), r.second, id, r.first});
+      if (eligible(id, r.first, r.second))
+        heap.push({m->keep(id, r.first), bytes, r.second, id, r.first});
   int32_t n = 0;
   while (static_cast<int64_t>(m->free_ids.size()) < n_free && !heap.empty()) {
     const Cand c = heap.top();
@@ -510,8 +570,8 @@ local_status_t local_kvm_evict(local_kvm_t* m, int32_t n_free, int32_t* freed, i
     const int32_t par = m->nodes[c.node].parent;
     if (par >= 0) {
       auto it = m->nodes[par].rec.find(c.k);
-      if (it != m->nodes[par].rec.end() && !m->has_child_record(par, c.k))
-        heap.push({m->keep(par, c.k), it->second, par, c.k});
+      if (it != m->nodes[par].rec.end() && eligible(par, c.k, it->second))
+        heap.push({m->keep(par, c.k), bytes, it->second, par, c.k});
     }
   }
   *n_freed = n;

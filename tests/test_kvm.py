@@ -44,9 +44,10 @@ def test_random_sequences_match_the_oracle(seed):
         o.set_committed(a, v)
     paths = _paths(rng, 14, vocab=3, max_blocks=6)
     next_version = {a: v + 1 for a, v in adapters.items()}
+    held = []  # block lists pinned by "active requests"
     for step in range(300):
         op = rng.choice(["lookup", "lookup", "fill", "stage", "publish", "discard", "evict",
-                         "plan"])
+                         "plan", "unpin"])
         a = int(rng.integers(0, 3))
         ns = int(rng.integers(0, 2))
         path = paths[int(rng.integers(len(paths)))]
@@ -57,6 +58,14 @@ def test_random_sequences_match_the_oracle(seed):
             d, s_, da = (float(x) for x in rng.uniform(0, 2, size=3))
             got = m.lookup(ns, a, v, path, d, s_, da)
             assert list(got) == o.lookup(ns, a, v, path, d, s_, da), step
+            if len(got) and rng.random() < 0.4:  # the request runs: it holds its blocks
+                m.pin(got)
+                o.pin(list(got))
+                held.append(list(got))
+        elif op == "unpin" and held:
+            blocks = held.pop(int(rng.integers(len(held))))
+            m.unpin(blocks)
+            o.unpin(blocks)
         elif op == "fill":
             # prefill what the lookup did not match, under the bound version
             v = staged if (staged and rng.random() < 0.5) else committed
@@ -77,10 +86,18 @@ def test_random_sequences_match_the_oracle(seed):
         elif op == "publish" and staged:
             assert m.publish(a) == o.publish(a)
         elif op == "discard" and staged:
-            assert m.discard_staged(a) == o.discard_staged(a)
+            pinned = any(o.pins.get(b, 0) for k, b in o.records.items()
+                         if k[2] == a and k[3] == staged)
+            if pinned:  # refused while an active request holds its KV
+                with pytest.raises(lk.LocalError):
+                    m.discard_staged(a)
+            else:
+                assert m.discard_staged(a) == o.discard_staged(a)
         elif op == "evict":
             target = int(rng.integers(0, nb + 1))
-            assert list(m.evict(target)) == o.evict(target), step
+            freed = m.evict(target)
+            assert list(freed) == o.evict(target), step
+            assert not set(freed) & {b for h in held for b in h}, step
         elif op == "plan" and staged:
             plan = m.plan_stale_prefill(a, 4)
             assert plan == o.plan_stale_prefill(a, 4), step
@@ -148,3 +165,62 @@ def test_errors_leave_the_manager_unchanged():
     with pytest.raises(lk.LocalError):
         lk.KVManager(4, dict(lambda_p=1.0))    # decay must be < 1
     assert m.stats() == (6, 2, 3)
+
+
+def test_a_pinned_block_survives_eviction_and_is_not_reallocated():
+    # §5.4: the KV an active request holds is not an offload candidate.
+    m = lk.KVManager(16)
+    m.set_committed(0, 1000)
+    hot, cold = np.arange(64, dtype=np.int32), np.arange(100, 148, dtype=np.int32)
+    bh = m.alloc(4, 1000)
+    m.insert(0, 0, 1000, hot, bh)
+    bc = m.alloc(3, 1000)
+    m.insert(0, 0, 1000, cold, bc)
+    held = m.lookup(0, 0, 1000, hot)
+    assert np.array_equal(held, bh)
+    m.pin(held)
+    freed = m.evict(16)                       # ask for everything
+    assert sorted(freed) == sorted(bc)        # only the unpinned path goes
+    assert np.all(m.tags()[bh] == 1000)
+    fresh = m.alloc(12, 1000)                 # every free block, none of the held ones
+    assert not set(fresh) & set(bh)
+    with pytest.raises(lk.LocalError):
+        m.alloc(1, 1000)                      # the pool is exhausted, the pins stand
+    m.release(fresh)
+    m.unpin(held)
+    assert sorted(m.evict(16)) == sorted(bh)
+    with pytest.raises(lk.LocalError):
+        m.unpin(held)                         # no pins left
+    with pytest.raises(lk.LocalError):
+        m.pin(bh)                             # freed blocks cannot be pinned
+
+
+def test_a_version_belongs_to_one_adapter():
+    # one tag must tell adapters apart: a version another adapter has used is
+    # refused, committed or staged, and nothing changes
+    m = lk.KVManager(8)
+    m.set_committed(0, 1000)
+    with pytest.raises(lk.LocalError):
+        m.set_committed(1, 1000)
+    m.set_committed(1, 2000)
+    with pytest.raises(lk.LocalError):
+        m.stage(1, 1000)
+    m.stage(0, 1001)
+    with pytest.raises(lk.LocalError):
+        m.set_committed(2, 1001)
+    assert m.versions(1) == (2000, 0) and m.versions(0) == (1000, 1001)
+    m.set_committed(1, 2000)                  # its own version again is fine
+
+
+def test_discard_waits_for_pinned_staged_records():
+    m = lk.KVManager(8)
+    m.set_committed(0, 1000)
+    m.stage(0, 1001)
+    b = m.alloc(2, 1001)
+    m.insert(0, 0, 1001, np.arange(32, dtype=np.int32), b)
+    m.pin(b[:1])
+    with pytest.raises(lk.LocalError):
+        m.discard_staged(0)
+    assert m.versions(0) == (1000, 1001) and m.stats()[1] == 2
+    m.unpin(b[:1])
+    assert m.discard_staged(0) == 2

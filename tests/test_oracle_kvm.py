@@ -65,7 +65,7 @@ def test_hkv_and_keep_by_hand():
 def test_validity_key_every_component_must_match():
     o = KVMOracle(16)
     o.set_committed(A, V)
-    o.set_committed(4, V)
+    o.set_committed(4, V + 7)  # versions identify one adapter each
     blocks = o.alloc(3, V)
     o.insert(0, A, V, toks(48), blocks)
     assert o.lookup(0, A, V, toks(48)) == blocks           # full match
@@ -124,3 +124,91 @@ def test_eviction_takes_cold_leaves_first():
     assert o.evict(5) == [hot[2], hot[1]]
     assert o.lookup(0, A, V, toks(48)) == hot[:1]
     assert o.stats() == (5, 1, 6)
+
+
+def test_versions_identify_one_adapter():
+    # One int32 tag carries both the adapter and the version of the validity
+    # key only while no version number is used by two adapters: the oracle
+    # refuses a version another adapter has had, committed or staged.
+    o = KVMOracle(8)
+    o.set_committed(A, V)
+    with pytest.raises(AssertionError):
+        o.set_committed(4, V)
+    o.set_committed(4, 7)
+    with pytest.raises(AssertionError):
+        o.stage(4, V)
+    o.stage(A, V2)
+    with pytest.raises(AssertionError):
+        o.set_committed(5, V2)
+    assert o.version_owner == {V: A, 7: 4, V2: A}
+
+
+def _two_paths_recorded(o):
+    """Adapter A at version V: path P (3 blocks) and path Q (2 blocks); P is
+    made hot by lookups, Q stays cold."""
+    o.set_committed(A, V)
+    P, Q = toks(48), [t + 1000 for t in toks(32)]
+    bp = o.alloc(3, V)
+    o.insert(0, A, V, P, bp)
+    bq = o.alloc(2, V)
+    o.insert(0, A, V, Q, bq)
+    for _ in range(5):
+        o.lookup(0, A, V, P)
+    return P, Q, bp, bq
+
+
+def test_offload_order_is_coldest_first_and_shortest_prefix():
+    # §5.4: ascending Pi_keep; leaves before their parents (a record past a
+    # missing one is never matched); the release stops at the first prefix of
+    # that order that reaches the target.
+    o = KVMOracle(8)
+    P, Q, bp, bq = _two_paths_recorded(o)
+    free0 = sum(st == "free" for st in o.state)
+    assert free0 == 3
+    keep_q = o.keep(o.node_ids[(0, tuple(Q))], A, V)
+    keep_p = o.keep(o.node_ids[(0, tuple(P))], A, V)
+    assert keep_q < keep_p                          # the cold path ranks first
+    assert o.evict(free0 + 1) == [bq[1]]            # exactly one block: the cold leaf
+    assert o.evict(free0 + 2) == [bq[0]]            # then its parent
+    assert o.evict(free0 + 3) == [bp[2]]            # then the hot path's leaf
+    assert o.evict(free0 + 3) == []                 # target reached: nothing more
+
+
+def test_pinned_records_are_not_eligible():
+    # §5.4: the active request's KV is not an offload candidate. A request
+    # holding the hot path's blocks keeps them (and, the leaf being pinned,
+    # its parents are never leaves either); the rest is released, and the
+    # pinned blocks are never handed out again while pinned.
+    o = KVMOracle(8)
+    P, Q, bp, bq = _two_paths_recorded(o)
+    held = o.lookup(0, A, V, P)
+    assert held == bp
+    o.pin(held)
+    freed = o.evict(8)
+    assert sorted(freed) == sorted(bq)               # everything but the pinned path
+    assert all(o.state[b] == "recorded" for b in bp)
+    assert not set(o.alloc(5, V)) & set(bp)          # never reallocated
+    o.release([b for b in range(8) if o.state[b] == "allocated"])
+    o.pin([bp[0]])                                   # a second request shares block 0
+    o.unpin(held)
+    assert o.evict(8) == [bp[2], bp[1]]              # block 0 still held
+    o.unpin([bp[0]])
+    assert o.evict(8) == [bp[0]]
+    with pytest.raises(AssertionError):
+        o.unpin([bp[0]])                             # not pinned any more
+    with pytest.raises(AssertionError):
+        o.pin([bp[0]])                               # not a recorded block
+
+
+def test_discarding_a_staged_version_waits_for_its_pins():
+    o = KVMOracle(8)
+    o.set_committed(A, V)
+    o.stage(A, V2)
+    b = o.alloc(2, V2)
+    o.insert(0, A, V2, toks(32), b)
+    o.pin(b[:1])                                     # a re-prefill chunk still running
+    with pytest.raises(AssertionError):
+        o.discard_staged(A)
+    assert o.staged == {A: V2}                       # unchanged
+    o.unpin(b[:1])
+    assert o.discard_staged(A) == 2
