@@ -319,6 +319,39 @@ local_status_t local_paged_attn_decode(
     void* ws, size_t* ws_bytes, void* stream);
 
 /*
+ * local_paged_attn_decode_checked — local_paged_attn_decode and
+ * local_block_version_check of the same requests in one call (§5.1: the
+ * stale blocks the validity key rejects are reported while attention skips
+ * them; §1: stale coverage is rejected, never reused). The attention reads
+ * every owned block's id and tag anyway; it records which are stale, and
+ * its merge launch writes the canonical list, so the check costs no launch
+ * of its own.
+ *
+ *  Arguments q .. lse and the results in out/lse: as local_paged_attn_decode.
+ *  stale_pairs, cap, n_stale, valid_tokens: as local_block_version_check over
+ *  block_table, ctx_lens, block_version (num_blocks tags), req_version, with
+ *  the same results bit for bit (the (b, j) list in canonical order, the
+ *  full count in *n_stale even past cap, the live tokens of valid blocks).
+ *
+ *  Sizes and errors as local_paged_attn_decode, and LOCAL_ERR_SHAPE for
+ *  cap < 0, LOCAL_ERR_NULL for a NULL n_stale (or valid_tokens with B > 0,
+ *  or stale_pairs with cap > 0), LOCAL_ERR_UNSUPPORTED for a table wider
+ *  than 32 * D blocks. B = 0 writes *n_stale = 0 and nothing else.
+ */
+local_status_t local_paged_attn_decode_checked(
+    const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new,
+    uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size,
+    const int32_t* block_table, int32_t max_blocks,
+    const int32_t* ctx_lens,
+    const int32_t* block_version, const int32_t* req_version,
+    float sm_scale,
+    uint16_t* out, float* lse,
+    int32_t* stale_pairs, int64_t cap, int32_t* n_stale, int32_t* valid_tokens,
+    void* ws, size_t* ws_bytes, void* stream);
+
+/*
  * local_paged_attn_decode_noalloc — local_paged_attn_decode for callers that
  * cannot allocate device memory or pass a workspace: code under HIP graph
  * capture that must not call hipMalloc, tight serving loops, harnesses that

@@ -9,7 +9,8 @@ from .binding import (BLOCK_SIZE, EXPORTS, LIB_PATH, Call, KVManager, LocalError
                       load_library, local_block_version_check, local_lora_grad,
                       local_lora_grad_grouped, local_lora_grad_input, local_lora_linear,
                       local_lora_linear_grouped, local_paged_attn_decode,
-                      local_paged_attn_decode_noalloc, local_paged_attn_prefill,
+                      local_paged_attn_decode_checked, local_paged_attn_decode_noalloc,
+                      local_paged_attn_prefill, prepare_paged_attn_decode_checked,
                       prepare_block_version_check, prepare_paged_attn_decode_noalloc,
                       prepare_lora_grad, prepare_lora_grad_grouped, prepare_lora_grad_input,
                       prepare_lora_linear,

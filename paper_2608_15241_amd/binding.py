@@ -28,6 +28,7 @@ EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
            "local_block_version_check", "local_lora_grad", "local_lora_grad_input",
            "local_lora_grad_grouped", "local_paged_attn_decode_noalloc",
+           "local_paged_attn_decode_checked",
            # host-side KV manager (local_kv.h)
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
@@ -79,6 +80,10 @@ def load_library(path: str = LIB_PATH):
     lib.local_paged_attn_decode.restype = ctypes.c_int
     lib.local_paged_attn_decode.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64, i32, P,
                                             i32, P, P, P, f32, P, P, P, SZ, P]
+    lib.local_paged_attn_decode_checked.restype = ctypes.c_int
+    lib.local_paged_attn_decode_checked.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64,
+                                                    i32, P, i32, P, P, P, f32, P, P, P, i64,
+                                                    P, P, P, SZ, P]
     lib.local_paged_attn_decode_noalloc.restype = ctypes.c_int
     lib.local_paged_attn_decode_noalloc.argtypes = [P, i32, i32, i32, i32, P, P, P, P, i64,
                                                     i32, P, i32, P, P, P, f32, P, P, P]
@@ -584,6 +589,60 @@ def local_paged_attn_decode(*args, **kwargs):
     q [B, Hq, D]; pools as documented in include/local.h; returns (out, lse).
     """
     return prepare_paged_attn_decode(*args, **kwargs)()
+
+
+def prepare_paged_attn_decode_checked(q, k_cache, v_cache, block_table, ctx_lens,
+                                      block_version, req_version, sm_scale: float, k_new=None,
+                                      v_new=None, Hkv: Optional[int] = None, out=None, lse=None,
+                                      cap: Optional[int] = None, stale_pairs=None, n_stale=None,
+                                      valid_tokens=None,
+                                      workspace: Optional[Workspace] = None) -> Call:
+    """Prepared decode attention with the version check of the same requests;
+    the call returns (out, lse, stale_pairs, n_stale, valid_tokens)."""
+    lib = load_library()
+    _req(q, "q", torch.bfloat16, 3)
+    B, Hq, D = q.shape
+    if Hkv is None:
+        if k_new is None:
+            raise ValueError("Hkv is required when k_new is not given")
+        Hkv = k_new.shape[1]
+    num_blocks = _pool_checks(k_cache, v_cache, Hkv, D)
+    _meta_checks(block_table, ctx_lens, block_version, req_version, B, num_blocks)
+    if k_new is not None:
+        _req(k_new, "k_new", torch.bfloat16, 3)
+        _req(v_new, "v_new", torch.bfloat16, 3)
+        if tuple(k_new.shape) != (B, Hkv, D) or tuple(v_new.shape) != (B, Hkv, D):
+            raise ValueError("k_new/v_new must be [B, Hkv, D]")
+    out, lse = _attn_out_checks(out, lse, B, Hq, D, q.device)
+    dev = q.device
+    if cap is None:
+        cap = block_table.numel()
+    if stale_pairs is None:
+        stale_pairs = torch.empty((max(cap, 1), 2), dtype=torch.int32, device=dev)
+    if n_stale is None:
+        n_stale = torch.empty((1,), dtype=torch.int32, device=dev)
+    if valid_tokens is None:
+        valid_tokens = torch.empty((B,), dtype=torch.int32, device=dev)
+    _req(stale_pairs, "stale_pairs", torch.int32, 2)
+    _req(n_stale, "n_stale", torch.int32, 1)
+    _req(valid_tokens, "valid_tokens", torch.int32, 1)
+    if stale_pairs.shape[0] < cap or stale_pairs.shape[1] != 2 or valid_tokens.shape[0] != B:
+        raise ValueError("stale_pairs must be [>= cap, 2] and valid_tokens [B]")
+    args = [_ptr(q), B, Hq, Hkv, D, _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+            num_blocks, BLOCK_SIZE, _ptr(block_table), block_table.shape[1], _ptr(ctx_lens),
+            _ptr(block_version), _ptr(req_version), float(sm_scale), _ptr(out), _ptr(lse),
+            _ptr(stale_pairs), cap, _ptr(n_stale), _ptr(valid_tokens)]
+    c = Call(lib.local_paged_attn_decode_checked, args, workspace, q.device,
+             keep=(q, k_new, v_new, k_cache, v_cache, block_table, ctx_lens, block_version,
+                   req_version, out, lse, stale_pairs, n_stale, valid_tokens))
+    c.outputs = (out, lse, stale_pairs, n_stale, valid_tokens)
+    return c
+
+
+def local_paged_attn_decode_checked(*args, **kwargs):
+    """Decode attention plus the version check of the same requests (see
+    include/local.h); returns (out, lse, stale_pairs, n_stale, valid_tokens)."""
+    return prepare_paged_attn_decode_checked(*args, **kwargs)()
 
 
 class NoWorkspaceCall:

@@ -14,10 +14,12 @@
 //      through an LDS ring by direct global-to-LDS loads, whole 128-byte rows
 //      per load instruction; fp32 partial sums per slice. Wider feature
 //      tiles for fewer tokens cut the re-reads of x.
-//    - SGMV shrink, when the stacked rows are too many to ride along:
-//      workgroups per (K slice, adapter) gather the tokens routed to that
-//      adapter and compute x_t . A[a,j,:] for their slice of K on the matrix
-//      cores; fp32 partial sums per slice.
+//    - SGMV shrink, when the stacked rows are too many to ride along (more
+//      than 4 extra row tiles a workgroup): workgroups per (K slice,
+//      adapter, projection) gather the
+//      tokens routed to that adapter and compute x_t . A[a,j,:] for j below
+//      its rank over their slice of K on the matrix cores; fp32 partial sums
+//      per slice.
 //    - epilogue: sums the base slices, forms U_s = bf16(s_t * u) for the
 //      token's own adapter and rank, adds U_s B_a^T and the residual, and
 //      rounds once to bf16.
@@ -310,8 +312,8 @@ __global__ __launch_bounds__(kStThreads) void lora_stream_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------- SGMV shrink
-// Decode-size shrink, segmented by adapter as in SGMV. Workgroup (z, a) takes
-// adapter a and the z-th of up_ks slices of K: the tokens routed to a are
+// Decode-size shrink, segmented by adapter as in SGMV. Workgroup (z, a, g)
+// takes adapter a of projection g and the z-th of up_ks slices of K: the tokens routed to a are
 // compacted (ascending) into groups of 16 that become the columns of
 // S^T = A_a X_g^T on the matrix cores, with the adapter's rank rows as MFMA
 // rows. Each of the 4 waves holds at most U steps of 32 k, so it loads its
@@ -333,10 +335,10 @@ __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a
   __shared__ int toks[kSgMaxTokens];
   __shared__ int wave_cnt[kSgWaves];
   __shared__ f32x4 red[kSgWaves][RT][kWave];
-  const int z = blockIdx.x, ad = blockIdx.y;
+  const int z = blockIdx.x, ad = blockIdx.y, g = blockIdx.z;  // slice, adapter, projection
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int col = lane % 16, kgrp = lane / 16;
-  const int rk = rank_of(a, ad);
+  const int rk = rank_g(a, g, ad);
   if (rk == 0) return;  // uniform: no row of this adapter is used
   const int tiles = (rk + 15) / 16;
 
@@ -350,7 +352,7 @@ __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a
   // A: rank rows 16i + col of the slice, loaded first (rows past the rank
   // read row 0 and are zeroed; steps past s_hi read a valid step and are
   // dropped below)
-  const uint16_t* abase = a.w + static_cast<int64_t>(ad) * a.r_max * a.K + 8 * kgrp;
+  const uint16_t* abase = pick(a.ga, g) + static_cast<int64_t>(ad) * a.r_max * a.K + 8 * kgrp;
   bool aok[RT];
   u32x4 av[U][RT];
 #pragma unroll
@@ -383,7 +385,7 @@ __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a
 #pragma unroll
     for (int i = 0; i < RT; ++i) av[u][i] = (aok[i] && s_lo + u < s_hi) ? av[u][i] : zero4;
 
-  float* pz = a.pout + static_cast<int64_t>(z) * a.T * a.r_max;
+  float* pz = a.pout + static_cast<int64_t>(z) * a.T * a.p_stride + g * a.r_max;
   for (int g0 = 0; g0 < n_tok; g0 += 16) {
     const bool xok = g0 + col < n_tok;
     const uint16_t* xrow = a.x + static_cast<int64_t>(toks[xok ? g0 + col : g0]) * a.K + 8 * kgrp;
@@ -412,7 +414,7 @@ __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a
       const int slot = g0 + l % 16;
       const int j = 16 * i + 4 * (l / 16);  // first of 4 rank rows
       if (slot < n_tok && j < rk) {
-        float* dst = pz + static_cast<int64_t>(toks[slot]) * a.r_max + j;
+        float* dst = pz + static_cast<int64_t>(toks[slot]) * a.p_stride + j;
         if (j + 4 <= rk) {
           *reinterpret_cast<f32x4*>(dst) = v;
         } else {
@@ -428,8 +430,9 @@ __global__ __launch_bounds__(kSgThreads) void lora_sgmv_shrink_kernel(GemmArgs a
 // enough slices that no wave has more than U steps.
 template <int RT, int U>
 local_status_t launch_sgmv_shrink(GemmArgs a, hipStream_t s) {
-  lora_sgmv_shrink_kernel<RT, U>
-      <<<dim3(static_cast<unsigned>(a.up_ks), static_cast<unsigned>(a.n_ad)), kSgThreads, 0, s>>>(a);
+  lora_sgmv_shrink_kernel<RT, U><<<dim3(static_cast<unsigned>(a.up_ks), static_cast<unsigned>(a.n_ad),
+                                        static_cast<unsigned>(a.G)),
+                                   kSgThreads, 0, s>>>(a);
   return local_check_launch("lora_linear (SGMV shrink)");
 }
 
@@ -524,7 +527,8 @@ __global__ __launch_bounds__(kEpThreads) void lora_epilogue_kernel(GemmArgs a) {
         const float sc = a.scale[t0 + et];
         const int rk = rank_g(a, g, ad);
         const float* p = a.pout + (t0 + et) * a.p_stride +
-                         (a.p_stacked ? static_cast<int64_t>(g) * a.R + ad * a.r_max : 0) + j;
+                         (a.p_stacked ? static_cast<int64_t>(g) * a.R + ad * a.r_max
+                                      : static_cast<int64_t>(g) * a.r_max) + j;
         for (int z0 = 0; z0 < a.up_ks; z0 += 8) {
           f32x4 sv[8];
 #pragma unroll
@@ -1360,8 +1364,12 @@ DecodePlan plan_decode(int64_t T, int64_t K, int G, const Proj* p, int n_ad, int
     ftiles = (n_total + 16 * d.shape.fn - 1) / (16 * d.shape.fn);
     d.xrows = partial_xrows(T, ftiles, G * R);
   }
+  // (Measured at 64 tokens over 16 adapters padded from ranks 8..64 to 64:
+  // taking the shrink out of the base product saves 6.8 us of streaming
+  // there, and its own SGMV launch costs 10.3 us; so the shrink rides along
+  // whenever it fits.)
   if (n_ad > 0 && d.xrows == 0) {
-    if (G > 1) {
+    if (T > kSgMaxTokens) {
       d.split = true;
       return d;
     }
@@ -1370,7 +1378,7 @@ DecodePlan plan_decode(int64_t T, int64_t K, int G, const Proj* p, int n_ad, int
   d.part_bytes = align256(static_cast<size_t>(d.shape.ksb) * T * n_total * sizeof(float));
   d.shrink_bytes =
       d.xrows > 0 ? align256(static_cast<size_t>(d.shape.ksb) * T * G * R * sizeof(float))
-                  : align256(static_cast<size_t>(d.slices) * T * r_max * sizeof(float));
+                  : align256(static_cast<size_t>(d.slices) * T * G * r_max * sizeof(float));
   return d;
 }
 
@@ -1454,13 +1462,12 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
     float* part = static_cast<float*>(ws);
     float* sp = reinterpret_cast<float*>(static_cast<char*>(ws) + d.part_bytes);
     const bool fused = d.xrows > 0;
-    if (n_adapters > 0 && !fused) {  // SGMV shrink (one projection): partial sums
+    if (n_adapters > 0 && !fused) {  // SGMV shrink of every projection: partial sums
       GemmArgs sh = g;
-      sh.w = p[0].A;
-      sh.ranks = p[0].ranks;
-      sh.N = R;
+      set_groups(sh, G, p);
       sh.pout = sp;
       sh.up_ks = d.slices;
+      sh.p_stride = G * r_max;
       if ((st = run_sgmv_shrink(sh, s)) != LOCAL_OK) return st;
     }
     GemmArgs m = g;  // base product (+ fused shrink): partial sums per K slice
@@ -1471,7 +1478,7 @@ local_status_t lora_impl(const uint16_t* x, int64_t T, int64_t K, int G, const P
     m.pout = sp;
     if ((st = run_partial(m, d.shape.fn, s)) != LOCAL_OK) return st;
     m.up_ks = fused ? d.shape.ksb : d.slices;  // epilogue: sums, up-projection, residual
-    m.p_stride = fused ? G * R : r_max;
+    m.p_stride = fused ? G * R : G * r_max;
     m.p_stacked = fused ? 1 : 0;
     m.ksplit = d.shape.ksb;
     return run_epilogue(m, s);

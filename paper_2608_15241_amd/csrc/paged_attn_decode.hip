@@ -59,6 +59,16 @@ struct DecodeArgs {
   float* lse;
   float* part_o;   // [B][Hq][n_parts][D]
   float* part_ml;  // [B][Hq][n_parts][2]  (max in log2 units, sum)
+  // The version check of the same call (null when not asked for): per
+  // (request, partition), the stale blocks as a bit mask (bit i = block
+  // j0 + i) and the live tokens of the valid ones, written by KV head 0's
+  // waves; the merge launch turns them into the canonical outputs.
+  uint32_t* vc_mask;    // [B][n_parts]
+  int32_t* vc_valid;    // [B][n_parts]
+  int32_t* vc_pairs;    // [cap][2] (b, j), or null when cap == 0
+  int64_t vc_cap;
+  int32_t* vc_n_stale;  // one int32
+  int32_t* vc_valid_tokens;  // [B]
   int64_t num_blocks;
   int Hq, Hkv, group, max_blocks, n_parts;
   float scale_log2;  // sm_scale * log2(e)
@@ -238,6 +248,18 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
     if (!ok) my_phys = 0;  // an id outside the pool is never dereferenced
   }
   uint64_t valid_mask = __ballot(ok);
+  if (a.vc_mask && g == 0) {  // the version check of this partition's blocks
+    const bool owned = lane < kBlocksPerPart && j0 + lane < jend;
+    const uint64_t stale = __ballot(owned && !ok);
+    int live = ok ? min(kBlockSize, L - kBlockSize * (j0 + lane)) : 0;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) live += __shfl_xor(live, off);
+    if (lane == 0) {
+      const int64_t slot = static_cast<int64_t>(b) * a.n_parts + part;
+      a.vc_mask[slot] = static_cast<uint32_t>(stale);
+      a.vc_valid[slot] = live;
+    }
+  }
 
   // Query heads of this KV head, as the B operand (column = head).
   bf16x8 qv[KC];
@@ -414,11 +436,77 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
 }
 
 // Merge the partitions of every (request, head) that has more than one.
+// The version check from the partitions' stale masks (one workgroup per
+// request, D threads): the request's offset in the canonical list is the
+// number of stale blocks of the requests before it; its own stale blocks
+// follow in ascending j (partitions in descending index). Deterministic, no
+// atomics.
+__device__ void decode_version_check(const DecodeArgs& a, int b, int B, int* sh) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  auto parts_of = [&](int bb) {
+    const int nbb = owned_blocks(a.ctx_lens[bb], a.max_blocks);
+    return max(1, (nbb + kBlocksPerPart - 1) / kBlocksPerPart);
+  };
+  int before = 0;
+  for (int e = tid; e < b * a.n_parts; e += nt) {
+    const int bb = e / a.n_parts, pp = e % a.n_parts;
+    if (pp < parts_of(bb)) before += __popc(a.vc_mask[e]);
+  }
+  const int np = parts_of(b);
+  // this request's partitions in ascending j: t-th is partition np - 1 - t
+  int cnt = 0, valid = 0;
+  uint32_t mask = 0u;
+  if (tid < np) {
+    const int64_t slot = static_cast<int64_t>(b) * a.n_parts + (np - 1 - tid);
+    mask = a.vc_mask[slot];
+    cnt = __popc(mask);
+    valid = a.vc_valid[slot];
+  }
+  // block-wide sums of `before` and `valid`, exclusive prefix of `cnt` over t
+  sh[tid] = cnt;
+  __syncthreads();
+  int pre = 0;
+  for (int t = 0; t < tid && t < np; ++t) pre += sh[t];
+  __syncthreads();
+  sh[tid] = before;
+  __syncthreads();
+  for (int w = nt / 2; w > 0; w >>= 1) {
+    if (tid < w) sh[tid] += sh[tid + w];
+    __syncthreads();
+  }
+  const int offset = sh[0];
+  __syncthreads();
+  sh[tid] = valid;
+  __syncthreads();
+  for (int w = nt / 2; w > 0; w >>= 1) {
+    if (tid < w) sh[tid] += sh[tid + w];
+    __syncthreads();
+  }
+  if (tid == 0) a.vc_valid_tokens[b] = sh[0];
+  if (tid < np) {  // (np <= n_parts <= nt: the host checks)
+    const int nbb = owned_blocks(a.ctx_lens[b], a.max_blocks);
+    const int p = np - 1 - tid;
+    const int j0 = max(0, nbb - kBlocksPerPart * (p + 1));
+    int64_t pos = static_cast<int64_t>(offset) + pre;
+    for (uint32_t m = mask; m; m &= m - 1u, ++pos) {
+      if (pos < a.vc_cap) {
+        a.vc_pairs[2 * pos] = b;
+        a.vc_pairs[2 * pos + 1] = j0 + __ffs(static_cast<int>(m)) - 1;
+      }
+    }
+    if (b == B - 1 && tid == np - 1) *a.vc_n_stale = offset + pre + cnt;
+  }
+}
+
 template <int D>
-__global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a, int B) {
   const int bh = blockIdx.x;
   const int b = bh / a.Hq;
   const int d = threadIdx.x;
+  if (a.vc_mask && bh % a.Hq == 0) {
+    __shared__ int sh[D];
+    decode_version_check(a, b, B, sh);
+  }
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
   const int np = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
@@ -485,7 +573,7 @@ local_status_t launch_decode(const DecodeArgs& a, int B, hipStream_t s) {
     else
       decode_attn_kernel<D, LOCAL_DECODE_DEPTH, false><<<grid, kWave, 0, s>>>(a, B);
   }
-  if (a.n_parts > 1) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a);
+  if (a.n_parts > 1 || a.vc_mask) decode_merge_kernel<D><<<B * a.Hq, D, 0, s>>>(a, B);
   return local_check_launch("paged_attn_decode");
 }
 
@@ -529,6 +617,12 @@ static local_status_t decode_setup(const uint16_t* q, int32_t B, int32_t Hq, int
   a->lse = lse;
   a->part_o = nullptr;
   a->part_ml = nullptr;
+  a->vc_mask = nullptr;
+  a->vc_valid = nullptr;
+  a->vc_pairs = nullptr;
+  a->vc_cap = 0;
+  a->vc_n_stale = nullptr;
+  a->vc_valid_tokens = nullptr;
   a->Hq = Hq;
   a->Hkv = Hkv;
   a->group = Hq / Hkv;
@@ -578,6 +672,59 @@ extern "C" local_status_t local_paged_attn_decode(
     return local_fail(LOCAL_ERR_WORKSPACE, "%s: workspace %zu < %zu", who, *ws_bytes, need);
   if (B == 0) return LOCAL_OK;
   if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
+  return decode_launch(a, B, D, ws, part_elems, stream);
+}
+
+// ---------------------------------------------------------------- checked
+namespace {
+__global__ void decode_vc_empty_kernel(int32_t* n_stale) { *n_stale = 0; }
+size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+}  // namespace
+
+extern "C" local_status_t local_paged_attn_decode_checked(
+    const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+    const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_blocks, int32_t block_size, const int32_t* block_table,
+    int32_t max_blocks, const int32_t* ctx_lens, const int32_t* block_version,
+    const int32_t* req_version, float sm_scale, uint16_t* out, float* lse,
+    int32_t* stale_pairs, int64_t cap, int32_t* n_stale, int32_t* valid_tokens, void* ws,
+    size_t* ws_bytes, void* stream) {
+  const char* who = "paged_attn_decode_checked";
+  if (!ws_bytes) return local_fail(LOCAL_ERR_WORKSPACE, "%s: ws_bytes is NULL", who);
+  DecodeArgs a;
+  size_t part_elems = 0, need = 0;
+  local_status_t st = decode_setup(q, B, Hq, Hkv, D, k_new, v_new, k_cache, v_cache,
+                                   num_blocks, block_size, block_table, max_blocks, ctx_lens,
+                                   block_version, req_version, sm_scale, out, lse, who, &a,
+                                   &part_elems, &need);
+  if (st != LOCAL_OK) return st;
+  if (cap < 0) return local_fail(LOCAL_ERR_SHAPE, "%s: cap=%lld", who, (long long)cap);
+  if (a.n_parts > D)
+    return local_fail(LOCAL_ERR_UNSUPPORTED, "%s: max_blocks=%d over %d blocks", who,
+                      max_blocks, D * kBlocksPerPart);
+  const size_t masks = static_cast<size_t>(B > 0 ? B : 1) * a.n_parts;
+  const size_t total = align256(need) + 2 * align256(masks * sizeof(int32_t));
+  if (!ws) {
+    *ws_bytes = total;
+    return LOCAL_OK;
+  }
+  if (*ws_bytes < total)
+    return local_fail(LOCAL_ERR_WORKSPACE, "%s: workspace %zu < %zu", who, *ws_bytes, total);
+  if (!n_stale || (B > 0 && !valid_tokens) || (cap > 0 && !stale_pairs))
+    return local_fail(LOCAL_ERR_NULL, "%s: NULL version-check output", who);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (B == 0) {
+    decode_vc_empty_kernel<<<1, 1, 0, s>>>(n_stale);
+    return local_check_launch(who);
+  }
+  if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
+  char* base = static_cast<char*>(ws);
+  a.vc_mask = reinterpret_cast<uint32_t*>(base + align256(need));
+  a.vc_valid = reinterpret_cast<int32_t*>(base + align256(need) + align256(masks * 4));
+  a.vc_pairs = stale_pairs;
+  a.vc_cap = cap;
+  a.vc_n_stale = n_stale;
+  a.vc_valid_tokens = valid_tokens;
   return decode_launch(a, B, D, ws, part_elems, stream);
 }
 

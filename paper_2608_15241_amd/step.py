@@ -1,7 +1,9 @@
 """One step of the mixed-adapter LoRA transformer path, as prepared C-ABI calls.
 
-A step is the version check (once per step, it is the same for every layer)
-followed, per layer, by
+A step is the version check (once per step, it is the same for every layer;
+in decode it is folded into the first layer's attention call,
+local_paged_attn_decode_checked, which reads the same tags anyway) followed,
+per layer, by
     q, k, v = LoRA projections of x            (local_lora_linear x3)
     o       = paged attention over the cache   (local_paged_attn_decode/_prefill,
               which first appends this step's k, v)
@@ -73,10 +75,18 @@ class Step:
         self.calls: List[bd.Call] = []
         self.buffers = {}
         cap = stale_cap if stale_cap is not None else meta.block_table.numel()
-        self.version_check = bd.prepare_block_version_check(
-            meta.block_table, meta.ctx_lens, meta.block_version, meta.req_version, cap=cap,
-            workspace=self.ws)
-        self.calls.append(self.version_check)
+        self.version_check = None  # a separate call only in prefill
+        if kind == "prefill":
+            self.version_check = bd.prepare_block_version_check(
+                meta.block_table, meta.ctx_lens, meta.block_version, meta.req_version, cap=cap,
+                workspace=self.ws)
+            self.calls.append(self.version_check)
+            self.version_outputs = self.version_check.outputs
+        else:
+            self.version_outputs = (
+                torch.empty((max(cap, 1), 2), dtype=torch.int32, device=dev),
+                torch.empty((1,), dtype=torch.int32, device=dev),
+                torch.empty((meta.B,), dtype=torch.int32, device=dev))
         sm_scale = 1.0 / math.sqrt(D)
         xs = [x]
         self.layer_calls = []
@@ -90,7 +100,15 @@ class Step:
             lse = torch.empty((T, hq), dtype=torch.float32, device=dev)
             lc = {"in": self._in_proj(lw, xin, {"q": q, "k": k, "v": v}, meta)}
             kc, vc = kv_pool[l, 0], kv_pool[l, 1]
-            if kind == "decode":
+            if kind == "decode" and l == 0:
+                pairs, n_stale, valid = self.version_outputs
+                lc["attn"] = bd.prepare_paged_attn_decode_checked(
+                    q.view(T, hq, D), kc, vc, meta.block_table, meta.ctx_lens,
+                    meta.block_version, meta.req_version, sm_scale,
+                    k_new=k.view(T, hkv, D), v_new=v.view(T, hkv, D), Hkv=hkv,
+                    out=o.view(T, hq, D), lse=lse, cap=cap, stale_pairs=pairs,
+                    n_stale=n_stale, valid_tokens=valid, workspace=self.ws)
+            elif kind == "decode":
                 lc["attn"] = bd.prepare_paged_attn_decode(
                     q.view(T, hq, D), kc, vc, meta.block_table, meta.ctx_lens,
                     meta.block_version, meta.req_version, sm_scale,

@@ -362,3 +362,44 @@ def test_prefill_long_prefixes_split_key_ranges(D):
     assert np.array_equal(host_u16(vc_d), vc), "appended V pool differs"
     assert_attn(f64(out), ro, "out", D)
     assert_lse(lse.cpu().numpy(), rl, "lse")
+
+
+@pytest.mark.parametrize("B,max_blocks,cap", [(40, None, None), (600, None, 50), (7, 300, 0),
+                                              (129, 64, None)])
+def test_decode_checked_equals_attention_and_version_check(B, max_blocks, cap):
+    # The attention call that also reports the version check: its attention
+    # results are the plain call's bit for bit, and its stale list, count and
+    # valid tokens are the separate version check's (and the oracle's) bit
+    # for bit, also truncated at cap, with empty contexts and a table wider
+    # than the contexts.
+    say("decode checked", B, max_blocks, cap)
+    rng = np.random.default_rng(3000 + B)
+    ctx = rng.integers(0, 3000, size=B).astype(np.int32)
+    if max_blocks is not None:
+        ctx = np.minimum(ctx, 16 * max_blocks)
+    ctx[::11] = 0
+    c = _decode_case(rng, ctx, 8, 2, 128, stale_frac=0.3, max_blocks=max_blocks)
+    ctx_d, tab, bv, rv = dev(c["ctx"]), dev(c["table"]), dev(c["bv"]), dev(c["rv"])
+    res = []
+    for fn in (lk.local_paged_attn_decode, lk.local_paged_attn_decode_checked):
+        kc, vc = dev_u16(c["kc"]), dev_u16(c["vc"])
+        kw = {} if fn is lk.local_paged_attn_decode else {"cap": cap}
+        r = fn(dev_u16(c["q"]), kc, vc, tab, ctx_d, bv, rv, 1.0 / math.sqrt(128),
+               k_new=dev_u16(c["kn"]), v_new=dev_u16(c["vn"]), Hkv=2, **kw)
+        torch.cuda.synchronize()
+        res.append((r, kc, vc))
+    (o1, l1), k1, v1 = res[0]
+    (o2, l2, pairs, n, valid), k2, v2 = res[1]
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
+    assert torch.equal(k1.view(torch.int16), k2.view(torch.int16))
+    assert torch.equal(v1.view(torch.int16), v2.view(torch.int16))
+    cap_ = c["table"].size if cap is None else cap
+    p_ref, n_ref, v_ref = lk.local_block_version_check(tab, ctx_d, bv, rv, cap=cap_)
+    torch.cuda.synchronize()
+    ep, en, ev = oracle.block_version_check(c["table"], c["ctx"], c["bv"], c["rv"], cap=cap_)
+    assert int(n.item()) == en == int(n_ref.item())
+    assert np.array_equal(valid.cpu().numpy(), ev)
+    k = min(en, cap_)
+    assert np.array_equal(pairs[:k].cpu().numpy(), ep)
+    assert np.array_equal(p_ref[:k].cpu().numpy(), ep)

@@ -201,7 +201,8 @@ GROUPED = [
     (300, 512, (512, 256), 4, 16, None),       # long chunk: one launch over both
     (520, 512, (256, 768, 512), 5, 16, [16, 3, 9, 16, 0]),  # long chunk, three projections
     (300, 256, (320, 256), 3, 8, None),        # long chunk, N % 256 != 0: one at a time
-    (16, 512, (64, 64), 16, 16, None),          # shrink too wide to fuse: one at a time
+    (16, 512, (64, 64), 16, 16, None),          # shrink too wide to fuse: grouped SGMV
+    (64, 1024, (512, 128, 128), 16, 64, [8, 16, 32, 64] * 4),  # padded ranks: grouped SGMV
     (32, 512, (512, 512, 512), 0, 0, None),
     (200, 256, (256, 256, 512, 256), 5, 32, [32, 1, 17, 32, 24]),
 ]

@@ -87,7 +87,7 @@ def _decode_chain_check(w, reqs, seed=0, layers_to_compare=None):
     st()
     torch.cuda.synchronize()
     # version check of the step: bit-exact
-    pairs, n, valid = st.version_check.outputs
+    pairs, n, valid = st.version_outputs
     ep, en, ev = oracle.block_version_check(meta.block_table, meta.ctx_lens,
                                             meta.block_version, meta.req_version)
     assert int(n.item()) == en
@@ -210,7 +210,7 @@ def test_prefill_7b_step():
               residual=False)
     st()
     torch.cuda.synchronize()
-    pairs, n, valid = st.version_check.outputs
+    pairs, n, valid = st.version_outputs
     ep, en, ev = oracle.block_version_check(meta.block_table, meta.ctx_lens,
                                             meta.block_version, meta.req_version)
     assert int(n.item()) == en and np.array_equal(valid.cpu().numpy(), ev)
@@ -254,12 +254,12 @@ def test_step_graph_replays_match_eager():
     st()
     torch.cuda.synchronize()
     ref = {k: v.clone() for k, v in st.buffers[0].items()}
-    ref_pairs = [t.clone() for t in st.version_check.outputs]
+    ref_pairs = [t.clone() for t in st.version_outputs]
     g = st.capture()
     for rep in range(4):
         for k in ("q", "o", "y", "lse"):
             st.buffers[0][k].fill_(float("nan") if k == "lse" else 7.0)
-        st.version_check.outputs[2].fill_(-1)
+        st.version_outputs[2].fill_(-1)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -267,7 +267,7 @@ def test_step_graph_replays_match_eager():
             assert torch.equal(st.buffers[0][k].view(torch.int16) if v.dtype == torch.bfloat16
                                else st.buffers[0][k], v.view(torch.int16)
                                if v.dtype == torch.bfloat16 else v), (rep, k)
-        for a_, b_ in zip(st.version_check.outputs, ref_pairs):
+        for a_, b_ in zip(st.version_outputs, ref_pairs):
             assert torch.equal(a_, b_), rep
     del st, pool, weights
     torch.cuda.empty_cache()
