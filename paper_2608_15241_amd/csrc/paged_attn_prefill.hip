@@ -8,6 +8,10 @@
 //    that block's new K slots as 16-byte pieces and its new V slots through
 //    an LDS transpose (V is dim-major in the pool), as whole 32-byte dim rows
 //    when the block is all new. Every attention workgroup runs after it.
+//    Workgroup 0 of that launch (a launch of its own without an append)
+//    writes the schedule of the attention grid: its units (a tile, or a key
+//    range of a long tile) longest first, each entry with its request's
+//    sizes, so an attention workgroup knows its work after one load.
 //  * Attention workgroup = (tile of 128 query rows, query head h, request b):
 //    4 waves of 32 rows (two 16-column MFMA tiles each). The request's
 //    non-stale blocks up to the tile's causal limit are listed in ascending
@@ -45,9 +49,11 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 }
 // Tiles whose causal range spans more than kPaSplitBlocks blocks are split
 // into up to kPaMaxSplit key ranges of equal length, each its own workgroup;
-// a merge launch combines their partial results.
+// a merge launch combines their partial results. (With the units dispatched
+// longest first, a high threshold pays: the partial results cost HBM
+// traffic, and a long unit that starts first does not set the end.)
 #ifndef LOCAL_PA_SPLIT_BLOCKS
-#define LOCAL_PA_SPLIT_BLOCKS 48
+#define LOCAL_PA_SPLIT_BLOCKS 96
 #endif
 #ifndef LOCAL_PA_MAX_SPLIT
 #define LOCAL_PA_MAX_SPLIT 4
@@ -69,6 +75,8 @@ struct PrefillArgs {
   uint16_t* out;
   float* lse;
   float* part;  // workspace: partial results of split tiles
+  int* plan_total;  // workspace: the number of units, then their schedule
+  int4* plan;       // (two int4 per unit, in dispatch order)
   int64_t T, num_blocks;
   int B, Hq, Hkv, group, max_blocks;
   float scale_log2;  // |sm_scale| * log2(e)
@@ -141,6 +149,9 @@ __device__ __forceinline__ void lds_load16(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 }
 
+constexpr int kPlanThreads = 256;  // threads of the workgroup that plans the units
+__device__ void plan_units(const PrefillArgs& a);
+
 // Append. Workgroup = (one block that request b's chunk writes, KV head g),
 // mapped from a 1D grid (heads fastest); the block's slots [lo, hi) are new
 // (positions P_b .. L_b - 1). Thread t handles slot t / (D/8), dims
@@ -149,7 +160,13 @@ template <int D>
 __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
   constexpr int C8 = D / 8;
   __shared__ uint16_t vt[D][kBlockSize + 2];  // V of the block, dim-major (+2: banks)
-  const int g = blockIdx.x % a.Hkv;
+  // workgroup 0 (dispatched first) plans the attention grid's units
+  if (blockIdx.x == 0) {
+    plan_units(a);
+    return;
+  }
+  const unsigned bid = blockIdx.x - 1;
+  const int g = bid % a.Hkv;
   int jb = 0;
   // blocks request b's chunk writes: from its first new position's block to
   // its last one's (none for an empty chunk or a chunk past the context)
@@ -161,7 +178,7 @@ __global__ __launch_bounds__(256) void prefill_append_kernel(PrefillArgs a) {
     const int P = max(L - n, 0);
     return (L - 1) / kBlockSize - P / kBlockSize + 1;
   };
-  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hkv), chunk_blocks, &jb);
+  const int b = unit_from_end(a.B, static_cast<int>(bid / a.Hkv), chunk_blocks, &jb);
   if (b < 0) return;
   const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
   if (!rows_ok(r0, r1, a.T)) return;  // never given a unit; checked before any row is read
@@ -231,6 +248,117 @@ __device__ __forceinline__ int64_t part_slot(int r0, int b, int t, int h, int Hq
   return (static_cast<int64_t>(r0 / kPaRows + b + t) * Hq + h) * kPaMaxSplit + split;
 }
 
+// Length class of the key ranges of a tile of nbl blocks split into ns:
+// classes of 8 blocks of the mean range, the last one open-ended; the grid
+// takes the classes longest first.
+constexpr int kPaClasses = 8;
+__device__ __forceinline__ int tile_class(int nbl, int ns) {
+  return min((nbl / ns) >> 3, kPaClasses - 1);
+}
+
+// The unit schedule, written once per call by one workgroup of
+// kPlanThreads threads before the attention grid runs. Entry k (two int4)
+// names the k-th unit in dispatch order: {b, tile | split << 24 |
+// nsplit << 28, r0, n} and {P, 0, 0, 0} (request b's first row, rows and
+// cached prefix). Units go longest first, by length class; within a class
+// from the last request backwards, a request's tiles from its last one, a
+// tile's key ranges ascending. So the longest units start first, whatever
+// request they belong to, and the grid ends on the short ones; an attention
+// workgroup reads its unit with one load instead of deriving it.
+__device__ void plan_units(const PrefillArgs& a) {
+  __shared__ int scan[kPaClasses][kPlanThreads];
+  __shared__ int totals[kPaClasses];
+  const int tid = threadIdx.x;
+  // request bb's first row, rows and prefix (false: no rows, or a bad range)
+  auto rows = [&](int bb, int* r0, int* n, int* P) {
+    const int q0 = a.q_indptr[bb], q1 = a.q_indptr[bb + 1];
+    if (!rows_ok(q0, q1, a.T) || q1 == q0) return false;
+    *r0 = q0;
+    *n = q1 - q0;
+    *P = a.ctx_lens[bb] - *n;
+    return true;
+  };
+  auto count = [&](int P, int n, int (&cnt)[kPaClasses]) {
+    for (int t = 0; t * kPaRows < n; ++t) {
+      const int nbl = tile_blocks(P, n, t, a.max_blocks), ns = tile_splits(nbl);
+      const int c = tile_class(nbl, ns);
+#pragma unroll
+      for (int cc = 0; cc < kPaClasses; ++cc) cnt[cc] += c == cc ? ns : 0;
+    }
+  };
+  if (tid < kPaClasses) totals[tid] = 0;
+  __syncthreads();
+  for (int bb = tid; bb < a.B; bb += kPlanThreads) {
+    int r0, n, P, cnt[kPaClasses];
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c) cnt[c] = 0;
+    if (!rows(bb, &r0, &n, &P)) continue;
+    count(P, n, cnt);
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c)
+      if (cnt[c]) atomicAdd(&totals[c], cnt[c]);
+  }
+  __syncthreads();
+  int first[kPaClasses];  // next entry of each class
+  {
+    int acc = 0;
+#pragma unroll
+    for (int c = kPaClasses - 1; c >= 0; --c) {
+      first[c] = acc;
+      acc += totals[c];
+    }
+    if (tid == 0) *a.plan_total = acc;
+  }
+  // requests from the last backwards, kPlanThreads at a time: each thread's
+  // request takes the next entries of its classes (a scan over the threads)
+  for (int chunk = 0; chunk < a.B; chunk += kPlanThreads) {
+    const int bb = a.B - 1 - chunk - tid;
+    int r0 = 0, n = 0, P = 0, cnt[kPaClasses];
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c) cnt[c] = 0;
+    const bool ok = bb >= 0 && rows(bb, &r0, &n, &P);
+    if (ok) count(P, n, cnt);
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c) scan[c][tid] = cnt[c];
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {
+      int v[kPaClasses];
+#pragma unroll
+      for (int c = 0; c < kPaClasses; ++c) v[c] = tid >= off ? scan[c][tid - off] : 0;
+      __syncthreads();
+#pragma unroll
+      for (int c = 0; c < kPaClasses; ++c) scan[c][tid] += v[c];
+      __syncthreads();
+    }
+    int pos[kPaClasses];
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c) pos[c] = first[c] + scan[c][tid] - cnt[c];
+    if (ok) {
+      for (int t = (n - 1) / kPaRows; t >= 0; --t) {
+        const int nbl = tile_blocks(P, n, t, a.max_blocks), ns = tile_splits(nbl);
+        const int c = tile_class(nbl, ns);
+        int e = 0;
+#pragma unroll
+        for (int cc = 0; cc < kPaClasses; ++cc) e = c == cc ? pos[cc] : e;
+        for (int sp = 0; sp < ns; ++sp) {
+          a.plan[2 * (e + sp)] = make_int4(bb, t | (sp << 24) | (ns << 28), r0, n);
+          a.plan[2 * (e + sp) + 1] = make_int4(P, 0, 0, 0);
+        }
+#pragma unroll
+        for (int cc = 0; cc < kPaClasses; ++cc) pos[cc] += c == cc ? ns : 0;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kPaClasses; ++c) first[c] += scan[c][kPlanThreads - 1];
+    __syncthreads();  // before the next chunk rewrites the scan
+  }
+}
+
+// The planner alone, for calls without an append.
+__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs a) {
+  plan_units(a);
+}
+
 template <int D>
 constexpr int64_t part_slot_floats() {
   return static_cast<int64_t>(kPaRows) * (D + 2);  // O [128][D], then (m, l) [128][2]
@@ -249,40 +377,18 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   __shared__ int wave_cnt[kPaWaves];
 
   // (query tile, key range, head h, request b) from a 1D grid, heads
-  // fastest: the last requests' last tiles (a chunk's later rows see more
-  // keys, and requests are commonly listed by growing prefix) are dispatched
-  // first, so that the longest workgroups do not start behind short ones. A
-  // tile with a long causal range is split into key ranges (units of their
-  // own) so that no workgroup holds far more work than the mean.
+  // fastest, the units in the planned order (longest first, so that no long
+  // workgroup starts behind short ones). A tile with a long causal range is
+  // split into key ranges (units of their own) so that no workgroup holds
+  // far more work than the mean. Workgroups past the units leave.
   const int h = blockIdx.x % a.Hq;
-  int unit = 0;
-  auto units_of = [&](int bb) {
-    const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
-    const int n = r1 - r0;
-    if (!rows_ok(r0, r1, a.T) || n <= 0) return 0;
-    const int P = a.ctx_lens[bb] - n;
-    int u = 0;
-    for (int t = 0; t * kPaRows < n; ++t) u += tile_splits(tile_blocks(P, n, t, a.max_blocks));
-    return u;
-  };
-  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / a.Hq), units_of, &unit);
-  if (b < 0) return;
-  const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
-  if (!rows_ok(r0, r1, a.T)) return;  // never given a unit
-  const int n_b = r1 - r0;
-  const int L = a.ctx_lens[b];
-  const int P = L - n_b;  // cached prefix
-  int qtile = 0, split = 0, n_split = 1;
-  for (int t = 0, u = unit; t * kPaRows < n_b; ++t) {
-    const int ns = tile_splits(tile_blocks(P, n_b, t, a.max_blocks));
-    if (u < ns) {
-      qtile = t;
-      split = u;
-      n_split = ns;
-      break;
-    }
-    u -= ns;
-  }
+  const int k = static_cast<int>(blockIdx.x / a.Hq);
+  const int n_units = *a.plan_total;
+  const int4 e0 = a.plan[2 * k], e1 = a.plan[2 * k + 1];
+  if (k >= n_units) return;
+  const int b = e0.x, qtile = e0.y & 0xffffff, split = (e0.y >> 24) & 15, n_split = e0.y >> 28;
+  const int r0 = e0.z, n_b = e0.w, P = e1.x;
+  const int L = P + n_b;
   const int row0 = qtile * kPaRows;
   if (row0 >= n_b) return;
   const int tid = threadIdx.x;
@@ -291,6 +397,14 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   const int g = h / a.group;
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
+
+  // this unit's key range: logical blocks [j_lo, j_hi) of the tile's range
+  const int nb_tile = tile_blocks(P, n_b, qtile, a.max_blocks);
+  const int j_lo = split * nb_tile / n_split, j_hi = (split + 1) * nb_tile / n_split;
+  // The first window's block-table entry goes out before the query, so that
+  // the version loads it feeds need not wait for the query.
+  int p_first = 0;
+  if (j_lo + tid < j_hi) p_first = table[j_lo + tid];
 
   // Query columns of this wave: rows row0 + 32 wave + 16 ct + col. For a
   // negative softmax scale the query's sign bits are flipped (exact), so
@@ -308,22 +422,10 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       qraw[ct][c] =
           ld_global<u32x4>(a.q + (static_cast<int64_t>(r0 + rc) * a.Hq + h) * D + 32 * c + 8 * kgrp);
   }
-  // the query is waited for here, before any direct load is issued (a wait
-  // for it after them would wait for them too)
-#pragma unroll
-  for (int ct = 0; ct < QT; ++ct)
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      asm volatile("" : "+v"(qraw[ct][c]));
-      qv[ct][c] = as_bf16x8(qraw[ct][c] ^ a.q_sign);
-    }
   const float scl = a.scale_log2;
   const int wave_last_row = min(row0 + (wave + 1) * 16 * QT, n_b) - 1;
   const int wave_limit = P + wave_last_row;  // largest key position this wave sees
   const int wave_first = P + row0 + wave * 16 * QT;  // position of its first row
-  const int nb_tile = tile_blocks(P, n_b, qtile, a.max_blocks);
-  // this unit's key range: logical blocks [j_lo, j_hi) of the tile's range
-  const int j_lo = split * nb_tile / n_split, j_hi = (split + 1) * nb_tile / n_split;
 
   f32x4 acc[QT][VT];
   float m_run[QT];             // running maximum in raw score units
@@ -348,53 +450,65 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   constexpr int NPIECE = 2 * DMA + VT;
   constexpr int PPW = NPIECE / kPaWaves;
   static_assert(NPIECE % kPaWaves == 0 && STAGE_B == NPIECE * 1024, "stage layout");
-  int piece_blk[PPW];             // 0: block A, 1: block B
-  uint32_t piece_src[PPW];        // byte offset within that block's tile
-  const uint16_t* piece_pool[PPW];
-#pragma unroll
-  for (int i = 0; i < PPW; ++i) {
-    const int pc = wave * PPW + i;
-    if (pc < 2 * DMA) {  // K: 1 KB piece pc % DMA of block pc / DMA
-      piece_blk[i] = pc / DMA;
-      piece_src[i] = static_cast<uint32_t>(1024 * (pc % DMA) + 16 * lane);
-      piece_pool[i] = a.k_cache;
-    } else {             // V row t: lanes 0-31 from A, 32-63 from B
-      const int t = pc - 2 * DMA;
-      const int cidx = lane & 31;
-      const int dl = cidx >> 1;  // dim within the row (d = 16 t + dl)
-      const int half = (cidx & 1) ^ ((dl >> 3) & 1);
-      piece_blk[i] = lane >> 5;
-      piece_src[i] = static_cast<uint32_t>(32 * (16 * t + dl) + 16 * half);
-      piece_pool[i] = a.v_cache;
-    }
+  // Waves 0 and 1 load K (block A, block B: 1 KB piece i of the tile at
+  // byte 1024 i, lane l's 16 bytes at 16 l); waves 2 and 3 load V rows
+  // (row t = PPW (wave - 2) + i at byte 512 t of each block's tile, lanes
+  // 0-31 from A, 32-63 from B, lane l's 16 bytes at its swizzled chunk).
+  static_assert(PPW == DMA && 2 * DMA == VT, "K and V pieces in separate waves");
+  const bool k_wave = wave < 2;
+  const bool lane_b = k_wave ? wave == 1 : lane >= 32;  // the lane reads block B
+  uint32_t lane_src;  // byte offset of piece 0's 16 bytes within the block's tile
+  if (k_wave) {
+    lane_src = static_cast<uint32_t>(16 * lane);
+  } else {
+    const int cidx = lane & 31;
+    const int dl = cidx >> 1;  // dim within the row (d = 16 t + dl)
+    const int half = (cidx & 1) ^ ((dl >> 3) & 1);
+    lane_src = static_cast<uint32_t>(512 * PPW * (wave - 2) + 32 * dl + 16 * half);
   }
   // this lane's value fragment in V row t of a stage (A's half; B's is 512
   // bytes on): dim 16 t + col, slots 4 kgrp .. +4
   const uint32_t v_off = 32 * col + 16 * ((kgrp >> 1) ^ ((col >> 3) & 1)) + 8 * (kgrp & 1);
 
-  for (int w0 = j_lo; w0 < j_hi; w0 += kPaWindow) {
-    // ---- list the non-stale blocks of this window, in ascending j
+  // ---- list the non-stale blocks of window w0 (ascending j); returns the
+  // count. p_pre is the window's table entry when already loaded.
+  auto build_list = [&](int w0, bool pre, int p_pre) {
     const int j = w0 + tid;
     bool ok = false;
     int p = 0;
     if (j < j_hi) {
-      p = table[j];
+      p = pre ? p_pre : table[j];
       ok = id_ok(p, a.num_blocks) && a.block_version[p] == rv;
     }
     const uint64_t mask = __ballot(ok);
     const int before = __popcll(mask & ((1ull << lane) - 1ull));
     if (lane == 0) wave_cnt[wave] = __popcll(mask);
     __syncthreads();
-    int off = 0, cnt = 0;
+    int off = 0, n = 0;
     for (int w = 0; w < kPaWaves; ++w) {
       if (w < wave) off += wave_cnt[w];
-      cnt += wave_cnt[w];
+      n += wave_cnt[w];
     }
     if (ok) {
       list[off + before] = j;
       list_p[off + before] = p;
     }
     __syncthreads();
+    return n;
+  };
+  int cnt = build_list(j_lo, true, p_first);
+  // The query is waited for here (the version loads above have waited for
+  // it already), before any direct load is issued: a wait for it after them
+  // would wait for them too.
+#pragma unroll
+  for (int ct = 0; ct < QT; ++ct)
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      asm volatile("" : "+v"(qraw[ct][c]));
+      qv[ct][c] = as_bf16x8(qraw[ct][c] ^ a.q_sign);
+    }
+  for (int w0 = j_lo; w0 < j_hi; w0 += kPaWindow) {
+    if (w0 != j_lo) cnt = build_list(w0, false, 0);
     if (cnt == 0) continue;
     const int steps = (cnt + 1) / 2;
 
@@ -408,12 +522,15 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       const int pa = list_p[min(2 * s, cnt - 1)];
       const int pb = list_p[min(2 * s + 1, cnt - 1)];
       uint8_t* dst = ring + stage * STAGE_B + wave * PPW * 1024;
+      const int64_t tile = (static_cast<int64_t>(lane_b ? pb : pa) * a.Hkv + g) * TILE;
+      if (k_wave) {
+        const uint8_t* src = reinterpret_cast<const uint8_t*>(a.k_cache + tile) + lane_src;
 #pragma unroll
-      for (int i = 0; i < PPW; ++i) {
-        const int pp = piece_blk[i] ? pb : pa;
-        const uint8_t* src = reinterpret_cast<const uint8_t*>(
-            piece_pool[i] + (static_cast<int64_t>(pp) * a.Hkv + g) * TILE);
-        lds_load16(src + piece_src[i], dst + 1024 * i);
+        for (int i = 0; i < PPW; ++i) lds_load16(src + 1024 * i, dst + 1024 * i);
+      } else {
+        const uint8_t* src = reinterpret_cast<const uint8_t*>(a.v_cache + tile) + lane_src;
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) lds_load16(src + 512 * i, dst + 1024 * i);
       }
     };
 #pragma unroll
@@ -649,21 +766,35 @@ __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillArgs a) {
   if (d0 == 0 && a.lse) a.lse[orow] = den > 0.f ? (M * scl + __log2f(den)) * kLn2 : -INFINITY;
 }
 
-// Workspace of the split tiles' partial results: one slot per (tile bound,
-// head, split).
+// Workspace: the split tiles' partial results (one slot per tile bound,
+// head and split), then the unit schedule (its count in 256 bytes, then two
+// int4 per unit: at most kPaMaxSplit per tile bound).
+template <int D>
+size_t prefill_part_bytes(int64_t T, int B, int Hq) {
+  const int64_t tiles = T / kPaRows + B;
+  const size_t v =
+      static_cast<size_t>(tiles) * Hq * kPaMaxSplit * part_slot_floats<D>() * sizeof(float);
+  return (v + 255) & ~static_cast<size_t>(255);
+}
 template <int D>
 size_t prefill_ws_bytes(int64_t T, int B, int Hq) {
   const int64_t tiles = T / kPaRows + B;
-  return static_cast<size_t>(tiles) * Hq * kPaMaxSplit * part_slot_floats<D>() * sizeof(float);
+  return prefill_part_bytes<D>(T, B, Hq) + 256 +
+         static_cast<size_t>(tiles) * kPaMaxSplit * 2 * sizeof(int4);
 }
 
 template <int D>
 local_status_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   if (a.k_new) {
-    // a chunk of n rows spans at most n / 16 + 2 blocks: T / 16 + 2 B in all
+    // a chunk of n rows spans at most n / 16 + 2 blocks: T / 16 + 2 B in all;
+    // workgroup 0 plans the attention units
     const int64_t units = a.T / kBlockSize + 2LL * a.B;
-    prefill_append_kernel<D><<<static_cast<unsigned>(units * a.Hkv), 256, 0, s>>>(a);
+    prefill_append_kernel<D><<<static_cast<unsigned>(units * a.Hkv + 1), 256, 0, s>>>(a);
     local_status_t st = local_check_launch("paged_attn_prefill (append)");
+    if (st != LOCAL_OK) return st;
+  } else {
+    prefill_plan_kernel<<<1, kPlanThreads, 0, s>>>(a);
+    local_status_t st = local_check_launch("paged_attn_prefill (plan)");
     if (st != LOCAL_OK) return st;
   }
   constexpr int kLds = kPaStages * 4 * 2 * kBlockSize * D;
@@ -746,6 +877,11 @@ extern "C" local_status_t local_paged_attn_prefill(
   a.group = Hq / Hkv;
   a.max_blocks = max_blocks;
   a.part = static_cast<float*>(ws);
+  {
+    const size_t pb = D == 64 ? prefill_part_bytes<64>(T, B, Hq) : prefill_part_bytes<128>(T, B, Hq);
+    a.plan_total = reinterpret_cast<int*>(static_cast<char*>(ws) + pb);
+    a.plan = reinterpret_cast<int4*>(static_cast<char*>(ws) + pb + 256);
+  }
   // |sm_scale|; a zero scale (every visible key weighs the same) runs as a
   // vanishing positive one, under which masked keys still weigh exactly 0
   a.scale_log2 = fmaxf(fabsf(sm_scale) * kLog2e, 1.0e-30f);
