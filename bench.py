@@ -593,10 +593,63 @@ def bench_prefill(torch, workloads, lk, dev, reps=20):
     ms = a.elapsed_time(b) / reps
     flops = prefill_gemm_flops(w, meta)
     tflops = flops / (ms / 1e3) / 1e12
+    del graphs
     return {"workload": w.name,
             "kernel": "local_lora_linear_grouped (q,k,v) + local_lora_linear (o), T=%d" % meta.T,
             "bound": "mfma", "flops_per_step": flops, "ms_per_step": round(ms, 5),
             "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / BF16_PEAK_TFLOPS, 4),
+            "yardstick": library_gemm_yardstick(torch, w, meta, dev, reps)}
+
+
+def library_gemm_yardstick(torch, w, meta, dev, reps):
+    """The same base products (x W_qkv^T and o W_o^T, no adapters) through
+    torch.mm, i.e. the vendor GEMM library, timed the same way: a reference
+    for what the matrix cores give a plain GEMM of these shapes on this machine."""
+    sets = []
+    for s in range(2):
+        wq = [torch.empty(w.proj_shape(n), dtype=torch.bfloat16, device=dev).normal_()
+              for n in ("q", "k", "v")]
+        wqkv_t = torch.cat(wq, 0).t().contiguous()   # [K, Nq + Nk + Nv]
+        N, K = w.proj_shape("o")
+        wo_t = torch.empty((N, K), dtype=torch.bfloat16, device=dev).normal_().t().contiguous()
+        x = torch.empty((meta.T, w.hidden), dtype=torch.bfloat16, device=dev).normal_()
+        o = torch.empty((meta.T, K), dtype=torch.bfloat16, device=dev).normal_()
+        y1 = torch.empty((meta.T, wqkv_t.shape[1]), dtype=torch.bfloat16, device=dev)
+        y2 = torch.empty((meta.T, N), dtype=torch.bfloat16, device=dev)
+        sets.append((x, wqkv_t, y1, o, wo_t, y2))
+    for x, wt, y1, o, wo, y2 in sets:
+        torch.mm(x, wt, out=y1)
+        torch.mm(o, wo, out=y2)
+    torch.cuda.synchronize()
+    graphs = []
+    for x, wt, y1, o, wo, y2 in sets:
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            with torch.cuda.graph(g, stream=st):
+                torch.mm(x, wt, out=y1)
+                torch.mm(o, wo, out=y2)
+        torch.cuda.current_stream().wait_stream(st)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for r in range(reps):
+        graphs[r % 2].replay()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flops = 2 * meta.T * (w.hidden * sets[0][1].shape[1] + sets[0][3].shape[1] * sets[0][5].shape[1])
+    tflops = flops / (ms / 1e3) / 1e12
+    del graphs, sets
+    return {"kernel": "torch.mm (the vendor GEMM library): the same base products, no adapters",
+            "flops_per_step": flops, "ms_per_step": round(ms, 5), "achieved": round(tflops, 1),
             "frac": round(tflops / BF16_PEAK_TFLOPS, 4)}
 
 
