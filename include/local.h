@@ -364,11 +364,13 @@ local_status_t local_paged_attn_decode_checked(
  *  on that GPU until the process ends. The call allocates nothing and calls
  *  no allocating routine.
  *
- *  Limit: the partials need B * Hq * ceil(max_blocks / 32) * (D + 2) * 4
- *  bytes (the size local_paged_attn_decode asks for); a call needing more
- *  than LOCAL_DECODE_NOALLOC_SCRATCH_BYTES returns LOCAL_ERR_UNSUPPORTED and
- *  launches nothing. (131072 partials at D = 128: for instance 128 requests x
- *  32 heads with a 1024-block table.)
+ *  Limit: the partials need B * Hq * ceil(max_blocks / P) * (D + 2) * 4
+ *  bytes (the size local_paged_attn_decode asks for), P the partition length
+ *  in blocks: 32 for tables up to 256 blocks wide, 48 up to 512, 64 beyond.
+ *  A call needing more than LOCAL_DECODE_NOALLOC_SCRATCH_BYTES returns
+ *  LOCAL_ERR_UNSUPPORTED and launches nothing. (131072 partials at D = 128:
+ *  for instance 512 requests x 32 heads with a 256-block table, or 256
+ *  requests x 32 heads with a 1024-block table.)
  *  Every call on one GPU shares that GPU's scratch: calls that overlap on one
  *  GPU (different streams, or different threads' streams) race and give
  *  undefined results. Calls ordered on one stream are safe. Nothing in the

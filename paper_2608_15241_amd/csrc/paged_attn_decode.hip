@@ -39,10 +39,14 @@
 namespace localk {
 namespace {
 
-#ifndef LOCAL_DECODE_PART_BLOCKS
-#define LOCAL_DECODE_PART_BLOCKS 32
-#endif
-constexpr int kBlocksPerPart = LOCAL_DECODE_PART_BLOCKS;  // one wave, 512 tokens
+// Blocks per partition (one wave each), by the width of the block table:
+// 32 up to 256 blocks, 48 up to 512, 64 beyond (at most 64: one bit per lane
+// in the stale masks). Measured: the 32-layer decode with contexts up to 16K
+// tokens (1024-block tables) is 3.2% faster a step with 64 than with 32, the
+// GQA decode with 512-block tables 2% faster with 48, and the MHA decode with
+// 256-block tables fastest with 32 (fewer, longer partitions: less merge
+// traffic and fewer waves; shorter ones: more parallelism per request).
+int part_blocks(int max_blocks) { return max_blocks <= 256 ? 32 : max_blocks <= 512 ? 48 : 64; }
 constexpr float kNegBig = -1.0e30f;
 
 struct DecodeArgs {
@@ -63,7 +67,7 @@ struct DecodeArgs {
   // (request, partition), the stale blocks as a bit mask (bit i = block
   // j0 + i) and the live tokens of the valid ones, written by KV head 0's
   // waves; the merge launch turns them into the canonical outputs.
-  uint32_t* vc_mask;    // [B][n_parts]
+  uint64_t* vc_mask;    // [B][n_parts]
   int32_t* vc_valid;    // [B][n_parts]
   int32_t* vc_pairs;    // [cap][2] (b, j), or null when cap == 0
   int64_t vc_cap;
@@ -71,6 +75,7 @@ struct DecodeArgs {
   int32_t* vc_valid_tokens;  // [B]
   int64_t num_blocks;
   int Hq, Hkv, group, max_blocks, n_parts;
+  int pb;            // blocks per partition (part_blocks of max_blocks)
   float scale_log2;  // sm_scale * log2(e)
 };
 
@@ -104,8 +109,8 @@ __device__ int decode_unit(const DecodeArgs& a, int B, int k, int* part) {
   for (int c = 0; c < kRankChunks; ++c) {
     const int b = c * kWave + lane;
     const int nb = b < B ? owned_blocks(a.ctx_lens[b], a.max_blocks) : -1;
-    nf[c] = nb > 0 ? nb / kBlocksPerPart : 0;
-    rem[c] = nb > 0 ? nb % kBlocksPerPart : 0;
+    nf[c] = nb > 0 ? nb / a.pb : 0;
+    rem[c] = nb > 0 ? nb % a.pb : 0;
     has_partial[c] = nb == 0 || rem[c] > 0;  // nb = -1: no request
   }
   // slots past the last unit leave before any ranking
@@ -138,7 +143,7 @@ __device__ int decode_unit(const DecodeArgs& a, int B, int k, int* part) {
     }
     k -= cnt;
   }
-  for (int v = kBlocksPerPart - 1; v >= 0; --v) {
+  for (int v = a.pb - 1; v >= 0; --v) {
 #pragma unroll
     for (int c = 0; c < kRankChunks; ++c) {
       if (c >= nc) break;
@@ -201,7 +206,7 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
 
   const int lane = threadIdx.x;
   const int col = lane % 16, kgrp = lane / 16;
-  // Partition p covers blocks [nb - 32(p+1), nb - 32p) of b: the full ones
+  // Partition p covers blocks [nb - P(p+1), nb - Pp) of b (P = a.pb): the full ones
   // counted from the end of the context, then at most one partial one at the
   // start. An empty context runs partition 0 with no block (zero output,
   // lse = -inf). The grid is 1D, KV heads fastest, sized for n_parts + 1
@@ -222,7 +227,7 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
   }
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  const int n_full = nb / kBlocksPerPart, rem = nb % kBlocksPerPart;
+  const int n_full = nb / a.pb, rem = nb % a.pb;
   if (!RANKED) {
     if (part < a.n_parts) {
       if (part >= n_full && !(nb == 0 && part == 0)) return;
@@ -231,9 +236,9 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
       part = n_full;
     }
   }
-  const int j_end_part = nb - part * kBlocksPerPart;
-  const int j0 = max(0, j_end_part - kBlocksPerPart);
-  const int n_parts_b = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
+  const int j_end_part = nb - part * a.pb;
+  const int j0 = max(0, j_end_part - a.pb);
+  const int n_parts_b = max(1, (nb + a.pb - 1) / a.pb);
   const int rv = a.req_version[b];
   const int32_t* table = a.block_table + static_cast<int64_t>(b) * a.max_blocks;
   const int G = a.group;
@@ -242,21 +247,21 @@ __global__ __launch_bounds__(kWave) void decode_attn_kernel(DecodeArgs a, int B)
   const int jend = j_end_part;
   int my_phys = 0;
   bool ok = false;
-  if (lane < kBlocksPerPart && j0 + lane < jend) {
+  if (lane < a.pb && j0 + lane < jend) {
     my_phys = table[j0 + lane];
     ok = my_phys >= 0 && my_phys < a.num_blocks && a.block_version[my_phys] == rv;
     if (!ok) my_phys = 0;  // an id outside the pool is never dereferenced
   }
   uint64_t valid_mask = __ballot(ok);
   if (a.vc_mask && g == 0) {  // the version check of this partition's blocks
-    const bool owned = lane < kBlocksPerPart && j0 + lane < jend;
+    const bool owned = lane < a.pb && j0 + lane < jend;
     const uint64_t stale = __ballot(owned && !ok);
     int live = ok ? min(kBlockSize, L - kBlockSize * (j0 + lane)) : 0;
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) live += __shfl_xor(live, off);
     if (lane == 0) {
       const int64_t slot = static_cast<int64_t>(b) * a.n_parts + part;
-      a.vc_mask[slot] = static_cast<uint32_t>(stale);
+      a.vc_mask[slot] = stale;
       a.vc_valid[slot] = live;
     }
   }
@@ -445,21 +450,21 @@ __device__ void decode_version_check(const DecodeArgs& a, int b, int B, int* sh)
   const int tid = threadIdx.x, nt = blockDim.x;
   auto parts_of = [&](int bb) {
     const int nbb = owned_blocks(a.ctx_lens[bb], a.max_blocks);
-    return max(1, (nbb + kBlocksPerPart - 1) / kBlocksPerPart);
+    return max(1, (nbb + a.pb - 1) / a.pb);
   };
   int before = 0;
   for (int e = tid; e < b * a.n_parts; e += nt) {
     const int bb = e / a.n_parts, pp = e % a.n_parts;
-    if (pp < parts_of(bb)) before += __popc(a.vc_mask[e]);
+    if (pp < parts_of(bb)) before += __popcll(a.vc_mask[e]);
   }
   const int np = parts_of(b);
   // this request's partitions in ascending j: t-th is partition np - 1 - t
   int cnt = 0, valid = 0;
-  uint32_t mask = 0u;
+  uint64_t mask = 0ull;
   if (tid < np) {
     const int64_t slot = static_cast<int64_t>(b) * a.n_parts + (np - 1 - tid);
     mask = a.vc_mask[slot];
-    cnt = __popc(mask);
+    cnt = __popcll(mask);
     valid = a.vc_valid[slot];
   }
   // block-wide sums of `before` and `valid`, exclusive prefix of `cnt` over t
@@ -486,12 +491,12 @@ __device__ void decode_version_check(const DecodeArgs& a, int b, int B, int* sh)
   if (tid < np) {  // (np <= n_parts <= nt: the host checks)
     const int nbb = owned_blocks(a.ctx_lens[b], a.max_blocks);
     const int p = np - 1 - tid;
-    const int j0 = max(0, nbb - kBlocksPerPart * (p + 1));
+    const int j0 = max(0, nbb - a.pb * (p + 1));
     int64_t pos = static_cast<int64_t>(offset) + pre;
-    for (uint32_t m = mask; m; m &= m - 1u, ++pos) {
+    for (uint64_t m = mask; m; m &= m - 1ull, ++pos) {
       if (pos < a.vc_cap) {
         a.vc_pairs[2 * pos] = b;
-        a.vc_pairs[2 * pos + 1] = j0 + __ffs(static_cast<int>(m)) - 1;
+        a.vc_pairs[2 * pos + 1] = j0 + __ffsll(static_cast<long long>(m)) - 1;
       }
     }
     if (b == B - 1 && tid == np - 1) *a.vc_n_stale = offset + pre + cnt;
@@ -509,7 +514,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a, int B) {
   }
   const int L = a.ctx_lens[b];
   const int nb = owned_blocks(L, a.max_blocks);
-  const int np = max(1, (nb + kBlocksPerPart - 1) / kBlocksPerPart);
+  const int np = max(1, (nb + a.pb - 1) / a.pb);
   if (np == 1) return;  // written by the main kernel
   // one pass over the partitions, 8 at a time with all their loads in flight;
   // the running sums are rescaled when a batch raises the maximum
@@ -601,7 +606,8 @@ static local_status_t decode_setup(const uint16_t* q, int32_t B, int32_t Hq, int
                       block_size, D, Hq / Hkv);
   if ((k_new == nullptr) != (v_new == nullptr))
     return local_fail(LOCAL_ERR_NULL, "%s: k_new and v_new must both be set", who);
-  const int n_parts = (max_blocks + kBlocksPerPart - 1) / kBlocksPerPart;
+  const int pb = part_blocks(max_blocks);
+  const int n_parts = (max_blocks + pb - 1) / pb;
   *part_elems = static_cast<size_t>(B > 0 ? B : 1) * Hq * n_parts;
   *need = *part_elems * (D + 2) * sizeof(float);
   a->q = q;
@@ -629,6 +635,7 @@ static local_status_t decode_setup(const uint16_t* q, int32_t B, int32_t Hq, int
   a->num_blocks = num_blocks;
   a->max_blocks = max_blocks;
   a->n_parts = n_parts;
+  a->pb = pb;
   a->scale_log2 = sm_scale * kLog2e;
   return LOCAL_OK;
 }
@@ -701,9 +708,10 @@ extern "C" local_status_t local_paged_attn_decode_checked(
   if (cap < 0) return local_fail(LOCAL_ERR_SHAPE, "%s: cap=%lld", who, (long long)cap);
   if (a.n_parts > D)
     return local_fail(LOCAL_ERR_UNSUPPORTED, "%s: max_blocks=%d over %d blocks", who,
-                      max_blocks, D * kBlocksPerPart);
+                      max_blocks, D * a.pb);
   const size_t masks = static_cast<size_t>(B > 0 ? B : 1) * a.n_parts;
-  const size_t total = align256(need) + 2 * align256(masks * sizeof(int32_t));
+  const size_t total =
+      align256(need) + align256(masks * sizeof(uint64_t)) + align256(masks * sizeof(int32_t));
   if (!ws) {
     *ws_bytes = total;
     return LOCAL_OK;
@@ -719,8 +727,8 @@ extern "C" local_status_t local_paged_attn_decode_checked(
   }
   if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
   char* base = static_cast<char*>(ws);
-  a.vc_mask = reinterpret_cast<uint32_t*>(base + align256(need));
-  a.vc_valid = reinterpret_cast<int32_t*>(base + align256(need) + align256(masks * 4));
+  a.vc_mask = reinterpret_cast<uint64_t*>(base + align256(need));
+  a.vc_valid = reinterpret_cast<int32_t*>(base + align256(need) + align256(masks * 8));
   a.vc_pairs = stale_pairs;
   a.vc_cap = cap;
   a.vc_n_stale = n_stale;
@@ -785,9 +793,9 @@ extern "C" local_status_t local_paged_attn_decode_noalloc(
   if (st != LOCAL_OK) return st;
   if (need > kNoAllocBytes)
     return local_fail(LOCAL_ERR_UNSUPPORTED,
-                      "%s: B*Hq*ceil(max_blocks/32)*(D+2)*4 = %zu bytes of partials exceed the "
+                      "%s: B*Hq*ceil(max_blocks/%d)*(D+2)*4 = %zu bytes of partials exceed the "
                       "library's fixed scratch of %zu bytes (use local_paged_attn_decode with a "
-                      "workspace)", who, need, kNoAllocBytes);
+                      "workspace)", who, a.pb, need, kNoAllocBytes);
   if (B == 0) return LOCAL_OK;
   if ((st = decode_pointers_ok(a, who)) != LOCAL_OK) return st;
   void* partials = scratch_of_current_device(&st);

@@ -365,7 +365,7 @@ def test_prefill_long_prefixes_split_key_ranges(D):
 
 
 @pytest.mark.parametrize("B,max_blocks,cap", [(40, None, None), (600, None, 50), (7, 300, 0),
-                                              (129, 64, None)])
+                                              (129, 64, None), (9, 700, None)])
 def test_decode_checked_equals_attention_and_version_check(B, max_blocks, cap):
     # The attention call that also reports the version check: its attention
     # results are the plain call's bit for bit, and its stale list, count and

@@ -253,10 +253,15 @@ def test_decode_noalloc_rejects_sizes_beyond_its_scratch(lib):
         return f(FAKE, B, Hq, Hkv, D, kn, vn, FAKE, FAKE, 100000, bs, FAKE, mb, FAKE, FAKE,
                  FAKE, 0.088, FAKE, FAKE, None)
 
-    assert 128 * 32 * 32 * (128 + 2) * 4 == limit      # exactly at the limit: accepted
-    assert call(B=129) == ERR_UNSUPPORTED               # one request more: refused
+    # partitions of 32 blocks for tables up to 256 wide, 48 up to 512, 64 beyond
+    assert 256 * 32 * 16 * (128 + 2) * 4 == limit      # 1024 blocks: 16 partitions
+    assert call(B=257) == ERR_UNSUPPORTED               # one request more: refused
     assert b"scratch" in lib.local_last_error()
-    assert call(B=1, Hq=32, mb=32 * 4097) == ERR_UNSUPPORTED
+    assert 512 * 32 * 8 * (128 + 2) * 4 == limit       # 256 blocks: 8 partitions
+    assert call(B=513, mb=256) == ERR_UNSUPPORTED
+    assert 372 * 32 * 11 <= 131072 < 373 * 32 * 11      # 512 blocks: 11 partitions of 48
+    assert call(B=373, mb=512) == ERR_UNSUPPORTED
+    assert call(B=1, Hq=32, mb=64 * 4097) == ERR_UNSUPPORTED
     assert call(B=0) == OK                              # nothing to do, nothing launched
     assert call(Hq=32, Hkv=6) == ERR_SHAPE
     assert call(D=96) == ERR_UNSUPPORTED

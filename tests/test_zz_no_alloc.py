@@ -80,13 +80,14 @@ def test_noalloc_matches_workspace_entry_point_twice():
 
 
 def test_noalloc_at_its_size_limit_and_beyond():
-    # 128 requests x 32 heads with a 1024-block table need exactly the
-    # library's scratch; one request more is refused before any launch.
+    # 256 requests x 32 heads with a 1024-block table (16 partitions of 64
+    # blocks) need exactly the library's scratch; one request more is refused
+    # before any launch.
     rng = np.random.default_rng(78)
     say("noalloc at the limit")
-    c = _case(rng, rng.integers(1, 700, size=128), 32, 8, 128, max_blocks=1024)
+    c = _case(rng, rng.integers(1, 1100, size=256), 32, 8, 128, max_blocks=1024)
     _check(c, _both(c))
-    big = _case(rng, rng.integers(1, 40, size=129), 32, 8, 128, max_blocks=1024)
+    big = _case(rng, rng.integers(1, 40, size=257), 32, 8, 128, max_blocks=1024)
     with pytest.raises(lk.LocalError, match="scratch"):
         lk.local_paged_attn_decode_noalloc(
             dev_u16(big["q"]), dev_u16(big["kc"]), dev_u16(big["vc"]), dev(big["table"]),
