@@ -208,13 +208,15 @@ def test_prefill_matches_oracle(Hq, Hkv, D):
     assert_lse(lse.cpu().numpy(), rl, "lse")
 
 
-@pytest.mark.parametrize("B", [65, 130])
-def test_prefill_many_requests(B):
-    # more requests than a wavefront scans at once: the device-side mapping of
-    # the grid onto (request, tile) and (request, block) takes several passes;
-    # empty chunks, chunks starting and ending inside a block, long chunks
-    say("prefill many requests", B)
-    rng = np.random.default_rng(B)
+@pytest.mark.parametrize("B,append", [(65, True), (130, True), (300, True), (300, False)])
+def test_prefill_many_requests(B, append):
+    # more requests than a wavefront scans at once, and (300) than the unit
+    # planner's workgroup lists in one pass: the device-side mapping of the
+    # grid onto (request, tile) and (request, block) takes several passes;
+    # empty chunks, chunks starting and ending inside a block, long chunks;
+    # without an append the planner runs as a launch of its own
+    say("prefill many requests", B, append)
+    rng = np.random.default_rng(B + (0 if append else 1))
     Hq, Hkv, D = 8, 2, 64
     prefix = rng.integers(0, 300, size=B)
     chunk = rng.integers(0, 150, size=B)
@@ -222,13 +224,14 @@ def test_prefill_many_requests(B):
     chunk[3] = 300
     c = _prefill_case(rng, prefix, chunk, Hq, Hkv, D, 0.1)
     kc_d, vc_d = dev_u16(c["kc"]), dev_u16(c["vc"])
+    kw = dict(k_new=dev_u16(c["kn"]), v_new=dev_u16(c["vn"])) if append else {}
     out, lse = lk.local_paged_attn_prefill(
         dev_u16(c["q"]), dev(c["qi"]), kc_d, vc_d, dev(c["table"]), dev(c["ctx"]),
-        dev(c["bv"]), dev(c["rv"]), 1.0 / math.sqrt(D), k_new=dev_u16(c["kn"]),
-        v_new=dev_u16(c["vn"]), Hkv=Hkv)
+        dev(c["bv"]), dev(c["rv"]), 1.0 / math.sqrt(D), Hkv=Hkv, **kw)
     torch.cuda.synchronize()
     kc, vc = c["kc"].copy(), c["vc"].copy()
-    oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
+    if append:
+        oracle.kv_append(kc, vc, Hkv, D, c["table"], c["qi"], c["ctx"], c["kn"], c["vn"])
     ro, rl = oracle.paged_attn(c["q"], c["qi"], Hq, Hkv, D, kc, vc, c["table"], c["ctx"],
                                c["bv"], c["rv"], 1.0 / math.sqrt(D))
     assert np.array_equal(host_u16(kc_d), kc), "appended K pool differs"
