@@ -75,8 +75,9 @@ struct PrefillArgs {
   uint16_t* out;
   float* lse;
   float* part;  // workspace: partial results of split tiles
-  int* plan_total;  // workspace: the number of units, then their schedule
-  int4* plan;       // (two int4 per unit, in dispatch order)
+  int* plan_total;  // workspace: the number of units and of split tiles,
+  int4* plan;       // the schedule (two int4 per unit, in dispatch order),
+  int4* splits;     // the split tiles (one int4 each, in any order)
   int64_t T, num_blocks;
   int B, Hq, Hkv, group, max_blocks;
   float scale_log2;  // |sm_scale| * log2(e)
@@ -268,6 +269,7 @@ __device__ __forceinline__ int tile_class(int nbl, int ns) {
 __device__ void plan_units(const PrefillArgs& a) {
   __shared__ int scan[kPaClasses][kPlanThreads];
   __shared__ int totals[kPaClasses];
+  __shared__ int n_split_tiles;
   const int tid = threadIdx.x;
   // request bb's first row, rows and prefix (false: no rows, or a bad range)
   auto rows = [&](int bb, int* r0, int* n, int* P) {
@@ -287,6 +289,7 @@ __device__ void plan_units(const PrefillArgs& a) {
     }
   };
   if (tid < kPaClasses) totals[tid] = 0;
+  if (tid == 0) n_split_tiles = 0;
   __syncthreads();
   for (int bb = tid; bb < a.B; bb += kPlanThreads) {
     int r0, n, P, cnt[kPaClasses];
@@ -344,6 +347,10 @@ __device__ void plan_units(const PrefillArgs& a) {
           a.plan[2 * (e + sp)] = make_int4(bb, t | (sp << 24) | (ns << 28), r0, n);
           a.plan[2 * (e + sp) + 1] = make_int4(P, 0, 0, 0);
         }
+        if (ns > 1) {  // a tile the merge launch combines
+          const int i = atomicAdd(&n_split_tiles, 1);
+          a.splits[i] = make_int4(bb, t | (ns << 28), r0, n);
+        }
 #pragma unroll
         for (int cc = 0; cc < kPaClasses; ++cc) pos[cc] += c == cc ? ns : 0;
       }
@@ -352,6 +359,7 @@ __device__ void plan_units(const PrefillArgs& a) {
     for (int c = 0; c < kPaClasses; ++c) first[c] += scan[c][kPlanThreads - 1];
     __syncthreads();  // before the next chunk rewrites the scan
   }
+  if (tid == 0) a.plan_total[1] = n_split_tiles;
 }
 
 // The planner alone, for calls without an append.
@@ -701,11 +709,10 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   }
 }
 
-// Merge of the split tiles: workgroup = (tile, head, group of rows), the
-// tile and head mapped as in the attention grid without the splits; tiles
-// that were not split were written in place and leave at once. A thread owns
-// 8 dims of one row and issues every load of every key range before any
-// arithmetic.
+// Merge of the split tiles: workgroup = (split tile, head, group of rows),
+// the split tiles from the planner's list (tiles that were not split were
+// written in place). A thread owns 8 dims of one row and issues every load of
+// every key range before any arithmetic.
 template <int D>
 __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillArgs a) {
   constexpr int TPR = D / 8;           // threads per row
@@ -713,20 +720,13 @@ __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillArgs a) {
   constexpr int RG = kPaRows / RPW;    // row groups per tile
   const int rg = blockIdx.x % RG;
   const int h = (blockIdx.x / RG) % a.Hq;
-  int qtile = 0;
-  auto row_tiles = [&](int bb) {
-    const int r0 = a.q_indptr[bb], r1 = a.q_indptr[bb + 1];
-    const int n = r1 - r0;
-    return rows_ok(r0, r1, a.T) && n > 0 ? (n + kPaRows - 1) / kPaRows : 0;
-  };
-  const int b = unit_from_end(a.B, static_cast<int>(blockIdx.x / (RG * a.Hq)), row_tiles, &qtile);
-  if (b < 0) return;
-  const int r0 = a.q_indptr[b], r1 = a.q_indptr[b + 1];
-  if (!rows_ok(r0, r1, a.T)) return;
-  const int n_b = r1 - r0;
-  const int P = a.ctx_lens[b] - n_b;
-  const int ns = tile_splits(tile_blocks(P, n_b, qtile, a.max_blocks));
-  if (ns == 1) return;
+  // the k-th split tile of the planner's list (workgroups past it leave)
+  const int k = static_cast<int>(blockIdx.x / (RG * a.Hq));
+  const int n_split_tiles = a.plan_total[1];
+  const int4 e0 = a.splits[k];
+  if (k >= n_split_tiles) return;
+  const int b = e0.x, qtile = e0.y & 0xffffff, ns = e0.y >> 28;
+  const int r0 = e0.z, n_b = e0.w;
   const int rl = rg * RPW + threadIdx.x / TPR;  // row within the tile
   const int d0 = 8 * (threadIdx.x % TPR);
   if (qtile * kPaRows + rl >= n_b) return;
@@ -767,8 +767,9 @@ __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillArgs a) {
 }
 
 // Workspace: the split tiles' partial results (one slot per tile bound,
-// head and split), then the unit schedule (its count in 256 bytes, then two
-// int4 per unit: at most kPaMaxSplit per tile bound).
+// head and split), then the plan: its counts in 256 bytes, the unit schedule
+// (two int4 per unit: at most kPaMaxSplit per tile bound) and the list of
+// split tiles (one int4 each: at most one per tile bound).
 template <int D>
 size_t prefill_part_bytes(int64_t T, int B, int Hq) {
   const int64_t tiles = T / kPaRows + B;
@@ -780,7 +781,7 @@ template <int D>
 size_t prefill_ws_bytes(int64_t T, int B, int Hq) {
   const int64_t tiles = T / kPaRows + B;
   return prefill_part_bytes<D>(T, B, Hq) + 256 +
-         static_cast<size_t>(tiles) * kPaMaxSplit * 2 * sizeof(int4);
+         static_cast<size_t>(tiles) * (2 * kPaMaxSplit + 1) * sizeof(int4);
 }
 
 template <int D>
@@ -881,6 +882,7 @@ extern "C" local_status_t local_paged_attn_prefill(
     const size_t pb = D == 64 ? prefill_part_bytes<64>(T, B, Hq) : prefill_part_bytes<128>(T, B, Hq);
     a.plan_total = reinterpret_cast<int*>(static_cast<char*>(ws) + pb);
     a.plan = reinterpret_cast<int4*>(static_cast<char*>(ws) + pb + 256);
+    a.splits = a.plan + 2 * (T / kPaRows + B) * kPaMaxSplit;
   }
   // |sm_scale|; a zero scale (every visible key weighs the same) runs as a
   // vanishing positive one, under which masked keys still weigh exactly 0

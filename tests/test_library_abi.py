@@ -110,11 +110,11 @@ def test_prefill_and_version_check_errors(lib):
     st, n = _size(lib.local_paged_attn_prefill, FAKE, FAKE, 4, 2048, 32, 32, 128, FAKE, FAKE,
                   FAKE, FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE)
     # partial results of split tiles: (T/128 + B) tiles x 32 heads x 4 key ranges x
-    # 128 rows x (D + 2) floats; then the unit schedule: a 256-byte count and
-    # two int4 per unit, 4 units per tile bound
+    # 128 rows x (D + 2) floats; then the plan: 256 bytes of counts and the schedule:
+    # two int4 per unit, 4 units per tile bound, then one int4 per split tile
     tiles = 2048 // 128 + 4
     parts = tiles * 32 * 4 * 128 * (128 + 2) * 4
-    assert st == OK and n == (parts + 255) // 256 * 256 + 256 + tiles * 4 * 32
+    assert st == OK and n == (parts + 255) // 256 * 256 + 256 + tiles * 4 * 32 + tiles * 16
     ws = ctypes.c_size_t(n - 1)
     assert lib.local_paged_attn_prefill(FAKE, FAKE, 4, 2048, 32, 32, 128, FAKE, FAKE, FAKE,
                                         FAKE, 352, 16, FAKE, 160, FAKE, FAKE, FAKE, 0.088, FAKE,
