@@ -107,6 +107,15 @@ __device__ __forceinline__ u32x2 buf_load8_stream(__amdgpu_buffer_rsrc_t r, uint
 }
 
 // ---------------------------------------------------------------- lanes
+// max(a, b) in one instruction: fmaxf of values the compiler cannot prove
+// canonical (a lane swap's result, say) adds a NaN-quieting maximum per
+// operand. The operands here are never NaN.
+__device__ __forceinline__ float max2f(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Maximum of v over lanes l and l ^ 16 (l ^ 32), by the gfx950 lane swaps of
 // the vector unit (no LDS round trip): swapping a register with itself
 // leaves each lane its own value in one result and its partner's in the
@@ -114,13 +123,13 @@ __device__ __forceinline__ u32x2 buf_load8_stream(__amdgpu_buffer_rsrc_t r, uint
 __device__ __forceinline__ float max_xor16(float v) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 __device__ __forceinline__ float max_xor32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // ---------------------------------------------------------------- math

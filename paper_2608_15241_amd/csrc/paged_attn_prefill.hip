@@ -526,11 +526,12 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     // end repeats its first (never used), and steps past the last repeat the
     // last into the free stage, so every step issues the same loads and the
     // wait counts hold.
-    auto issue = [&](int stage, int s) {
-      const int pa = list_p[min(2 * s, cnt - 1)];
-      const int pb = list_p[min(2 * s + 1, cnt - 1)];
+    auto ids = [&](int s) {
+      return int2{list_p[min(2 * s, cnt - 1)], list_p[min(2 * s + 1, cnt - 1)]};
+    };
+    auto issue = [&](int stage, int2 p) {
       uint8_t* dst = ring + stage * STAGE_B + wave * PPW * 1024;
-      const int64_t tile = (static_cast<int64_t>(lane_b ? pb : pa) * a.Hkv + g) * TILE;
+      const int64_t tile = (static_cast<int64_t>(lane_b ? p.y : p.x) * a.Hkv + g) * TILE;
       if (k_wave) {
         const uint8_t* src = reinterpret_cast<const uint8_t*>(a.k_cache + tile) + lane_src;
 #pragma unroll
@@ -542,7 +543,12 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       }
     };
 #pragma unroll
-    for (int s = 0; s < kPaStages - 1; ++s) issue(s, min(s, steps - 1));
+    for (int s = 0; s < kPaStages - 1; ++s) issue(s, ids(min(s, steps - 1)));
+    // The list entries a pass needs (the ids its loads fetch, the blocks it
+    // computes on) are read one pass ahead, so that no LDS round trip stands
+    // between the barrier and the loads or the arithmetic of a pass.
+    int2 p_next = ids(min(kPaStages - 1, steps - 1));
+    int2 j_next = {list[0], list[min(1, cnt - 1)]};
 
     for (int s = 0; s < steps; ++s) {
       // this wave's loads of step s are done (those of the two later steps
@@ -550,10 +556,12 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       // step s - 1 is free for step s + 3
       wait_vmcnt<PPW * (kPaStages - 2)>();
       wait_lgkm0_barrier();
-      issue((s + kPaStages - 1) % kPaStages, min(s + kPaStages - 1, steps - 1));
-      const int jA = list[2 * s];
+      issue((s + kPaStages - 1) % kPaStages, p_next);
+      const int jA = j_next.x;
       const bool hasB = 2 * s + 1 < cnt;
-      const int jB = hasB ? list[2 * s + 1] : jA;
+      const int jB = hasB ? j_next.y : jA;
+      p_next = ids(min(s + kPaStages, steps - 1));
+      j_next = int2{list[min(2 * s + 2, cnt - 1)], list[min(2 * s + 3, cnt - 1)]};
       if (jA * kBlockSize > wave_limit) continue;  // wholly past this wave's rows
       // every key of the step precedes every row of the wave (so it is also
       // before the context end): no masking
@@ -568,28 +576,14 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         kfa[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kA + c * 512 + lane * 8));
         kfb[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kB + c * 512 + lane * 8));
       }
-      // V fragments: slots 4 kgrp .. +4 of each block. Slots at or past the
-      // context end may hold anything and are zeroed; only a step that holds
-      // the context end (or has no second block) needs it, and that is the
-      // same for the whole wave.
+      // V fragments: slots 4 kgrp .. +4 of each block (read here, zeroed
+      // past the context end just before the value product).
       bf16x8 vf[VT];
 #pragma unroll
       for (int t = 0; t < VT; ++t) {
         const u32x2 va = *reinterpret_cast<const u32x2*>(vrow + 1024 * t);
         const u32x2 vb = *reinterpret_cast<const u32x2*>(vrow + 1024 * t + 512);
         vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
-      }
-      const bool tail = !hasB || (jA + 1) * kBlockSize > L || (jB + 1) * kBlockSize > L;
-      if (tail) {
-        const int la = L - jA * kBlockSize - 4 * kgrp;
-        const int lb = hasB ? L - jB * kBlockSize - 4 * kgrp : 0;
-        const u32x4 mk = {la >= 2 ? ~0u : (la == 1 ? 0xffffu : 0u),
-                          la >= 4 ? ~0u : (la == 3 ? 0xffffu : 0u),
-                          lb >= 2 ? ~0u : (lb == 1 ? 0xffffu : 0u),
-                          lb >= 4 ? ~0u : (lb == 3 ? 0xffffu : 0u)};
-#pragma unroll
-        for (int t = 0; t < VT; ++t)
-          vf[t] = as_bf16x8(__builtin_bit_cast(u32x4, vf[t]) & mk);
       }
       // S^T of both column tiles: 2 * QT independent chains of KC MFMAs,
       // interleaved so that no MFMA waits on the one before it (raw scores:
@@ -638,9 +632,9 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
         float mx = max3f(max3f(sc[ct][0], sc[ct][1], sc[ct][2]),
-                         max3f(sc[ct][3], sc[ct][4], sc[ct][5]), fmaxf(sc[ct][6], sc[ct][7]));
+                         max3f(sc[ct][3], sc[ct][4], sc[ct][5]), max2f(sc[ct][6], sc[ct][7]));
         mx = max_xor32(max_xor16(mx));
-        m_new[ct] = fmaxf(m_run[ct], mx);
+        m_new[ct] = max2f(m_run[ct], mx);
         grow = grow || (m_new[ct] - m_run[ct]) * scl > kPaLazy;
       }
       if (__ballot(grow) != 0ull) {
@@ -666,6 +660,22 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
           pb[ct][i] = static_cast<__bf16>(pr[i]);
         }
         l_run[ct] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+      }
+      // Slots at or past the context end may hold anything and are zeroed;
+      // only a step that holds the context end (or has no second block)
+      // needs it, and that is the same for the whole wave. (Here, after the
+      // score products, so that those wait only for the K fragments.)
+      const bool tail = !hasB || (jA + 1) * kBlockSize > L || (jB + 1) * kBlockSize > L;
+      if (tail) {
+        const int la = L - jA * kBlockSize - 4 * kgrp;
+        const int lb = hasB ? L - jB * kBlockSize - 4 * kgrp : 0;
+        const u32x4 mk = {la >= 2 ? ~0u : (la == 1 ? 0xffffu : 0u),
+                          la >= 4 ? ~0u : (la == 3 ? 0xffffu : 0u),
+                          lb >= 2 ? ~0u : (lb == 1 ? 0xffffu : 0u),
+                          lb >= 4 ? ~0u : (lb == 3 ? 0xffffu : 0u)};
+#pragma unroll
+        for (int t = 0; t < VT; ++t)
+          vf[t] = as_bf16x8(__builtin_bit_cast(u32x4, vf[t]) & mk);
       }
 #pragma unroll
       for (int t = 0; t < VT; ++t)
