@@ -585,22 +585,21 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         const u32x2 vb = *reinterpret_cast<const u32x2*>(vrow + 1024 * t + 512);
         vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
       }
-      // S^T of both column tiles: 2 * QT independent chains of KC MFMAs,
-      // interleaved so that no MFMA waits on the one before it (raw scores:
-      // the scale is applied in the exponent)
+      // S^T of both column tiles, one column tile after the other (its two
+      // chains of KC MFMAs interleaved), so that the first tile's maxima can
+      // start while the second's products run (raw scores: the scale is
+      // applied in the exponent)
       f32x4 sA[QT], sB[QT];
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
         sA[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
         sB[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
 #pragma unroll
-      for (int c = 0; c < KC; ++c)
-#pragma unroll
-        for (int ct = 0; ct < QT; ++ct) {
+        for (int c = 0; c < KC; ++c) {
           sA[ct] = mfma16x16x32(kfa[c], qv[ct][c], sA[ct]);
           sB[ct] = mfma16x16x32(kfb[c], qv[ct][c], sB[ct]);
         }
+      }
       // raw scores; near the diagonal or the context end a key a row may
       // not see gets kMaskedScore, whose weight 2^(scale (s - m)) is 0 (the
       // scale is never 0: a zero scale runs as a vanishing positive one)
@@ -647,24 +646,12 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
           m_run[ct] = m_new[ct];
         }
       }
-      // p = 2^(scale (s - m)), one fused multiply-add and one exponent each;
-      // the float32 sum as a pairwise tree
-      bf16x8 pb[QT];
-#pragma unroll
-      for (int ct = 0; ct < QT; ++ct) {
-        const float nms = -m_run[ct] * scl;
-        float pr[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          pr[i] = fast_exp2(__builtin_fmaf(sc[ct][i], scl, nms));
-          pb[ct][i] = static_cast<__bf16>(pr[i]);
-        }
-        l_run[ct] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
-      }
       // Slots at or past the context end may hold anything and are zeroed;
       // only a step that holds the context end (or has no second block)
       // needs it, and that is the same for the whole wave. (Here, after the
-      // score products, so that those wait only for the K fragments.)
+      // score products, so that those wait only for the K fragments, and
+      // before the exponentials, which share one block with the value
+      // products.)
       const bool tail = !hasB || (jA + 1) * kBlockSize > L || (jB + 1) * kBlockSize > L;
       if (tail) {
         const int la = L - jA * kBlockSize - 4 * kgrp;
@@ -677,10 +664,32 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         for (int t = 0; t < VT; ++t)
           vf[t] = as_bf16x8(__builtin_bit_cast(u32x4, vf[t]) & mk);
       }
+      // p = 2^(scale (s - m)), one fused multiply-add and one exponent each;
+      // the float32 sum as a pairwise tree
+      // then each column tile's value product; the scheduling groups below
+      // interleave one tile's value product with the next tile's
+      // exponentials (the matrix cores and the vector unit work side by side)
 #pragma unroll
-      for (int t = 0; t < VT; ++t)
+      for (int ct = 0; ct < QT; ++ct) {
+        const float nms = -m_run[ct] * scl;
+        float pr[8];
+        bf16x8 pb;
 #pragma unroll
-        for (int ct = 0; ct < QT; ++ct) acc[ct][t] = mfma16x16x32(vf[t], pb[ct], acc[ct][t]);
+        for (int i = 0; i < 8; ++i) {
+          pr[i] = fast_exp2(__builtin_fmaf(sc[ct][i], scl, nms));
+          pb[i] = static_cast<__bf16>(pr[i]);
+        }
+        l_run[ct] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+#pragma unroll
+        for (int t = 0; t < VT; ++t) acc[ct][t] = mfma16x16x32(vf[t], pb, acc[ct][t]);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x402, 32, 0);  // exponentials of tile 0
+#pragma unroll
+      for (int i = 0; i < VT; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a value MFMA of tile 0
+        __builtin_amdgcn_sched_group_barrier(0x402, 4, 0);  // exponentials of tile 1
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, VT, 0);  // value MFMAs of tile 1
     }
     // every load has landed before the ring or the list is reused
     wait_vmcnt<0>();
