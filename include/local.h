@@ -460,6 +460,39 @@ local_status_t local_block_version_check(
     int32_t* valid_tokens,
     void* ws, size_t* ws_bytes, void* stream);
 
+/*
+ * local_kv_pool_import / local_kv_pool_export — convert one layer's paged KV
+ * pool between the token-major layout and this library's pool layout (§2.2
+ * "KV cache": fixed-size blocks of key/value states addressed through a block
+ * table). Block ids, slots and values are unchanged: the block table and the
+ * tags stay valid across the conversion; only the in-block order differs.
+ *
+ *   token-major  k_tok, v_tok [num_blocks][Hkv][16][D] bf16: K(p,g,slot,d)
+ *                at ((p*Hkv + g)*16 + slot)*D + d (V alike)
+ *   library      k_cache [num_blocks][Hkv][D/8][16][8], v_cache
+ *                [num_blocks][Hkv][D][16] bf16 (the pool layout above)
+ *
+ *  import reads k_tok, v_tok and writes k_cache, v_cache; export reads
+ *  k_cache, v_cache and writes k_tok, v_tok. Every element is copied exactly
+ *  (a permutation of 2-byte values, bit for bit).
+ *
+ *  Sizes: num_blocks >= 0 (0: nothing is launched and the pointers may be
+ *  NULL), Hkv >= 1, D in {64,128}, block_size == 16. Errors: LOCAL_ERR_NULL
+ *  for a NULL pool,
+ *  LOCAL_ERR_SHAPE for a negative num_blocks, Hkv < 1, or pools that
+ *  overlap (the conversion is not in place), LOCAL_ERR_UNSUPPORTED for
+ *  another D or block_size. No workspace.
+ */
+local_status_t local_kv_pool_import(
+    const uint16_t* k_tok, const uint16_t* v_tok,
+    int64_t num_blocks, int32_t Hkv, int32_t D, int32_t block_size,
+    uint16_t* k_cache, uint16_t* v_cache, void* stream);
+
+local_status_t local_kv_pool_export(
+    const uint16_t* k_cache, const uint16_t* v_cache,
+    int64_t num_blocks, int32_t Hkv, int32_t D, int32_t block_size,
+    uint16_t* k_tok, uint16_t* v_tok, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

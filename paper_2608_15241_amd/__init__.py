@@ -8,6 +8,7 @@ from .binding import (BLOCK_SIZE, EXPORTS, LIB_PATH, Call, KVManager, LocalError
                       Workspace,
                       load_library, local_block_version_check, local_lora_grad,
                       local_lora_grad_grouped, local_lora_grad_input, local_lora_linear,
+                      local_kv_pool_export, local_kv_pool_import,
                       local_lora_linear_grouped, local_paged_attn_decode,
                       local_paged_attn_decode_checked, local_paged_attn_decode_noalloc,
                       local_paged_attn_prefill, prepare_paged_attn_decode_checked,

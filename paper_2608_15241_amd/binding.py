@@ -28,7 +28,7 @@ EXPORTS = ("local_last_error", "local_version", "local_lora_linear",
            "local_lora_linear_grouped", "local_paged_attn_decode", "local_paged_attn_prefill",
            "local_block_version_check", "local_lora_grad", "local_lora_grad_input",
            "local_lora_grad_grouped", "local_paged_attn_decode_noalloc",
-           "local_paged_attn_decode_checked",
+           "local_paged_attn_decode_checked", "local_kv_pool_import", "local_kv_pool_export",
            # host-side KV manager (local_kv.h)
            "local_kvm_default_params", "local_kvm_create", "local_kvm_destroy",
            "local_kvm_tags", "local_kvm_set_committed", "local_kvm_stage", "local_kvm_publish",
@@ -102,6 +102,10 @@ def load_library(path: str = LIB_PATH):
     lib.local_lora_grad_input.restype = ctypes.c_int
     lib.local_lora_grad_input.argtypes = [P, i64, i64, P, i64, P, P, i32, i32, P, P, P, P, P,
                                           SZ, P]
+    for name in ("local_kv_pool_import", "local_kv_pool_export"):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
     _declare_kvm(lib)
     _declare_sched(lib)
     _lib = lib
@@ -776,6 +780,53 @@ def local_block_version_check(*args, **kwargs
     Only the first min(n_stale, cap) rows of stale_pairs are written.
     """
     return prepare_block_version_check(*args, **kwargs)()
+
+
+def _pool_pair(a, b, what):
+    _req(a, what[0], torch.bfloat16, 4)
+    _req(b, what[1], torch.bfloat16, 4)
+    if a.shape != b.shape:
+        raise ValueError("%s and %s must have one shape" % what)
+
+
+def local_kv_pool_import(k_tok, v_tok, k_cache=None, v_cache=None):
+    """Token-major pools [num_blocks, Hkv, 16, D] (bf16) -> the library's pool
+    layout; returns (k_cache [num_blocks, Hkv, 16*D], v_cache alike)."""
+    lib = load_library()
+    _pool_pair(k_tok, v_tok, ("k_tok", "v_tok"))
+    nb, hkv, bs, D = k_tok.shape
+    if k_cache is None:
+        k_cache = torch.empty((nb, hkv, bs * D), dtype=torch.bfloat16, device=k_tok.device)
+    if v_cache is None:
+        v_cache = torch.empty((nb, hkv, bs * D), dtype=torch.bfloat16, device=k_tok.device)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _req(t, n, torch.bfloat16, 3)
+        if tuple(t.shape) != (nb, hkv, bs * D):
+            raise ValueError("%s must be [num_blocks, Hkv, 16*D]" % n)
+    _check(lib.local_kv_pool_import(_ptr(k_tok), _ptr(v_tok), nb, hkv, D, bs, _ptr(k_cache),
+                                    _ptr(v_cache), _stream()))
+    return k_cache, v_cache
+
+
+def local_kv_pool_export(k_cache, v_cache, D, k_tok=None, v_tok=None):
+    """The library's pools [num_blocks, Hkv, 16*D] (bf16) -> token-major
+    [num_blocks, Hkv, 16, D]; returns (k_tok, v_tok)."""
+    lib = load_library()
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _req(t, n, torch.bfloat16, 3)
+    if k_cache.shape != v_cache.shape or k_cache.shape[2] != BLOCK_SIZE * D:
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16*D]")
+    nb, hkv = k_cache.shape[0], k_cache.shape[1]
+    if k_tok is None:
+        k_tok = torch.empty((nb, hkv, BLOCK_SIZE, D), dtype=torch.bfloat16, device=k_cache.device)
+    if v_tok is None:
+        v_tok = torch.empty((nb, hkv, BLOCK_SIZE, D), dtype=torch.bfloat16, device=k_cache.device)
+    _pool_pair(k_tok, v_tok, ("k_tok", "v_tok"))
+    if tuple(k_tok.shape) != (nb, hkv, BLOCK_SIZE, D):
+        raise ValueError("k_tok and v_tok must be [num_blocks, Hkv, 16, D]")
+    _check(lib.local_kv_pool_export(_ptr(k_cache), _ptr(v_cache), nb, hkv, D, BLOCK_SIZE,
+                                    _ptr(k_tok), _ptr(v_tok), _stream()))
+    return k_tok, v_tok
 
 
 # ------------------------------------------------------------ KV manager

@@ -267,3 +267,21 @@ def test_decode_noalloc_rejects_sizes_beyond_its_scratch(lib):
     assert call(D=96) == ERR_UNSUPPORTED
     assert call(bs=8) == ERR_UNSUPPORTED
     assert call(kn=None) == ERR_NULL
+
+
+def test_kv_pool_conversion_errors(lib):
+    A, B, C, D_ = (ctypes.c_void_p(x) for x in (0x100000, 0x200000, 0x300000, 0x400000))
+    for f in (lib.local_kv_pool_import, lib.local_kv_pool_export):
+        # 0 blocks: nothing to do, nothing launched
+        assert f(A, B, 0, 8, 128, 16, C, D_, None) == OK
+        assert f(None, None, 0, 8, 128, 16, None, None, None) == OK
+        assert f(None, B, 4, 8, 128, 16, C, D_, None) == ERR_NULL
+        assert f(A, B, 4, 8, 128, 16, C, None, None) == ERR_NULL
+        assert f(A, B, -1, 8, 128, 16, C, D_, None) == ERR_SHAPE
+        assert f(A, B, 4, 0, 128, 16, C, D_, None) == ERR_SHAPE
+        assert f(A, B, 4, 8, 96, 16, C, D_, None) == ERR_UNSUPPORTED
+        assert f(A, B, 4, 8, 128, 8, C, D_, None) == ERR_UNSUPPORTED
+        # 4 blocks x 8 heads x 4 KB = 128 KB per pool: these ranges overlap
+        assert f(A, B, 4, 8, 128, 16, ctypes.c_void_p(0x110000), D_, None) == ERR_SHAPE
+        assert f(A, B, 4, 8, 128, 16, C, ctypes.c_void_p(0x310000), None) == ERR_SHAPE
+        assert b"overlap" in lib.local_last_error()
