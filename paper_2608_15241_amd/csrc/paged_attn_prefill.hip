@@ -26,6 +26,8 @@
 //    Causal masking per key, dead slots past the context end zeroed in V,
 //    online softmax in the log2 domain. Steps wholly past a wave's causal
 //    limit skip its arithmetic (the wave still takes part in the loads).
+#include <utility>
+
 #include "common.hpp"
 
 namespace localk {
@@ -148,6 +150,45 @@ __device__ __forceinline__ void wait_lgkm0_barrier() {
 // one 16-byte direct load: lane l of the wave writes at lds + 16 l
 __device__ __forceinline__ void lds_load16(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+
+// LDS reads issued exactly as written: the compiler neither pairs them into
+// ds_read2 forms nor waits for them (the kernel waits on the LDS counter
+// itself, then passes the registers through an empty asm so that nothing
+// reads them earlier). addr is a byte address in LDS.
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read8(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+template <int N>
+__device__ __forceinline__ void lds_wait() {  // at most N LDS operations outstanding
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p));
+}
+// f(IC<0>{}), ..., f(IC<N-1>{}): loop indices usable as template arguments
+template <int I>
+struct IC {
+  static constexpr int v = I;
+};
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_(F&& f, std::integer_sequence<int, I...>) {
+  (f(IC<I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_(f, std::make_integer_sequence<int, N>{});
 }
 
 constexpr int kPlanThreads = 256;  // threads of the workgroup that plans the units
@@ -566,24 +607,37 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       // every key of the step precedes every row of the wave (so it is also
       // before the context end): no masking
       const bool unmasked = hasB && jB * kBlockSize + kBlockSize - 1 <= wave_first;
-      const uint8_t* st = ring + (s % kPaStages) * STAGE_B;
-      const uint16_t* kA = reinterpret_cast<const uint16_t*>(st);
-      const uint16_t* kB = reinterpret_cast<const uint16_t*>(st + TILE_B);
-      const uint8_t* vrow = st + 2 * TILE_B + v_off;
+      // Operand reads of the stage: K of A and B (1 KB contiguous per
+      // instruction), then V (slots 4 kgrp .. +4 of each block; zeroed past
+      // the context end just before the value product) as single 8-byte
+      // reads. Compiled, the V reads of A and B (512 bytes apart) would be
+      // paired into ds_read2st64_b64, whose two addresses per lane share a
+      // bank: measured on gfx950, 77 bytes per clock and compute unit
+      // against 215 for single 8-byte reads and 256 for 16-byte ones.
+      const uint32_t st_addr = lds_addr(ring) + static_cast<uint32_t>((s % kPaStages) * STAGE_B);
+      const uint32_t k_addr = st_addr + 16 * lane;
+      const uint32_t v_addr = st_addr + 2 * TILE_B + v_off;
+      u32x4 kra[KC], krb[KC];
+      u32x2 vra[VT], vrb[VT];
+      static_for<KC>([&](auto c) {
+        kra[c.v] = lds_read16<1024 * c.v>(k_addr);
+        krb[c.v] = lds_read16<TILE_B + 1024 * c.v>(k_addr);
+      });
+      static_for<VT / 2>([&](auto t) {
+        vra[t.v] = lds_read8<1024 * t.v>(v_addr);
+        vrb[t.v] = lds_read8<1024 * t.v + 512>(v_addr);
+      });
+      lds_wait<VT>();  // the K reads have landed (the VT V reads may not)
+      static_for<VT / 2>([&](auto t) {
+        vra[VT / 2 + t.v] = lds_read8<1024 * (VT / 2 + t.v)>(v_addr);
+        vrb[VT / 2 + t.v] = lds_read8<1024 * (VT / 2 + t.v) + 512>(v_addr);
+      });
       bf16x8 kfa[KC], kfb[KC];
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
-        kfa[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kA + c * 512 + lane * 8));
-        kfb[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(kB + c * 512 + lane * 8));
-      }
-      // V fragments: slots 4 kgrp .. +4 of each block (read here, zeroed
-      // past the context end just before the value product).
-      bf16x8 vf[VT];
-#pragma unroll
-      for (int t = 0; t < VT; ++t) {
-        const u32x2 va = *reinterpret_cast<const u32x2*>(vrow + 1024 * t);
-        const u32x2 vb = *reinterpret_cast<const u32x2*>(vrow + 1024 * t + 512);
-        vf[t] = as_bf16x8(u32x4{va.x, va.y, vb.x, vb.y});
+        asm volatile("" : "+v"(kra[c]), "+v"(krb[c]));
+        kfa[c] = as_bf16x8(kra[c]);
+        kfb[c] = as_bf16x8(krb[c]);
       }
       // S^T of both column tiles, one column tile after the other (its two
       // chains of KC MFMAs interleaved), so that the first tile's maxima can
@@ -652,6 +706,13 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       // score products, so that those wait only for the K fragments, and
       // before the exponentials, which share one block with the value
       // products.)
+      lds_wait<0>();  // the V reads have landed
+      bf16x8 vf[VT];
+#pragma unroll
+      for (int t = 0; t < VT; ++t) {
+        asm volatile("" : "+v"(vra[t]), "+v"(vrb[t]));
+        vf[t] = as_bf16x8(u32x4{vra[t].x, vra[t].y, vrb[t].x, vrb[t].y});
+      }
       const bool tail = !hasB || (jA + 1) * kBlockSize > L || (jB + 1) * kBlockSize > L;
       if (tail) {
         const int la = L - jA * kBlockSize - 4 * kgrp;
