@@ -421,8 +421,9 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   constexpr int DMA = TILE_B / 1024;       // 1 KB direct loads per tile
   constexpr int STAGE_B = 4 * TILE_B;      // K and V tiles of two blocks
   extern __shared__ __attribute__((aligned(16))) uint8_t ring[];  // [kPaStages][STAGE_B]
-  __shared__ int list[kPaWindow];    // logical blocks j, ascending
-  __shared__ int list_p[kPaWindow];  // their physical ids
+  // the listed blocks, ascending: {logical block j, physical id}, the last
+  // entry repeated once past the end (so a step's pair is one 16-byte read)
+  __shared__ __attribute__((aligned(16))) int2 ent[kPaWindow + 2];
   __shared__ int wave_cnt[kPaWaves];
 
   // (query tile, key range, head h, request b) from a 1D grid, heads
@@ -488,24 +489,25 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
   }
 
   // A ring stage holds one step (two blocks A, B): K_A [KC][1 KB], K_B
-  // [KC][1 KB], then V as VT rows of 1 KB, row t = (A's dims 16t .. 16t+15,
-  // then B's), 512 bytes each. Within a 512-byte V row the 16-byte chunks are
-  // swizzled: chunk (dim d, slots 8 half .. +8) sits at chunk index
+  // [KC][1 KB], then V of A as VT rows of 512 bytes (row t: dims 16t ..
+  // 16t+15), then V of B alike. Within a 512-byte V row the 16-byte chunks
+  // are swizzled: chunk (dim d, slots 8 half .. +8) sits at chunk index
   // 2 (d % 16) + (half ^ bit 3 of d), so that the 32 lanes of each half of a
-  // value-fragment read cover 256 contiguous bytes of banks, and a lane's
-  // fragments of A and B are one paired read 512 bytes apart. The stage is
+  // value-fragment read cover 256 contiguous bytes of banks. The stage is
   // filled by NPIECE direct 1 KB loads, NPIECE / 4 per wave; lane l of a
   // piece fetches the 16 bytes that land at byte 16 l of it.
   constexpr int NPIECE = 2 * DMA + VT;
   constexpr int PPW = NPIECE / kPaWaves;
   static_assert(NPIECE % kPaWaves == 0 && STAGE_B == NPIECE * 1024, "stage layout");
-  // Waves 0 and 1 load K (block A, block B: 1 KB piece i of the tile at
-  // byte 1024 i, lane l's 16 bytes at 16 l); waves 2 and 3 load V rows
-  // (row t = PPW (wave - 2) + i at byte 512 t of each block's tile, lanes
-  // 0-31 from A, 32-63 from B, lane l's 16 bytes at its swizzled chunk).
+  // Every wave loads from one block, so that the tile's address is
+  // wave-uniform (scalar arithmetic): waves 0 and 2 read block A, waves 1
+  // and 3 block B. Waves 0 and 1 load K (1 KB piece i of the tile at byte
+  // 1024 i, lane l's 16 bytes at 16 l); waves 2 and 3 load V, piece i
+  // holding rows 2i (lanes 0-31) and 2i + 1 (lanes 32-63), row t at byte
+  // 512 t of the tile, lane l's 16 bytes at its swizzled chunk.
   static_assert(PPW == DMA && 2 * DMA == VT, "K and V pieces in separate waves");
   const bool k_wave = wave < 2;
-  const bool lane_b = k_wave ? wave == 1 : lane >= 32;  // the lane reads block B
+  const bool wave_b = (wave & 1) != 0;  // the wave reads block B
   uint32_t lane_src;  // byte offset of piece 0's 16 bytes within the block's tile
   if (k_wave) {
     lane_src = static_cast<uint32_t>(16 * lane);
@@ -513,9 +515,9 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     const int cidx = lane & 31;
     const int dl = cidx >> 1;  // dim within the row (d = 16 t + dl)
     const int half = (cidx & 1) ^ ((dl >> 3) & 1);
-    lane_src = static_cast<uint32_t>(512 * PPW * (wave - 2) + 32 * dl + 16 * half);
+    lane_src = static_cast<uint32_t>(512 * (lane >> 5) + 32 * dl + 16 * half);
   }
-  // this lane's value fragment in V row t of a stage (A's half; B's is 512
+  // this lane's value fragment in V row t of a stage (A's; B's is VT * 512
   // bytes on): dim 16 t + col, slots 4 kgrp .. +4
   const uint32_t v_off = 32 * col + 16 * ((kgrp >> 1) ^ ((col >> 3) & 1)) + 8 * (kgrp & 1);
 
@@ -539,8 +541,8 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       n += wave_cnt[w];
     }
     if (ok) {
-      list[off + before] = j;
-      list_p[off + before] = p;
+      ent[off + before] = int2{j, p};
+      if (off + before == n - 1) ent[n] = int2{j, p};
     }
     __syncthreads();
     return n;
@@ -567,29 +569,24 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     // end repeats its first (never used), and steps past the last repeat the
     // last into the free stage, so every step issues the same loads and the
     // wait counts hold.
-    auto ids = [&](int s) {
-      return int2{list_p[min(2 * s, cnt - 1)], list_p[min(2 * s + 1, cnt - 1)]};
-    };
-    auto issue = [&](int stage, int2 p) {
+    // entries 2s and 2s + 1 of the list: {jA, pA, jB, pB}
+    auto pair = [&](int s) { return *reinterpret_cast<const int4*>(&ent[2 * s]); };
+    auto issue = [&](int stage, int4 e) {
       uint8_t* dst = ring + stage * STAGE_B + wave * PPW * 1024;
-      const int64_t tile = (static_cast<int64_t>(lane_b ? p.y : p.x) * a.Hkv + g) * TILE;
-      if (k_wave) {
-        const uint8_t* src = reinterpret_cast<const uint8_t*>(a.k_cache + tile) + lane_src;
+      const int pw = __builtin_amdgcn_readfirstlane(wave_b ? e.w : e.y);
+      const int64_t tile = (static_cast<int64_t>(pw) * a.Hkv + g) * TILE;
+      const uint8_t* src =
+          reinterpret_cast<const uint8_t*>((k_wave ? a.k_cache : a.v_cache) + tile) + lane_src;
 #pragma unroll
-        for (int i = 0; i < PPW; ++i) lds_load16(src + 1024 * i, dst + 1024 * i);
-      } else {
-        const uint8_t* src = reinterpret_cast<const uint8_t*>(a.v_cache + tile) + lane_src;
-#pragma unroll
-        for (int i = 0; i < PPW; ++i) lds_load16(src + 512 * i, dst + 1024 * i);
-      }
+      for (int i = 0; i < PPW; ++i) lds_load16(src + 1024 * i, dst + 1024 * i);
     };
 #pragma unroll
-    for (int s = 0; s < kPaStages - 1; ++s) issue(s, ids(min(s, steps - 1)));
+    for (int s = 0; s < kPaStages - 1; ++s) issue(s, pair(min(s, steps - 1)));
     // The list entries a pass needs (the ids its loads fetch, the blocks it
     // computes on) are read one pass ahead, so that no LDS round trip stands
     // between the barrier and the loads or the arithmetic of a pass.
-    int2 p_next = ids(min(kPaStages - 1, steps - 1));
-    int2 j_next = {list[0], list[min(1, cnt - 1)]};
+    int4 e_load = pair(min(kPaStages - 1, steps - 1));
+    int4 e_comp = pair(0);
 
     for (int s = 0; s < steps; ++s) {
       // this wave's loads of step s are done (those of the two later steps
@@ -597,12 +594,13 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       // step s - 1 is free for step s + 3
       wait_vmcnt<PPW * (kPaStages - 2)>();
       wait_lgkm0_barrier();
-      issue((s + kPaStages - 1) % kPaStages, p_next);
-      const int jA = j_next.x;
+      issue((s + kPaStages - 1) % kPaStages, e_load);
+      // the step's blocks (wave-uniform, so that their tests are scalar)
+      const int jA = __builtin_amdgcn_readfirstlane(e_comp.x);
       const bool hasB = 2 * s + 1 < cnt;
-      const int jB = hasB ? j_next.y : jA;
-      p_next = ids(min(s + kPaStages, steps - 1));
-      j_next = int2{list[min(2 * s + 2, cnt - 1)], list[min(2 * s + 3, cnt - 1)]};
+      const int jB = hasB ? __builtin_amdgcn_readfirstlane(e_comp.z) : jA;
+      e_load = pair(min(s + kPaStages, steps - 1));
+      e_comp = pair(min(s + 1, steps - 1));
       if (jA * kBlockSize > wave_limit) continue;  // wholly past this wave's rows
       // every key of the step precedes every row of the wave (so it is also
       // before the context end): no masking
@@ -624,13 +622,13 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         krb[c.v] = lds_read16<TILE_B + 1024 * c.v>(k_addr);
       });
       static_for<VT / 2>([&](auto t) {
-        vra[t.v] = lds_read8<1024 * t.v>(v_addr);
-        vrb[t.v] = lds_read8<1024 * t.v + 512>(v_addr);
+        vra[t.v] = lds_read8<512 * t.v>(v_addr);
+        vrb[t.v] = lds_read8<512 * (VT + t.v)>(v_addr);
       });
       lds_wait<VT>();  // the K reads have landed (the VT V reads may not)
       static_for<VT / 2>([&](auto t) {
-        vra[VT / 2 + t.v] = lds_read8<1024 * (VT / 2 + t.v)>(v_addr);
-        vrb[VT / 2 + t.v] = lds_read8<1024 * (VT / 2 + t.v) + 512>(v_addr);
+        vra[VT / 2 + t.v] = lds_read8<512 * (VT / 2 + t.v)>(v_addr);
+        vrb[VT / 2 + t.v] = lds_read8<512 * (VT + VT / 2 + t.v)>(v_addr);
       });
       bf16x8 kfa[KC], kfb[KC];
 #pragma unroll
