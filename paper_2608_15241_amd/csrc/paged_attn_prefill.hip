@@ -42,6 +42,7 @@ constexpr int kPaWindow = 256;                  // block-table entries listed pe
 constexpr float kNegBigPf = -1.0e30f;      // initial running maximum (finite)
 constexpr float kMaskedScore = -3.0e38f;   // score of a key a row may not see
 constexpr float kPaLazy = 8.0f;            // log2 of the largest weight before a rescale
+constexpr float kPaLazyWeight = 256.0f;    // 2^kPaLazy
 
 // max(a, b, c) in one instruction (fmaxf chains add NaN-quieting maxima)
 __device__ __forceinline__ float max3f(float a, float b, float c) {
@@ -675,29 +676,6 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
             sc[ct][4 + i] = (hasB && posB <= qpos[ct]) ? sc[ct][4 + i] : kMaskedScore;
           }
       }
-      // Lazy rescale: the running maximum moves only when a column's maximum
-      // exceeds it by more than 2^kPaLazy in weight; weights up to that stay
-      // exact in float32 and bf16 alike, so the result is the same softmax.
-      bool grow = false;
-      float m_new[QT];
-#pragma unroll
-      for (int ct = 0; ct < QT; ++ct) {
-        float mx = max3f(max3f(sc[ct][0], sc[ct][1], sc[ct][2]),
-                         max3f(sc[ct][3], sc[ct][4], sc[ct][5]), max2f(sc[ct][6], sc[ct][7]));
-        mx = max_xor32(max_xor16(mx));
-        m_new[ct] = max2f(m_run[ct], mx);
-        grow = grow || (m_new[ct] - m_run[ct]) * scl > kPaLazy;
-      }
-      if (__ballot(grow) != 0ull) {
-#pragma unroll
-        for (int ct = 0; ct < QT; ++ct) {
-          const float alpha = fast_exp2((m_run[ct] - m_new[ct]) * scl);
-          l_run[ct] *= alpha;
-#pragma unroll
-          for (int t = 0; t < VT; ++t) acc[ct][t] *= alpha;
-          m_run[ct] = m_new[ct];
-        }
-      }
       // Slots at or past the context end may hold anything and are zeroed;
       // only a step that holds the context end (or has no second block)
       // needs it, and that is the same for the whole wave. (Here, after the
@@ -723,32 +701,61 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
         for (int t = 0; t < VT; ++t)
           vf[t] = as_bf16x8(__builtin_bit_cast(u32x4, vf[t]) & mk);
       }
-      // p = 2^(scale (s - m)), one fused multiply-add and one exponent each;
-      // the float32 sum as a pairwise tree
-      // then each column tile's value product; the scheduling groups below
-      // interleave one tile's value product with the next tile's
-      // exponentials (the matrix cores and the vector unit work side by side)
+      // p = 2^(scale (s - m)) with the running maximum m, one fused
+      // multiply-add and one exponent each. Lazy rescale: m moves only when
+      // a column's maximum exceeds it by more than 2^kPaLazy in weight, i.e.
+      // when some p exceeds 2^kPaLazy (weights up to that stay exact in
+      // float32 and bf16 alike, so the result is the same softmax); then m,
+      // the sums and the weights are redone, which is rare after the first
+      // step. Testing the weights instead of the scores leaves the common
+      // step without the cross-lane maxima.
+      float pr[QT][8];
+      auto weights = [&](int ct) {
+        const float nms = -m_run[ct] * scl;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pr[ct][i] = fast_exp2(__builtin_fmaf(sc[ct][i], scl, nms));
+      };
+      auto rescale_if_needed = [&](int ct) {
+        const float pm = max3f(max3f(pr[ct][0], pr[ct][1], pr[ct][2]),
+                               max3f(pr[ct][3], pr[ct][4], pr[ct][5]), max2f(pr[ct][6], pr[ct][7]));
+        if (__ballot(pm > kPaLazyWeight) != 0ull) {
+          float mx = max3f(max3f(sc[ct][0], sc[ct][1], sc[ct][2]),
+                           max3f(sc[ct][3], sc[ct][4], sc[ct][5]), max2f(sc[ct][6], sc[ct][7]));
+          mx = max_xor32(max_xor16(mx));
+          const float m_new = max2f(m_run[ct], mx);
+          const float alpha = fast_exp2((m_run[ct] - m_new) * scl);
+          l_run[ct] *= alpha;
+#pragma unroll
+          for (int t = 0; t < VT; ++t) acc[ct][t] *= alpha;
+          m_run[ct] = m_new;
+          weights(ct);
+        }
+      };
+      // Each column tile's value product follows its weights; the
+      // scheduling groups interleave one tile's value product with the next
+      // tile's exponentials (the matrix cores and the vector unit work side
+      // by side). The float32 row sums as pairwise trees.
+      weights(0);
+      rescale_if_needed(0);
 #pragma unroll
       for (int ct = 0; ct < QT; ++ct) {
-        const float nms = -m_run[ct] * scl;
-        float pr[8];
         bf16x8 pb;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          pr[i] = fast_exp2(__builtin_fmaf(sc[ct][i], scl, nms));
-          pb[i] = static_cast<__bf16>(pr[i]);
-        }
-        l_run[ct] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+        for (int i = 0; i < 8; ++i) pb[i] = static_cast<__bf16>(pr[ct][i]);
+        l_run[ct] += ((pr[ct][0] + pr[ct][1]) + (pr[ct][2] + pr[ct][3])) +
+                     ((pr[ct][4] + pr[ct][5]) + (pr[ct][6] + pr[ct][7]));
 #pragma unroll
         for (int t = 0; t < VT; ++t) acc[ct][t] = mfma16x16x32(vf[t], pb, acc[ct][t]);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x402, 32, 0);  // exponentials of tile 0
+        if (ct + 1 < QT) {
+          weights(ct + 1);
 #pragma unroll
-      for (int i = 0; i < VT; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a value MFMA of tile 0
-        __builtin_amdgcn_sched_group_barrier(0x402, 4, 0);  // exponentials of tile 1
+          for (int i = 0; i < VT; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a value MFMA of tile ct
+            __builtin_amdgcn_sched_group_barrier(0x402, 4, 0);  // exponentials of tile ct + 1
+          }
+          rescale_if_needed(ct + 1);
+        }
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, VT, 0);  // value MFMAs of tile 1
     }
     // every load has landed before the ring or the list is reused
     wait_vmcnt<0>();
