@@ -152,6 +152,10 @@ __device__ __forceinline__ void wait_lgkm0_barrier() {
 __device__ __forceinline__ void lds_load16(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 }
+// the same through a buffer descriptor: the lane reads at byte off of it
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint32_t off, void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
+}
 
 // LDS reads issued exactly as written: the compiler neither pairs them into
 // ds_read2 forms nor waits for them (the kernel waits on the LDS counter
@@ -518,6 +522,9 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
     const int half = (cidx & 1) ^ ((dl >> 3) & 1);
     lane_src = static_cast<uint32_t>(512 * (lane >> 5) + 32 * dl + 16 * half);
   }
+  uint32_t piece_src[PPW];  // byte offsets of the lane's 16 bytes of each piece
+#pragma unroll
+  for (int i = 0; i < PPW; ++i) piece_src[i] = lane_src + 1024 * i;
   // this lane's value fragment in V row t of a stage (A's; B's is VT * 512
   // bytes on): dim 16 t + col, slots 4 kgrp .. +4
   const uint32_t v_off = 32 * col + 16 * ((kgrp >> 1) ^ ((col >> 3) & 1)) + 8 * (kgrp & 1);
@@ -576,10 +583,14 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       uint8_t* dst = ring + stage * STAGE_B + wave * PPW * 1024;
       const int pw = __builtin_amdgcn_readfirstlane(wave_b ? e.w : e.y);
       const int64_t tile = (static_cast<int64_t>(pw) * a.Hkv + g) * TILE;
-      const uint8_t* src =
-          reinterpret_cast<const uint8_t*>((k_wave ? a.k_cache : a.v_cache) + tile) + lane_src;
+      // a buffer descriptor of the tile (scalar registers) and the lane's
+      // fixed offsets: the loads take no vector arithmetic (the immediate
+      // offset of an LDS-destination buffer load would move the LDS address
+      // too, so the piece offset rides in the lane's offset register)
+      const __amdgpu_buffer_rsrc_t r = make_rsrc((k_wave ? a.k_cache : a.v_cache) + tile, TILE_B);
 #pragma unroll
-      for (int i = 0; i < PPW; ++i) lds_load16(src + 1024 * i, dst + 1024 * i);
+      for (int i = 0; i < PPW; ++i)
+        lds_load16(r, piece_src[i], dst + 1024 * i);
     };
 #pragma unroll
     for (int s = 0; s < kPaStages - 1; ++s) issue(s, pair(min(s, steps - 1)));
