@@ -592,28 +592,24 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
       for (int i = 0; i < PPW; ++i)
         lds_load16(r, piece_src[i], dst + 1024 * i);
     };
-#pragma unroll
-    for (int s = 0; s < kPaStages - 1; ++s) issue(s, pair(min(s, steps - 1)));
-    // The list entries a pass needs (the ids its loads fetch, the blocks it
-    // computes on) are read one pass ahead, so that no LDS round trip stands
-    // between the barrier and the loads or the arithmetic of a pass.
-    int4 e_load = pair(min(kPaStages - 1, steps - 1));
-    int4 e_comp = pair(0);
+    // Two steps per barrier: after the barrier of steps s, s + 1 (their
+    // loads were issued one pair earlier), the loads of steps s + 2, s + 3
+    // go into the stages of the previous pair. The list entries a pair needs
+    // (the ids its loads fetch, the blocks it computes on) are read one pair
+    // ahead, so that no LDS round trip stands between the barrier and the
+    // loads or the arithmetic.
+    static_assert(kPaStages == 4, "two stages per pair of steps");
+    issue(0, pair(0));
+    issue(1, pair(min(1, steps - 1)));
+    int4 e_l0 = pair(min(2, steps - 1)), e_l1 = pair(min(3, steps - 1));
+    int4 e_c0 = pair(0), e_c1 = pair(min(1, steps - 1));
 
-    for (int s = 0; s < steps; ++s) {
-      // this wave's loads of step s are done (those of the two later steps
-      // may still fly); after the barrier everyone's are, and the stage of
-      // step s - 1 is free for step s + 3
-      wait_vmcnt<PPW * (kPaStages - 2)>();
-      wait_lgkm0_barrier();
-      issue((s + kPaStages - 1) % kPaStages, e_load);
+    auto compute = [&](int s, int4 e) {
       // the step's blocks (wave-uniform, so that their tests are scalar)
-      const int jA = __builtin_amdgcn_readfirstlane(e_comp.x);
+      const int jA = __builtin_amdgcn_readfirstlane(e.x);
       const bool hasB = 2 * s + 1 < cnt;
-      const int jB = hasB ? __builtin_amdgcn_readfirstlane(e_comp.z) : jA;
-      e_load = pair(min(s + kPaStages, steps - 1));
-      e_comp = pair(min(s + 1, steps - 1));
-      if (jA * kBlockSize > wave_limit) continue;  // wholly past this wave's rows
+      const int jB = hasB ? __builtin_amdgcn_readfirstlane(e.z) : jA;
+      if (jA * kBlockSize > wave_limit) return;  // wholly past this wave's rows
       // every key of the step precedes every row of the wave (so it is also
       // before the context end): no masking
       const bool unmasked = hasB && jB * kBlockSize + kBlockSize - 1 <= wave_first;
@@ -767,6 +763,21 @@ __global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(PrefillArgs
           rescale_if_needed(ct + 1);
         }
       }
+    };
+    for (int s = 0; s < steps; s += 2) {
+      // this wave's loads of steps s, s + 1 are done; after the barrier
+      // everyone's are, and the stages of steps s - 2, s - 1 are free
+      wait_vmcnt<0>();
+      wait_lgkm0_barrier();
+      issue((s + 2) % kPaStages, e_l0);
+      issue((s + 3) % kPaStages, e_l1);
+      const int4 c0 = e_c0, c1 = e_c1;
+      e_l0 = pair(min(s + 4, steps - 1));
+      e_l1 = pair(min(s + 5, steps - 1));
+      e_c0 = pair(min(s + 2, steps - 1));
+      e_c1 = pair(min(s + 3, steps - 1));
+      compute(s, c0);
+      if (s + 1 < steps) compute(s + 1, c1);
     }
     // every load has landed before the ring or the list is reused
     wait_vmcnt<0>();
